@@ -1,0 +1,38 @@
+"""Write tests/golden/configs.json: the frozen peak threshold of each workload.
+
+For workload c the threshold is 0.10 x the largest vote mass of the CPU
+oracle's histogram on the calibration frame (seed [260916874, c, 999]), so
+that a peak must collect at least a tenth of the strongest bin's votes.  Only
+the generator and the oracle are called.  Run from the repository root:
+
+    python -m tests.golden.make_configs
+"""
+import json
+import os
+
+import oracle
+from paper_2609_16874_amd import synth
+
+OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "configs.json")
+FRACTION = 0.10
+
+
+def main():
+    out = {"fraction_of_max": FRACTION, "configs": {}}
+    for c, spec in synth.CONFIGS.items():
+        f = synth.make_frame(c, calibration=True)
+        r = oracle.decode_frame(f, peak_threshold=0.0)
+        hmax = int(r["hist"].max())
+        out["configs"][str(c)] = {
+            "name": spec.name, "bins": spec.bins, "fg_threshold": spec.fg_threshold,
+            "capacity": ((spec.bins + 1) // 2) ** 2,
+            "calibration_max_vote_mass": hmax * 2.0 ** -30,
+            "peak_threshold": FRACTION * hmax * 2.0 ** -30,
+        }
+        print(c, out["configs"][str(c)])
+    with open(OUT, "w") as fh:
+        json.dump(out, fh, indent=1)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,91 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle source, builds it on the
+CPU with the same compiler flags, and checks that at least one pin of
+``test_oracle_pins`` fails against the mutant.  The committed oracle itself
+is untouched.
+"""
+import os
+import shutil
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+# (name, original, replacement[, original, replacement ...]) -- each original
+# text must occur exactly once in the source
+MUTANTS = [
+    ("transposed histogram", "Hv[b * bins_w + a] += (uint64_t)qx[a] * (uint64_t)qy[b];",
+     "Hv[(a * bins_h + b) % (bins_w * bins_h)] += (uint64_t)qx[a] * (uint64_t)qy[b];"),
+    ("dropped channel", "for (int32_t c = 0; c < twoF; c++) {\n            int64_t diff",
+     "for (int32_t c = 1; c < twoF; c++) {\n            int64_t diff"),
+    ("wrong sign in distance", "(int64_t)X[c] - (int64_t)pal[a * twoF + c]", "(int64_t)X[c] + (int64_t)pal[a * twoF + c]"),
+    ("bin centre off by one", "double centre = ((double)(a + 1) * (double)extent) / (double)(n + 1);\n        for (int32_t k = 0; k < F; k++) {\n            double phase",
+     "double centre = ((double)(a) * (double)extent) / (double)(n + 1);\n        for (int32_t k = 0; k < F; k++) {\n            double phase"),
+    ("sin/cos swapped", "pal[a * 2 * F + 2 * k] = (int16_t)rint(4096.0 * sin(phase));",
+     "pal[a * 2 * F + 2 * k] = (int16_t)rint(4096.0 * cos(phase));"),
+    ("y block read from x channels", "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, lut, rx, qx);",
+     "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, lut, rx, qx);"),
+    ("x palette used for y", "axis_profile(Y, Ph, bins_h, twoF, lut, ry, qy);", "axis_profile(Y, Pw, bins_h, twoF, lut, ry, qy);"),
+    ("weight index floored", "int32_t idx = (int32_t)rintf(ra * 0.0625f);", "int32_t idx = (int32_t)(ra * 0.0625f);"),
+    ("LUT scale", "lut[i] = (uint16_t)rint(32768.0 * exp(-(double)i / 256.0));",
+     "lut[i] = (uint16_t)rint(32767.0 * exp(-(double)i / 256.0));"),
+    ("non-strict local max", "if (!(v > h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64",
+     "if (!(v >= h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64"),
+    ("4-neighbourhood", "if (!da && !db) continue;\n            int32_t nb = b + db, na = a + da;\n            if (nb < 0 || nb >= bh || na < 0 || na >= bw) continue;\n            if (!(v > h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64",
+     "if (!da == !db) continue;\n            int32_t nb = b + db, na = a + da;\n            if (nb < 0 || nb >= bh || na < 0 || na >= bw) continue;\n            if (!(v > h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64"),
+    ("threshold not strict", "if (v > cut && is_peak_u64", "if (v >= cut - 1000000 && is_peak_u64"),
+    ("tie goes to the last candidate", "if (dk < best_d) {", "if (dk <= best_d) {"),
+    ("assignment ignores the y axis", "float dk = rx[peak_a[k]] + ry[peak_b[k]];", "float dk = rx[peak_a[k]];",
+     "float best_d = rx[peak_a[0]] + ry[peak_b[0]];", "float best_d = rx[peak_a[0]];"),
+    ("background pixels vote", "if (!(load_value(fg, dtype, p) > fg_threshold)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]",
+     "if (!(load_value(fg, dtype, p) > -1e30f)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]"),
+    ("no clamp", "if (t > (float)X_CLAMP) return X_CLAMP;", "if (t > (float)X_CLAMP * 4) return X_CLAMP;"),
+]
+
+PIN_CASES = [
+    (pins.test_lut_closed_form, ()),
+    (pins.test_palette_is_gamma_at_bin_centres, ()),
+    (pins.test_palette_unit_circle_and_mirror, ()),
+    (pins.test_histogram_matches_eq11_within_quantisation_bound, (pins.np.float32, 4, 12)),
+    (pins.test_histogram_matches_eq11_within_quantisation_bound, (pins.np.float16, 16, 32)),
+    (pins.test_histogram_catches_axis_swap, ()),
+    (pins.test_peaks_match_library_local_max, (0,)),
+    (pins.test_oracle_equals_exhaustive_search, (0, pins.np.float32, 2, 5, 4, 6)),
+    (pins.test_oracle_equals_exhaustive_search, (1, pins.np.float16, 3, 6, 6, 2)),
+    (pins.test_noise_free_decodes_generating_centroids_and_labels, (0,)),
+    (pins.test_invariants, (0,)),
+    (pins.test_clamp_saturates, ()),
+    (pins.test_plateau_gives_no_peak_and_single_bin_is_a_peak, ()),
+    (pins.test_threshold_is_strict, ()),
+    (pins.test_exact_tie_goes_to_lowest_index, ()),
+]
+
+
+def _fails(fn, args):
+    try:
+        fn(*args)
+    except (AssertionError, ValueError, IndexError):
+        return True
+    return False
+
+
+@pytest.mark.parametrize("mutant", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, mutant):
+    name, edits = mutant[0], mutant[1:]
+    src = open(oracle.SRC).read()
+    for old, new in zip(edits[0::2], edits[1::2]):
+        assert src.count(old) == 1, f"mutation site for '{name}' not unique"
+        src = src.replace(old, new)
+    path = tmp_path / "cpe_oracle.c"
+    path.write_text(src)
+    shutil.copy(os.path.join(oracle.HERE, "cpe_oracle.h"), tmp_path / "cpe_oracle.h")
+    lib = oracle.build(src=str(path), out=str(tmp_path / "libmutant.so"))
+    with oracle.using_library(lib):
+        caught = [fn.__name__ for fn, args in PIN_CASES if _fails(fn, args)]
+    assert caught, f"no pin catches the planted mistake '{name}'"
+
+
+def test_unmutated_passes_all_pins():
+    assert not [fn.__name__ for fn, args in PIN_CASES if _fails(fn, args)]

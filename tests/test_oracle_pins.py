@@ -1,0 +1,352 @@
+"""Pins of the CPU oracle against facts fixed by the paper and the mathematics.
+
+None of these re-types the oracle's loops: the checks are closed forms, the
+paper's matrix form of the vote (Eq11) evaluated in fp64 by numpy within a
+derived error bound, a library local-maximum filter, a pure-Python exhaustive
+search on tiny frames, a noise-free special case whose answer is known in
+advance, and invariants of the decoder's definition.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_16874_amd import synth
+from tests import refmath
+
+
+def paper_freqs(H, W, L=4):
+    """The paper's L harmonics (Eq2) in rad/px: 2^l pi over the normalised axis."""
+    fx = np.array([2.0 * math.pi * 2 ** l / W for l in range(L)])
+    fy = np.array([2.0 * math.pi * 2 ** l / H for l in range(L)])
+    return fx, fy
+
+
+# --------------------------------------------------------------------------
+# S0 constants
+# --------------------------------------------------------------------------
+def _tiny_decode(bins_w=32, bins_h=32, H=8, W=8, F=4):
+    emb = np.zeros((H, W, 4 * F), np.float32)
+    fg = np.zeros((H, W), np.float32)
+    fx, fy = paper_freqs(H, W, F)
+    return oracle.decode(emb, fg, fx, fy, bins_w, bins_h, 4, 0.5, 0.0), fx, fy
+
+
+def test_lut_closed_form():
+    lut = _tiny_decode()[0]["lut"].astype(np.int64)
+    assert len(lut) == 2841
+    assert lut[0] == 32768                 # e^0 scaled by 2^15
+    assert lut[256] == 12055               # 32768 / e = 12054.63...
+    assert lut[512] == 4435                # 32768 / e^2 = 4434.6...
+    assert lut[2839] == 1 and lut[2840] == 0
+    assert np.all(np.diff(lut) <= 0)
+
+
+def test_palette_is_gamma_at_bin_centres():
+    """Eq9: each palette row is 4096*gamma(bin centre) rounded (|err| <= 1/2),
+    with the x block / y block and (sin, cos) layout of Eq1/Eq3."""
+    H, W = 48, 80
+    res, fx, fy = _tiny_decode(bins_w=7, bins_h=5, H=H, W=W)
+    px, py = refmath.palettes_real(H, W, fx, fy, 7, 5)
+    assert np.abs(res["pal_x"] - 4096.0 * px).max() <= 0.5 + 1e-9
+    assert np.abs(res["pal_y"] - 4096.0 * py).max() <= 0.5 + 1e-9
+
+
+def test_palette_unit_circle_and_mirror():
+    """sin^2 + cos^2 = 1 per harmonic; mirror symmetry about the frame centre
+    when every harmonic completes whole periods over the axis."""
+    H = W = 64
+    res, fx, fy = _tiny_decode(bins_w=32, bins_h=32, H=H, W=W, F=8)
+    P = res["pal_x"].astype(np.int64)
+    F = 8
+    pair = P[:, 0::2] ** 2 + P[:, 1::2] ** 2
+    assert np.abs(pair - 4096 ** 2).max() <= 4096 * math.sqrt(2) + 0.5
+    assert np.abs(P[::-1, 0::2] + P[:, 0::2]).max() <= 1
+    assert np.abs(P[::-1, 1::2] - P[:, 1::2]).max() <= 1
+    assert P.shape == (32, 2 * F)
+
+
+# --------------------------------------------------------------------------
+# S1+S2: the vote histogram against the paper's matrix form
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,F,bins", [(np.float32, 4, 12), (np.float16, 4, 9), (np.float32, 8, 16),
+                                          (np.float16, 16, 32)])
+def test_histogram_matches_eq11_within_quantisation_bound(dtype, F, bins):
+    rng = np.random.default_rng(11 + F + bins)
+    H, W = 24, 31
+    fx, fy = paper_freqs(H, W, F)
+    # a few instances with random centroids, small noise (no clamping)
+    inst = rng.integers(0, 4, size=(H, W))
+    cx, cy = rng.uniform(0, W, 4), rng.uniform(0, H, 4)
+    clean = synth.encode_positions(cx[inst], cy[inst], fx, fy)
+    emb = (clean + 0.05 * rng.standard_normal(clean.shape)).astype(dtype)
+    fg = (inst > 0).astype(dtype)
+    assert np.abs(emb.astype(np.float64)).max() < 1.5
+    res = oracle.decode(emb, fg, fx, fy, bins, bins, 8, 0.5, 0.0)
+    h_real, ex, ey = refmath.real_histogram(emb, fg, fx, fy, bins, bins)
+    h_can = res["hist"].astype(np.float64) * 2.0 ** -30
+    bound = refmath.quant_bound(ex, ey, 2 * F)
+    assert np.all(np.abs(h_can - h_real) <= bound)
+    # the bound is tight enough to catch a transposed histogram
+    assert not np.all(np.abs(h_can.T - h_real.T[::-1]) <= bound)
+
+
+def test_histogram_catches_axis_swap():
+    """A decoder that swapped the x and y blocks would miss the bound."""
+    rng = np.random.default_rng(5)
+    H, W, F = 20, 20, 4
+    fx, fy = paper_freqs(H, W, F)
+    inst = rng.integers(0, 3, size=(H, W))
+    cx, cy = np.array([0, 3.0, 15.0]), np.array([0, 17.0, 4.0])
+    emb = synth.encode_positions(cx[inst], cy[inst], fx, fy).astype(np.float32)
+    fg = (inst > 0).astype(np.float32)
+    res = oracle.decode(emb, fg, fx, fy, 10, 10, 8, 0.5, 0.0)
+    swapped = np.concatenate([emb[..., 2 * F:], emb[..., :2 * F]], -1)
+    h_real, ex, ey = refmath.real_histogram(swapped, fg, fx, fy, 10, 10)
+    bound = refmath.quant_bound(ex, ey, 2 * F)
+    assert not np.all(np.abs(res["hist"] * 2.0 ** -30 - h_real) <= bound)
+
+
+# --------------------------------------------------------------------------
+# S3: local maxima against a library filter
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_peaks_match_library_local_max(cfg):
+    f = synth.make_frame(cfg)
+    res = oracle.decode_frame(f, peak_threshold=0.3, capacity=1024)
+    cut = math.floor(0.3 * 2 ** 30)
+    m = refmath.strict_local_maxima(res["hist"].astype(np.int64), cut)
+    bb, aa = np.nonzero(m)                      # row-major = ascending b*Bw + a
+    assert res["K"] == len(aa)
+    assert np.array_equal(res["centroids"]["bin_x"], aa)
+    assert np.array_equal(res["centroids"]["bin_y"], bb)
+    assert np.all(res["centroids"]["score"] > 0.3)
+
+
+def test_plateau_gives_no_peak_and_single_bin_is_a_peak():
+    H = W = 6
+    F = 2
+    fx, fy = paper_freqs(H, W, F)
+    emb = np.zeros((H, W, 4 * F), np.float32)
+    fg = np.zeros((H, W), np.float32)          # empty S: H == 0 everywhere
+    r = oracle.decode(emb, fg, fx, fy, 5, 5, 4, 0.5, -1.0)
+    assert r["K"] == 0 and not r["labels"].any()
+    r1 = oracle.decode(emb, fg, fx, fy, 1, 1, 4, 0.5, -1.0)
+    assert r1["K"] == 1 and not r1["labels"].any()
+
+
+# --------------------------------------------------------------------------
+# whole decoder: pure-Python exhaustive search on tiny frames
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("seed,dtype,F,bw,bh,cap", [(0, np.float32, 2, 5, 4, 6), (1, np.float16, 3, 6, 6, 2),
+                                                    (2, np.float32, 1, 3, 7, 8), (3, np.float16, 4, 8, 5, 1)])
+def test_oracle_equals_exhaustive_search(seed, dtype, F, bw, bh, cap):
+    rng = np.random.default_rng(seed)
+    H, W = 7, 9
+    fx, fy = paper_freqs(H, W, F)
+    inst = rng.integers(0, 4, size=(H, W))
+    cx, cy = rng.uniform(0, W, 4), rng.uniform(0, H, 4)
+    emb = (synth.encode_positions(cx[inst], cy[inst], fx, fy) + 0.2 * rng.standard_normal((H, W, 4 * F))).astype(dtype)
+    fg = ((inst > 0) + 0.05 * rng.standard_normal((H, W))).astype(dtype)
+    theta = 0.05 * (inst > 0).sum()
+    hist, peaks, K, labels = refmath.brute_decode(emb, fg, fx, fy, bw, bh, cap, 0.5, theta)
+    res = oracle.decode(emb, fg, fx, fy, bw, bh, cap, 0.5, theta)
+    assert np.array_equal(res["hist"], np.array(hist, dtype=np.uint64))
+    assert res["K"] == K
+    got = list(zip(res["centroids"]["bin_x"].tolist(), res["centroids"]["bin_y"].tolist()))
+    assert got == peaks[:cap]
+    assert np.array_equal(res["labels"], np.array(labels, dtype=np.int32))
+
+
+# --------------------------------------------------------------------------
+# noise-free special case: exact recovery of the generating centroids
+# --------------------------------------------------------------------------
+def _snapped_frame(H, W, bins, cells, half, F=4):
+    """Square instances centred on chosen bin centres; the embedding is the
+    encoding of that exact bin centre, so every instance pixel has distance 0
+    to its own bin."""
+    fx, fy = paper_freqs(H, W, F)
+    xa = refmath.bin_centres(bins, W)
+    yb = refmath.bin_centres(bins, H)
+    inst = np.zeros((H, W), np.int32)
+    for k, (a, b) in enumerate(cells, start=1):
+        x0, y0 = int(xa[a]), int(yb[b])
+        inst[max(0, y0 - half):y0 + half, max(0, x0 - half):x0 + half] = k
+    cx = np.concatenate([[0.0], [xa[a] for a, _ in cells]])
+    cy = np.concatenate([[0.0], [yb[b] for _, b in cells]])
+    emb = synth.encode_positions(cx[inst], cy[inst], fx, fy)
+    emb[inst == 0] = 0.0
+    return emb.astype(np.float32), (inst > 0).astype(np.float32), inst, fx, fy
+
+
+@pytest.mark.parametrize("order", [0, 1])
+def test_noise_free_decodes_generating_centroids_and_labels(order):
+    H = W = 96
+    bins = 16
+    # two instances share a column and two share a row, so an assignment that
+    # ignored one axis would tie and mislabel them
+    cells = [(3, 3), (11, 4), (3, 12), (12, 12), (8, 8)]
+    if order:
+        cells = cells[::-1]                     # instance order must not matter
+    emb, fg, inst, fx, fy = _snapped_frame(H, W, bins, cells, half=5)
+    sizes = np.bincount(inst.ravel())[1:]
+    theta = 0.5 * sizes.min()
+    res = oracle.decode(emb, fg, fx, fy, bins, bins, 64, 0.5, theta)
+    got = sorted(zip(res["centroids"]["bin_x"].tolist(), res["centroids"]["bin_y"].tolist()),
+                 key=lambda ab: ab[1] * bins + ab[0])
+    want = sorted(cells, key=lambda ab: ab[1] * bins + ab[0])
+    assert res["K"] == len(cells) and got == want
+    # labels equal the generating map up to the bin-order renumbering
+    rank = {ab: i + 1 for i, ab in enumerate(want)}
+    expect = np.zeros_like(inst)
+    for k, ab in enumerate(cells, start=1):
+        expect[inst == k] = rank[ab]
+    assert np.array_equal(res["labels"], expect)
+    assert np.array_equal(res["centroids"]["npix"], np.bincount(expect.ravel(), minlength=len(cells) + 1)[1:])
+    # zero distance means weight 2^15 on both axes: score >= |Omega_k|
+    for c in res["centroids"]:
+        k = [kk for kk, ab in enumerate(cells, start=1) if ab == (c["bin_x"], c["bin_y"])][0]
+        assert c["score"] >= sizes[k - 1]
+
+
+# --------------------------------------------------------------------------
+# invariants on the workloads
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_invariants(cfg):
+    f = synth.make_frame(cfg)
+    theta = 0.5
+    res = oracle.decode_frame(f, peak_threshold=theta)
+    lab = res["labels"]
+    cents = res["centroids"]
+    K = res["K"]
+    bins = f.spec.bins
+    S = f.fg.astype(np.float32) > np.float32(f.spec.fg_threshold)
+    assert 1 <= K <= ((bins + 1) // 2) ** 2
+    assert np.array_equal(lab > 0, S)                       # partition of the foreground
+    assert lab.max() <= len(cents)
+    assert cents["npix"].sum() == S.sum()
+    assert np.array_equal(cents["npix"], np.bincount(lab.ravel(), minlength=len(cents) + 1)[1:])
+    idx = cents["bin_y"] * bins + cents["bin_x"]
+    assert np.all(np.diff(idx) > 0)
+    a, b = cents["bin_x"], cents["bin_y"]
+    cheb = np.maximum(np.abs(a[:, None] - a[None]), np.abs(b[:, None] - b[None]))
+    np.fill_diagonal(cheb, 99)
+    assert cheb.min() >= 2
+    assert np.all(cents["score"] > theta)
+    xa = refmath.bin_centres(bins, f.spec.W).astype(np.float32)
+    assert np.array_equal(cents["x"], xa[a])
+
+
+def test_pixel_permutation_invariance():
+    """H is a sum over S and each label depends only on its own pixel, so
+    permuting the pixels of a frame permutes the labels and nothing else."""
+    f = synth.make_frame(0)
+    rng = np.random.default_rng(3)
+    H, W, D = f.emb.shape
+    perm = rng.permutation(H * W)
+    emb2 = f.emb.reshape(-1, D)[perm].reshape(H, W, D)
+    fg2 = f.fg.reshape(-1)[perm].reshape(H, W)
+    fx, fy = f.spec.freqs()
+    r1 = oracle.decode(f.emb, f.fg, fx, fy, 32, 32, None, 0.5, 0.5)
+    r2 = oracle.decode(emb2, fg2, fx, fy, 32, 32, None, 0.5, 0.5)
+    assert np.array_equal(r1["hist"], r2["hist"])
+    assert np.array_equal(r1["centroids"], r2["centroids"])
+    assert np.array_equal(r1["labels"].reshape(-1)[perm], r2["labels"].reshape(-1))
+
+
+def test_capacity_overflow_and_empty():
+    f = synth.make_frame(0)
+    full = oracle.decode_frame(f, peak_threshold=0.5)
+    small = oracle.decode_frame(f, peak_threshold=0.5, capacity=3)
+    assert small["K"] == full["K"] and len(small["centroids"]) == 3
+    assert np.array_equal(small["centroids"][["bin_x", "bin_y", "score"]], full["centroids"][:3][["bin_x", "bin_y", "score"]])
+    assert small["labels"].max() == 3
+    none = oracle.decode_frame(f, peak_threshold=1e9)
+    assert none["K"] == 0 and not none["labels"].any() and not none["score_map"].any()
+
+
+def test_score_map_is_exp_of_distance():
+    f = synth.make_frame(0)
+    res = oracle.decode_frame(f, peak_threshold=0.5)
+    lab = res["labels"]
+    sm = res["score_map"]
+    assert np.all(sm[lab == 0] == 0)
+    assert np.all((sm[lab > 0] > 0) & (sm[lab > 0] <= 1))
+
+
+def test_real_mode_close_to_canonical():
+    """Diagnostic: the canonical arithmetic changes very few decisions."""
+    f = synth.make_frame(1)
+    fx, fy = f.spec.freqs()
+    can = oracle.decode_frame(f, peak_threshold=2.0)
+    real = oracle.decode_real(f.emb, f.fg, fx, fy, 32, 32, None, 0.5, 2.0)
+    assert real["K"] == can["K"]
+    assert (real["labels"] == can["labels"]).mean() > 0.999
+
+
+def test_argument_errors():
+    emb = np.zeros((4, 4, 16), np.float32)
+    fg = np.zeros((4, 4), np.float32)
+    fx, fy = paper_freqs(4, 4, 4)
+    for kw in [dict(bins_w=0), dict(bins_h=129), dict(capacity=0), dict(fg_threshold=float("nan")),
+               dict(peak_threshold=float("nan"))]:
+        args = dict(bins_w=4, bins_h=4, capacity=4, fg_threshold=0.5, peak_threshold=0.0)
+        args.update(kw)
+        assert oracle.decode(emb, fg, fx, fy, check=False, **args)["rc"] == 1
+    assert oracle.decode(emb[..., :12], fg, fx, fy, 4, 4, 4, 0.5, 0.0, check=False)["rc"] == 1
+
+
+def test_clamp_saturates():
+    """Input reading: values beyond +-1.5 saturate at +-1.5, +-inf likewise,
+    NaN reads as 0 -- so such frames decode exactly like their clipped copies."""
+    rng = np.random.default_rng(9)
+    H, W, F = 6, 7, 2
+    fx, fy = paper_freqs(H, W, F)
+    base = rng.uniform(-1.0, 1.0, (H, W, 4 * F)).astype(np.float32)
+    fg = np.ones((H, W), np.float32)
+    wild = base.copy()
+    wild[0, 0, 0], wild[1, 2, 3], wild[2, 2, 5] = 7.5, -np.inf, np.nan
+    wild[3, 3, 1] = 1e30
+    clipped = base.copy()
+    clipped[0, 0, 0], clipped[1, 2, 3], clipped[2, 2, 5], clipped[3, 3, 1] = 1.5, -1.5, 0.0, 1.5
+    r1 = oracle.decode(wild, fg, fx, fy, 4, 4, 16, 0.5, 0.0)
+    r2 = oracle.decode(clipped, fg, fx, fy, 4, 4, 16, 0.5, 0.0)
+    assert np.array_equal(r1["hist"], r2["hist"]) and np.array_equal(r1["labels"], r2["labels"])
+    unclipped = base.copy()
+    unclipped[0, 0, 0] = 1.4                    # inside the range: no saturation
+    r3 = oracle.decode(unclipped, fg, fx, fy, 4, 4, 16, 0.5, 0.0)
+    assert not np.array_equal(r3["hist"], r2["hist"])
+
+
+def test_threshold_is_strict():
+    """'exceeds a predefined threshold': a peak whose vote mass equals the
+    threshold is dropped, one unit below it is kept."""
+    f = synth.make_frame(0)
+    base = oracle.decode_frame(f, peak_threshold=0.0, capacity=1024)
+    top = base["centroids"][np.argmax(base["centroids"]["score"])]
+    s = float(top["score"])                     # exactly H * 2^-30
+    at = oracle.decode_frame(f, peak_threshold=s, capacity=1024)
+    below = oracle.decode_frame(f, peak_threshold=s - 2.0 ** -30, capacity=1024)
+    assert at["K"] == 0 and below["K"] == 1
+    assert below["centroids"][0]["bin_x"] == top["bin_x"] and below["centroids"][0]["bin_y"] == top["bin_y"]
+
+
+def test_exact_tie_goes_to_lowest_index():
+    """With one harmonic of period W/2 the first and last of three x bins get
+    bit-identical palettes, so both are peaks with identical votes and every
+    pixel is at exactly the same distance from both: the lower index wins."""
+    H = W = 16
+    fx = np.array([4.0 * math.pi / W])
+    fy = np.array([4.0 * math.pi / H])
+    emb = np.zeros((H, W, 4), np.float32)
+    emb[..., 0], emb[..., 1] = 0.0, -1.0         # gamma(x = 4) = gamma(x = 12)
+    emb[..., 2], emb[..., 3] = 0.0, 1.0
+    fg = np.ones((H, W), np.float32)
+    res = oracle.decode(emb, fg, fx, fy, 3, 1, 4, 0.5, 1.0)
+    assert res["pal_x"][0].tolist() == res["pal_x"][2].tolist()
+    assert res["K"] == 2
+    assert res["centroids"]["bin_x"].tolist() == [0, 2]
+    assert np.all(res["labels"] == 1)
+    assert res["centroids"]["npix"].tolist() == [H * W, 0]
