@@ -1,0 +1,154 @@
+/*
+ * cpe_decode.h -- C ABI of the MI355X (gfx950) decoder for sinusoidal
+ * centroid positional encodings (instance segmentation).
+ *
+ * A frame is an H x W map of per-pixel embeddings T^ = concat(x^, y^)
+ * (Section 3.1, Eq3) plus a foreground channel.  The decoder
+ *   1. compares every foreground pixel's x^ and y^ with the encodings of the
+ *      bin centres along each axis (palettes, Eq9; distances Eq4/Eq10),
+ *   2. accumulates the soft votes e^-d into a B_w x B_h histogram (Eq5, Eq6,
+ *      Eq11),
+ *   3. extracts the bins that are strict 8-neighbour local maxima above a
+ *      threshold and compacts them into a centroid list (local-maxima search
+ *      paragraph of Section 3.2),
+ *   4. assigns every foreground pixel to its nearest centroid in the encoded
+ *      space (Eq7) and counts the pixels of each (mask-aggregation paragraph),
+ *   5. writes an int32 label map (0 = background, k+1 = centroid k).
+ *
+ * Arithmetic.  All discrete decisions use a fixed-point arithmetic that any
+ * correct implementation reproduces bit for bit: inputs and palettes scaled
+ * by 4096 and rounded, exact integer squared distances, the IEEE fp32 square
+ * root, a 2841-entry table of 2^15 e^{-i/256} indexed by rint(256 d), exact
+ * 64-bit vote sums, lowest-index tie-breaking.  Vote masses are reported as
+ * H * 2^-30 (so a pixel at distance 0 on both axes adds 1.0).
+ *
+ * Layouts (all row-major, channels last):
+ *   emb    [H][W][D], D = 4F: channels [0,2F) encode x, [2F,4F) encode y;
+ *          within a block channel 2k = sin(w_k p), 2k+1 = cos(w_k p)
+ *   fg     [H][W], same dtype as emb; a pixel participates iff fg > threshold
+ *   labels [H][W] int32
+ *   score  [H][W] float (optional): e^{-d} of the assigned centroid, 0 on
+ *          unlabelled pixels
+ *
+ * Ownership.  The caller owns every buffer passed to cpe_decode (device
+ * memory).  The handle owns the palettes, the table and all scratch; they
+ * are allocated once in cpe_decode_create and freed by cpe_decode_destroy.
+ * cpe_decode itself never allocates, never synchronises and never copies
+ * to the host: it only enqueues work on `stream`.
+ *
+ * Errors.  Argument errors are detected on the host before any work is
+ * enqueued and return CPE_ERR_INVALID_ARG; a failed launch returns
+ * CPE_ERR_HIP.  Data-dependent outcomes (no centroid, more centroids than
+ * the capacity) are reported through the device outputs, never as errors.
+ *
+ * Threading.  A handle may be used by one stream at a time (its scratch is
+ * per handle); separate handles are independent.
+ */
+#ifndef CPE_DECODE_H
+#define CPE_DECODE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CPE_OK = 0,
+    CPE_ERR_INVALID_ARG = 1,
+    CPE_ERR_UNSUPPORTED = 2,
+    CPE_ERR_OUT_OF_MEMORY = 3,
+    CPE_ERR_HIP = 4
+} cpe_status;
+
+typedef enum { CPE_F32 = 0, CPE_F16 = 1 } cpe_dtype;
+
+/* One decoded centroid (32 bytes). */
+typedef struct {
+    int32_t bin_x, bin_y; /* histogram bin (a_k, b_k)                               */
+    float x, y;           /* bin centre in pixels: (a+1) W/(B_w+1), (b+1) H/(B_h+1)  */
+    double score;         /* vote mass H(a_k, b_k) * 2^-30                           */
+    int32_t npix;         /* number of pixels labelled k+1                           */
+    int32_t reserved;     /* 0                                                       */
+} cpe_centroid;
+
+typedef struct cpe_decoder cpe_decoder;
+
+/*
+ * Build a decoder for frames of H x W pixels with D = 4*n_freq channels.
+ * Section 3.2 (Eq9): the palettes P_w, P_h are the encodings of the bin
+ * centres and are computed here once, on the host in fp64, then kept on the
+ * device with the weight table ("preloaded ... without recomputing").
+ *   out          receives the handle (set to NULL on failure)
+ *   H, W         frame size, H*W <= 2^31-1
+ *   D            channels per pixel, must equal 4*n_freq
+ *   dtype        element type of emb and fg
+ *   freq_x/y     host arrays of n_freq angular frequencies in rad/pixel
+ *                (harmonic k of the x and y encodings), copied
+ *   n_freq       1..16
+ *   bins_w/h     1..128 histogram bins along x / y
+ *   centroid_capacity  >= 1 and <= bins_w*bins_h; the number of centroid
+ *                records cpe_decode may write.  ceil(B_w/2)*ceil(B_h/2) can
+ *                never overflow (strict local maxima are pairwise
+ *                non-adjacent).
+ * Uses the current HIP device; the handle must be used on that device.
+ * Returns CPE_ERR_INVALID_ARG, CPE_ERR_OUT_OF_MEMORY or CPE_ERR_HIP on failure.
+ */
+cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D, cpe_dtype dtype,
+                             const double *freq_x, const double *freq_y, int32_t n_freq,
+                             int32_t bins_w, int32_t bins_h, int32_t centroid_capacity);
+
+/*
+ * Decode one frame (Sections 3.1-3.2: Eq4-Eq7, local-maxima search, mask
+ * aggregation), asynchronously on `stream`.
+ *   emb, fg        device inputs, layouts above; emb 16-byte aligned, fg
+ *                  aligned to its element size
+ *   H, W           must equal the values given to cpe_decode_create
+ *   fg_threshold   pixel p votes and is labelled iff (float)fg[p] > fg_threshold
+ *   peak_threshold a bin can be a centroid only if its vote mass exceeds this
+ *                  (compared as H > floor(peak_threshold * 2^30))
+ *   centroids      device [centroid_capacity]: records 0..min(K,cap)-1 are
+ *                  written, in ascending bin order b*B_w + a
+ *   num_centroids  device int32: the true number K of local maxima (may
+ *                  exceed the capacity; then only the first cap are used)
+ *   labels         device [H][W] int32, 16-byte aligned
+ *   score_map      device [H][W] float or NULL
+ * Non-finite thresholds are rejected.
+ */
+cpe_status cpe_decode(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg,
+                      int32_t H, int32_t W, float fg_threshold, double peak_threshold,
+                      cpe_centroid *centroids, int32_t *num_centroids, int32_t *labels,
+                      float *score_map);
+
+/* Release a decoder (waits for nothing; the caller must have synchronised
+ * the streams that used it).  NULL is a no-op. */
+cpe_status cpe_decode_destroy(cpe_decoder *h);
+
+/* Static string describing a status code. */
+const char *cpe_status_string(cpe_status s);
+
+/*
+ * Inspection (tests and profiling).  Host copies of the constants built by
+ * cpe_decode_create: pal_x [bins_w][2F] and pal_y [bins_h][2F] int16 (Eq9
+ * palettes x4096, rounded), lut [2841] uint16.  Any pointer may be NULL.
+ */
+cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *lut);
+
+/*
+ * Enqueue on `stream` a device-to-device copy of the vote histogram of the
+ * most recent cpe_decode on this handle (Eq6/Eq11 in fixed point): [bins_h]
+ * [bins_w] uint64, entry [b][a] = sum over foreground pixels of
+ * q_x(a) q_y(b).
+ */
+cpe_status cpe_decode_get_histogram(cpe_decoder *h, hipStream_t stream, uint64_t *hist);
+
+/* Bytes of device memory the handle holds (constants + scratch). */
+size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CPE_DECODE_H */

@@ -1,0 +1,168 @@
+"""ctypes binding of ``libcpe_decode.so`` (the gfx950 decoder's C ABI).
+
+Argument marshalling only: every step of the decode runs in the HIP kernels
+behind the C ABI.  Device buffers are torch tensors on the GPU; their raw
+pointers and torch's current HIP stream are passed through unchanged.  If
+the library has not been built this module raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcpe_decode.so")
+
+CPE_OK, CPE_ERR_INVALID_ARG, CPE_ERR_UNSUPPORTED, CPE_ERR_OUT_OF_MEMORY, CPE_ERR_HIP = range(5)
+CPE_F32, CPE_F16 = 0, 1
+LUT_LEN = 2841
+
+CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y", "<f4"),
+                           ("score", "<f8"), ("npix", "<i4"), ("reserved", "<i4")])
+
+# Every entry point declared in include/cpe_decode.h.
+EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_destroy", "cpe_status_string",
+           "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes")
+
+_lib = None
+
+
+class CpeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+def library():
+    """Load the built library (raises if it is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, i32 = ctypes.c_void_p, ctypes.c_int32
+        lib.cpe_decode_create.restype = i32
+        lib.cpe_decode_create.argtypes = [ctypes.POINTER(P), i32, i32, i32, i32, P, P, i32, i32, i32, i32]
+        lib.cpe_decode.restype = i32
+        lib.cpe_decode.argtypes = [P, P, P, P, i32, i32, ctypes.c_float, ctypes.c_double, P, P, P, P]
+        lib.cpe_decode_destroy.restype = i32
+        lib.cpe_decode_destroy.argtypes = [P]
+        lib.cpe_status_string.restype = ctypes.c_char_p
+        lib.cpe_status_string.argtypes = [i32]
+        lib.cpe_decode_get_tables.restype = i32
+        lib.cpe_decode_get_tables.argtypes = [P, P, P, P]
+        lib.cpe_decode_get_histogram.restype = i32
+        lib.cpe_decode_get_histogram.argtypes = [P, P, P]
+        lib.cpe_decode_workspace_bytes.restype = ctypes.c_size_t
+        lib.cpe_decode_workspace_bytes.argtypes = [P]
+        _lib = lib
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return library().cpe_status_string(int(status)).decode()
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream_ptr(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(int(s.cuda_stream))
+
+
+class Decoder:
+    """Handle of one decoder (fixed frame size, dtype, frequencies, bins)."""
+
+    def __init__(self, H: int, W: int, n_freq: int, dtype: str, freq_x, freq_y,
+                 bins_w: int = 32, bins_h: int = 32, capacity: Optional[int] = None, D: Optional[int] = None):
+        lib = library()
+        self.H, self.W, self.F = int(H), int(W), int(n_freq)
+        self.D = 4 * self.F if D is None else int(D)
+        self.dtype = dtype
+        self.bins_w, self.bins_h = int(bins_w), int(bins_h)
+        self.capacity = int(capacity if capacity is not None else ((bins_w + 1) // 2) * ((bins_h + 1) // 2))
+        fx = np.ascontiguousarray(freq_x, dtype=np.float64)
+        fy = np.ascontiguousarray(freq_y, dtype=np.float64)
+        code = {"f32": CPE_F32, "f16": CPE_F16}[dtype]
+        h = ctypes.c_void_p()
+        st = lib.cpe_decode_create(ctypes.byref(h), self.H, self.W, self.D, code, fx.ctypes.data, fy.ctypes.data,
+                                   len(fx), self.bins_w, self.bins_h, self.capacity)
+        if st != CPE_OK:
+            raise CpeError(st, "cpe_decode_create")
+        self._h = h
+
+    # -- the C ABI, one call each ------------------------------------------------
+    def decode(self, emb, fg, fg_threshold: float, peak_threshold: float, centroids, num_centroids, labels,
+               score_map=None, stream=None, H: Optional[int] = None, W: Optional[int] = None) -> int:
+        """Enqueue one frame.  ``centroids`` is a device uint8 tensor of
+        capacity*32 bytes, ``num_centroids`` a device int32 tensor, ``labels``
+        device int32 [H][W], ``score_map`` device float32 [H][W] or None."""
+        st = library().cpe_decode(self._h, _stream_ptr(stream), _ptr(emb), _ptr(fg),
+                                  self.H if H is None else H, self.W if W is None else W,
+                                  float(fg_threshold), float(peak_threshold), _ptr(centroids), _ptr(num_centroids),
+                                  _ptr(labels), _ptr(score_map))
+        return st
+
+    def histogram(self, out, stream=None) -> int:
+        return library().cpe_decode_get_histogram(self._h, _stream_ptr(stream), _ptr(out))
+
+    def tables(self):
+        pal_x = np.empty((self.bins_w, 2 * self.F), np.int16)
+        pal_y = np.empty((self.bins_h, 2 * self.F), np.int16)
+        lut = np.empty(LUT_LEN, np.uint16)
+        st = library().cpe_decode_get_tables(self._h, pal_x.ctypes.data, pal_y.ctypes.data, lut.ctypes.data)
+        if st != CPE_OK:
+            raise CpeError(st, "cpe_decode_get_tables")
+        return pal_x, pal_y, lut
+
+    def workspace_bytes(self) -> int:
+        return int(library().cpe_decode_workspace_bytes(self._h))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            library().cpe_decode_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- convenience (allocation happens here, outside the C ABI) ----------------
+    def new_outputs(self, device="cuda", score=False):
+        import torch
+        out = {
+            "centroids": torch.zeros(self.capacity * 32, dtype=torch.uint8, device=device),
+            "num_centroids": torch.zeros(1, dtype=torch.int32, device=device),
+            "labels": torch.empty((self.H, self.W), dtype=torch.int32, device=device),
+            "score_map": torch.empty((self.H, self.W), dtype=torch.float32, device=device) if score else None,
+        }
+        return out
+
+    def run(self, emb, fg, fg_threshold, peak_threshold, score=True, stream=None, outputs=None):
+        """Decode one frame, synchronise, and return host numpy results."""
+        import torch
+        out = outputs or self.new_outputs(emb.device, score)
+        st = self.decode(emb, fg, fg_threshold, peak_threshold, out["centroids"], out["num_centroids"],
+                         out["labels"], out["score_map"], stream)
+        if st != CPE_OK:
+            raise CpeError(st, "cpe_decode")
+        torch.cuda.synchronize()
+        K = int(out["num_centroids"].item())
+        cents = out["centroids"].cpu().numpy().view(CENTROID_DTYPE)[:min(K, self.capacity)].copy()
+        res = {"K": K, "centroids": cents, "labels": out["labels"].cpu().numpy()}
+        if out["score_map"] is not None:
+            res["score_map"] = out["score_map"].cpu().numpy()
+        return res
+
+
+def torch_dtype(dtype: str):
+    import torch
+    return {"f32": torch.float32, "f16": torch.float16}[dtype]

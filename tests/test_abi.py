@@ -1,0 +1,60 @@
+"""The C-ABI library: it loads, exports every entry point include/*.h
+declares, and rejects bad arguments on the host (no GPU work is issued)."""
+import ctypes
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_16874_amd import native
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(cpe_\w+)\s*\(", text))
+    return names
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == set(native.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = native.library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_null_handles():
+    lib = native.library()
+    assert native.status_string(0) == "ok"
+    assert "invalid" in native.status_string(1)
+    assert lib.cpe_decode_destroy(None) == 0
+    assert lib.cpe_decode(None, None, None, None, 4, 4, 0.5, 0.0, None, None, None, None) == native.CPE_ERR_INVALID_ARG
+    assert lib.cpe_decode_get_tables(None, None, None, None) == native.CPE_ERR_INVALID_ARG
+    assert lib.cpe_decode_get_histogram(None, None, None) == native.CPE_ERR_INVALID_ARG
+    assert lib.cpe_decode_workspace_bytes(None) == 0
+
+
+@pytest.mark.parametrize("kw", [dict(H=0), dict(W=-1), dict(D=17), dict(n_freq=0), dict(n_freq=17, D=68),
+                                dict(dtype=7), dict(bins_w=0), dict(bins_h=129), dict(cap=0), dict(cap=10 ** 6),
+                                dict(H=65536, W=65536), dict(freq_nan=True)])
+def test_create_rejects_bad_arguments(kw):
+    lib = native.library()
+    a = dict(H=16, W=16, D=16, dtype=0, n_freq=4, bins_w=8, bins_h=8, cap=16)
+    a.update({k: v for k, v in kw.items() if k != "freq_nan"})
+    fx = np.ones(max(a["n_freq"], 1))
+    if kw.get("freq_nan"):
+        fx[0] = np.nan
+    h = ctypes.c_void_p(123)
+    st = lib.cpe_decode_create(ctypes.byref(h), a["H"], a["W"], a["D"], a["dtype"], fx.ctypes.data, fx.ctypes.data,
+                               a["n_freq"], a["bins_w"], a["bins_h"], a["cap"])
+    assert st == native.CPE_ERR_INVALID_ARG
+    assert h.value is None
