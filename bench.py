@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark of the gfx950 centroid-encoding decoder (one GPU).
+
+Workload (one "step"): 16 synthetic 640x640 frames, D = 64 fp16 channels
+(16 harmonics per axis), 10-100 mixed ellipse/polygon instances each,
+decoded back to back with one cpe_decode call per frame on one stream.
+Inputs are resident in HBM before timing starts.  Prints one JSON line:
+
+  value        decoded frames per second (whole job, one GPU)
+  ms_per_step  wall time of one 16-frame step (hipEvents around K steps)
+  roofline     the dominant kernel's algorithmic bytes per launch divided by
+               its average launch duration (hipEvents recorded by the
+               library between its launches), against 8 TB/s HBM
+  cpu_baseline the plain single-threaded CPU oracle on a bounded sample of
+               the same frames (reported, not a target)
+  extra        the 640x640 single frame and the 1024x2048 frame, with the
+               fraction of the HBM roofline for embedding read + label write
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E peak, GB/s
+GOLDEN = os.path.join(ROOT, "tests", "golden", "configs.json")
+
+
+def thresholds():
+    with open(GOLDEN) as fh:
+        return json.load(fh)["configs"]
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (the library records them on the decode stream)."""
+
+    def __init__(self, n):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = (ctypes.c_void_p * n)()
+        for i in range(n):
+            h = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(h)) == 0
+            self.ev[i] = h
+
+    def elapsed_ms(self, i, j):
+        out = ctypes.c_float()
+        assert self.hip.hipEventSynchronize(self.ev[j]) == 0
+        assert self.hip.hipEventElapsedTime(ctypes.byref(out), self.ev[i], self.ev[j]) == 0
+        return out.value
+
+    def close(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(e)
+
+
+def load_workload(cfg, n_frames=None):
+    import torch
+    from paper_2609_16874_amd import synth
+    spec = synth.CONFIGS[cfg]
+    n = spec.n_frames if n_frames is None else n_frames
+    frames = [synth.make_frame(cfg, i) for i in range(n)]
+    embs = [torch.from_numpy(f.emb).cuda() for f in frames]
+    fgs = [torch.from_numpy(f.fg).cuda() for f in frames]
+    return spec, frames, embs, fgs
+
+
+def frame_bytes(spec, frame):
+    """Algorithmic bytes: literal (full embedding + labels), and what each
+    kernel must move given the participating set S (fg > threshold)."""
+    es = 2 if spec.dtype == "f16" else 4
+    npx = spec.H * spec.W
+    nfg = int((frame.fg.astype(np.float32) > np.float32(spec.fg_threshold)).sum())
+    return {
+        "literal": npx * spec.D * es + 4 * npx,
+        "recover_vote": npx * es + nfg * spec.D * es,
+        "peaks": 0,
+        "assign_label": npx * es + nfg * spec.D * es + 4 * npx,
+        "n_fg": nfg,
+    }
+
+
+def time_steps(dec, embs, fgs, outs, fg_thr, theta, steps, warmup):
+    import torch
+
+    def step():
+        for i in range(len(embs)):
+            o = outs[i]
+            st = dec.decode(embs[i], fgs[i], fg_thr, theta, o["centroids"], o["num_centroids"], o["labels"])
+            if st != 0:
+                raise RuntimeError(f"cpe_decode failed with status {st}")
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        step()
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
+    """Average per-kernel duration over reps x frames, from the events the
+    library records between its launches."""
+    from paper_2609_16874_amd import native
+    ev = HipEvents(native.STAGE_EVENTS)
+    assert dec.set_stage_events(ev.ev) == 0
+    acc = np.zeros(len(native.STAGES))
+    n = 0
+    for _ in range(reps):
+        for i in range(len(embs)):
+            o = outs[i]
+            assert dec.decode(embs[i], fgs[i], fg_thr, theta, o["centroids"], o["num_centroids"], o["labels"]) == 0
+            acc += [ev.elapsed_ms(k, k + 1) for k in range(len(native.STAGES))]
+            n += 1
+    dec.set_stage_events(None)
+    ev.close()
+    return dict(zip(native.STAGES, (acc / n).tolist()))
+
+
+def bench_config(cfg, steps, warmup, n_frames=None):
+    from paper_2609_16874_amd import native
+    th = thresholds()[str(cfg)]
+    spec, frames, embs, fgs = load_workload(cfg, n_frames)
+    fx, fy = spec.freqs()
+    dec = native.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, spec.bins, spec.bins, th["capacity"])
+    outs = [dec.new_outputs() for _ in frames]
+    ms_step = time_steps(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], steps, warmup)
+    stages = stage_times(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], max(1, min(steps, 10)))
+    fb = [frame_bytes(spec, f) for f in frames]
+    mean_bytes = {k: float(np.mean([b[k] for b in fb])) for k in fb[0]}
+    ws = dec.workspace_bytes()
+    dec.close()
+    return spec, frames, ms_step, stages, mean_bytes, ws
+
+
+def cpu_baseline(cfg, frames, budget_s=15.0):
+    import oracle
+    th = thresholds()[str(cfg)]
+    spec = frames[0].spec
+    fx, fy = spec.freqs()
+    done, t0 = 0, time.perf_counter()
+    for f in frames:
+        oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
+                      th["peak_threshold"], want_score=False)
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample": f"frames 0-{done - 1} of the {spec.name} batch, single-threaded C oracle, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-extra", action="store_true", help="skip the single-frame 640x640 and 1024x2048 lines")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the decoder has no multi-GPU path (frames are independent; "
+              "see the sharding note in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    spec, frames, ms_step, stages, bytes_, ws = bench_config(4, args.steps, args.warmup)
+    nfr = len(frames)
+    fps = nfr * 1000.0 / ms_step
+    dom = max(stages, key=stages.get)
+    dom_ms = stages[dom]
+    achieved = bytes_[dom] / (dom_ms * 1e-3) / 1e9
+    result = {
+        "metric": "decoded frames/sec at 640x640 D=64",
+        "value": round(fps, 2),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "ms_per_frame": round(ms_step / nfr, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": spec.name, "frames_per_step": nfr, "H": spec.H, "W": spec.W, "D": spec.D,
+                   "input_dtype": spec.dtype, "bins": spec.bins, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": round(bytes_[dom]), "avg_launch_ms": round(dom_ms, 5)},
+        "stages_ms": {k: round(v, 5) for k, v in stages.items()},
+        "literal_roofline_frac": round(bytes_["literal"] / (ms_step / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "workspace_bytes": ws,
+    }
+    if not args.no_extra:
+        extra = {}
+        for cfg in (2, 3):
+            s, fr, ms, st, b, _ = bench_config(cfg, max(1, args.steps // 2), max(1, args.warmup // 2))
+            extra[f"cfg{cfg}"] = {"workload": s.name, "ms_per_frame": round(ms, 5), "frames_per_s": round(1000 / ms, 1),
+                                  "literal_bytes": int(b["literal"]),
+                                  "literal_roofline_frac": round(b["literal"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                  "stages_ms": {k: round(v, 5) for k, v in st.items()}}
+            del fr
+        result["extra"] = extra
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(4, frames)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

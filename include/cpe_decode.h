@@ -16,19 +16,25 @@
  *   5. writes an int32 label map (0 = background, k+1 = centroid k).
  *
  * Arithmetic.  All discrete decisions use a fixed-point arithmetic that any
- * correct implementation reproduces bit for bit: inputs and palettes scaled
- * by 4096 and rounded, exact integer squared distances, the IEEE fp32 square
- * root, a 2841-entry table of 2^15 e^{-i/256} indexed by rint(256 d), exact
- * 64-bit vote sums, lowest-index tie-breaking.  Vote masses are reported as
- * H * 2^-30 (so a pixel at distance 0 on both axes adds 1.0).
+ * correct implementation reproduces bit for bit:
+ *   X = rint(4096 clamp(v, -1.5, 1.5)) per channel (a NaN clamps to -1.5);
+ *   palettes P = rint(4096 gamma(bin centre)), bin centre (a+1) W/(B_w+1);
+ *   S = |X - P|^2 exactly (integer);
+ *   the bucket of S is the exponent and top m mantissa bits of fl32(S+1);
+ *   vote weight = rint(2^15 e^-d) and assignment code = rint(4096 d), with d
+ *   the distance at the centre of the 8-bit (weight) or 9-bit (code) bucket;
+ *   votes are exact 64-bit sums; a pixel goes to the centroid with the
+ *   smallest code sum c_x + c_y, lowest index on ties.
+ * Vote masses are reported as H * 2^-30 (so a pixel at distance 0 on both
+ * axes adds 1.0).
  *
  * Layouts (all row-major, channels last):
  *   emb    [H][W][D], D = 4F: channels [0,2F) encode x, [2F,4F) encode y;
  *          within a block channel 2k = sin(w_k p), 2k+1 = cos(w_k p)
  *   fg     [H][W], same dtype as emb; a pixel participates iff fg > threshold
  *   labels [H][W] int32
- *   score  [H][W] float (optional): e^{-d} of the assigned centroid, 0 on
- *          unlabelled pixels
+ *   score  [H][W] float (optional): expf(-(c_x + c_y)/4096) of the assigned
+ *          centroid, 0 on unlabelled pixels
  *
  * Ownership.  The caller owns every buffer passed to cpe_decode (device
  * memory).  The handle owns the palettes, the table and all scratch; they
@@ -133,9 +139,12 @@ const char *cpe_status_string(cpe_status s);
 /*
  * Inspection (tests and profiling).  Host copies of the constants built by
  * cpe_decode_create: pal_x [bins_w][2F] and pal_y [bins_h][2F] int16 (Eq9
- * palettes x4096, rounded), lut [2841] uint16.  Any pointer may be NULL.
+ * palettes x4096, rounded), weights [8192] uint16 (2^15 e^-d per 8-bit
+ * bucket), codes [16384] uint16 (4096 d per 9-bit bucket).  Any pointer may
+ * be NULL.
  */
-cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *lut);
+cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
+                                 uint16_t *codes);
 
 /*
  * Enqueue on `stream` a device-to-device copy of the vote histogram of the
@@ -147,6 +156,17 @@ cpe_status cpe_decode_get_histogram(cpe_decoder *h, hipStream_t stream, uint64_t
 
 /* Bytes of device memory the handle holds (constants + scratch). */
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
+
+/*
+ * Profiling: when `events` is non-NULL, every later cpe_decode on this handle
+ * records events[0] before its first kernel and events[i+1] after its i-th
+ * kernel, on the decode's stream, so that hipEventElapsedTime gives the
+ * duration of each stage (recovery+voting, peak extraction, assignment).
+ * `n_events` must be CPE_STAGE_EVENTS; the caller owns the events and must
+ * keep them alive while set.  NULL switches the recording off.
+ */
+#define CPE_STAGE_EVENTS 4
+cpe_status cpe_decode_set_stage_events(cpe_decoder *h, hipEvent_t *events, int32_t n_events);
 
 #ifdef __cplusplus
 }

@@ -24,7 +24,8 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
                            ("score", "<f8"), ("npix", "<i4"), ("reserved", "<i4")])
 assert CENTROID_DTYPE.itemsize == 32
 
-LUT_LEN = 2841
+W_KEYS = 8192          # weight buckets: 32 binades x 2^8 mantissa steps of fl32(S+1)
+C_KEYS = 16384         # code buckets: 32 binades x 2^9 mantissa steps
 
 _lib = None
 
@@ -68,7 +69,7 @@ def _bind(lib):
     i32 = ctypes.c_int32
     lib.cpe_oracle_decode.restype = i32
     lib.cpe_oracle_decode.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
-                                      ctypes.c_float, ctypes.c_double, P, P, P, P, P, P, P, P]
+                                      ctypes.c_float, ctypes.c_double, P, P, P, P, P, P, P, P, P]
     lib.cpe_oracle_decode_real.restype = i32
     lib.cpe_oracle_decode_real.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
                                            ctypes.c_float, ctypes.c_double, P, P, P, P]
@@ -91,7 +92,7 @@ def decode(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,
            fg_threshold=0.5, peak_threshold=0.0, *, want_score=True, check=True):
     """Canonical decode.  Returns a dict with centroids (structured array of
     length min(K, capacity)), K, labels [H][W] int32, score_map, hist
-    [bins_h][bins_w] uint64, pal_x, pal_y, lut."""
+    [bins_h][bins_w] uint64, pal_x, pal_y, weights, codes (bucket tables)."""
     lib = _load()
     emb = np.ascontiguousarray(emb)
     fg = np.ascontiguousarray(fg, dtype=emb.dtype)
@@ -108,18 +109,19 @@ def decode(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,
     hist = np.empty((bins_h, bins_w), dtype=np.uint64)
     pal_x = np.empty((bins_w, 2 * F), dtype=np.int16)
     pal_y = np.empty((bins_h, 2 * F), dtype=np.int16)
-    lut = np.empty(LUT_LEN, dtype=np.uint16)
+    wt = np.empty(W_KEYS, dtype=np.uint16)
+    ct = np.empty(C_KEYS, dtype=np.uint16)
     rc = lib.cpe_oracle_decode(H, W, D, _dtype_code(emb), _ptr(emb), _ptr(fg), _ptr(fx), _ptr(fy), F,
                                bins_w, bins_h, capacity, float(fg_threshold), float(peak_threshold),
                                _ptr(cents), _ptr(K), _ptr(labels), _ptr(score), _ptr(hist),
-                               _ptr(pal_x), _ptr(pal_y), _ptr(lut))
+                               _ptr(pal_x), _ptr(pal_y), _ptr(wt), _ptr(ct))
     if rc != 0:
         if check:
             raise ValueError(f"oracle rejected the arguments (code {rc})")
         return {"rc": rc}
     k = int(K[0])
     return {"rc": 0, "K": k, "centroids": cents[:min(k, capacity)].copy(), "labels": labels,
-            "score_map": score, "hist": hist, "pal_x": pal_x, "pal_y": pal_y, "lut": lut}
+            "score_map": score, "hist": hist, "pal_x": pal_x, "pal_y": pal_y, "weights": wt, "codes": ct}
 
 
 def decode_real(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,

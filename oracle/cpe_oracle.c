@@ -3,7 +3,7 @@
  *
  * TEST INFRASTRUCTURE ONLY (see cpe_oracle.h).  Single-threaded, no SIMD, no
  * blocking, no reordering beyond what each step's definition states.  Built
- * with gcc -O2 and without -ffast-math so that rintf/sqrtf/(float) casts are
+ * with gcc -O2 and without -ffast-math so that rintf/(float) casts are
  * the IEEE round-to-nearest-even operations the canonical arithmetic names.
  *
  * The steps follow Section 3 of the paper in its own order:
@@ -20,20 +20,27 @@
  *                 Eq9 with u = 2x/W - 1 and continuous pixel coordinates)
  *   palette       P[a][2k] = rint(4096 sin(w_k x_a)), P[a][2k+1] =
  *                 rint(4096 cos(w_k x_a)), fp64, stored as int16
- *   LUT           LUT[i] = rint(32768 exp(-i/256)), i = 0..2840, uint16
- *   input         X = clamp(rintf(4096.0f * v), -6144, 6144); NaN -> 0
+ *   input         X = rintf(4096.0f * clamp(v, -1.5, 1.5)), fp32, where a
+ *                 NaN channel clamps to -1.5
  *   participation p in S  <=>  (float)fg(p) > fg_threshold
- *   distance      S_x = sum_c (X_c - P[a][c])^2 (exact integer),
- *                 r_x = sqrtf((float)S_x), d_x = r_x / 4096
- *   weight        q_x = LUT[min(rint(r_x * 0.0625f), 2840)]  ~ 2^15 e^-d_x
- *   votes         H[b][a] = sum_{p in S} q_x(p,a) q_y(p,b)    (exact uint64)
+ *   distance      S_x = sum_c (X_c - P[a][c])^2 (exact integer); with
+ *                 u = fl32(S+1) = 2^e (1 + f), 0 <= f < 1, the m-bit bucket
+ *                 of S is key_m(S) = e 2^m + floor(f 2^m) (exponent and top
+ *                 m mantissa bits of u), its centre distance
+ *                 d~_m(key) = sqrt(2^e (1 + (t+0.5)/2^m) - 1)/4096, t =
+ *                 key mod 2^m (0 for the bucket of S = 0)
+ *   weight        q = WT[key_8(S)] = rint(2^15 e^{-d~_8})    (Eq5/Eq10)
+ *   code          c = CT[key_9(S)] = rint(4096 d~_9)         (distance, 1/4096)
+ *   votes         H[b][a] = sum_{p in S} q_x(p,a) q_y(p,b)  (exact uint64)
  *   peaks         H[b][a] > floor(theta_peak 2^30) and > every in-range
  *                 8-neighbour; listed in ascending b*B_w + a
- *   assignment    D_k = fl32(r_x(a_k) + r_y(b_k)); the smallest k with the
- *                 minimal D_k wins; label = k+1, background 0
+ *   assignment    D_k = c_x(a_k) + c_y(b_k) (integer); the smallest k with
+ *                 the minimal D_k wins; label = k+1, background 0
+ *   score map     expf(-D_m / 4096) for labelled pixels
  *
  * Pins (tests/test_oracle_*.py), each independent of this file's code:
- *   - LUT closed-form values and monotonicity; palette sin^2+cos^2 = 1;
+ *   - bucket tables against e^-d and 256 d over each bucket's exact range;
+ *     palette sin^2+cos^2 = 1 and its values against gamma at the centres;
  *   - the vote histogram against the paper's matrix form E_x^T E_y in fp64
  *     (numpy), within the quantisation error bound;
  *   - brute force on tiny frames: exhaustive scan of every grid position for
@@ -51,10 +58,12 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define FIX_SCALE 4096.0f       /* input and palette fixed-point scale   */
-#define X_CLAMP 6144            /* |X| <= 1.5 * 4096                      */
-#define LUT_LEN 2841            /* indices 0..2840 (rint(256 d))          */
-#define LUT_LAST 2840
+#define FIX_SCALE 4096.0f       /* input and palette fixed-point scale      */
+#define V_CLAMP 1.5f            /* inputs are clamped to [-1.5, 1.5]         */
+#define W_MANT 8                /* mantissa bits of fl32(S+1): weight bucket */
+#define C_MANT 9                /* mantissa bits of fl32(S+1): code bucket   */
+#define W_KEYS (32 << W_MANT)   /* 32 binades of S+1 in [1, 2^32)            */
+#define C_KEYS (32 << C_MANT)
 
 /* IEEE binary16 -> binary32, exact (every half is a float). */
 static float half_to_float(uint16_t h)
@@ -79,14 +88,32 @@ static float load_value(const void *base, int32_t dtype, size_t index)
     return half_to_float(((const uint16_t *)base)[index]);
 }
 
-/* Input to fixed point. */
+/* Input to fixed point: clamp to [-1.5, 1.5] (NaN -> -1.5), scale, round. */
 static int32_t to_fixed(float v)
 {
-    if (isnan(v)) return 0;
-    float t = rintf(FIX_SCALE * v);
-    if (t < (float)-X_CLAMP) return -X_CLAMP;
-    if (t > (float)X_CLAMP) return X_CLAMP;
-    return (int32_t)t;
+    float c = v;
+    if (isnan(c) || c < -V_CLAMP) c = -V_CLAMP;
+    if (c > V_CLAMP) c = V_CLAMP;
+    return (int32_t)rintf(FIX_SCALE * c);
+}
+
+/* m-bit distance bucket of an exact squared distance S: the exponent and
+ * the top m mantissa bits of the binary32 value of S+1. */
+static int32_t dist_key(uint32_t S, int32_t m)
+{
+    float u = (float)(uint32_t)(S + 1u);
+    uint32_t bits;
+    memcpy(&bits, &u, sizeof bits);
+    return (int32_t)(bits >> (23 - m)) - (127 << m);
+}
+
+/* Bucket centre expressed as a distance in embedding units. */
+static double key_distance(int32_t key, int32_t m)
+{
+    if (key == 0) return 0.0;
+    const int32_t e = key >> m, t = key & ((1 << m) - 1);
+    const double s_mid = ldexp(1.0 + ((double)t + 0.5) / (double)(1 << m), e) - 1.0;
+    return sqrt(s_mid) / 4096.0;
 }
 
 /* Eq9: palette of n bins along an axis of `extent` pixels, 2F channels. */
@@ -102,28 +129,27 @@ static void build_palette(int32_t n, int32_t extent, const double *freq, int32_t
     }
 }
 
-static void build_lut(uint16_t *lut)
+/* Eq5 weights e^-d of the 8-bit buckets and distance codes of the 9-bit
+ * buckets. */
+static void build_tables(uint16_t *wt, uint16_t *ct)
 {
-    for (int32_t i = 0; i < LUT_LEN; i++) lut[i] = (uint16_t)rint(32768.0 * exp(-(double)i / 256.0));
+    for (int32_t key = 0; key < W_KEYS; key++) wt[key] = (uint16_t)rint(32768.0 * exp(-key_distance(key, W_MANT)));
+    for (int32_t key = 0; key < C_KEYS; key++) ct[key] = (uint16_t)rint(4096.0 * key_distance(key, C_MANT));
 }
 
-/* Eq4/Eq10 for one axis of one pixel: r[a] = sqrtf(S(a)), q[a] = weight. */
+/* Eq4/Eq10 for one axis of one pixel: distance bucket of every palette
+ * entry, giving its vote weight q[a] and distance code c[a]. */
 static void axis_profile(const int32_t *X, const int16_t *pal, int32_t n, int32_t twoF,
-                         const uint16_t *lut, float *r, uint32_t *q)
+                         const uint16_t *wt, const uint16_t *ct, uint32_t *q, int32_t *c)
 {
     for (int32_t a = 0; a < n; a++) {
         uint64_t s = 0;
-        for (int32_t c = 0; c < twoF; c++) {
-            int64_t diff = (int64_t)X[c] - (int64_t)pal[a * twoF + c];
+        for (int32_t ch = 0; ch < twoF; ch++) {
+            int64_t diff = (int64_t)X[ch] - (int64_t)pal[a * twoF + ch];
             s += (uint64_t)(diff * diff);
         }
-        float ra = sqrtf((float)(uint32_t)s);
-        r[a] = ra;
-        if (q) {
-            int32_t idx = (int32_t)rintf(ra * 0.0625f);
-            if (idx > LUT_LAST) idx = LUT_LAST;
-            q[a] = lut[idx];
-        }
+        if (q) q[a] = wt[dist_key((uint32_t)s, W_MANT)];
+        if (c) c[a] = ct[dist_key((uint32_t)s, C_MANT)];
     }
 }
 
@@ -182,7 +208,7 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       float fg_threshold, double peak_threshold,
                       cpe_oracle_centroid *centroids, int32_t *num_centroids,
                       int32_t *labels, float *score_map,
-                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *lut_out)
+                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out, uint16_t *ct_out)
 {
     if (check_args(H, W, D, dtype, emb, fg, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
                    fg_threshold, peak_threshold) != CPE_ORACLE_OK ||
@@ -195,18 +221,18 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
 
     int16_t *Pw = malloc(sizeof(int16_t) * bins_w * twoF);
     int16_t *Ph = malloc(sizeof(int16_t) * bins_h * twoF);
-    uint16_t lut[LUT_LEN];
+    uint16_t *wt = malloc(sizeof(uint16_t) * W_KEYS), *ct = malloc(sizeof(uint16_t) * C_KEYS);
     uint64_t *Hv = calloc((size_t)nbins, sizeof(uint64_t));
     int32_t *X = malloc(sizeof(int32_t) * twoF);
     int32_t *Y = malloc(sizeof(int32_t) * twoF);
-    float *rx = malloc(sizeof(float) * bins_w), *ry = malloc(sizeof(float) * bins_h);
+    int32_t *cx = malloc(sizeof(int32_t) * bins_w), *cy = malloc(sizeof(int32_t) * bins_h);
     uint32_t *qx = malloc(sizeof(uint32_t) * bins_w), *qy = malloc(sizeof(uint32_t) * bins_h);
     int32_t *peak_a = malloc(sizeof(int32_t) * nbins), *peak_b = malloc(sizeof(int32_t) * nbins);
 
-    /* palettes, preloaded once (Section 3.2, Eq9) and the weight table */
+    /* palettes, preloaded once (Section 3.2, Eq9), and the bucket tables */
     build_palette(bins_w, W, freq_x, F, Pw);
     build_palette(bins_h, H, freq_y, F, Ph);
-    build_lut(lut);
+    build_tables(wt, ct);
 
     /* histogram accumulation: H(a,b) = sum_{p in S} E_x(p,a) E_y(p,b) */
     for (size_t p = 0; p < npix; p++) {
@@ -215,8 +241,8 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
             Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));
         }
-        axis_profile(X, Pw, bins_w, twoF, lut, rx, qx);
-        axis_profile(Y, Ph, bins_h, twoF, lut, ry, qy);
+        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);
+        axis_profile(Y, Ph, bins_h, twoF, wt, ct, qy, NULL);
         for (int32_t b = 0; b < bins_h; b++)
             for (int32_t a = 0; a < bins_w; a++)
                 Hv[b * bins_w + a] += (uint64_t)qx[a] * (uint64_t)qy[b];
@@ -256,12 +282,12 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
             Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));
         }
-        axis_profile(X, Pw, bins_w, twoF, lut, rx, NULL);
-        axis_profile(Y, Ph, bins_h, twoF, lut, ry, NULL);
+        axis_profile(X, Pw, bins_w, twoF, wt, ct, NULL, cx);
+        axis_profile(Y, Ph, bins_h, twoF, wt, ct, NULL, cy);
         int32_t best = 0;
-        float best_d = rx[peak_a[0]] + ry[peak_b[0]];
+        int32_t best_d = cx[peak_a[0]] + cy[peak_b[0]];
         for (int32_t k = 1; k < Kc; k++) {
-            float dk = rx[peak_a[k]] + ry[peak_b[k]];
+            int32_t dk = cx[peak_a[k]] + cy[peak_b[k]];
             if (dk < best_d) {
                 best_d = dk;
                 best = k;
@@ -269,16 +295,17 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
         }
         labels[p] = best + 1;
         centroids[best].npix += 1;
-        if (score_map) score_map[p] = expf(-(best_d * 0x1p-12f));
+        if (score_map) score_map[p] = expf(-((float)best_d * 0x1p-12f));
     }
 
     if (hist) memcpy(hist, Hv, sizeof(uint64_t) * (size_t)nbins);
     if (pal_x) memcpy(pal_x, Pw, sizeof(int16_t) * bins_w * twoF);
     if (pal_y) memcpy(pal_y, Ph, sizeof(int16_t) * bins_h * twoF);
-    if (lut_out) memcpy(lut_out, lut, sizeof(lut));
+    if (wt_out) memcpy(wt_out, wt, sizeof(uint16_t) * W_KEYS);
+    if (ct_out) memcpy(ct_out, ct, sizeof(uint16_t) * C_KEYS);
 
-    free(Pw); free(Ph); free(Hv); free(X); free(Y);
-    free(rx); free(ry); free(qx); free(qy); free(peak_a); free(peak_b);
+    free(Pw); free(Ph); free(wt); free(ct); free(Hv); free(X); free(Y);
+    free(cx); free(cy); free(qx); free(qy); free(peak_a); free(peak_b);
     return CPE_ORACLE_OK;
 }
 

@@ -18,10 +18,14 @@
  * Two arithmetic modes:
  *   cpe_oracle_decode       canonical fixed-point arithmetic: integer inputs
  *                           and palettes (x4096), exact integer squared
- *                           distances, IEEE fp32 square root, a 2841-entry
- *                           e^{-i/256} table scaled by 2^15, exact 64-bit vote
- *                           sums.  Every discrete decision is reproducible
- *                           bit for bit by any correct implementation.
+ *                           distances, distance buckets given by the
+ *                           exponent and top mantissa bits of fl32(S+1) with
+ *                           tables of 2^15 e^-d weights (8-bit buckets) and
+ *                           1/4096 distance codes (9-bit buckets), exact
+ *                           64-bit vote sums, integer distance sums for the
+ *                           assignment.  Every discrete decision
+ *                           is reproducible bit for bit by any correct
+ *                           implementation.
  *   cpe_oracle_decode_real  the real-valued definition in fp64 with no
  *                           quantisation (diagnostic only).
  *
@@ -50,7 +54,8 @@ typedef struct {
  * emb: [H][W][D] channels-last, D = 4*n_freq; fg: [H][W]; both host memory.
  * Outputs (host): centroids[capacity], *num_centroids (true count K),
  * labels[H*W]; optional (may be NULL): score_map[H*W], hist[bins_h*bins_w]
- * (row-major [b][a]), pal_x[bins_w*2F], pal_y[bins_h*2F], lut[2841]. */
+ * (row-major [b][a]), pal_x[bins_w*2F], pal_y[bins_h*2F], weights[8192]
+ * (indexed by the 8-bit bucket), codes[16384] (indexed by the 9-bit bucket). */
 int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       const void *emb, const void *fg,
                       const double *freq_x, const double *freq_y, int32_t n_freq,
@@ -58,7 +63,8 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       float fg_threshold, double peak_threshold,
                       cpe_oracle_centroid *centroids, int32_t *num_centroids,
                       int32_t *labels, float *score_map,
-                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *lut);
+                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
+                      uint16_t *codes);
 
 /* Real-valued fp64 decoder (no quantisation, no threshold tau).  Outputs:
  * hist[bins_h*bins_w] (double), peak list (bin index b*bins_w+a, ascending)

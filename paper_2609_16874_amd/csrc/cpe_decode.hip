@@ -34,9 +34,10 @@
 
 namespace {
 
-constexpr int kLutLen = 2841;       // table indices 0..2840 = rint(256 d)
-constexpr int kLutLast = 2840;
-constexpr int kLutPad = 2848;       // padded length in LDS (16-byte multiple)
+constexpr int kWMant = 8;                  // weight bucket: top 8 mantissa bits of fl32(S+1)
+constexpr int kCMant = 9;                  // code bucket: top 9 mantissa bits
+constexpr int kWKeys = 32 << kWMant;       // 8192 weight buckets
+constexpr int kCKeys = 32 << kCMant;       // 16384 code buckets
 constexpr int kReplicas = 16;       // replicated global histograms (atomic spread)
 constexpr int kMaxF = 16;
 constexpr int kMaxBins = 128;
@@ -49,7 +50,8 @@ struct Tables {
     const int32_t *pal_y;   // [Bh][F]
     const uint32_t *n2_x;   // [Bw]  sum of squared palette entries
     const uint32_t *n2_y;   // [Bh]
-    const uint16_t *lut;    // [kLutPad] 2^15 e^{-i/256}
+    const uint16_t *wt;     // [kWKeys] 2^15 e^-d per 8-bit bucket
+    const uint16_t *ct;     // [kCKeys] 4096 d per 9-bit bucket
     const float *cx;        // [Bw] bin centres (pixels)
     const float *cy;        // [Bh]
 };
@@ -63,7 +65,7 @@ struct cpe_decoder {
     cpe_dtype dtype;
     int device;
     std::vector<int16_t> pal_x, pal_y;   // host copies, [bins][2F]
-    std::vector<uint16_t> lut;
+    std::vector<uint16_t> wt, ct;        // host copies of the bucket tables
     unsigned char *dev;                  // single device allocation
     size_t dev_bytes;
     Tables tb;
@@ -71,6 +73,8 @@ struct cpe_decoder {
     unsigned long long *hlast;           // [nb]
     int32_t *peaks;                      // [cap] a | b << 16
     int32_t *kinfo;                      // [0] = min(K, cap), [1] = K
+    hipEvent_t stage_ev[CPE_STAGE_EVENTS];
+    bool stage_on;
 };
 
 // ---------------------------------------------------------------------------
@@ -78,12 +82,11 @@ struct cpe_decoder {
 // ---------------------------------------------------------------------------
 namespace {
 
-// Input to fixed point: clamp(rint(4096 v), -6144, 6144); NaN reads as 0.
+// Input to fixed point: rint(4096 clamp(v, -1.5, 1.5)); a NaN clamps to -1.5.
 __device__ __forceinline__ int32_t to_fixed(float v)
 {
-    float t = rintf(v * 4096.0f);
-    t = fminf(fmaxf(t, -6144.0f), 6144.0f);
-    return (v != v) ? 0 : (int32_t)t;
+    const float c = fminf(fmaxf(v, -1.5f), 1.5f);   // maxnum/minnum: NaN -> -1.5
+    return (int32_t)rintf(c * 4096.0f);
 }
 
 __device__ __forceinline__ int32_t pack2(int32_t lo, int32_t hi)
@@ -128,18 +131,18 @@ __device__ __forceinline__ int32_t dot_pk(const int32_t (&x)[F], const int32_t *
     return acc;
 }
 
-// Squared distance -> fp32 distance r = sqrtf((float)S) (units of 1/4096).
 // S = |X|^2 + |P|^2 - 2 X.P is exact modulo 2^32 and lies in [0, 2^32).
-__device__ __forceinline__ float axis_r(uint32_t nX, uint32_t nP, int32_t dot)
+__device__ __forceinline__ uint32_t axis_s(uint32_t nX, uint32_t nP, int32_t dot)
 {
-    uint32_t s = nX + nP - 2u * (uint32_t)dot;
-    return sqrtf((float)s);
+    return nX + nP - 2u * (uint32_t)dot;
 }
 
-__device__ __forceinline__ int lut_index(float r)
+// m-bit distance bucket: exponent and top m mantissa bits of fl32(S+1).
+template <int M>
+__device__ __forceinline__ int dist_key(uint32_t s)
 {
-    int i = (int)rintf(r * 0.0625f);
-    return i < kLutLast ? i : kLutLast;
+    const uint32_t bits = __float_as_uint((float)(s + 1u));
+    return (int)(bits >> (23 - M)) - (127 << M);
 }
 
 template <typename T, int F>
@@ -166,15 +169,15 @@ __global__ __launch_bounds__(256) void k_vote(const T *__restrict__ emb, const T
     uint32_t *s_ny = s_nx + Bw;
     int32_t *s_list = reinterpret_cast<int32_t *>(s_ny + Bh);   // [TP]
     int32_t *s_n = s_list + TP;                                  // [4]
-    uint16_t *s_lut = reinterpret_cast<uint16_t *>(s_n + 4);     // [kLutPad]
-    uint16_t *s_qx = s_lut + kLutPad;                            // [Bw][TP]
+    uint16_t *s_wt = reinterpret_cast<uint16_t *>(s_n + 4);      // [kWKeys]
+    uint16_t *s_qx = s_wt + kWKeys;                              // [Bw][TP]
     uint16_t *s_qy = s_qx + Bw * TP;                             // [Bh][TP]
 
     for (int i = tid; i < Bw * F; i += TP) s_px[i] = tb.pal_x[i];
     for (int i = tid; i < Bh * F; i += TP) s_py[i] = tb.pal_y[i];
     for (int i = tid; i < Bw; i += TP) s_nx[i] = tb.n2_x[i];
     for (int i = tid; i < Bh; i += TP) s_ny[i] = tb.n2_y[i];
-    for (int i = tid; i < kLutPad; i += TP) s_lut[i] = tb.lut[i];
+    for (int i = tid; i < kWKeys; i += TP) s_wt[i] = tb.wt[i];
 
     using L = PixelLayout<T, F>;
     const int nb = Bw * Bh;
@@ -209,9 +212,9 @@ __global__ __launch_bounds__(256) void k_vote(const T *__restrict__ emb, const T
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
             for (int a = 0; a < Bw; a++)
-                s_qx[a * TP + tid] = s_lut[lut_index(axis_r(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)))];
+                s_qx[a * TP + tid] = s_wt[dist_key<kWMant>(axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)))];
             for (int b = 0; b < Bh; b++)
-                s_qy[b * TP + tid] = s_lut[lut_index(axis_r(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)))];
+                s_qy[b * TP + tid] = s_wt[dist_key<kWMant>(axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)))];
         }
         __syncthreads();
         if (nchunks == 1) {
@@ -356,7 +359,8 @@ __global__ __launch_bounds__(256) void k_assign(const T *__restrict__ emb, const
     int32_t *s_list = reinterpret_cast<int32_t *>(s_ny + Bh);   // [TP]
     int32_t *s_n = s_list + TP;                                  // [4]
     int32_t *s_cnt = s_n + 4;                                    // [kCountCap]
-    float *s_r = reinterpret_cast<float *>(s_cnt + kCountCap);  // [Bw + Bh][TP]
+    int32_t *s_r = s_cnt + kCountCap;                            // [Bw + Bh][TP] codes
+    uint16_t *s_ct = reinterpret_cast<uint16_t *>(s_r + (Bw + Bh) * TP);   // [kCKeys]
 
     const int Kc = kinfo[0];
     const int ncnt = Kc < kCountCap ? Kc : kCountCap;
@@ -365,6 +369,7 @@ __global__ __launch_bounds__(256) void k_assign(const T *__restrict__ emb, const
     for (int i = tid; i < Bw; i += TP) s_nx[i] = tb.n2_x[i];
     for (int i = tid; i < Bh; i += TP) s_ny[i] = tb.n2_y[i];
     for (int i = tid; i < ncnt; i += TP) s_cnt[i] = 0;
+    for (int i = tid; i < kCKeys; i += TP) s_ct[i] = tb.ct[i];
 
     using L = PixelLayout<T, F>;
     for (int64_t tile = blockIdx.x; tile * TP < npix; tile += gridDim.x) {
@@ -391,21 +396,23 @@ __global__ __launch_bounds__(256) void k_assign(const T *__restrict__ emb, const
             load_block<T, F, L::kAlignY>(row + 2 * F, yk);
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
-            for (int a = 0; a < Bw; a++) s_r[a * TP + tid] = axis_r(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F));
-            for (int b = 0; b < Bh; b++) s_r[(Bw + b) * TP + tid] = axis_r(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F));
+            for (int a = 0; a < Bw; a++)
+                s_r[a * TP + tid] = s_ct[dist_key<kCMant>(axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)))];
+            for (int b = 0; b < Bh; b++)
+                s_r[(Bw + b) * TP + tid] = s_ct[dist_key<kCMant>(axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)))];
             int best = 0;
             const int32_t pk0 = peaks[0];
-            float bd = s_r[(pk0 & 0xffff) * TP + tid] + s_r[(Bw + (pk0 >> 16)) * TP + tid];
+            int32_t bd = s_r[(pk0 & 0xffff) * TP + tid] + s_r[(Bw + (pk0 >> 16)) * TP + tid];
             for (int k = 1; k < Kc; k++) {
                 const int32_t pk = peaks[k];
-                const float d = s_r[(pk & 0xffff) * TP + tid] + s_r[(Bw + (pk >> 16)) * TP + tid];
+                const int32_t d = s_r[(pk & 0xffff) * TP + tid] + s_r[(Bw + (pk >> 16)) * TP + tid];
                 if (d < bd) {
                     bd = d;
                     best = k;
                 }
             }
             labels[pp] = best + 1;
-            if (score_map) score_map[pp] = expf(-(bd * 0x1p-12f));
+            if (score_map) score_map[pp] = expf(-((float)bd * 0x1p-12f));
             if (best < kCountCap)
                 atomicAdd(s_cnt + best, 1);
             else
@@ -437,26 +444,33 @@ cpe_status launch_all(cpe_decoder *h, hipStream_t stream, const void *emb, const
     const int npix = h->H * h->W;
     const T *e = static_cast<const T *>(emb);
     const T *g = static_cast<const T *>(fg);
+    auto mark = [&](int i) {
+        if (h->stage_on) (void)hipEventRecord(h->stage_ev[i], stream);
+    };
+    mark(0);
 
     const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
-    const size_t vote_fixed = tables + 16 + kLutPad * 2;
+    const size_t vote_fixed = tables + 16 + kWKeys * 2;
     const int tp1 = pick_tile(vote_fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
     const size_t lds1 = vote_fixed + (size_t)tp1 * 4 + (size_t)(Bw + Bh) * tp1 * 2;
     const int64_t tiles1 = ((int64_t)npix + tp1 - 1) / tp1;
     const int grid1 = (int)(tiles1 < 1024 ? tiles1 : 1024);
     hipLaunchKernelGGL((k_vote<T, F>), dim3(grid1), dim3(tp1), lds1, stream, e, g, npix, fg_thr, h->tb, Bw, Bh,
                        h->hrep);
+    mark(1);
 
     hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8, stream, h->hrep, h->hlast, Bw, Bh, cut, h->cap,
                        h->tb.cx, h->tb.cy, cents, num, h->peaks, h->kinfo);
+    mark(2);
 
-    const size_t asg_fixed = tables + 16 + kCountCap * 4;
-    const int tp3 = pick_tile(asg_fixed, (size_t)(Bw + Bh) * 4 + 4, 96 * 1024);
+    const size_t asg_fixed = tables + 16 + kCountCap * 4 + kCKeys * 2;
+    const int tp3 = pick_tile(asg_fixed, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
     const size_t lds3 = asg_fixed + (size_t)tp3 * 4 + (size_t)(Bw + Bh) * tp3 * 4;
     const int64_t tiles3 = ((int64_t)npix + tp3 - 1) / tp3;
     const int grid3 = (int)(tiles3 < 2048 ? tiles3 : 2048);
     hipLaunchKernelGGL((k_assign<T, F>), dim3(grid3), dim3(tp3), lds3, stream, e, g, npix, fg_thr, h->tb, Bw, Bh,
                        h->peaks, h->kinfo, cents, labels, score);
+    mark(3);
     return hipGetLastError() == hipSuccess ? CPE_OK : CPE_ERR_HIP;
 }
 
@@ -553,8 +567,17 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     std::vector<float> cx, cy;
     palette(bins_w, W, freq_x, h->pal_x, cx);
     palette(bins_h, H, freq_y, h->pal_y, cy);
-    h->lut.assign(kLutPad, 0);
-    for (int i = 0; i < kLutLen; i++) h->lut[i] = (uint16_t)std::rint(32768.0 * std::exp(-(double)i / 256.0));
+    // bucket tables: weight 2^15 e^-d (8-bit buckets), code 4096 d (9-bit
+    // buckets), d taken at the bucket centre of fl32(S+1)
+    auto centre_distance = [](int key, int m) {
+        if (key == 0) return 0.0;
+        const int e = key >> m, t = key & ((1 << m) - 1);
+        return std::sqrt(std::ldexp(1.0 + ((double)t + 0.5) / (double)(1 << m), e) - 1.0) / 4096.0;
+    };
+    h->wt.resize(kWKeys);
+    h->ct.resize(kCKeys);
+    for (int k = 0; k < kWKeys; k++) h->wt[k] = (uint16_t)std::rint(32768.0 * std::exp(-centre_distance(k, kWMant)));
+    for (int k = 0; k < kCKeys; k++) h->ct[k] = (uint16_t)std::rint(4096.0 * centre_distance(k, kCMant));
 
     auto pack = [&](int n, const std::vector<int16_t> &pal, std::vector<int32_t> &pk, std::vector<uint32_t> &n2) {
         pk.assign((size_t)n * F, 0);
@@ -583,7 +606,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     };
     const size_t o_px = carve(pkx.size() * 4), o_py = carve(pky.size() * 4);
     const size_t o_nx = carve(n2x.size() * 4), o_ny = carve(n2y.size() * 4);
-    const size_t o_lut = carve(kLutPad * 2);
+    const size_t o_wt = carve(kWKeys * 2), o_ct = carve(kCKeys * 2);
     const size_t o_cx = carve(cx.size() * 4), o_cy = carve(cy.size() * 4);
     const size_t o_hrep = carve((size_t)kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
@@ -599,7 +622,8 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               hipMemcpy(d + o_py, pky.data(), pky.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(d + o_nx, n2x.data(), n2x.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(d + o_ny, n2y.data(), n2y.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
-              hipMemcpy(d + o_lut, h->lut.data(), kLutPad * 2, hipMemcpyHostToDevice) == hipSuccess &&
+              hipMemcpy(d + o_wt, h->wt.data(), kWKeys * 2, hipMemcpyHostToDevice) == hipSuccess &&
+              hipMemcpy(d + o_ct, h->ct.data(), kCKeys * 2, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(d + o_cx, cx.data(), cx.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemcpy(d + o_cy, cy.data(), cy.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
               hipMemset(d + o_hrep, 0, (size_t)kReplicas * nb * 8) == hipSuccess &&
@@ -614,14 +638,14 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->tb.pal_y = reinterpret_cast<const int32_t *>(d + o_py);
     h->tb.n2_x = reinterpret_cast<const uint32_t *>(d + o_nx);
     h->tb.n2_y = reinterpret_cast<const uint32_t *>(d + o_ny);
-    h->tb.lut = reinterpret_cast<const uint16_t *>(d + o_lut);
+    h->tb.wt = reinterpret_cast<const uint16_t *>(d + o_wt);
+    h->tb.ct = reinterpret_cast<const uint16_t *>(d + o_ct);
     h->tb.cx = reinterpret_cast<const float *>(d + o_cx);
     h->tb.cy = reinterpret_cast<const float *>(d + o_cy);
     h->hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
     h->hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
     h->peaks = reinterpret_cast<int32_t *>(d + o_peaks);
     h->kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
-    h->lut.resize(kLutLen);
     *out = h;
     return CPE_OK;
 }
@@ -654,12 +678,14 @@ cpe_status cpe_decode_destroy(cpe_decoder *h)
     return e == hipSuccess ? CPE_OK : CPE_ERR_HIP;
 }
 
-cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *lut)
+cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
+                                 uint16_t *codes)
 {
     if (!h) return CPE_ERR_INVALID_ARG;
     if (pal_x) std::memcpy(pal_x, h->pal_x.data(), h->pal_x.size() * sizeof(int16_t));
     if (pal_y) std::memcpy(pal_y, h->pal_y.data(), h->pal_y.size() * sizeof(int16_t));
-    if (lut) std::memcpy(lut, h->lut.data(), (size_t)kLutLen * sizeof(uint16_t));
+    if (weights) std::memcpy(weights, h->wt.data(), h->wt.size() * sizeof(uint16_t));
+    if (codes) std::memcpy(codes, h->ct.data(), h->ct.size() * sizeof(uint16_t));
     return CPE_OK;
 }
 
@@ -671,5 +697,21 @@ cpe_status cpe_decode_get_histogram(cpe_decoder *h, hipStream_t stream, uint64_t
 }
 
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h) { return h ? h->dev_bytes : 0; }
+
+cpe_status cpe_decode_set_stage_events(cpe_decoder *h, hipEvent_t *events, int32_t n_events)
+{
+    if (!h) return CPE_ERR_INVALID_ARG;
+    if (!events) {
+        h->stage_on = false;
+        return CPE_OK;
+    }
+    if (n_events != CPE_STAGE_EVENTS) return CPE_ERR_INVALID_ARG;
+    for (int i = 0; i < CPE_STAGE_EVENTS; i++) {
+        if (!events[i]) return CPE_ERR_INVALID_ARG;
+        h->stage_ev[i] = events[i];
+    }
+    h->stage_on = true;
+    return CPE_OK;
+}
 
 }  // extern "C"

@@ -18,14 +18,17 @@ LIB_PATH = os.path.join(HERE, "libcpe_decode.so")
 
 CPE_OK, CPE_ERR_INVALID_ARG, CPE_ERR_UNSUPPORTED, CPE_ERR_OUT_OF_MEMORY, CPE_ERR_HIP = range(5)
 CPE_F32, CPE_F16 = 0, 1
-LUT_LEN = 2841
+W_KEYS, C_KEYS = 8192, 16384
 
 CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y", "<f4"),
                            ("score", "<f8"), ("npix", "<i4"), ("reserved", "<i4")])
 
 # Every entry point declared in include/cpe_decode.h.
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_destroy", "cpe_status_string",
-           "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes")
+           "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
+           "cpe_decode_set_stage_events")
+STAGE_EVENTS = 4
+STAGES = ("recover_vote", "peaks", "assign_label")
 
 _lib = None
 
@@ -53,11 +56,13 @@ def library():
         lib.cpe_status_string.restype = ctypes.c_char_p
         lib.cpe_status_string.argtypes = [i32]
         lib.cpe_decode_get_tables.restype = i32
-        lib.cpe_decode_get_tables.argtypes = [P, P, P, P]
+        lib.cpe_decode_get_tables.argtypes = [P, P, P, P, P]
         lib.cpe_decode_get_histogram.restype = i32
         lib.cpe_decode_get_histogram.argtypes = [P, P, P]
         lib.cpe_decode_workspace_bytes.restype = ctypes.c_size_t
         lib.cpe_decode_workspace_bytes.argtypes = [P]
+        lib.cpe_decode_set_stage_events.restype = i32
+        lib.cpe_decode_set_stage_events.argtypes = [P, P, i32]
         _lib = lib
     return _lib
 
@@ -115,11 +120,19 @@ class Decoder:
     def tables(self):
         pal_x = np.empty((self.bins_w, 2 * self.F), np.int16)
         pal_y = np.empty((self.bins_h, 2 * self.F), np.int16)
-        lut = np.empty(LUT_LEN, np.uint16)
-        st = library().cpe_decode_get_tables(self._h, pal_x.ctypes.data, pal_y.ctypes.data, lut.ctypes.data)
+        wt = np.empty(W_KEYS, np.uint16)
+        ct = np.empty(C_KEYS, np.uint16)
+        st = library().cpe_decode_get_tables(self._h, pal_x.ctypes.data, pal_y.ctypes.data, wt.ctypes.data,
+                                             ct.ctypes.data)
         if st != CPE_OK:
             raise CpeError(st, "cpe_decode_get_tables")
-        return pal_x, pal_y, lut
+        return pal_x, pal_y, wt, ct
+
+    def set_stage_events(self, events) -> int:
+        """``events``: a ctypes array of CPE_STAGE_EVENTS hipEvent_t handles, or None."""
+        if events is None:
+            return library().cpe_decode_set_stage_events(self._h, None, 0)
+        return library().cpe_decode_set_stage_events(self._h, ctypes.cast(events, ctypes.c_void_p), len(events))
 
     def workspace_bytes(self) -> int:
         return int(library().cpe_decode_workspace_bytes(self._h))

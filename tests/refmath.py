@@ -60,25 +60,27 @@ def real_histogram(emb, fg, fx, fy, bw, bh, fg_threshold=0.5):
 def quant_bound(ex, ey, twoF):
     """Bound on |H_canonical * 2^-30 - H_real| per bin, as [b][a].
 
-    Per pixel and axis the canonical weight is q = LUT[i] with
-    i = rint(256 d'), where d' differs from the real distance d by at most
-    sqrt(2F) * 2^-12 (input and palette each rounded to 1/4096 per channel,
-    triangle inequality) plus the fp32 rounding of S and of its square root
-    (relative 2^-23, < 2^-10 absolute for d < 12).  The index rounding adds
-    1/512 and the table entry rounding 2^-16 absolute, and indices past 2840
-    read 0 where e^-d < 2^-16.  Hence
-        |q/2^15 - e^-d| <= (e^delta - 1) e^-d + 2^-16,
-        delta = 1/512 + sqrt(2F) 2^-12 + 2^-10,
-    and for the product of two such weights
-        |w' - w| <= (e^{2 delta} - 1) w + 2^-16 e^delta (E_x + E_y) + 2^-32.
-    Summed over the participating pixels this gives the bound below.
+    Per pixel and axis the canonical distance differs from the real one by
+    (i) input and palette rounding to 1/4096 per channel: at most
+    sqrt(2F) 2^-12 (triangle inequality, no clamping);
+    (ii) the 8-bit weight bucket: fl32(S+1) falls in [L, L(1+2^-8)) and the
+    bucket centre S_mid+1 is within a factor e^(2^-9 + 2^-23) of S+1, so its
+    square root is within e^(2^-10 + 2^-24) of sqrt(S+1); replacing S+1 by S
+    moves sqrt by at most 1, i.e. 2^-12 in embedding units, on each side.
+    Hence |d~ - d| <= delta(d) = sqrt(2F) 2^-12 + 2^-11 + 2^-10 (d + 0.01).
+    The weight table rounds 2^15 e^-d~ to an integer (2^-16 absolute), so per
+    axis eps = e^-d (e^delta(d) - 1) + 2^-16 bounds |q/2^15 - e^-d|, and for
+    a product of two weights the error is at most
+    eps_x E_y + eps_y E_x + eps_x eps_y, summed over the pixels.
     """
-    delta = 1.0 / 512 + math.sqrt(twoF) * 2.0 ** -12 + 2.0 ** -10
-    h = (ex.T @ ey).T
-    n = ex.shape[0]
-    sx = ex.sum(0)[None, :]
-    sy = ey.sum(0)[:, None]
-    return (math.exp(2 * delta) - 1.0) * h + 2.0 ** -16 * math.exp(delta) * (sx + sy) + n * 2.0 ** -32 + 1e-12
+    def eps(e):
+        d = -np.log(np.maximum(e, 1e-300))
+        delta = math.sqrt(twoF) * 2.0 ** -12 + 2.0 ** -11 + 2.0 ** -10 * (d + 0.01) + 1e-9
+        return e * np.expm1(delta) + 2.0 ** -16
+
+    epx, epy = eps(ex), eps(ey)
+    b = epx.T @ ey + ex.T @ epy + epx.T @ epy
+    return b.T + 1e-12
 
 
 def strict_local_maxima(h: np.ndarray, cut) -> np.ndarray:
@@ -94,15 +96,58 @@ def strict_local_maxima(h: np.ndarray, cut) -> np.ndarray:
 # --------------------------------------------------------------------------
 # pure-Python brute force for tiny frames (canonical arithmetic written out)
 # --------------------------------------------------------------------------
+W_MANT, C_MANT = 8, 9
+
+
 def _f32(x):
     return float(np.float32(x))
 
 
-def _fixed(v: float) -> int:
-    if math.isnan(v):
-        return 0
-    t = float(np.rint(np.float32(np.float32(4096.0) * np.float32(v))))
-    return int(min(max(t, -6144.0), 6144.0))
+def fixed(v: float) -> int:
+    """rint(4096 clamp(v, -1.5, 1.5)) in binary32, NaN clamping to -1.5."""
+    c = np.float32(v)
+    if np.isnan(c) or c < np.float32(-1.5):
+        c = np.float32(-1.5)
+    if c > np.float32(1.5):
+        c = np.float32(1.5)
+    return int(np.rint(np.float32(4096.0) * c))
+
+
+def dist_key(S: int, m: int) -> int:
+    """m-bit bucket of a squared distance: exponent and top m mantissa bits of fl32(S+1)."""
+    bits = int(np.array(np.float32(S + 1)).view(np.uint32))
+    return (bits >> (23 - m)) - (127 << m)
+
+
+def key_distance(key: int, m: int) -> float:
+    if key == 0:
+        return 0.0
+    e, t = key >> m, key & ((1 << m) - 1)
+    return math.sqrt(math.ldexp(1.0 + (t + 0.5) / (1 << m), e) - 1.0) / 4096.0
+
+
+def _first_at_least(x: float) -> int:
+    """Smallest integer n >= 1 with fl32(n) >= x (fl32 is monotone in n)."""
+    lo, hi = 1, 2 ** 33
+    while lo < hi:
+        mid = (lo + hi) // 2
+        if float(np.float32(mid)) >= x:
+            hi = mid
+        else:
+            lo = mid + 1
+    return lo
+
+
+def bucket_range(key: int, m: int):
+    """Smallest and largest integer S whose fl32(S+1) lies in the m-bit bucket
+    [2^e (1 + t/2^m), 2^e (1 + (t+1)/2^m)); None if no integer does."""
+    e, t = key >> m, key & ((1 << m) - 1)
+    lo = math.ldexp(1.0 + t / (1 << m), e)
+    hi = math.ldexp(1.0 + (t + 1) / (1 << m), e)
+    first, stop = _first_at_least(lo), _first_at_least(hi)
+    if first >= stop:
+        return None
+    return first - 1, stop - 2
 
 
 def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold):
@@ -116,26 +161,27 @@ def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold
               for k in range(F) for f in (math.sin, math.cos)] for a in range(bw)]
     pal_y = [[int(np.rint(4096.0 * f(fy[k] * ((b + 1) * H / (bh + 1)))))
               for k in range(F) for f in (math.sin, math.cos)] for b in range(bh)]
-    lut = [int(np.rint(32768.0 * math.exp(-i / 256.0))) for i in range(2841)]
 
-    def r_of(vec, pal_row):
-        s = sum((x - p) ** 2 for x, p in zip(vec, pal_row))
-        return float(np.sqrt(np.float32(s)))
+    def s_of(vec, pal_row):
+        return sum((x - p) ** 2 for x, p in zip(vec, pal_row))
 
-    def q_of(r):
-        return lut[min(int(np.rint(np.float32(r) * np.float32(0.0625))), 2840)]
+    def q_of(S):
+        return int(np.rint(32768.0 * math.exp(-key_distance(dist_key(S, W_MANT), W_MANT))))
+
+    def c_of(S):
+        return int(np.rint(4096.0 * key_distance(dist_key(S, C_MANT), C_MANT)))
 
     pix = []
     for i in range(H):
         for j in range(W):
             if float(np.float32(fg[i, j])) > _f32(fg_threshold):
-                X = [_fixed(float(emb[i, j, c])) for c in range(2 * F)]
-                Y = [_fixed(float(emb[i, j, 2 * F + c])) for c in range(2 * F)]
+                X = [fixed(float(emb[i, j, c])) for c in range(2 * F)]
+                Y = [fixed(float(emb[i, j, 2 * F + c])) for c in range(2 * F)]
                 pix.append((i, j, X, Y))
     hist = [[0] * bw for _ in range(bh)]
     for b in range(bh):
         for a in range(bw):
-            hist[b][a] = sum(q_of(r_of(X, pal_x[a])) * q_of(r_of(Y, pal_y[b])) for (_, _, X, Y) in pix)
+            hist[b][a] = sum(q_of(s_of(X, pal_x[a])) * q_of(s_of(Y, pal_y[b])) for (_, _, X, Y) in pix)
     cut = math.floor(peak_threshold * 2.0 ** 30)
     peaks = []
     for b in range(bh):
@@ -154,7 +200,7 @@ def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold
     for (i, j, X, Y) in pix:
         if not use:
             break
-        ds = [np.float32(r_of(X, pal_x[a])) + np.float32(r_of(Y, pal_y[b])) for (a, b) in use]
+        ds = [c_of(s_of(X, pal_x[a])) + c_of(s_of(Y, pal_y[b])) for (a, b) in use]
         best = min(range(len(use)), key=lambda k: (ds[k], k))
         labels[i][j] = best + 1
     return hist, peaks, K, labels

@@ -38,7 +38,7 @@ def test_status_strings_and_null_handles():
     assert "invalid" in native.status_string(1)
     assert lib.cpe_decode_destroy(None) == 0
     assert lib.cpe_decode(None, None, None, None, 4, 4, 0.5, 0.0, None, None, None, None) == native.CPE_ERR_INVALID_ARG
-    assert lib.cpe_decode_get_tables(None, None, None, None) == native.CPE_ERR_INVALID_ARG
+    assert lib.cpe_decode_get_tables(None, None, None, None, None) == native.CPE_ERR_INVALID_ARG
     assert lib.cpe_decode_get_histogram(None, None, None) == native.CPE_ERR_INVALID_ARG
     assert lib.cpe_decode_workspace_bytes(None) == 0
 

@@ -121,11 +121,11 @@ def test_tables_match_oracle():
     spec = synth.CONFIGS[2]
     fx, fy = spec.freqs()
     dec = native().Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, 32, 32)
-    pal_x, pal_y, lut = dec.tables()
+    pal_x, pal_y, wt, ct = dec.tables()
     ref = oracle.decode(np.zeros((spec.H, spec.W, spec.D), np.float16), np.zeros((spec.H, spec.W), np.float16),
                         fx, fy, 32, 32)
     assert np.array_equal(pal_x, ref["pal_x"]) and np.array_equal(pal_y, ref["pal_y"])
-    assert np.array_equal(lut, ref["lut"])
+    assert np.array_equal(wt, ref["weights"]) and np.array_equal(ct, ref["codes"])
     dec.close()
 
 

@@ -18,34 +18,39 @@ from tests import test_oracle_pins as pins
 MUTANTS = [
     ("transposed histogram", "Hv[b * bins_w + a] += (uint64_t)qx[a] * (uint64_t)qy[b];",
      "Hv[(a * bins_h + b) % (bins_w * bins_h)] += (uint64_t)qx[a] * (uint64_t)qy[b];"),
-    ("dropped channel", "for (int32_t c = 0; c < twoF; c++) {\n            int64_t diff",
-     "for (int32_t c = 1; c < twoF; c++) {\n            int64_t diff"),
-    ("wrong sign in distance", "(int64_t)X[c] - (int64_t)pal[a * twoF + c]", "(int64_t)X[c] + (int64_t)pal[a * twoF + c]"),
+    ("dropped channel", "for (int32_t ch = 0; ch < twoF; ch++) {\n            int64_t diff",
+     "for (int32_t ch = 1; ch < twoF; ch++) {\n            int64_t diff"),
+    ("wrong sign in distance", "(int64_t)X[ch] - (int64_t)pal[a * twoF + ch]", "(int64_t)X[ch] + (int64_t)pal[a * twoF + ch]"),
     ("bin centre off by one", "double centre = ((double)(a + 1) * (double)extent) / (double)(n + 1);\n        for (int32_t k = 0; k < F; k++) {\n            double phase",
      "double centre = ((double)(a) * (double)extent) / (double)(n + 1);\n        for (int32_t k = 0; k < F; k++) {\n            double phase"),
     ("sin/cos swapped", "pal[a * 2 * F + 2 * k] = (int16_t)rint(4096.0 * sin(phase));",
      "pal[a * 2 * F + 2 * k] = (int16_t)rint(4096.0 * cos(phase));"),
-    ("y block read from x channels", "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, lut, rx, qx);",
-     "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, lut, rx, qx);"),
-    ("x palette used for y", "axis_profile(Y, Ph, bins_h, twoF, lut, ry, qy);", "axis_profile(Y, Pw, bins_h, twoF, lut, ry, qy);"),
-    ("weight index floored", "int32_t idx = (int32_t)rintf(ra * 0.0625f);", "int32_t idx = (int32_t)(ra * 0.0625f);"),
-    ("LUT scale", "lut[i] = (uint16_t)rint(32768.0 * exp(-(double)i / 256.0));",
-     "lut[i] = (uint16_t)rint(32767.0 * exp(-(double)i / 256.0));"),
+    ("y block read from x channels", "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);",
+     "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);"),
+    ("x palette used for y", "axis_profile(Y, Ph, bins_h, twoF, wt, ct, qy, NULL);", "axis_profile(Y, Pw, bins_h, twoF, wt, ct, qy, NULL);"),
+    ("weight e^-2d", "wt[key] = (uint16_t)rint(32768.0 * exp(-key_distance(key, W_MANT)));",
+     "wt[key] = (uint16_t)rint(32768.0 * exp(-2.0 * key_distance(key, W_MANT)));"),
+    ("weight scale", "wt[key] = (uint16_t)rint(32768.0 * exp(", "wt[key] = (uint16_t)rint(32767.0 * exp("),
+    ("code scale", "ct[key] = (uint16_t)rint(4096.0 * key_distance", "ct[key] = (uint16_t)rint(2048.0 * key_distance"),
+    ("squared distance used as distance", "return sqrt(s_mid) / 4096.0;", "return s_mid / 16777216.0;"),
+    ("code read with the weight bucket", "if (c) c[a] = ct[dist_key((uint32_t)s, C_MANT)];",
+     "if (c) c[a] = ct[dist_key((uint32_t)s, W_MANT)];"),
+    ("NaN not clamped", "if (isnan(c) || c < -V_CLAMP) c = -V_CLAMP;", "if (c < -V_CLAMP) c = -V_CLAMP;"),
     ("non-strict local max", "if (!(v > h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64",
      "if (!(v >= h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64"),
     ("4-neighbourhood", "if (!da && !db) continue;\n            int32_t nb = b + db, na = a + da;\n            if (nb < 0 || nb >= bh || na < 0 || na >= bw) continue;\n            if (!(v > h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64",
      "if (!da == !db) continue;\n            int32_t nb = b + db, na = a + da;\n            if (nb < 0 || nb >= bh || na < 0 || na >= bw) continue;\n            if (!(v > h[nb * bw + na])) return 0;\n        }\n    return 1;\n}\n\nstatic int is_peak_f64"),
     ("threshold not strict", "if (v > cut && is_peak_u64", "if (v >= cut - 1000000 && is_peak_u64"),
     ("tie goes to the last candidate", "if (dk < best_d) {", "if (dk <= best_d) {"),
-    ("assignment ignores the y axis", "float dk = rx[peak_a[k]] + ry[peak_b[k]];", "float dk = rx[peak_a[k]];",
-     "float best_d = rx[peak_a[0]] + ry[peak_b[0]];", "float best_d = rx[peak_a[0]];"),
+    ("assignment ignores the y axis", "int32_t dk = cx[peak_a[k]] + cy[peak_b[k]];", "int32_t dk = cx[peak_a[k]];",
+     "int32_t best_d = cx[peak_a[0]] + cy[peak_b[0]];", "int32_t best_d = cx[peak_a[0]];"),
     ("background pixels vote", "if (!(load_value(fg, dtype, p) > fg_threshold)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]",
      "if (!(load_value(fg, dtype, p) > -1e30f)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]"),
-    ("no clamp", "if (t > (float)X_CLAMP) return X_CLAMP;", "if (t > (float)X_CLAMP * 4) return X_CLAMP;"),
+    ("clamp too wide", "if (c > V_CLAMP) c = V_CLAMP;", "if (c > 1.6f) c = 1.6f;"),
 ]
 
 PIN_CASES = [
-    (pins.test_lut_closed_form, ()),
+    (pins.test_bucket_tables_bound_e_minus_d_over_each_bucket, ()),
     (pins.test_palette_is_gamma_at_bin_centres, ()),
     (pins.test_palette_unit_circle_and_mirror, ()),
     (pins.test_histogram_matches_eq11_within_quantisation_bound, (pins.np.float32, 4, 12)),
@@ -60,6 +65,7 @@ PIN_CASES = [
     (pins.test_plateau_gives_no_peak_and_single_bin_is_a_peak, ()),
     (pins.test_threshold_is_strict, ()),
     (pins.test_exact_tie_goes_to_lowest_index, ()),
+    (pins.test_assignment_agrees_with_eq7_real_distances, (1,)),
 ]
 
 
