@@ -1,0 +1,87 @@
+// cpe_common.hpp -- constants, device tables and arithmetic helpers shared by
+// the decoder's kernels.  Every helper implements one step of the fixed-point
+// contract stated in include/cpe_decode.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "cpe_decode.h"
+
+namespace cpe {
+
+constexpr int kWMant = 8;             // weight bucket: top 8 mantissa bits of fl32(S+1)
+constexpr int kCMant = 9;             // code bucket: top 9 mantissa bits
+constexpr int kWKeys = 32 << kWMant;  // 8192 weight buckets (32 binades)
+constexpr int kCKeys = 32 << kCMant;  // 16384 code buckets
+constexpr int kReplicas = 16;         // replicated global histograms (spread of the atomics)
+constexpr int kMaxF = 16;             // harmonics per axis
+constexpr int kMaxBins = 128;
+constexpr int kCountCap = 1024;       // centroids whose pixel counts are privatised in LDS
+constexpr int kMfmaBins = 32;         // bin grids up to 32 x 32 take the matrix-core path
+
+typedef short v2s __attribute__((ext_vector_type(2)));
+
+// Device-resident constants built once by cpe_decode_create.
+struct Tables {
+    const int32_t *pal_x;     // [Bw][F]: harmonic k = (sin | cos << 16), int16 each, x4096
+    const int32_t *pal_y;     // [Bh][F]
+    const uint32_t *n2_x;     // [Bw] sum of squared palette entries
+    const uint32_t *n2_y;     // [Bh]
+    const uint16_t *wt;       // [kWKeys] 2^15 e^-d per 8-bit bucket (bucket order)
+    const uint16_t *ct;       // [kCKeys] 4096 d per 9-bit bucket (bucket order)
+    const float *cx;          // [Bw] bin centres (pixels)
+    const float *cy;          // [Bh]
+    // matrix-core path (bins <= 32)
+    const int8_t *qx;         // [2][32][32]: limbs (hi, lo) of -2 P_w[bin][ch], -2P = 128 hi + lo
+    const int8_t *qy;         // [2][32][32]
+    const uint32_t *np1_x;    // [32] |P_w[bin]|^2 + 1 (1 for padded bins)
+    const uint32_t *np1_y;    // [32]
+    const uint32_t *wt_pk;    // [kWKeys] weight as two fp16 limbs (q & 255) | (q >> 8) << 16,
+                              //          at LDS position ((e + 31) & 31) * 256 + t
+    const uint16_t *ct_pm;    // [kCKeys] code at LDS position ((e + 31) & 31) * 512 + t
+};
+
+// Input to fixed point: rint(4096 clamp(v, -1.5, 1.5)); a NaN clamps to -1.5
+// (fmaxf/fminf return the non-NaN operand).
+__device__ __forceinline__ int32_t to_fixed(float v)
+{
+    const float c = fminf(fmaxf(v, -1.5f), 1.5f);
+    return (int32_t)rintf(c * 4096.0f);
+}
+
+__device__ __forceinline__ int32_t pack2(int32_t lo, int32_t hi)
+{
+    return (int32_t)(((uint32_t)lo & 0xffffu) | ((uint32_t)hi << 16));
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t bits)
+{
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
+}
+
+template <typename T> __device__ __forceinline__ float load_scalar(const T *p);
+template <> __device__ __forceinline__ float load_scalar<float>(const float *p) { return *p; }
+template <> __device__ __forceinline__ float load_scalar<_Float16>(const _Float16 *p) { return (float)*p; }
+
+// S = |X|^2 + |P|^2 - 2 X.P is exact modulo 2^32 and lies in [0, 2^32).
+__device__ __forceinline__ uint32_t axis_s(uint32_t nX, uint32_t nP, int32_t dot)
+{
+    return nX + nP - 2u * (uint32_t)dot;
+}
+
+// m-bit distance bucket: exponent and top m mantissa bits of fl32(S+1).
+template <int M>
+__device__ __forceinline__ int dist_key(uint32_t s)
+{
+    const uint32_t bits = __float_as_uint((float)(s + 1u));
+    return (int)(bits >> (23 - M)) - (127 << M);
+}
+
+__device__ __forceinline__ int lane_prefix(unsigned long long mask)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+}
+
+}  // namespace cpe

@@ -1,0 +1,51 @@
+// cpe_decoder.hpp -- the decoder handle and the launch sequence of one frame
+// (private to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "cpe_common.hpp"
+
+struct cpe_decoder {
+    int32_t H, W, D, F, bins_w, bins_h, cap;
+    cpe_dtype dtype;
+    int device;
+    std::vector<int16_t> pal_x, pal_y;   // host copies, [bins][2F]
+    std::vector<uint16_t> wt, ct;        // host copies of the bucket tables (bucket order)
+    unsigned char *dev;                  // single device allocation
+    size_t dev_bytes;
+    cpe::Tables tb;
+    unsigned long long *hrep;            // [kReplicas][nb]
+    unsigned long long *hlast;           // [nb]
+    int32_t *peaks;                      // [cap] a | b << 16
+    int32_t *kinfo;                      // [0] = min(K, cap), [1] = K
+    uint32_t *rowmask;                   // [32]
+    uint16_t *rank;                      // [32 * 32]
+    hipEvent_t stage_ev[CPE_STAGE_EVENTS];
+    bool stage_on;
+};
+
+namespace cpe {
+
+// Arguments of one frame's launch sequence.
+struct FrameArgs {
+    hipStream_t stream;
+    const void *emb, *fg;
+    float fg_thr;
+    long long cut;               // floor(peak_threshold * 2^30), saturated
+    cpe_centroid *cents;
+    int32_t *num, *labels;
+    float *score;
+};
+
+// Enqueue the kernels of one frame for element type T and F harmonics; each
+// is defined in one of the launch_*.hip translation units.
+cpe_status launch_f32_lo(cpe_decoder *h, const FrameArgs &a);   // F = 1..8
+cpe_status launch_f32_hi(cpe_decoder *h, const FrameArgs &a);   // F = 9..16
+cpe_status launch_f16_lo(cpe_decoder *h, const FrameArgs &a);
+cpe_status launch_f16_hi(cpe_decoder *h, const FrameArgs &a);
+
+}  // namespace cpe

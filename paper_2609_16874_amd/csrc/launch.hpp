@@ -1,0 +1,100 @@
+// launch.hpp -- the launch sequence of one frame, instantiated per element
+// type and harmonic count by the launch_*.hip translation units.
+#pragma once
+
+#include "cpe_decoder.hpp"
+#include "k_generic.hpp"
+#include "k_mfma.hpp"
+#include "k_peaks.hpp"
+
+namespace cpe {
+
+constexpr size_t kVoteMfmaLds = (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kWpb * 96 * 4 + kWpb * 64 * 4;
+
+// Largest pixel tile (threads per block) whose LDS footprint fits the budget.
+inline int pick_tile(size_t fixed, size_t per_px, size_t budget)
+{
+    for (int tp = 256; tp >= 64; tp >>= 1)
+        if (fixed + per_px * (size_t)tp <= budget) return tp;
+    return 64;
+}
+
+template <typename T, int F>
+cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
+{
+    hipStream_t stream = fa.stream;
+    const float fg_thr = fa.fg_thr;
+    const long long cut = fa.cut;
+    cpe_centroid *cents = fa.cents;
+    int32_t *num = fa.num, *labels = fa.labels;
+    float *score = fa.score;
+    const void *emb = fa.emb, *fg = fa.fg;
+    const int Bw = h->bins_w, Bh = h->bins_h, nb = Bw * Bh;
+    const int npix = h->H * h->W;
+    const T *e = static_cast<const T *>(emb);
+    const T *g = static_cast<const T *>(fg);
+    auto mark = [&](int i) {
+        if (h->stage_on) (void)hipEventRecord(h->stage_ev[i], stream);
+    };
+    const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;
+    const int64_t chunks = ((int64_t)npix + kChunk - 1) / kChunk;
+    const int64_t wgs = (chunks + kWpb - 1) / kWpb;
+    const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
+
+    mark(0);
+    if (mfma) {
+        const int grid = (int)(wgs < 768 ? wgs : 768);
+        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(kWpb * 64), kVoteMfmaLds, stream, e, g, npix, fg_thr,
+                           h->tb, Bw, Bh, h->hrep);
+    } else {
+        const size_t fixed = tables + 16 + kWKeys * 2;
+        const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
+        const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 2;
+        const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
+        const int grid = (int)(tiles < 1024 ? tiles : 1024);
+        hipLaunchKernelGGL((k_vote_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb, Bw,
+                           Bh, h->hrep);
+    }
+    mark(1);
+
+    PeakOut po{cents, num, h->peaks, h->kinfo, h->rowmask, h->rank};
+    hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8, stream, h->hrep, h->hlast, Bw, Bh, cut, h->cap,
+                       h->tb.cx, h->tb.cy, po);
+    mark(2);
+
+    if (mfma) {
+        const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
+        const int grid = (int)(wgs2 < 256 ? wgs2 : 256);
+        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid), dim3(kWpb2 * 64), kAssignLds, stream, e, g, npix,
+                           fg_thr, h->tb, h->rowmask, h->rank, h->kinfo, cents, labels, score);
+    } else {
+        const size_t fixed = tables + 16 + kCountCap * 4 + kCKeys * 2;
+        const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
+        const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 4;
+        const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
+        const int grid = (int)(tiles < 2048 ? tiles : 2048);
+        hipLaunchKernelGGL((k_assign_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb,
+                           Bw, Bh, h->peaks, h->kinfo, cents, labels, score);
+    }
+    mark(3);
+    return hipGetLastError() == hipSuccess ? CPE_OK : CPE_ERR_HIP;
+}
+
+
+#define CPE_LAUNCH_RANGE(NAME, T, F0)                                       \
+    cpe_status NAME(cpe_decoder *h, const FrameArgs &a)                     \
+    {                                                                       \
+        switch (h->F - (F0)) {                                              \
+        case 0: return launch_all<T, (F0) + 0>(h, a);                       \
+        case 1: return launch_all<T, (F0) + 1>(h, a);                       \
+        case 2: return launch_all<T, (F0) + 2>(h, a);                       \
+        case 3: return launch_all<T, (F0) + 3>(h, a);                       \
+        case 4: return launch_all<T, (F0) + 4>(h, a);                       \
+        case 5: return launch_all<T, (F0) + 5>(h, a);                       \
+        case 6: return launch_all<T, (F0) + 6>(h, a);                       \
+        case 7: return launch_all<T, (F0) + 7>(h, a);                       \
+        default: return CPE_ERR_UNSUPPORTED;                                \
+        }                                                                   \
+    }
+
+}  // namespace cpe

@@ -1,0 +1,8 @@
+// launch_f32_lo.hip -- kernels and launch sequence for float inputs with
+// F = 1..8 harmonics per axis (one translation unit per range so that
+// the instantiations compile in parallel).
+#include "launch.hpp"
+
+namespace cpe {
+CPE_LAUNCH_RANGE(launch_f32_lo, float, 1)
+}  // namespace cpe
