@@ -172,6 +172,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-extra", action="store_true", help="skip the single-frame 640x640 and 1024x2048 lines")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--only-config", type=int, default=None,
+                    help="time only this config (0-4) and print its per-stage line; for profiler runs")
+    ap.add_argument("--copy-calibration", type=int, default=None, metavar="MIB",
+                    help="time a plain device copy of MIB MiB instead (reference for profiler byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the decoder has no multi-GPU path (frames are independent; "
@@ -179,6 +183,34 @@ def main():
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    if args.copy_calibration is not None:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        print(json.dumps({"copy_bytes": n, "ms_per_copy": round(ms, 5),
+                          "gbs_read_plus_write": round(2 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
+        return
+    if args.only_config is not None:
+        cfg = args.only_config
+        s, fr, ms, st, b, ws = bench_config(cfg, args.steps, args.warmup)
+        nfr = len(fr)
+        print(json.dumps({"workload": s.name, "ms_per_frame": round(ms / nfr, 5),
+                          "frames_per_s": round(nfr * 1000 / ms, 1), "literal_bytes": int(b["literal"]),
+                          "literal_roofline_frac": round(b["literal"] / (ms / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "n_fg": int(b["n_fg"]), "stages_ms": {k: round(v, 5) for k, v in st.items()},
+                          "workspace_bytes": ws}), flush=True)
+        return
 
     spec, frames, ms_step, stages, bytes_, ws = bench_config(4, args.steps, args.warmup)
     nfr = len(frames)

@@ -202,7 +202,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
     const size_t o_kinfo = carve(16);
-    const size_t o_rowmask = carve(kMfmaBins * 4);
+    const size_t o_bofs = carve((size_t)(kMaxBatch + 1) * 16), o_bhdr = carve((size_t)(kMaxBatch + 1) * 4);
     const size_t o_rank = carve(kMfmaBins * kMfmaBins * 2);
     h->dev_bytes = off;
     if (hipMalloc(&h->dev, off) != hipSuccess) {
@@ -223,7 +223,8 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               hipMemset(d + o_hrep, 0, (size_t)kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
               hipMemset(d + o_kinfo, 0, 16) == hipSuccess &&
-              hipMemset(d + o_rowmask, 0, kMfmaBins * 4) == hipSuccess &&
+              hipMemset(d + o_bofs, 0, (size_t)(kMaxBatch + 1) * 16) == hipSuccess &&
+              hipMemset(d + o_bhdr, 0, (size_t)(kMaxBatch + 1) * 4) == hipSuccess &&
               hipMemset(d + o_rank, 0, kMfmaBins * kMfmaBins * 2) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
     if (!ok) {
         (void)hipFree(h->dev);
@@ -248,7 +249,8 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
     h->peaks = reinterpret_cast<int32_t *>(d + o_peaks);
     h->kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
-    h->rowmask = reinterpret_cast<uint32_t *>(d + o_rowmask);
+    h->bofs = reinterpret_cast<uint32_t *>(d + o_bofs);
+    h->bhdr = reinterpret_cast<uint32_t *>(d + o_bhdr);
     h->rank = reinterpret_cast<uint16_t *>(d + o_rank);
     *out = h;
     return CPE_OK;

@@ -21,8 +21,9 @@ struct cpe_decoder {
     unsigned long long *hrep;            // [kReplicas][nb]
     unsigned long long *hlast;           // [nb]
     int32_t *peaks;                      // [cap] a | b << 16
-    int32_t *kinfo;                      // [0] = min(K, cap), [1] = K
-    uint32_t *rowmask;                   // [32]
+    int32_t *kinfo;                      // [0] = min(K, cap), [1] = K, [2] = candidate batches
+    uint32_t *bofs;                      // [kMaxBatch + 1][4] candidate batch column offsets
+    uint32_t *bhdr;                      // [kMaxBatch + 1] candidate batch row words
     uint16_t *rank;                      // [32 * 32]
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;

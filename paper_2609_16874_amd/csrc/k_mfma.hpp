@@ -1,17 +1,19 @@
 // k_mfma.hpp -- matrix-core decoder kernels for bin grids up to 32 x 32.
 //
 // Both passes stream the frame in chunks of 512 pixels per wave: a wave
-// reads the foreground channel, compacts the participating pixels with a
-// ballot into a per-wave queue in LDS and processes them in tiles of 32.
+// ballot-compacts the participating pixels of a whole chunk into a per-wave
+// queue in LDS (the foreground values of its next chunk are already being
+// fetched), then works through the queue in tiles of 32 pixels, issuing the
+// embedding loads of the next tile before it computes the current one.
 //
 // Per-axis distances (Eq4/Eq10).  S = |X - P|^2 = |X|^2 + |P|^2 - 2 X.P,
 // where X.(-2P) is a dense [pixels x channels] x [channels x bins]
 // contraction: v_mfma_f32_32x32x16_f16 with X as fp16 (for fp16 inputs every
 // clamped, scaled, rounded value is exactly representable; fp32 inputs add
 // the residual X - fp16(X) as a second operand) against -2P split into two
-// fp16 limbs, -2P = 128 hi + lo with |hi|, |lo| <= 64.  Every partial sum is an integer below 2^24 in
-// magnitude, so both fp32 accumulators are exact and S is assembled exactly
-// in 32-bit integer arithmetic.
+// fp16 limbs, -2P = 128 hi + lo with |hi|, |lo| <= 64.  Every partial sum is
+// an integer below 2^24 in magnitude, so both fp32 accumulators are exact
+// and S is assembled exactly in 32-bit integer arithmetic.
 //
 // Pass 1, k_vote_mfma (recovery + soft voting, Eq5/Eq6/Eq11).  With pixels
 // as the MFMA rows, the distance result leaves in each lane one bin and 16
@@ -19,15 +21,16 @@
 // H = Qx^T Qy over pixels, so the weights feed the second MFMA without any
 // data exchange between lanes.  A weight q <= 2^15 is split into fp16 limbs
 // q = 256 hi + lo; the four limb products accumulate in fp32 exactly as long
-// as at most 256 pixels are summed, after which they are folded into 64-bit
-// integer sums.
+// as at most 256 pixels are summed, after which they are added into a 64-bit
+// histogram in LDS.
 //
 // Pass 2, k_assign_mfma (assignment, Eq7, and label write-out).  With the
 // palette as MFMA rows each lane holds one pixel and 16 bins; the distance
 // codes go through LDS, transposed so that one lane serves one pixel, and
-// the candidate search walks the peak rows: the key (c_x + c_y) * 2^14 +
-// (128 b + a) is minimised over the peaks, which selects the smallest code
-// sum and, on ties, the lowest bin index, i.e. the lowest centroid index.
+// the candidate search walks the peak kernel's batches of 4 columns of one
+// row: the key (c_x + c_y) * 2^14 + (128 b + a) is minimised over the peaks,
+// which selects the smallest code sum and, on ties, the lowest bin index,
+// i.e. the lowest centroid index.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -40,8 +43,10 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kChunk = 512;          // pixels scanned per wave step (8 x 64)
-constexpr int kWpb = 4;              // waves per workgroup
+constexpr int kChunk = 512;          // pixels scanned per chunk (8 x 64)
+constexpr int kWpb = 4;              // waves per workgroup of the vote kernel
+constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
+constexpr int kQueue = kChunk + 64;  // per-wave queue: one chunk + the carried-over remainder
 
 template <int F>
 struct AxisShape {
@@ -85,57 +90,92 @@ struct Fix8 {
 template <typename T>
 constexpr bool kNeedsRest = sizeof(T) == 4;
 
-// Fixed-point values of the 8 channels [16 j + 8 g, 16 j + 8 g + 8) of one
-// axis block (channels past 2F read as 0), plus their squares added to n2.
+// Raw input words of one lane's operand slices: for each axis and K-step j
+// the 8 channels [16 j + 8 g, 16 j + 8 g + 8) of one pixel (channels past 2F
+// read as 0).  Loaded one tile ahead of their use.
 template <typename T, int F>
-__device__ __forceinline__ Fix8 load_fix8(const T *__restrict__ blk, int j, int g, int32_t &n2)
-{
-    constexpr int C = 2 * F;
-    const int c0 = 16 * j + 8 * g;
-    Fix8 out;
-    out.rest = (f16x8){};
-    if constexpr (sizeof(T) == 2 && C % 16 == 0) {
-        const u32x4 w = *reinterpret_cast<const u32x4 *>(__builtin_assume_aligned(blk + c0, 16));
-        const uint32_t words[4] = {w.x, w.y, w.z, w.w};
-        u32x4 res;
+struct RawSlices {
+    static constexpr int C = 2 * F;
+    static constexpr int KS = AxisShape<F>::KS;
+    static constexpr bool kVecH = sizeof(T) == 2 && C % 16 == 0;   // 16-byte fp16 slices
+    static constexpr bool kVecF = sizeof(T) == 4 && C % 16 == 0;   // 32-byte fp32 slices
+    static constexpr int kWords = kVecH ? 4 : 8;
+    uint32_t w[2][KS][kWords];
+
+    // `row` = first channel of the pixel; the host guarantees 16-byte
+    // alignment of the embedding, so with 2F a multiple of 16 every slice is
+    // 16-byte aligned.
+    __device__ __forceinline__ void load(const T *__restrict__ row, int g)
+    {
 #pragma unroll
-        for (int q = 0; q < 4; q++) {
-            const uint32_t word = words[q];
-            f16x2 v;
-            __builtin_memcpy(&v, &word, 4);
-            const f16x2 r = fix_pair_f16(v, n2);
-            uint32_t o;
-            __builtin_memcpy(&o, &r, 4);
-            res[q] = o;
-        }
-        out.main = __builtin_bit_cast(f16x8, res);
-    } else {
-        float v[8];
-        if constexpr (sizeof(T) == 4 && C % 16 == 0) {
-            const float4 *p = reinterpret_cast<const float4 *>(__builtin_assume_aligned(blk + c0, 16));
-            const float4 a = p[0], b = p[1];
-            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-        } else {
+        for (int ax = 0; ax < 2; ax++)
 #pragma unroll
-            for (int s = 0; s < 8; s++) v[s] = (c0 + s) < C ? load_scalar<T>(blk + c0 + s) : 0.0f;
-        }
+            for (int j = 0; j < KS; j++) {
+                const T *blk = row + ax * C + 16 * j + 8 * g;
+                if constexpr (kVecH) {
+                    const u32x4 v = *reinterpret_cast<const u32x4 *>(__builtin_assume_aligned(blk, 16));
+                    w[ax][j][0] = v.x;
+                    w[ax][j][1] = v.y;
+                    w[ax][j][2] = v.z;
+                    w[ax][j][3] = v.w;
+                } else if constexpr (kVecF) {
+                    const float4 *p = reinterpret_cast<const float4 *>(__builtin_assume_aligned(blk, 16));
+                    const float4 a = p[0], b = p[1];
+                    w[ax][j][0] = __float_as_uint(a.x);
+                    w[ax][j][1] = __float_as_uint(a.y);
+                    w[ax][j][2] = __float_as_uint(a.z);
+                    w[ax][j][3] = __float_as_uint(a.w);
+                    w[ax][j][4] = __float_as_uint(b.x);
+                    w[ax][j][5] = __float_as_uint(b.y);
+                    w[ax][j][6] = __float_as_uint(b.z);
+                    w[ax][j][7] = __float_as_uint(b.w);
+                } else {
 #pragma unroll
-        for (int q = 0; q < 4; q++) {
-            short s0, s1;
-            _Float16 m0, m1, r0, r1;
-            fix_f32(v[2 * q], m0, r0, s0);
-            fix_f32(v[2 * q + 1], m1, r1, s1);
-            out.main[2 * q] = m0;
-            out.main[2 * q + 1] = m1;
-            out.rest[2 * q] = r0;
-            out.rest[2 * q + 1] = r1;
-            const v2s si = {s0, s1};
-            n2 = __builtin_amdgcn_sdot2(si, si, n2, false);
+                    for (int s = 0; s < 8; s++)
+                        w[ax][j][s] =
+                            __float_as_uint((16 * j + 8 * g + s) < C ? load_scalar<T>(blk + s) : 0.0f);
+                }
+            }
+    }
+
+    // Fixed-point operands of one axis and its partial squared norm.
+    __device__ __forceinline__ void convert(int ax, Fix8 (&X)[KS], int32_t &n2) const
+    {
+#pragma unroll
+        for (int j = 0; j < KS; j++) {
+            Fix8 &out = X[j];
+            out.rest = (f16x8){};
+            if constexpr (kVecH) {
+                u32x4 res;
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const uint32_t word = w[ax][j][q];
+                    f16x2 v;
+                    __builtin_memcpy(&v, &word, 4);
+                    const f16x2 r = fix_pair_f16(v, n2);
+                    uint32_t o;
+                    __builtin_memcpy(&o, &r, 4);
+                    res[q] = o;
+                }
+                out.main = __builtin_bit_cast(f16x8, res);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    short s0, s1;
+                    _Float16 m0, m1, r0, r1;
+                    fix_f32(__uint_as_float(w[ax][j][2 * q]), m0, r0, s0);
+                    fix_f32(__uint_as_float(w[ax][j][2 * q + 1]), m1, r1, s1);
+                    out.main[2 * q] = m0;
+                    out.main[2 * q + 1] = m1;
+                    out.rest[2 * q] = r0;
+                    out.rest[2 * q + 1] = r1;
+                    const v2s si = {s0, s1};
+                    n2 = __builtin_amdgcn_sdot2(si, si, n2, false);
+                }
+            }
         }
     }
-    return out;
-}
+};
 
 // Palette operand of lane (bin = lane & 31, group g) for K-step j: the limb
 // of -2P at channels [16 j + 8 g, +8), from the [32 bins][32 channels] table.
@@ -155,11 +195,91 @@ __device__ __forceinline__ f32x16 mfma16(f16x8 a, f16x8 b, f32x16 c)
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
+// -2 X.P of one axis as two limb accumulators (exact integers in fp32).
+// PIX_ROWS: pixels are the MFMA rows (pass 1) or its columns (pass 2).
+template <typename T, int KS, bool PIX_ROWS>
+__device__ __forceinline__ void axis_dot(const Fix8 (&X)[KS], const f16x8 (&ph)[KS], const f16x8 (&pl)[KS],
+                                         f32x16 &ah, f32x16 &al)
+{
+    ah = (f32x16){};
+    al = (f32x16){};
+#pragma unroll
+    for (int j = 0; j < KS; j++) {
+        if constexpr (PIX_ROWS) {
+            ah = mfma16(X[j].main, ph[j], ah);
+            al = mfma16(X[j].main, pl[j], al);
+            if constexpr (kNeedsRest<T>) {
+                ah = mfma16(X[j].rest, ph[j], ah);
+                al = mfma16(X[j].rest, pl[j], al);
+            }
+        } else {
+            ah = mfma16(ph[j], X[j].main, ah);
+            al = mfma16(pl[j], X[j].main, al);
+            if constexpr (kNeedsRest<T>) {
+                ah = mfma16(ph[j], X[j].rest, ah);
+                al = mfma16(pl[j], X[j].rest, al);
+            }
+        }
+    }
+}
+
+// Bits of fl32(S + 1) from the two limb accumulators of -2 X.P, |X|^2 and
+// |P|^2 + 1 (the integer sum is exact modulo 2^32 and S + 1 < 2^32).
+__device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t nx, uint32_t np1)
+{
+    const uint32_t s1 = (uint32_t)((int32_t)ah * 128 + (int32_t)al) + nx + np1;
+    return __float_as_uint((float)s1);
+}
+
+// Foreground values of chunk c, 8 per lane.
+template <typename T>
+__device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npix, int lane, float (&fv)[8])
+{
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const int p = c * kChunk + 64 * i + lane;
+        fv[i] = p < npix ? load_scalar<T>(fg + p) : 0.0f;
+    }
+}
+
+// Ballot-compact the participating pixels of chunk c into q[qn ...]; returns
+// the new queue length.  `background(p)` runs for every in-range pixel that
+// does not participate.
+template <typename BG>
+__device__ __forceinline__ int enqueue_chunk(const float (&fv)[8], int c, int npix, float fg_thr, int lane,
+                                             int32_t *q, int qn, BG background)
+{
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const int p = c * kChunk + 64 * i + lane;
+        const bool f = p < npix && fv[i] > fg_thr;
+        if (p < npix && !f) background(p);
+        const unsigned long long m = __ballot(f);
+        if (f) q[qn + lane_prefix(m)] = p;
+        qn += __popcll(m);
+    }
+    return qn;
+}
+
+// Move queue entries [from, from + n), n < 64, to the front.
+__device__ __forceinline__ void queue_shift(int32_t *q, int from, int n, int lane)
+{
+    const int v = lane < n ? q[from + lane] : 0;
+    if (lane < n) q[lane] = v;
+}
+
 // ---------------------------------------------------------------------------
 // Pass 1: recovery + soft voting
 // ---------------------------------------------------------------------------
+// LDS bytes of k_vote_mfma: packed weight table, 64-bit histogram, and per
+// wave a queue and the squared norms of one tile.
+constexpr size_t kVoteLds =
+    (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + (size_t)kWpb * kQueue * 4 + (size_t)kWpb * 64 * 4;
+
+// Two waves per SIMD: without the bound the compiler keeps the accumulators
+// in a separate AGPR allocation and the kernel drops to one wave per SIMD.
 template <typename T, int F>
-__global__ __launch_bounds__(256) void k_vote_mfma(const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_vote_mfma(const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix,
                                                    float fg_thr, Tables tb, int32_t Bw, int32_t Bh,
                                                    unsigned long long *__restrict__ hrep)
 {
@@ -167,9 +287,9 @@ __global__ __launch_bounds__(256) void k_vote_mfma(const T *__restrict__ emb, co
     constexpr int D = 4 * F;
     extern __shared__ __align__(16) unsigned char smem[];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys]
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32]
-    int32_t *s_q = reinterpret_cast<int32_t *>(s_h + kMfmaBins * kMfmaBins);         // [kWpb][96]
-    int32_t *s_nrm = s_q + kWpb * 96;                                                 // [kWpb][64]
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
+    int32_t *s_q = reinterpret_cast<int32_t *>(s_h + kMfmaBins * kMfmaBins);         // [kWpb][kQueue]
+    int32_t *s_nrm = s_q + kWpb * kQueue;                                             // [kWpb][64]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -187,90 +307,66 @@ __global__ __launch_bounds__(256) void k_vote_mfma(const T *__restrict__ emb, co
     }
     const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
 
-    int32_t *q = s_q + wv * 96;
+    int32_t *q = s_q + wv * kQueue;
     int32_t *nrm = s_nrm + wv * 64;
     f32x16 acc2 = {}, acc1 = {}, acc0 = {};
-    unsigned long long H[16];
-#pragma unroll
-    for (int r = 0; r < 16; r++) H[r] = 0ull;
     int ntile = 0;
 
+    // Add the limb sums into the workgroup's histogram (this wave owns every
+    // (a, b) exactly once, so its own atomics never collide).
     auto fold = [&]() {
 #pragma unroll
         for (int r = 0; r < 16; r++) {
-            H[r] += ((unsigned long long)(uint32_t)acc2[r] << 16) + ((unsigned long long)(uint32_t)acc1[r] << 8) +
-                    (unsigned long long)(uint32_t)acc0[r];
+            const unsigned long long v = ((unsigned long long)(uint32_t)acc2[r] << 16) +
+                                         ((unsigned long long)(uint32_t)acc1[r] << 8) +
+                                         (unsigned long long)(uint32_t)acc0[r];
+            atomicAdd(&s_h[ln * kMfmaBins + acc_row(r, g)], v);
             acc2[r] = 0.0f;
             acc1[r] = 0.0f;
             acc0[r] = 0.0f;
         }
     };
 
-    // One tile of up to 32 queued pixels: slot m = lane & 31 of the tile.
-    auto tile = [&](int nvalid) {
-        const int pix = q[ln < nvalid ? ln : 0];
-        const T *row = emb + (size_t)pix * D;
+    // Packed weights of the 16 (pixel, bin) results of one axis.
+    auto weights = [&](const f32x16 &ah, const f32x16 &al, int nbase, uint32_t np1, uint32_t (&e)[16]) {
+#pragma unroll
+        for (int r4 = 0; r4 < 4; r4++) {
+            const i32x4 n4 = *reinterpret_cast<const i32x4 *>(nrm + nbase + 8 * r4 + 4 * g);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int r = 4 * r4 + i;
+                e[r] = s_wt[(s1_bits(ah[r], al[r], (uint32_t)n4[i], np1) >> 15) & (kWKeys - 1)];
+            }
+        }
+    };
+
+    // One tile of up to 32 pixels (queue slot m = lane & 31) from prefetched input.
+    auto tile = [&](const RawSlices<T, F> &raw, int nvalid) {
         int32_t n2x = 0, n2y = 0;
         Fix8 X[KS], Y[KS];
-#pragma unroll
-        for (int j = 0; j < KS; j++) {
-            X[j] = load_fix8<T, F>(row, j, g, n2x);
-            Y[j] = load_fix8<T, F>(row + 2 * F, j, g, n2y);
-        }
+        raw.convert(0, X, n2x);
+        raw.convert(1, Y, n2y);
         n2x += __shfl_xor(n2x, 32);
         n2y += __shfl_xor(n2y, 32);
         if (g == 0) {
             nrm[ln] = n2x;
             nrm[32 + ln] = n2y;
         }
-        f32x16 ah = {}, al = {};
-#pragma unroll
-        for (int j = 0; j < KS; j++) {
-            ah = mfma16(X[j].main, pxh[j], ah);
-            al = mfma16(X[j].main, pxl[j], al);
-            if constexpr (kNeedsRest<T>) {
-                ah = mfma16(X[j].rest, pxh[j], ah);
-                al = mfma16(X[j].rest, pxl[j], al);
-            }
-        }
         uint32_t ex[16], ey[16];
-#pragma unroll
-        for (int r4 = 0; r4 < 4; r4++) {
-            const i32x4 n4 = *reinterpret_cast<const i32x4 *>(nrm + 8 * r4 + 4 * g);
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int r = 4 * r4 + i;
-                const uint32_t s1 = (uint32_t)((int32_t)ah[r] * 128 + (int32_t)al[r]) + (uint32_t)n4[i] + np1x;
-                const uint32_t bits = __float_as_uint((float)s1);
-                ex[r] = s_wt[(bits >> 15) & (kWKeys - 1)];
-            }
+        {
+            f32x16 ah, al;
+            axis_dot<T, KS, true>(X, pxh, pxl, ah, al);
+            weights(ah, al, 0, np1x, ex);
+        }
+        {
+            f32x16 ah, al;
+            axis_dot<T, KS, true>(Y, pyh, pyl, ah, al);
+            weights(ah, al, 32, np1y, ey);
         }
         if (nvalid < 32) {
 #pragma unroll
             for (int r = 0; r < 16; r++)
                 if (acc_row(r, g) >= nvalid) ex[r] = 0u;
-        }
-        ah = (f32x16){};
-        al = (f32x16){};
-#pragma unroll
-        for (int j = 0; j < KS; j++) {
-            ah = mfma16(Y[j].main, pyh[j], ah);
-            al = mfma16(Y[j].main, pyl[j], al);
-            if constexpr (kNeedsRest<T>) {
-                ah = mfma16(Y[j].rest, pyh[j], ah);
-                al = mfma16(Y[j].rest, pyl[j], al);
-            }
-        }
-#pragma unroll
-        for (int r4 = 0; r4 < 4; r4++) {
-            const i32x4 n4 = *reinterpret_cast<const i32x4 *>(nrm + 32 + 8 * r4 + 4 * g);
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int r = 4 * r4 + i;
-                const uint32_t s1 = (uint32_t)((int32_t)ah[r] * 128 + (int32_t)al[r]) + (uint32_t)n4[i] + np1y;
-                const uint32_t bits = __float_as_uint((float)s1);
-                ey[r] = s_wt[(bits >> 15) & (kWKeys - 1)];
-            }
         }
         // vote: K = the 16 pixels of this lane, in two MFMAs of 8
 #pragma unroll
@@ -297,41 +393,40 @@ __global__ __launch_bounds__(256) void k_vote_mfma(const T *__restrict__ emb, co
         }
     };
 
+    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot] * D; };
+
     const int nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
     const int nw = gridDim.x * kWpb;
-    int qn = 0;
-    for (int c = blockIdx.x * kWpb + wv; c < nchunks; c += nw) {
-        const int base = c * kChunk;
-        float fv[8];
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const int p = base + 64 * i + lane;
-            fv[i] = p < npix ? load_scalar<T>(fg + p) : 0.0f;
-        }
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const int p = base + 64 * i + lane;
-            const bool f = p < npix && fv[i] > fg_thr;
-            const unsigned long long m = __ballot(f);
-            if (f) q[qn + lane_prefix(m)] = p;
-            qn += __popcll(m);
-            while (qn >= 32) {
-                tile(32);
-                qn -= 32;
-                const int moved = lane < qn ? q[32 + lane] : 0;
-                if (lane < qn) q[lane] = moved;
+    int qn = 0;                      // queue length, < 32 between chunks
+    int c = blockIdx.x * kWpb + wv;
+    float fv[8];
+    if (c < nchunks) load_fg(fg, c, npix, lane, fv);
+    while (c < nchunks) {
+        qn = enqueue_chunk(fv, c, npix, fg_thr, lane, q, qn, [](int) {});   // qn <= 31 + 512 < kQueue
+        const int cn = c + nw;
+        if (cn < nchunks) load_fg(fg, cn, npix, lane, fv);
+        const int nt = qn >> 5;
+        if (nt > 0) {
+            RawSlices<T, F> raw;
+            raw.load(pixel_row(ln), g);
+            for (int t = 0; t < nt; t++) {
+                const RawSlices<T, F> cur = raw;
+                if (t + 1 < nt) raw.load(pixel_row(32 * (t + 1) + ln), g);
+                tile(cur, 32);
             }
+            queue_shift(q, 32 * nt, qn - 32 * nt, lane);
+            qn -= 32 * nt;
         }
+        c = cn;
     }
-    if (qn > 0) tile(qn);
+    if (qn > 0) {
+        RawSlices<T, F> raw;
+        raw.load(pixel_row(ln < qn ? ln : 0), g);
+        tile(raw, qn);
+    }
     fold();
 
-    // block reduction of the 32 x 32 histogram, then one atomic per bin
-#pragma unroll
-    for (int r = 0; r < 16; r++) {
-        const int a = acc_row(r, g), b = ln;
-        if (a < Bw && b < Bh && H[r]) atomicAdd(&s_h[b * kMfmaBins + a], H[r]);
-    }
+    // one global atomic per bin of the grid
     __syncthreads();
     const int nb = Bw * Bh;
     unsigned long long *dst = hrep + (size_t)(blockIdx.x % kReplicas) * nb;
@@ -344,18 +439,18 @@ __global__ __launch_bounds__(256) void k_vote_mfma(const T *__restrict__ emb, co
 // ---------------------------------------------------------------------------
 // Pass 2: assignment + label write-out
 // ---------------------------------------------------------------------------
-constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
-
 // LDS bytes of k_assign_mfma: code table, bin -> centroid table, counts,
-// row masks, and per wave a queue, x keys [32 bins][64 lanes] (u32) and
-// y codes [32 bins][64 lanes] (u16).
+// candidate batches, and per wave a queue, x keys [32 bins][64 pixels] (u32)
+// and y codes [32 bins][64 pixels] (u16).
 constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                              kMfmaBins * 4 + (size_t)kWpb2 * (128 * 4 + kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
+                              (size_t)(kMaxBatch + 1) * 20 +
+                              (size_t)kWpb2 * (kQueue * 4 + kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
 
 template <typename T, int F>
 __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const T *__restrict__ fg,
                                                      int32_t npix, float fg_thr, Tables tb,
-                                                     const uint32_t *__restrict__ rowmask,
+                                                     const uint32_t *__restrict__ bofs,
+                                                     const uint32_t *__restrict__ bhdr,
                                                      const uint16_t *__restrict__ rank,
                                                      const int32_t *__restrict__ kinfo,
                                                      cpe_centroid *__restrict__ cents, int32_t *__restrict__ labels,
@@ -364,12 +459,13 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                          // [kCKeys]
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(smem);                                 // [kMaxBatch + 1]
+    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch + 1);           // [kMaxBatch + 1]
+    uint16_t *s_ct = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch + 1);           // [kCKeys]
     uint16_t *s_rank = s_ct + kCKeys;                                              // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);  // [1024]
-    uint32_t *s_rm = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins); // [32]
-    int32_t *s_q = reinterpret_cast<int32_t *>(s_rm + kMfmaBins);                 // [kWpb2][128]
-    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_q + kWpb2 * 128);             // [kWpb2][32][64]
+    int32_t *s_q = s_cnt + kMfmaBins * kMfmaBins;                                  // [kWpb2][kQueue]
+    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_q + kWpb2 * kQueue);          // [kWpb2][32][64]
     uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -391,12 +487,17 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         return;
     }
 
+    const int nbat = min(kinfo[2], kMaxBatch);
+    // The offsets are masked to the per-wave arrays' extents (columns and rows < 32).
+    for (int i = tid; i <= nbat; i += blockDim.x) {
+        s_bo[i] = (u32x4){bofs[4 * i], bofs[4 * i + 1], bofs[4 * i + 2], bofs[4 * i + 3]} & 0x1f00u;
+        s_bh[i] = bhdr[i] & 0xf80u;
+    }
     for (int i = tid; i < kCKeys; i += blockDim.x) s_ct[i] = tb.ct_pm[i];
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
         s_rank[i] = rank[i];
         s_cnt[i] = 0;
     }
-    if (tid < kMfmaBins) s_rm[tid] = rowmask[tid];
     __syncthreads();
 
     f16x8 pxh[KS], pxl[KS], pyh[KS], pyl[KS];
@@ -414,124 +515,114 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         npy[r] = tb.np1_y[acc_row(r, g)];
     }
 
-    int32_t *q = s_q + wv * 128;
+    int32_t *q = s_q + wv * kQueue;
     uint32_t *kx = s_kx + wv * kMfmaBins * 64;     // x key of bin a, pixel slot p: kx[a * 64 + p]
     uint16_t *cyb = s_cy + wv * kMfmaBins * 64;    // y code of bin b, pixel slot p: cyb[b * 64 + p]
 
-    // Keys of one tile of 32 pixels (queue slots 32 t .. 32 t + 31).
-    auto codes = [&](int t, int nvalid) {
-        const int slot = 32 * t + ln;
-        const int pix = q[slot < nvalid ? slot : 0];
-        const T *row = emb + (size_t)pix * D;
+    // Keys of one tile of 32 pixels (pixel slots 32 h + (lane & 31)).
+    auto codes = [&](const RawSlices<T, F> &raw, int h) {
+        const int slot = 32 * h + ln;
         int32_t n2x = 0, n2y = 0;
         Fix8 X[KS], Y[KS];
-#pragma unroll
-        for (int j = 0; j < KS; j++) {
-            X[j] = load_fix8<T, F>(row, j, g, n2x);
-            Y[j] = load_fix8<T, F>(row + 2 * F, j, g, n2y);
-        }
+        raw.convert(0, X, n2x);
+        raw.convert(1, Y, n2y);
         n2x += __shfl_xor(n2x, 32);
         n2y += __shfl_xor(n2y, 32);
-        f32x16 ah = {}, al = {};
+        {
+            f32x16 ah, al;
+            axis_dot<T, KS, false>(X, pxh, pxl, ah, al);
 #pragma unroll
-        for (int j = 0; j < KS; j++) {
-            ah = mfma16(pxh[j], X[j].main, ah);
-            al = mfma16(pxl[j], X[j].main, al);
-            if constexpr (kNeedsRest<T>) {
-                ah = mfma16(pxh[j], X[j].rest, ah);
-                al = mfma16(pxl[j], X[j].rest, al);
+            for (int r = 0; r < 16; r++) {
+                const uint32_t code = s_ct[(s1_bits(ah[r], al[r], (uint32_t)n2x, npx[r]) >> 14) & (kCKeys - 1)];
+                const int a = acc_row(r, g);
+                kx[a * 64 + slot] = (code << 14) | (uint32_t)a;
             }
         }
+        {
+            f32x16 ah, al;
+            axis_dot<T, KS, false>(Y, pyh, pyl, ah, al);
 #pragma unroll
-        for (int r = 0; r < 16; r++) {
-            const uint32_t s1 = (uint32_t)((int32_t)ah[r] * 128 + (int32_t)al[r]) + (uint32_t)n2x + npx[r];
-            const uint32_t bits = __float_as_uint((float)s1);
-            const uint32_t code = s_ct[(bits >> 14) & (kCKeys - 1)];
-            const int a = acc_row(r, g);
-            kx[a * 64 + slot] = (code << 14) | (uint32_t)a;
-        }
-        ah = (f32x16){};
-        al = (f32x16){};
-#pragma unroll
-        for (int j = 0; j < KS; j++) {
-            ah = mfma16(pyh[j], Y[j].main, ah);
-            al = mfma16(pyl[j], Y[j].main, al);
-            if constexpr (kNeedsRest<T>) {
-                ah = mfma16(pyh[j], Y[j].rest, ah);
-                al = mfma16(pyl[j], Y[j].rest, al);
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-            const uint32_t s1 = (uint32_t)((int32_t)ah[r] * 128 + (int32_t)al[r]) + (uint32_t)n2y + npy[r];
-            const uint32_t bits = __float_as_uint((float)s1);
-            cyb[acc_row(r, g) * 64 + slot] = s_ct[(bits >> 14) & (kCKeys - 1)];
+            for (int r = 0; r < 16; r++)
+                cyb[acc_row(r, g) * 64 + slot] =
+                    s_ct[(s1_bits(ah[r], al[r], (uint32_t)n2y, npy[r]) >> 14) & (kCKeys - 1)];
         }
     };
 
-    // Candidate search for up to 64 queued pixels (lane p: queue slot p):
-    // per peak row b, m = min over its peak columns a of x key, then
-    // best = min(best, m + y key of b).
-    auto group = [&](int nvalid) {
-        codes(0, nvalid);
-        if (nvalid > 32) codes(1, nvalid);
-        const uint32_t *kxl = kx + lane;
+    // Candidate search for the pixels in queue slots base .. base + nvalid - 1
+    // (lane p: slot p of the key arrays): per batch, the smallest of its 4 x
+    // keys plus the row's y key.  The row word 128 b is both the byte offset
+    // of row b in the y-code array and the row's bits of the key.  The batch
+    // list is read one entry ahead.
+    auto search = [&](int base, int nvalid) {
+        __builtin_amdgcn_wave_barrier();
+        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + lane);
+        const unsigned char *cyl = reinterpret_cast<const unsigned char *>(cyb + lane);
         uint32_t best = 0xffffffffu;
-#pragma unroll
-        for (int b = 0; b < kMfmaBins; b++) {
-            uint32_t mb = __builtin_amdgcn_readfirstlane(s_rm[b]);
-            if (mb) {
-                const uint32_t ky = ((uint32_t)cyb[b * 64 + lane] << 14) | ((uint32_t)b << 7);
-                uint32_t m = 0xffffffffu;
-                while (mb) {
-                    const int a = __builtin_ctz(mb);
-                    mb &= mb - 1u;
-                    m = min(m, kxl[a * 64]);
-                }
-                best = min(best, m + ky);
-            }
+        u32x4 o = s_bo[0];
+        uint32_t hb = s_bh[0];
+        for (int i = 0; i < nbat; i++) {
+            const u32x4 on = s_bo[i + 1];
+            const uint32_t hn = s_bh[i + 1];
+            const uint32_t v0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
+            const uint32_t v1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
+            const uint32_t v2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
+            const uint32_t v3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+            const uint32_t cy = *reinterpret_cast<const uint16_t *>(cyl + hb);
+            const uint32_t m = min(min(v0, v1), min(v2, v3));
+            best = min(best, m + ((cy << 14) | hb));
+            o = on;
+            hb = hn;
         }
         if (lane < nvalid) {
-            const int pix = q[lane];
-            // a, b < 32 here (the row masks only hold bins of the grid); the
-            // masks keep the table reads in bounds regardless
+            const int pix = q[base + lane];
             const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
             const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
             labels[pix] = k + 1;
             if (score_map) score_map[pix] = expf(-((float)(best >> 14) * 0x1p-12f));
             atomicAdd(s_cnt + k, 1);
         }
+        __builtin_amdgcn_wave_barrier();
     };
 
-    int qn = 0;
-    for (int c = blockIdx.x * kWpb2 + wv; c < nchunks; c += nw) {
-        const int base = c * kChunk;
-        float fv[8];
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const int p = base + 64 * i + lane;
-            fv[i] = p < npix ? load_scalar<T>(fg + p) : 0.0f;
-        }
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const int p = base + 64 * i + lane;
-            const bool f = p < npix && fv[i] > fg_thr;
-            if (p < npix && !f) {
-                labels[p] = 0;
-                if (score_map) score_map[p] = 0.0f;
+    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot] * D; };
+    auto background = [&](int p) {
+        labels[p] = 0;
+        if (score_map) score_map[p] = 0.0f;
+    };
+
+    int qn = 0;                      // queue length, < 64 between chunks
+    int c = blockIdx.x * kWpb2 + wv;
+    float fv[8];
+    if (c < nchunks) load_fg(fg, c, npix, lane, fv);
+    while (c < nchunks) {
+        qn = enqueue_chunk(fv, c, npix, fg_thr, lane, q, qn, background);   // qn <= 63 + 512 < kQueue
+        const int cn = c + nw;
+        if (cn < nchunks) load_fg(fg, cn, npix, lane, fv);
+        const int nt = (qn >> 6) * 2;    // tiles of the full groups of 64
+        if (nt > 0) {
+            RawSlices<T, F> raw;
+            raw.load(pixel_row(ln), g);
+            for (int t = 0; t < nt; t++) {
+                const RawSlices<T, F> cur = raw;
+                if (t + 1 < nt) raw.load(pixel_row(32 * (t + 1) + ln), g);
+                codes(cur, t & 1);
+                if (t & 1) search(32 * (t - 1), 64);
             }
-            const unsigned long long m = __ballot(f);
-            if (f) q[qn + lane_prefix(m)] = p;
-            qn += __popcll(m);
-            if (qn >= 64) {
-                group(64);
-                qn -= 64;
-                const int moved = lane < qn ? q[64 + lane] : 0;
-                if (lane < qn) q[lane] = moved;
-            }
+            queue_shift(q, 32 * nt, qn - 32 * nt, lane);
+            qn -= 32 * nt;
         }
+        c = cn;
     }
-    if (qn > 0) group(qn);
+    if (qn > 0) {
+        RawSlices<T, F> raw;
+        raw.load(pixel_row(ln < qn ? ln : 0), g);
+        codes(raw, 0);
+        if (qn > 32) {
+            raw.load(pixel_row(32 + ln < qn ? 32 + ln : 0), g);
+            codes(raw, 1);
+        }
+        search(0, qn);
+    }
     __syncthreads();
     for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)
         if (s_cnt[i]) atomicAdd(&cents[i].npix, s_cnt[i]);

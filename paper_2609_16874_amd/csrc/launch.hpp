@@ -9,8 +9,6 @@
 
 namespace cpe {
 
-constexpr size_t kVoteMfmaLds = (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kWpb * 96 * 4 + kWpb * 64 * 4;
-
 // Largest pixel tile (threads per block) whose LDS footprint fits the budget.
 inline int pick_tile(size_t fixed, size_t per_px, size_t budget)
 {
@@ -44,7 +42,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
     mark(0);
     if (mfma) {
         const int grid = (int)(wgs < 768 ? wgs : 768);
-        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(kWpb * 64), kVoteMfmaLds, stream, e, g, npix, fg_thr,
+        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(kWpb * 64), kVoteLds, stream, e, g, npix, fg_thr,
                            h->tb, Bw, Bh, h->hrep);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
@@ -57,7 +55,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
     }
     mark(1);
 
-    PeakOut po{cents, num, h->peaks, h->kinfo, h->rowmask, h->rank};
+    PeakOut po{cents, num, h->peaks, h->kinfo, h->bofs, h->bhdr, h->rank};
     hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8, stream, h->hrep, h->hlast, Bw, Bh, cut, h->cap,
                        h->tb.cx, h->tb.cy, po);
     mark(2);
@@ -66,7 +64,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
         const int grid = (int)(wgs2 < 256 ? wgs2 : 256);
         hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid), dim3(kWpb2 * 64), kAssignLds, stream, e, g, npix,
-                           fg_thr, h->tb, h->rowmask, h->rank, h->kinfo, cents, labels, score);
+                           fg_thr, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
     } else {
         const size_t fixed = tables + 16 + kCountCap * 4 + kCKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
