@@ -106,10 +106,13 @@ def time_steps(dec, embs, fgs, outs, fg_thr, theta, steps, warmup):
     torch.cuda.synchronize()
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0.record()
+    h0 = time.perf_counter()
     for _ in range(steps):
         step()
+    host_s = time.perf_counter() - h0
     t1.record()
     torch.cuda.synchronize()
+    time_steps.host_us_per_call = host_s / (steps * len(embs)) * 1e6
     return t0.elapsed_time(t1) / steps
 
 
@@ -209,6 +212,7 @@ def main():
                           "frames_per_s": round(nfr * 1000 / ms, 1), "literal_bytes": int(b["literal"]),
                           "literal_roofline_frac": round(b["literal"] / (ms / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "n_fg": int(b["n_fg"]), "stages_ms": {k: round(v, 5) for k, v in st.items()},
+                          "host_enqueue_us_per_frame": round(time_steps.host_us_per_call, 2),
                           "workspace_bytes": ws}), flush=True)
         return
 
@@ -239,6 +243,7 @@ def main():
                      "bytes_per_launch": round(bytes_[dom]), "avg_launch_ms": round(dom_ms, 5)},
         "stages_ms": {k: round(v, 5) for k, v in stages.items()},
         "literal_roofline_frac": round(bytes_["literal"] / (ms_step / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "host_enqueue_us_per_frame": round(time_steps.host_us_per_call, 2),
         "workspace_bytes": ws,
     }
     if not args.no_extra:

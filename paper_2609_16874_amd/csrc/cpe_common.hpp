@@ -41,6 +41,8 @@ struct Tables {
     const int8_t *qy;         // [2][32][32]
     const uint32_t *np1_x;    // [32] |P_w[bin]|^2 + 1 (1 for padded bins)
     const uint32_t *np1_y;    // [32]
+    const uint32_t *pop;      // [axis][limb][K-step j][64 lanes][4 words]: the fp16 palette operand
+                              //   of lane l (bin l & 31, channels 16 j + 8 (l >> 5) + 0..7)
     const uint32_t *wt_pk;    // [kWKeys] weight as two fp16 limbs (q & 255) | (q >> 8) << 16,
                               //          at LDS position ((e + 31) & 31) * 256 + t
     const uint16_t *ct_pm;    // [kCKeys] code at LDS position ((e + 31) & 31) * 512 + t

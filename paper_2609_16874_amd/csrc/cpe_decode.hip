@@ -39,6 +39,16 @@ long long peak_cut(double theta)
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// IEEE binary16 bit pattern of an integer with |v| <= 1024 (exact).
+uint16_t half_of_small_int(int v)
+{
+    if (v == 0) return 0;
+    const uint16_t sign = v < 0 ? 0x8000u : 0u;
+    const int a = v < 0 ? -v : v;
+    const int e = 31 - __builtin_clz((unsigned)a);
+    return (uint16_t)(sign | ((e + 15) << 10) | ((a << (10 - e)) & 0x3ff));
+}
+
 // Distance at the centre of an m-bit bucket of fl32(S+1) (0 for S = 0).
 double centre_distance(int key, int m)
 {
@@ -183,6 +193,17 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     std::vector<uint32_t> np1x, np1y;
     limbs(bins_w, h->pal_x, n2x, qx, np1x);
     limbs(bins_h, h->pal_y, n2y, qy, np1y);
+    // the same limbs as the per-lane fp16 MFMA operands (two K-steps of 16 channels)
+    std::vector<uint16_t> pop((size_t)2 * 2 * 2 * 64 * 8);
+    for (int ax = 0; ax < 2; ax++)
+        for (int limb = 0; limb < 2; limb++)
+            for (int j = 0; j < 2; j++)
+                for (int l = 0; l < 64; l++)
+                    for (int e = 0; e < 8; e++) {
+                        const std::vector<int8_t> &q = ax ? qy : qx;
+                        const int v = q[limb * 1024 + (l & 31) * 32 + 16 * j + 8 * (l >> 5) + e];
+                        pop[((((size_t)ax * 2 + limb) * 2 + j) * 64 + l) * 8 + e] = half_of_small_int(v);
+                    }
 
     // one allocation: constants, replicated histograms, last histogram, peak list, counters
     size_t off = 0;
@@ -197,6 +218,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_cx = carve(cx.size() * 4), o_cy = carve(cy.size() * 4);
     const size_t o_qx = carve(qx.size()), o_qy = carve(qy.size());
     const size_t o_npx = carve(np1x.size() * 4), o_npy = carve(np1y.size() * 4);
+    const size_t o_pop = carve(pop.size() * 2);
     const size_t o_wpk = carve(wt_pk.size() * 4), o_cpm = carve(ct_pm.size() * 2);
     const size_t o_hrep = carve((size_t)kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
@@ -204,6 +226,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_kinfo = carve(16);
     const size_t o_bofs = carve((size_t)(kMaxBatch + 1) * 16), o_bhdr = carve((size_t)(kMaxBatch + 1) * 4);
     const size_t o_rank = carve(kMfmaBins * kMfmaBins * 2);
+    const size_t o_ticket = carve(4 * 32);
     h->dev_bytes = off;
     if (hipMalloc(&h->dev, off) != hipSuccess) {
         delete h;
@@ -219,13 +242,15 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               up(o_cx, cx.data(), cx.size() * 4) && up(o_cy, cy.data(), cy.size() * 4) &&
               up(o_qx, qx.data(), qx.size()) && up(o_qy, qy.data(), qy.size()) &&
               up(o_npx, np1x.data(), np1x.size() * 4) && up(o_npy, np1y.data(), np1y.size() * 4) &&
+              up(o_pop, pop.data(), pop.size() * 2) &&
               up(o_wpk, wt_pk.data(), wt_pk.size() * 4) && up(o_cpm, ct_pm.data(), ct_pm.size() * 2) &&
               hipMemset(d + o_hrep, 0, (size_t)kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
               hipMemset(d + o_kinfo, 0, 16) == hipSuccess &&
               hipMemset(d + o_bofs, 0, (size_t)(kMaxBatch + 1) * 16) == hipSuccess &&
               hipMemset(d + o_bhdr, 0, (size_t)(kMaxBatch + 1) * 4) == hipSuccess &&
-              hipMemset(d + o_rank, 0, kMfmaBins * kMfmaBins * 2) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
+              hipMemset(d + o_rank, 0, kMfmaBins * kMfmaBins * 2) == hipSuccess &&
+              hipMemset(d + o_ticket, 0, 4 * 32) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
     if (!ok) {
         (void)hipFree(h->dev);
         delete h;
@@ -243,6 +268,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->tb.qy = reinterpret_cast<const int8_t *>(d + o_qy);
     h->tb.np1_x = reinterpret_cast<const uint32_t *>(d + o_npx);
     h->tb.np1_y = reinterpret_cast<const uint32_t *>(d + o_npy);
+    h->tb.pop = reinterpret_cast<const uint32_t *>(d + o_pop);
     h->tb.wt_pk = reinterpret_cast<const uint32_t *>(d + o_wpk);
     h->tb.ct_pm = reinterpret_cast<const uint16_t *>(d + o_cpm);
     h->hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
@@ -252,6 +278,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->bofs = reinterpret_cast<uint32_t *>(d + o_bofs);
     h->bhdr = reinterpret_cast<uint32_t *>(d + o_bhdr);
     h->rank = reinterpret_cast<uint16_t *>(d + o_rank);
+    h->ticket = reinterpret_cast<uint32_t *>(d + o_ticket);
     *out = h;
     return CPE_OK;
 }

@@ -25,6 +25,7 @@ struct cpe_decoder {
     uint32_t *bofs;                      // [kMaxBatch + 1][4] candidate batch column offsets
     uint32_t *bhdr;                      // [kMaxBatch + 1] candidate batch row words
     uint16_t *rank;                      // [32 * 32]
+    uint32_t *ticket;                    // [32] completion counters of the vote kernel (0 between frames)
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;
 };

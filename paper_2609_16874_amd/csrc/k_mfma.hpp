@@ -34,6 +34,7 @@
 #pragma once
 
 #include "cpe_common.hpp"
+#include "k_peaks.hpp"
 
 namespace cpe {
 
@@ -43,10 +44,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kChunk = 512;          // pixels scanned per chunk (8 x 64)
-constexpr int kWpb = 4;              // waves per workgroup of the vote kernel
+constexpr int kChunk = 128;          // pixels scanned per chunk
+constexpr int kChunkRows = kChunk / 64;
 constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
-constexpr int kQueue = kChunk + 64;  // per-wave queue: one chunk + the carried-over remainder
+constexpr int kRing1 = 256;          // per-wave ring queues of participating pixels (powers of two):
+constexpr int kRing2 = 512;          //   vote kernel (refilled below 64), assignment kernel (below 128)
+constexpr int kPopBytes = 2 * 2 * 2 * 64 * 16;   // palette operands of both axes, limbs and K-steps
+constexpr int kTicketGroups = 16;    // first level of the vote kernel's completion count
 
 template <int F>
 struct AxisShape {
@@ -54,14 +58,17 @@ struct AxisShape {
     static constexpr int KS = (C + 15) / 16;    // MFMA K-steps of 16 channels
 };
 
-// Clamp, scale and round a pair of fp16 inputs to fixed-point integers (kept
-// as fp16, exact) and accumulate their squares.
+// Scale, clamp and round a pair of fp16 inputs to fixed-point integers (kept
+// as fp16, exact) and accumulate their squares.  Scaling first is exact (a
+// power of two; overflow gives +-inf, which the clamp maps like any value
+// beyond 1.5), and it lets the clamp see a canonical operand: a NaN becomes
+// -6144 because max returns the non-NaN operand.
 __device__ __forceinline__ f16x2 fix_pair_f16(f16x2 v, int32_t &n2)
 {
-    const f16x2 lo = {(_Float16)-1.5f, (_Float16)-1.5f}, hi = {(_Float16)1.5f, (_Float16)1.5f};
+    const f16x2 lo = {(_Float16)-6144.0f, (_Float16)-6144.0f}, hi = {(_Float16)6144.0f, (_Float16)6144.0f};
+    v = v * (f16x2){(_Float16)4096.0f, (_Float16)4096.0f};
     v = __builtin_elementwise_max(v, lo);
     v = __builtin_elementwise_min(v, hi);
-    v = v * (f16x2){(_Float16)4096.0f, (_Float16)4096.0f};
     f16x2 r;
     r[0] = __builtin_rintf16(v[0]);
     r[1] = __builtin_rintf16(v[1]);
@@ -75,7 +82,7 @@ __device__ __forceinline__ f16x2 fix_pair_f16(f16x2 v, int32_t &n2)
 // residual X - fp16(X) (|residual| <= 2), both accumulated into the same sums.
 __device__ __forceinline__ void fix_f32(float v, _Float16 &main, _Float16 &rest, short &si)
 {
-    const float t = rintf(fminf(fmaxf(v, -1.5f), 1.5f) * 4096.0f);
+    const float t = rintf(fminf(fmaxf(v * 4096.0f, -6144.0f), 6144.0f));
     si = (short)t;
     main = (_Float16)t;
     rest = (_Float16)(t - (float)main);
@@ -177,14 +184,12 @@ struct RawSlices {
     }
 };
 
-// Palette operand of lane (bin = lane & 31, group g) for K-step j: the limb
-// of -2P at channels [16 j + 8 g, +8), from the [32 bins][32 channels] table.
-__device__ __forceinline__ f16x8 palette_operand(const int8_t *__restrict__ limb, int bin, int j, int g)
+// Palette operand of lane `lane` (bin lane & 31, channels 16 j + 8 (lane >> 5)
+// + 0..7) for axis ax (0 = x, 1 = y), limb (0 = hi, 1 = lo) and K-step j.
+__device__ __forceinline__ f16x8 palette_operand(const uint32_t *__restrict__ pop, int ax, int limb, int j, int lane)
 {
-    f16x8 out;
-#pragma unroll
-    for (int s = 0; s < 8; s++) out[s] = (_Float16)(float)limb[bin * 32 + 16 * j + 8 * g + s];
-    return out;
+    const u32x4 w = *reinterpret_cast<const u32x4 *>(pop + ((((ax * 2 + limb) * 2 + j) * 64 + lane) * 4));
+    return __builtin_bit_cast(f16x8, w);
 }
 
 // Row of the 32 x 32 MFMA result held by register r of a lane in group g.
@@ -231,83 +236,138 @@ __device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t nx, uin
     return __float_as_uint((float)s1);
 }
 
-// Foreground values of chunk c, 8 per lane.
+// Foreground values of chunk c, kChunkRows per lane.
 template <typename T>
-__device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npix, int lane, float (&fv)[8])
+__device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npix, int lane, float (&fv)[kChunkRows])
 {
 #pragma unroll
-    for (int i = 0; i < 8; i++) {
+    for (int i = 0; i < kChunkRows; i++) {
         const int p = c * kChunk + 64 * i + lane;
         fv[i] = p < npix ? load_scalar<T>(fg + p) : 0.0f;
     }
 }
 
-// Ballot-compact the participating pixels of chunk c into q[qn ...]; returns
-// the new queue length.  `background(p)` runs for every in-range pixel that
-// does not participate.
-template <typename BG>
-__device__ __forceinline__ int enqueue_chunk(const float (&fv)[8], int c, int npix, float fg_thr, int lane,
-                                             int32_t *q, int qn, BG background)
+// Ballot-compact the participating pixels of chunk c into the ring queue at
+// positions tail, tail + 1, ...; returns the new tail.  `background(p)` runs
+// for every in-range pixel that does not participate.
+template <int RING, typename BG>
+__device__ __forceinline__ int enqueue_chunk(const float (&fv)[kChunkRows], int c, int npix, float fg_thr, int lane,
+                                             int32_t *q, int tail, BG background)
 {
 #pragma unroll
-    for (int i = 0; i < 8; i++) {
+    for (int i = 0; i < kChunkRows; i++) {
         const int p = c * kChunk + 64 * i + lane;
         const bool f = p < npix && fv[i] > fg_thr;
         if (p < npix && !f) background(p);
         const unsigned long long m = __ballot(f);
-        if (f) q[qn + lane_prefix(m)] = p;
-        qn += __popcll(m);
+        if (f) q[(tail + lane_prefix(m)) & (RING - 1)] = p;
+        tail += __popcll(m);
     }
-    return qn;
+    return tail;
 }
 
-// Move queue entries [from, from + n), n < 64, to the front.
-__device__ __forceinline__ void queue_shift(int32_t *q, int from, int n, int lane)
+// One wave's stream of chunks c0, c0 + stride, ... feeding a ring queue: the
+// foreground values of the next chunk are always in flight while the queue
+// is being consumed.
+template <typename T>
+struct ChunkFeed {
+    const T *fg;
+    int npix, nchunks, stride, c;
+    float fg_thr;
+    float fv[kChunkRows];
+
+    __device__ __forceinline__ void start(const T *fg_, int npix_, float thr, int c0, int stride_, int lane)
+    {
+        fg = fg_;
+        npix = npix_;
+        fg_thr = thr;
+        nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
+        stride = stride_;
+        c = c0;
+        if (c < nchunks) load_fg(fg, c, npix, lane, fv);
+    }
+    __device__ __forceinline__ bool more() const { return c < nchunks; }
+    // Enqueue chunks until the queue holds at least WANT pixels or the
+    // stream ends; the queue never exceeds WANT - 1 + kChunk entries.
+    template <int RING, int WANT, typename BG>
+    __device__ __forceinline__ int top_up(int32_t *q, int head, int tail, int lane, BG background)
+    {
+        static_assert(WANT - 1 + kChunk <= RING, "ring queue too small");
+        while (tail - head < WANT && c < nchunks) {
+            tail = enqueue_chunk<RING>(fv, c, npix, fg_thr, lane, q, tail, background);
+            c += stride;
+            if (c < nchunks) load_fg(fg, c, npix, lane, fv);
+        }
+        return tail;
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Pass 1: recovery + soft voting (+ the peak extraction in the last workgroup)
+// ---------------------------------------------------------------------------
+// LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
+// and per wave a ring queue and the squared norms of one tile.
+constexpr size_t kVoteLds(int wpb)
 {
-    const int v = lane < n ? q[from + lane] : 0;
-    if (lane < n) q[lane] = v;
+    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * kRing1 * 4 + (size_t)wpb * 64 * 4;
 }
 
-// ---------------------------------------------------------------------------
-// Pass 1: recovery + soft voting
-// ---------------------------------------------------------------------------
-// LDS bytes of k_vote_mfma: packed weight table, 64-bit histogram, and per
-// wave a queue and the squared norms of one tile.
-constexpr size_t kVoteLds =
-    (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + (size_t)kWpb * kQueue * 4 + (size_t)kWpb * 64 * 4;
-
-// Two waves per SIMD: without the bound the compiler keeps the accumulators
-// in a separate AGPR allocation and the kernel drops to one wave per SIMD.
+// Waves per SIMD the register allocation must allow: three for fp16 inputs
+// with up to 8 or exactly 16 harmonics (one workgroup of 12 waves per compute
+// unit), two otherwise (fp32 residual operands, scalar channel loads),
+// where three would spill.  Without a bound the compiler keeps the
+// accumulators in a separate AGPR allocation and the kernel drops to one wave
+// per SIMD.
 template <typename T, int F>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_vote_mfma(const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix,
-                                                   float fg_thr, Tables tb, int32_t Bw, int32_t Bh,
-                                                   unsigned long long *__restrict__ hrep)
+constexpr int kVoteWaves = (sizeof(T) == 2 && (F <= 8 || F == 16)) ? 3 : 2;
+// Waves per workgroup of the vote kernel: one workgroup per compute unit.
+template <typename T, int F>
+constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
+//
+// The workgroup that finishes last (a ticket counter, taken after a release
+// fence) runs the peak extraction on the summed replicas and resets the
+// counter for the next frame.
+template <typename T, int F>
+__global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
+    const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix, float fg_thr, Tables tb, int32_t Bw,
+    int32_t Bh, unsigned long long *__restrict__ hrep, unsigned long long *__restrict__ hlast, long long cut,
+    int32_t cap, PeakOut po, uint32_t *__restrict__ ticket)
 {
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
+    constexpr int kWpb = kVoteWpb<T, F>;
     extern __shared__ __align__(16) unsigned char smem[];
-    uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys]
+    uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
-    int32_t *s_q = reinterpret_cast<int32_t *>(s_h + kMfmaBins * kMfmaBins);         // [kWpb][kQueue]
-    int32_t *s_nrm = s_q + kWpb * kQueue;                                             // [kWpb][64]
+    uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
+    int32_t *s_q = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);              // [kWpb][kRing1]
+    int32_t *s_nrm = s_q + kWpb * kRing1;                                             // [kWpb][64]
+    __shared__ PeakScratch ps;
+    __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
-    for (int i = tid; i < kWKeys; i += blockDim.x) s_wt[i] = tb.wt_pk[i];
-    for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) s_h[i] = 0ull;
-    __syncthreads();
-
-    f16x8 pxh[KS], pxl[KS], pyh[KS], pyl[KS];
+    {
+        constexpr int kThreads = kWpb * 64, kN = kWKeys / 4, kPer = (kN + kThreads - 1) / kThreads;
+        u32x4 w[kPer];
 #pragma unroll
-    for (int j = 0; j < KS; j++) {
-        pxh[j] = palette_operand(tb.qx, ln, j, g);
-        pxl[j] = palette_operand(tb.qx + 1024, ln, j, g);
-        pyh[j] = palette_operand(tb.qy, ln, j, g);
-        pyl[j] = palette_operand(tb.qy + 1024, ln, j, g);
+        for (int k = 0; k < kPer; k++) {
+            const int i = k * kThreads + tid;
+            w[k] = reinterpret_cast<const u32x4 *>(tb.wt_pk)[i < kN ? i : 0];
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; k++) {
+            const int i = k * kThreads + tid;
+            if (i < kN) reinterpret_cast<u32x4 *>(s_wt)[i] = w[k];
+        }
+        for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_h[i] = 0ull;
+        for (int i = tid; i < kPopBytes / 16; i += kThreads)
+            reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
     }
+    __syncthreads();
     const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
 
-    int32_t *q = s_q + wv * kQueue;
+    int32_t *q = s_q + wv * kRing1;
     int32_t *nrm = s_nrm + wv * 64;
     f32x16 acc2 = {}, acc1 = {}, acc0 = {};
     int ntile = 0;
@@ -327,7 +387,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         }
     };
 
-    // Packed weights of the 16 (pixel, bin) results of one axis.
+    // Packed weight limbs of the 16 (pixel, bin) results of one axis.
     auto weights = [&](const f32x16 &ah, const f32x16 &al, int nbase, uint32_t np1, uint32_t (&e)[16]) {
 #pragma unroll
         for (int r4 = 0; r4 < 4; r4++) {
@@ -354,16 +414,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         }
         uint32_t ex[16], ey[16];
         {
+            f16x8 ph[KS], pl[KS];
+#pragma unroll
+            for (int j = 0; j < KS; j++) {
+                ph[j] = palette_operand(s_pop, 0, 0, j, lane);
+                pl[j] = palette_operand(s_pop, 0, 1, j, lane);
+            }
             f32x16 ah, al;
-            axis_dot<T, KS, true>(X, pxh, pxl, ah, al);
+            axis_dot<T, KS, true>(X, ph, pl, ah, al);
             weights(ah, al, 0, np1x, ex);
         }
         {
+            f16x8 ph[KS], pl[KS];
+#pragma unroll
+            for (int j = 0; j < KS; j++) {
+                ph[j] = palette_operand(s_pop, 1, 0, j, lane);
+                pl[j] = palette_operand(s_pop, 1, 1, j, lane);
+            }
             f32x16 ah, al;
-            axis_dot<T, KS, true>(Y, pyh, pyl, ah, al);
+            axis_dot<T, KS, true>(Y, ph, pl, ah, al);
             weights(ah, al, 32, np1y, ey);
         }
-        if (nvalid < 32) {
+        if (nvalid < 32) {        // pixels past the end of the queue vote nothing
 #pragma unroll
             for (int r = 0; r < 16; r++)
                 if (acc_row(r, g) >= nvalid) ex[r] = 0u;
@@ -393,36 +465,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         }
     };
 
-    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot] * D; };
+    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot & (kRing1 - 1)] * D; };
 
-    const int nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
-    const int nw = gridDim.x * kWpb;
-    int qn = 0;                      // queue length, < 32 between chunks
-    int c = blockIdx.x * kWpb + wv;
-    float fv[8];
-    if (c < nchunks) load_fg(fg, c, npix, lane, fv);
-    while (c < nchunks) {
-        qn = enqueue_chunk(fv, c, npix, fg_thr, lane, q, qn, [](int) {});   // qn <= 31 + 512 < kQueue
-        const int cn = c + nw;
-        if (cn < nchunks) load_fg(fg, cn, npix, lane, fv);
-        const int nt = qn >> 5;
-        if (nt > 0) {
-            RawSlices<T, F> raw;
-            raw.load(pixel_row(ln), g);
-            for (int t = 0; t < nt; t++) {
-                const RawSlices<T, F> cur = raw;
-                if (t + 1 < nt) raw.load(pixel_row(32 * (t + 1) + ln), g);
-                tile(cur, 32);
-            }
-            queue_shift(q, 32 * nt, qn - 32 * nt, lane);
-            qn -= 32 * nt;
-        }
-        c = cn;
+    // Consume the queue 32 pixels at a time; the rows of the next tile are
+    // loaded before the current one is computed, also across chunks.
+    ChunkFeed<T> feed;
+    feed.start(fg, npix, fg_thr, blockIdx.x * kWpb + wv, gridDim.x * kWpb, lane);
+    int head = 0, tail = 0;
+    bool pend = false;                      // raw holds the tile at head
+    RawSlices<T, F> raw;
+    for (;;) {
+        tail = feed.template top_up<kRing1, 64>(q, head, tail, lane, [](int) {});
+        const int avail = tail - head;
+        if (avail < 32) break;
+        if (!pend) raw.load(pixel_row(head + ln), g);
+        const RawSlices<T, F> cur = raw;
+        pend = avail >= 64;
+        if (pend) raw.load(pixel_row(head + 32 + ln), g);
+        tile(cur, 32);
+        head += 32;
     }
-    if (qn > 0) {
-        RawSlices<T, F> raw;
-        raw.load(pixel_row(ln < qn ? ln : 0), g);
-        tile(raw, qn);
+    if (tail > head) {
+        const int n = tail - head;
+        raw.load(pixel_row(head + (ln < n ? ln : 0)), g);
+        tile(raw, n);
     }
     fold();
 
@@ -434,6 +500,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         const int b = i / kMfmaBins, a = i % kMfmaBins;
         if (a < Bw && b < Bh && s_h[i]) atomicAdd(dst + b * Bw + a, s_h[i]);
     }
+
+    // The last workgroup to finish extracts the peaks.  Every wave waits for
+    // its own histogram atomics; one release fence per workgroup then orders
+    // them before its count.  Counting is two-level (workgroup b counts in
+    // group b % kTicketGroups, the last of each group in the top counter), so
+    // that no counter is hit by more than about gridDim / kTicketGroups
+    // atomics.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __syncthreads();
+    if (tid == 0) {
+        const int G = gridDim.x, k = blockIdx.x % kTicketGroups;
+        const int gsize = (G - k + kTicketGroups - 1) / kTicketGroups;
+        const int ngroups = G < kTicketGroups ? G : kTicketGroups;
+        bool last = false;
+        __threadfence();
+        if (atomicAdd(ticket + k, 1u) == (uint32_t)(gsize - 1)) {
+            __threadfence();
+            last = atomicAdd(ticket + kTicketGroups, 1u) == (uint32_t)(ngroups - 1);
+        }
+        s_last = last;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    peak_extract<2>(hrep, hlast, Bw, Bh, cut, cap, tb.cx, tb.cy, po, s_h, ps);
+    if (tid <= kTicketGroups) __hip_atomic_store(ticket + tid, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------------------
@@ -444,7 +536,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 // and y codes [32 bins][64 pixels] (u16).
 constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
                               (size_t)(kMaxBatch + 1) * 20 +
-                              (size_t)kWpb2 * (kQueue * 4 + kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
+                              (size_t)kWpb2 * (kRing2 * 4 + kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
 
 template <typename T, int F>
 __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const T *__restrict__ fg,
@@ -459,13 +551,13 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
     extern __shared__ __align__(16) unsigned char smem[];
-    u32x4 *s_bo = reinterpret_cast<u32x4 *>(smem);                                 // [kMaxBatch + 1]
+    uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                           // [kCKeys]
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatch + 1]
     uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch + 1);           // [kMaxBatch + 1]
-    uint16_t *s_ct = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch + 1);           // [kCKeys]
-    uint16_t *s_rank = s_ct + kCKeys;                                              // [32 * 32]
+    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch + 1);         // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);  // [1024]
-    int32_t *s_q = s_cnt + kMfmaBins * kMfmaBins;                                  // [kWpb2][kQueue]
-    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_q + kWpb2 * kQueue);          // [kWpb2][32][64]
+    int32_t *s_q = s_cnt + kMfmaBins * kMfmaBins;                                  // [kWpb2][kRing2]
+    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_q + kWpb2 * kRing2);          // [kWpb2][32][64]
     uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -477,7 +569,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     if (Kc == 0) {              // no centroid: every pixel is unlabelled
         for (int c = blockIdx.x * kWpb2 + wv; c < nchunks; c += nw)
 #pragma unroll
-            for (int i = 0; i < 8; i++) {
+            for (int i = 0; i < kChunkRows; i++) {
                 const int p = c * kChunk + 64 * i + lane;
                 if (p < npix) {
                     labels[p] = 0;
@@ -493,7 +585,15 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         s_bo[i] = (u32x4){bofs[4 * i], bofs[4 * i + 1], bofs[4 * i + 2], bofs[4 * i + 3]} & 0x1f00u;
         s_bh[i] = bhdr[i] & 0xf80u;
     }
-    for (int i = tid; i < kCKeys; i += blockDim.x) s_ct[i] = tb.ct_pm[i];
+    {
+        constexpr int kThreads = kWpb2 * 64;
+        u32x4 w[kCKeys / 8 / kThreads];
+#pragma unroll
+        for (int k = 0; k < kCKeys / 8 / kThreads; k++)
+            w[k] = reinterpret_cast<const u32x4 *>(tb.ct_pm)[k * kThreads + tid];
+#pragma unroll
+        for (int k = 0; k < kCKeys / 8 / kThreads; k++) reinterpret_cast<u32x4 *>(s_ct)[k * kThreads + tid] = w[k];
+    }
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
         s_rank[i] = rank[i];
         s_cnt[i] = 0;
@@ -503,19 +603,24 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     f16x8 pxh[KS], pxl[KS], pyh[KS], pyl[KS];
 #pragma unroll
     for (int j = 0; j < KS; j++) {
-        pxh[j] = palette_operand(tb.qx, ln, j, g);
-        pxl[j] = palette_operand(tb.qx + 1024, ln, j, g);
-        pyh[j] = palette_operand(tb.qy, ln, j, g);
-        pyl[j] = palette_operand(tb.qy + 1024, ln, j, g);
+        pxh[j] = palette_operand(tb.pop, 0, 0, j, lane);
+        pxl[j] = palette_operand(tb.pop, 0, 1, j, lane);
+        pyh[j] = palette_operand(tb.pop, 1, 0, j, lane);
+        pyl[j] = palette_operand(tb.pop, 1, 1, j, lane);
     }
     uint32_t npx[16], npy[16];
 #pragma unroll
-    for (int r = 0; r < 16; r++) {
-        npx[r] = tb.np1_x[acc_row(r, g)];
-        npy[r] = tb.np1_y[acc_row(r, g)];
+    for (int r4 = 0; r4 < 4; r4++) {
+        const u32x4 vx = *reinterpret_cast<const u32x4 *>(tb.np1_x + 8 * r4 + 4 * g);
+        const u32x4 vy = *reinterpret_cast<const u32x4 *>(tb.np1_y + 8 * r4 + 4 * g);
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            npx[4 * r4 + i] = vx[i];
+            npy[4 * r4 + i] = vy[i];
+        }
     }
 
-    int32_t *q = s_q + wv * kQueue;
+    int32_t *q = s_q + wv * kRing2;
     uint32_t *kx = s_kx + wv * kMfmaBins * 64;     // x key of bin a, pixel slot p: kx[a * 64 + p]
     uint16_t *cyb = s_cy + wv * kMfmaBins * 64;    // y code of bin b, pixel slot p: cyb[b * 64 + p]
 
@@ -574,7 +679,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
             hb = hn;
         }
         if (lane < nvalid) {
-            const int pix = q[base + lane];
+            const int pix = q[(base + lane) & (kRing2 - 1)];
             const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
             const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
             labels[pix] = k + 1;
@@ -584,44 +689,44 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot] * D; };
+    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot & (kRing2 - 1)] * D; };
     auto background = [&](int p) {
         labels[p] = 0;
         if (score_map) score_map[p] = 0.0f;
     };
 
-    int qn = 0;                      // queue length, < 64 between chunks
-    int c = blockIdx.x * kWpb2 + wv;
-    float fv[8];
-    if (c < nchunks) load_fg(fg, c, npix, lane, fv);
-    while (c < nchunks) {
-        qn = enqueue_chunk(fv, c, npix, fg_thr, lane, q, qn, background);   // qn <= 63 + 512 < kQueue
-        const int cn = c + nw;
-        if (cn < nchunks) load_fg(fg, cn, npix, lane, fv);
-        const int nt = (qn >> 6) * 2;    // tiles of the full groups of 64
-        if (nt > 0) {
-            RawSlices<T, F> raw;
-            raw.load(pixel_row(ln), g);
-            for (int t = 0; t < nt; t++) {
-                const RawSlices<T, F> cur = raw;
-                if (t + 1 < nt) raw.load(pixel_row(32 * (t + 1) + ln), g);
-                codes(cur, t & 1);
-                if (t & 1) search(32 * (t - 1), 64);
-            }
-            queue_shift(q, 32 * nt, qn - 32 * nt, lane);
-            qn -= 32 * nt;
-        }
-        c = cn;
+    // Consume the queue 64 pixels (two tiles) at a time; the rows of the next
+    // tile are loaded before the current one is computed, also across groups
+    // and chunks.
+    ChunkFeed<T> feed;
+    feed.start(fg, npix, fg_thr, blockIdx.x * kWpb2 + wv, nw, lane);
+    int head = 0, tail = 0;
+    bool pend = false;                      // raw holds the tile at head
+    RawSlices<T, F> raw;
+    for (;;) {
+        tail = feed.template top_up<kRing2, 128>(q, head, tail, lane, background);
+        const int avail = tail - head;
+        if (avail < 64) break;
+        if (!pend) raw.load(pixel_row(head + ln), g);
+        RawSlices<T, F> cur = raw;
+        raw.load(pixel_row(head + 32 + ln), g);
+        codes(cur, 0);
+        cur = raw;
+        pend = avail >= 128;
+        if (pend) raw.load(pixel_row(head + 64 + ln), g);
+        codes(cur, 1);
+        search(head, 64);
+        head += 64;
     }
-    if (qn > 0) {
-        RawSlices<T, F> raw;
-        raw.load(pixel_row(ln < qn ? ln : 0), g);
+    if (tail > head) {
+        const int n = tail - head;
+        raw.load(pixel_row(head + (ln < n ? ln : 0)), g);
         codes(raw, 0);
-        if (qn > 32) {
-            raw.load(pixel_row(32 + ln < qn ? 32 + ln : 0), g);
+        if (n > 32) {
+            raw.load(pixel_row(head + (32 + ln < n ? 32 + ln : 0)), g);
             codes(raw, 1);
         }
-        search(0, qn);
+        search(head, n);
     }
     __syncthreads();
     for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)

@@ -1,5 +1,5 @@
 // k_peaks.hpp -- local-maxima search and compaction (Section 3.2, "Local
-// Maxima Search"), one workgroup of 1024 threads per frame.
+// Maxima Search") by one workgroup.
 //
 // Sums the replicated vote histograms (and clears them for the next frame),
 // marks every bin whose count exceeds the threshold and every in-range
@@ -8,6 +8,9 @@
 // centroid records, the true count K, the compact peak list and, for grids up
 // to 32 x 32, the candidate batches and the bin -> centroid-index table used
 // by the matrix-core assignment kernel.
+//
+// For grids up to 32 x 32 this runs in the tail of the vote kernel, in the
+// last workgroup to finish; larger grids use the stand-alone kernel k_peaks.
 //
 // Candidate batches.  The first min(K, cap) peaks are grouped by row b into
 // batches of 4 columns (a row's last batch repeats its last column, which
@@ -27,38 +30,66 @@ struct PeakOut {
     cpe_centroid *cents;          // caller's centroid records [cap]
     int32_t *num;                 // caller's K
     int32_t *peaks;               // [cap] a | b << 16
-    int32_t *kinfo;               // [0] = min(K, cap), [1] = K
+    int32_t *kinfo;               // [0] = min(K, cap), [1] = K, [2] = candidate batches
     uint32_t *bofs;               // [kMaxBatch + 1][4] candidate batch column offsets
     uint32_t *bhdr;               // [kMaxBatch + 1] candidate batch row words
     uint16_t *rank;               // [32 * 32] centroid index of peak bin (a, b) at b * 32 + a
 };
 
-namespace {   // one private copy per translation unit that launches it
+// Block-level scratch of peak_extract (static LDS).
+struct PeakScratch {
+    int wave[16];
+    int base;
+    uint32_t rowmask[kMfmaBins];  // bit a of row b: (a, b) is one of the first min(K, cap) peaks
+    int nbt[kMfmaBins];
+};
 
-__global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__ hrep,
-                                                unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
-                                                long long cut, int32_t cap, const float *__restrict__ cx,
-                                                const float *__restrict__ cy, PeakOut po)
+// The whole extraction; every thread of the block calls it.  s_h: LDS
+// scratch of Bw * Bh u64.  The replicas are read with device-scope atomic
+// loads, so this is also correct in the workgroup that finishes the vote
+// kernel (after its acquire fence).  KU bins per thread are summed at a time
+// (KU x kReplicas loads in flight).
+template <int KU>
+__device__ __forceinline__ void peak_extract(unsigned long long *__restrict__ hrep,
+                                             unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
+                                             long long cut, int32_t cap, const float *__restrict__ cx,
+                                             const float *__restrict__ cy, const PeakOut &po,
+                                             unsigned long long *s_h, PeakScratch &ps)
 {
-    extern __shared__ __align__(16) unsigned char smem[];
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem);   // [nb]
-    __shared__ int s_wave[16];
-    __shared__ int s_base;
-    __shared__ uint32_t s_rowmask[kMfmaBins];   // bit a of row b: (a, b) is one of the first min(K, cap) peaks
-    __shared__ int s_nbt[kMfmaBins];
     const int tid = threadIdx.x;
     const int nb = Bw * Bh;
-    for (int i = tid; i < nb; i += blockDim.x) {
-        unsigned long long s = 0;
+    // KU bins per thread and pass, all their loads issued before any is used
+    // (out-of-range bins read bin 0 and are discarded)
+    constexpr int kU = KU;
+    for (int i0 = 0; i0 < nb; i0 += kU * (int)blockDim.x) {
+        int idx[kU];
 #pragma unroll
-        for (int r = 0; r < kReplicas; r++) s += hrep[(size_t)r * nb + i];
+        for (int u = 0; u < kU; u++) {
+            const int i = i0 + u * (int)blockDim.x + tid;
+            idx[u] = i < nb ? i : 0;
+        }
+        unsigned long long v[kReplicas][kU];
 #pragma unroll
-        for (int r = 0; r < kReplicas; r++) hrep[(size_t)r * nb + i] = 0ull;
-        s_h[i] = s;
-        hlast[i] = s;
+        for (int r = 0; r < kReplicas; r++)
+#pragma unroll
+            for (int u = 0; u < kU; u++)
+                v[r][u] = __hip_atomic_load(hrep + (size_t)r * nb + idx[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int u = 0; u < kU; u++) {
+            unsigned long long s = 0;
+#pragma unroll
+            for (int r = 0; r < kReplicas; r++) s += v[r][u];
+            const int i = i0 + u * (int)blockDim.x + tid;
+            if (i < nb) {
+#pragma unroll
+                for (int r = 0; r < kReplicas; r++) hrep[(size_t)r * nb + i] = 0ull;
+                s_h[i] = s;
+                hlast[i] = s;
+            }
+        }
     }
-    if (tid == 0) s_base = 0;
-    if (tid < kMfmaBins) s_rowmask[tid] = 0u;
+    if (tid == 0) ps.base = 0;
+    if (tid < kMfmaBins) ps.rowmask[tid] = 0u;
     __syncthreads();
 
     const bool small = Bw <= kMfmaBins && Bh <= kMfmaBins;
@@ -83,10 +114,10 @@ __global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__
         }
         const unsigned long long mask = __ballot(flag);
         const int before = lane_prefix(mask);
-        if (lane == 0) s_wave[wid] = __popcll(mask);
+        if (lane == 0) ps.wave[wid] = __popcll(mask);
         __syncthreads();
-        int off = s_base;
-        for (int w = 0; w < wid; w++) off += s_wave[w];
+        int off = ps.base;
+        for (int w = 0; w < wid; w++) off += ps.wave[w];
         if (flag) {
             const int pos = off + before;
             if (pos < cap) {
@@ -101,7 +132,7 @@ __global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__
                 po.cents[pos] = rec;
                 po.peaks[pos] = a | (b << 16);
                 if (small) {
-                    atomicOr(&s_rowmask[b], 1u << a);
+                    atomicOr(&ps.rowmask[b], 1u << a);
                     po.rank[b * kMfmaBins + a] = (uint16_t)pos;
                 }
             }
@@ -109,25 +140,25 @@ __global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__
         __syncthreads();
         if (tid == 0) {
             int tot = 0;
-            for (int w = 0; w < nwaves; w++) tot += s_wave[w];
-            s_base += tot;
+            for (int w = 0; w < nwaves; w++) tot += ps.wave[w];
+            ps.base += tot;
         }
         __syncthreads();
     }
     if (small) {                  // uniform: every thread takes the same branch
         // strict maxima are never horizontally adjacent: <= 16 per row, <= 4 batches
-        if (tid < kMfmaBins) s_nbt[tid] = min((__popc(s_rowmask[tid]) + 3) >> 2, kMaxBatch / kMfmaBins);
+        if (tid < kMfmaBins) ps.nbt[tid] = min((__popc(ps.rowmask[tid]) + 3) >> 2, kMaxBatch / kMfmaBins);
         __syncthreads();
         if (tid < kMfmaBins) {
             const int b = tid;
             int start = 0, total = 0;
             for (int r = 0; r < kMfmaBins; r++) {
-                const int n = s_nbt[r];
+                const int n = ps.nbt[r];
                 start += r < b ? n : 0;
                 total += n;
             }
-            uint32_t m = s_rowmask[b], last = 0;
-            const int nbt = s_nbt[b];
+            uint32_t m = ps.rowmask[b], last = 0;
+            const int nbt = ps.nbt[b];
             for (int j = 0; j < nbt; j++) {
                 uint32_t o[4];
                 for (int s = 0; s < 4; s++) {
@@ -152,10 +183,22 @@ __global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__
         }
     }
     if (tid == 0) {
-        *po.num = s_base;
-        po.kinfo[0] = s_base < cap ? s_base : cap;
-        po.kinfo[1] = s_base;
+        *po.num = ps.base;
+        po.kinfo[0] = ps.base < cap ? ps.base : cap;
+        po.kinfo[1] = ps.base;
     }
+}
+
+namespace {   // one private copy per translation unit that launches it
+
+__global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__ hrep,
+                                                unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
+                                                long long cut, int32_t cap, const float *__restrict__ cx,
+                                                const float *__restrict__ cy, PeakOut po)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ PeakScratch ps;
+    peak_extract<1>(hrep, hlast, Bw, Bh, cut, cap, cx, cy, po, reinterpret_cast<unsigned long long *>(smem), ps);
 }
 
 }  // namespace

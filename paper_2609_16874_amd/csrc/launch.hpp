@@ -9,6 +9,11 @@
 
 namespace cpe {
 
+// Grid caps of the matrix-core kernels: one resident vote workgroup (8 or 12
+// waves) and one assignment workgroup of 8 waves per compute unit.
+constexpr int64_t kVoteGrid = 256;
+constexpr int64_t kAssignGrid = 256;
+
 // Largest pixel tile (threads per block) whose LDS footprint fits the budget.
 inline int pick_tile(size_t fixed, size_t per_px, size_t budget)
 {
@@ -36,14 +41,23 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
     };
     const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;
     const int64_t chunks = ((int64_t)npix + kChunk - 1) / kChunk;
-    const int64_t wgs = (chunks + kWpb - 1) / kWpb;
     const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
 
+    PeakOut po{cents, num, h->peaks, h->kinfo, h->bofs, h->bhdr, h->rank};
     mark(0);
     if (mfma) {
-        const int grid = (int)(wgs < 768 ? wgs : 768);
-        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(kWpb * 64), kVoteLds, stream, e, g, npix, fg_thr,
-                           h->tb, Bw, Bh, h->hrep);
+        // recovery + voting, and the peak extraction in the last workgroup
+        constexpr int wpb = kVoteWpb<T, F>;
+        const int64_t wgs = (chunks + wpb - 1) / wpb;
+        const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
+        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), kVoteLds(wpb), stream, e, g, npix, fg_thr,
+                           h->tb, Bw, Bh, h->hrep, h->hlast, cut, h->cap, po, h->ticket);
+        mark(1);
+        mark(2);
+        const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
+        const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
+        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), kAssignLds, stream, e, g, npix,
+                           fg_thr, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
@@ -52,26 +66,16 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const int grid = (int)(tiles < 1024 ? tiles : 1024);
         hipLaunchKernelGGL((k_vote_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb, Bw,
                            Bh, h->hrep);
-    }
-    mark(1);
-
-    PeakOut po{cents, num, h->peaks, h->kinfo, h->bofs, h->bhdr, h->rank};
-    hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8, stream, h->hrep, h->hlast, Bw, Bh, cut, h->cap,
-                       h->tb.cx, h->tb.cy, po);
-    mark(2);
-
-    if (mfma) {
-        const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
-        const int grid = (int)(wgs2 < 256 ? wgs2 : 256);
-        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid), dim3(kWpb2 * 64), kAssignLds, stream, e, g, npix,
-                           fg_thr, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
-    } else {
-        const size_t fixed = tables + 16 + kCountCap * 4 + kCKeys * 2;
-        const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
-        const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 4;
-        const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
-        const int grid = (int)(tiles < 2048 ? tiles : 2048);
-        hipLaunchKernelGGL((k_assign_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb,
+        mark(1);
+        hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8, stream, h->hrep, h->hlast, Bw, Bh, cut,
+                           h->cap, h->tb.cx, h->tb.cy, po);
+        mark(2);
+        const size_t fixed2 = tables + 16 + kCountCap * 4 + kCKeys * 2;
+        const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
+        const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
+        const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
+        const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
+        hipLaunchKernelGGL((k_assign_generic<T, F>), dim3(grid2), dim3(tp2), lds2, stream, e, g, npix, fg_thr, h->tb,
                            Bw, Bh, h->peaks, h->kinfo, cents, labels, score);
     }
     mark(3);
