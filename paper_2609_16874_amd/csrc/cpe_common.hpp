@@ -15,7 +15,7 @@ constexpr int kWMant = 8;             // weight bucket: top 8 mantissa bits of f
 constexpr int kCMant = 9;             // code bucket: top 9 mantissa bits
 constexpr int kWKeys = 32 << kWMant;  // 8192 weight buckets (32 binades)
 constexpr int kCKeys = 32 << kCMant;  // 16384 code buckets
-constexpr int kReplicas = 16;         // replicated global histograms (spread of the atomics)
+constexpr int kReplicas = 4;          // replicated global histograms (spread of the atomics)
 constexpr int kMaxF = 16;             // harmonics per axis
 constexpr int kMaxBins = 128;
 constexpr int kCountCap = 1024;       // centroids whose pixel counts are privatised in LDS

@@ -47,8 +47,8 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kChunk = 128;          // pixels scanned per chunk
 constexpr int kChunkRows = kChunk / 64;
 constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
-constexpr int kRing1 = 256;          // per-wave ring queues of participating pixels (powers of two):
-constexpr int kRing2 = 512;          //   vote kernel (refilled below 64), assignment kernel (below 128)
+constexpr int kRound1 = 24;          // chunks per workgroup and round, at most: vote kernel
+constexpr int kRound2 = 32;          //   assignment kernel
 constexpr int kPopBytes = 2 * 2 * 2 * 64 * 16;   // palette operands of both axes, limbs and K-steps
 constexpr int kTicketGroups = 16;    // first level of the vote kernel's completion count
 
@@ -247,69 +247,121 @@ __device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npi
     }
 }
 
-// Ballot-compact the participating pixels of chunk c into the ring queue at
-// positions tail, tail + 1, ...; returns the new tail.  `background(p)` runs
-// for every in-range pixel that does not participate.
-template <int RING, typename BG>
-__device__ __forceinline__ int enqueue_chunk(const float (&fv)[kChunkRows], int c, int npix, float fg_thr, int lane,
-                                             int32_t *q, int tail, BG background)
-{
-#pragma unroll
-    for (int i = 0; i < kChunkRows; i++) {
-        const int p = c * kChunk + 64 * i + lane;
-        const bool f = p < npix && fv[i] > fg_thr;
-        if (p < npix && !f) background(p);
-        const unsigned long long m = __ballot(f);
-        if (f) q[(tail + lane_prefix(m)) & (RING - 1)] = p;
-        tail += __popcll(m);
-    }
-    return tail;
-}
-
-// One wave's stream of chunks c0, c0 + stride, ... feeding a ring queue: the
-// foreground values of the next chunk are always in flight while the queue
-// is being consumed.
-template <typename T>
-struct ChunkFeed {
+// Rounds.  Workgroup b owns the chunks b, b + G, b + 2G, ... (G = gridDim.x),
+// spread over the whole frame, and takes them in equal rounds of at most
+// ROUND chunks.  In a round
+// every wave scans its share of the chunks and appends the participating
+// pixels to one list in LDS (a slot reservation per 64-pixel row); after a
+// barrier the waves take 32- or 64-pixel tiles of the list from a counter in
+// LDS, so that all of them finish within about one tile of each other however
+// the foreground is distributed and however the SIMDs favour older waves.
+// The foreground values of a wave's next-round chunks are loaded while the
+// current round is being processed.
+template <typename T, int WPB, int ROUND>
+struct RoundScan {
+    static constexpr int kPer = (ROUND + WPB - 1) / WPB;    // chunks per wave and round, at most
+    static constexpr int kList = ROUND * kChunk;            // participating pixels of a round, at most
     const T *fg;
-    int npix, nchunks, stride, c;
+    int npix, nchunks, my_chunks, nrounds, per, wv;
     float fg_thr;
-    float fv[kChunkRows];
+    float fv[kPer][kChunkRows];             // foreground values of the wave's next chunks
 
-    __device__ __forceinline__ void start(const T *fg_, int npix_, float thr, int c0, int stride_, int lane)
+    __device__ __forceinline__ void start(const T *fg_, int npix_, float thr, int wv_, int lane)
     {
         fg = fg_;
         npix = npix_;
         fg_thr = thr;
+        wv = wv_;
         nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
-        stride = stride_;
-        c = c0;
-        if (c < nchunks) load_fg(fg, c, npix, lane, fv);
+        my_chunks = nchunks > (int)blockIdx.x ? (nchunks - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
+        nrounds = (my_chunks + ROUND - 1) / ROUND;
+        per = nrounds ? (my_chunks + nrounds - 1) / nrounds : 0;   // <= ROUND
+        prefetch(0, lane);
     }
-    __device__ __forceinline__ bool more() const { return c < nchunks; }
-    // Enqueue chunks until the queue holds at least WANT pixels or the
-    // stream ends; the queue never exceeds WANT - 1 + kChunk entries.
-    template <int RING, int WANT, typename BG>
-    __device__ __forceinline__ int top_up(int32_t *q, int head, int tail, int lane, BG background)
+    // chunk scanned by this wave in round r, slot u (-1 if none)
+    __device__ __forceinline__ int chunk(int r, int u) const
     {
-        static_assert(WANT - 1 + kChunk <= RING, "ring queue too small");
-        while (tail - head < WANT && c < nchunks) {
-            tail = enqueue_chunk<RING>(fv, c, npix, fg_thr, lane, q, tail, background);
-            c += stride;
-            if (c < nchunks) load_fg(fg, c, npix, lane, fv);
+        const int i = wv + u * WPB, k = r * per + i;
+        return (i < per && k < my_chunks) ? (int)blockIdx.x + k * (int)gridDim.x : -1;
+    }
+    __device__ __forceinline__ void prefetch(int r, int lane)
+    {
+#pragma unroll
+        for (int u = 0; u < kPer; u++) {
+            const int c = r < nrounds ? chunk(r, u) : -1;
+            if (c >= 0) {
+                load_fg(fg, c, npix, lane, fv[u]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < kChunkRows; i++) fv[u][i] = 0.0f;
+            }
         }
-        return tail;
+    }
+    // Append this wave's participating pixels of round r to list[], counting
+    // in *count (LDS): one reservation per chunk (PER_CHUNK) or per 64-pixel
+    // row (fewer live registers).  `background(p)` runs for every other
+    // in-range pixel.
+    template <bool PER_CHUNK, typename BG>
+    __device__ __forceinline__ void scan(int r, int32_t *list, int *count, int lane, BG background)
+    {
+#pragma unroll
+        for (int u = 0; u < kPer; u++) {
+            const int c = chunk(r, u);
+            if (c < 0) continue;
+            if constexpr (PER_CHUNK) {
+                unsigned long long m[kChunkRows];
+                int total = 0;
+#pragma unroll
+                for (int i = 0; i < kChunkRows; i++) {
+                    const int p = c * kChunk + 64 * i + lane;
+                    const bool f = p < npix && fv[u][i] > fg_thr;
+                    if (p < npix && !f) background(p);
+                    m[i] = __ballot(f);
+                    total += __popcll(m[i]);
+                }
+                int base = 0;
+                if (lane == 0 && total) base = atomicAdd(count, total);
+                base = __builtin_amdgcn_readfirstlane(base);
+#pragma unroll
+                for (int i = 0; i < kChunkRows; i++) {
+                    if ((m[i] >> lane) & 1ull) list[base + lane_prefix(m[i])] = c * kChunk + 64 * i + lane;
+                    base += __popcll(m[i]);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < kChunkRows; i++) {
+                    const int p = c * kChunk + 64 * i + lane;
+                    const bool f = p < npix && fv[u][i] > fg_thr;
+                    if (p < npix && !f) background(p);
+                    const unsigned long long m = __ballot(f);
+                    int base = 0;
+                    if (lane == 0 && m) base = atomicAdd(count, __popcll(m));
+                    base = __builtin_amdgcn_readfirstlane(base);
+                    if (f) list[base + lane_prefix(m)] = p;
+                }
+            }
+        }
     }
 };
+
+// Next tile (or group) index of the round from an LDS counter, wave-uniform.
+__device__ __forceinline__ int take_next(int *counter, int lane)
+{
+    int k = 0;
+    if (lane == 0) k = atomicAdd(counter, 1);
+    return __builtin_amdgcn_readfirstlane(k);
+}
 
 // ---------------------------------------------------------------------------
 // Pass 1: recovery + soft voting (+ the peak extraction in the last workgroup)
 // ---------------------------------------------------------------------------
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
-// and per wave a ring queue and the squared norms of one tile.
+// the palette operands, the round's pixel list, and per wave the squared
+// norms of one tile.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * kRing1 * 4 + (size_t)wpb * 64 * 4;
+    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)kRound1 * kChunk * 4 +
+           (size_t)wpb * 64 * 4;
 }
 
 // Waves per SIMD the register allocation must allow: three for fp16 inputs
@@ -340,10 +392,11 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
-    int32_t *s_q = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);              // [kWpb][kRing1]
-    int32_t *s_nrm = s_q + kWpb * kRing1;                                             // [kWpb][64]
+    int32_t *s_list = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);           // [kRound1 * kChunk]
+    int32_t *s_nrm = s_list + kRound1 * kChunk;                                       // [kWpb][64]
     __shared__ PeakScratch ps;
     __shared__ int s_last;
+    __shared__ int s_count[2], s_take[2];   // round list length, next tile (by round parity)
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -361,13 +414,16 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             if (i < kN) reinterpret_cast<u32x4 *>(s_wt)[i] = w[k];
         }
         for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_h[i] = 0ull;
+        if (tid < 2) {
+            s_count[tid] = 0;
+            s_take[tid] = 0;
+        }
         for (int i = tid; i < kPopBytes / 16; i += kThreads)
             reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
     }
     __syncthreads();
     const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
 
-    int32_t *q = s_q + wv * kRing1;
     int32_t *nrm = s_nrm + wv * 64;
     f32x16 acc2 = {}, acc1 = {}, acc0 = {};
     int ntile = 0;
@@ -465,30 +521,34 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot & (kRing1 - 1)] * D; };
-
-    // Consume the queue 32 pixels at a time; the rows of the next tile are
-    // loaded before the current one is computed, also across chunks.
-    ChunkFeed<T> feed;
-    feed.start(fg, npix, fg_thr, blockIdx.x * kWpb + wv, gridDim.x * kWpb, lane);
-    int head = 0, tail = 0;
-    bool pend = false;                      // raw holds the tile at head
+    RoundScan<T, kWpb, kRound1> rs;
+    rs.start(fg, npix, fg_thr, wv, lane);
     RawSlices<T, F> raw;
-    for (;;) {
-        tail = feed.template top_up<kRing1, 64>(q, head, tail, lane, [](int) {});
-        const int avail = tail - head;
-        if (avail < 32) break;
-        if (!pend) raw.load(pixel_row(head + ln), g);
-        const RawSlices<T, F> cur = raw;
-        pend = avail >= 64;
-        if (pend) raw.load(pixel_row(head + 32 + ln), g);
-        tile(cur, 32);
-        head += 32;
-    }
-    if (tail > head) {
-        const int n = tail - head;
-        raw.load(pixel_row(head + (ln < n ? ln : 0)), g);
-        tile(raw, n);
+    for (int r = 0; r < rs.nrounds; r++) {
+        const int par = r & 1;
+        if (tid == 0) {                  // the other parity's counters were last used in round r - 1
+            s_count[par ^ 1] = 0;
+            s_take[par ^ 1] = 0;
+        }
+        rs.template scan<false>(r, s_list, &s_count[par], lane, [](int) {});
+        rs.prefetch(r + 1, lane);
+        __syncthreads();
+        const int n = s_count[par], ntiles = (n + 31) >> 5;
+        // lane m of a tile reads list entry 32 j + m (entry 32 j past the end)
+        auto pixel_row = [&](int j) {
+            const int i = 32 * j + ln;
+            return emb + (size_t)s_list[i < n ? i : 32 * j] * D;
+        };
+        int j = take_next(&s_take[par], lane);
+        if (j < ntiles) raw.load(pixel_row(j), g);
+        while (j < ntiles) {
+            const int jn = take_next(&s_take[par], lane);
+            const RawSlices<T, F> cur = raw;
+            if (jn < ntiles) raw.load(pixel_row(jn), g);
+            tile(cur, min(32, n - 32 * j));
+            j = jn;
+        }
+        __syncthreads();                 // the list is rewritten in the next round
     }
     fold();
 
@@ -535,8 +595,8 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // candidate batches, and per wave a queue, x keys [32 bins][64 pixels] (u32)
 // and y codes [32 bins][64 pixels] (u16).
 constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                              (size_t)(kMaxBatch + 1) * 20 +
-                              (size_t)kWpb2 * (kRing2 * 4 + kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
+                              (size_t)(kMaxBatch + 1) * 20 + (size_t)kRound2 * kChunk * 4 +
+                              (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
 
 template <typename T, int F>
 __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const T *__restrict__ fg,
@@ -556,8 +616,8 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch + 1);           // [kMaxBatch + 1]
     uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch + 1);         // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);  // [1024]
-    int32_t *s_q = s_cnt + kMfmaBins * kMfmaBins;                                  // [kWpb2][kRing2]
-    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_q + kWpb2 * kRing2);          // [kWpb2][32][64]
+    int32_t *s_list = s_cnt + kMfmaBins * kMfmaBins;                               // [kRound2 * kChunk]
+    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_list + kRound2 * kChunk);      // [kWpb2][32][64]
     uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -594,9 +654,14 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
 #pragma unroll
         for (int k = 0; k < kCKeys / 8 / kThreads; k++) reinterpret_cast<u32x4 *>(s_ct)[k * kThreads + tid] = w[k];
     }
+    __shared__ int s_count[2], s_take[2];   // round list length, next tile (by round parity)
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
         s_rank[i] = rank[i];
         s_cnt[i] = 0;
+    }
+    if (tid < 2) {
+        s_count[tid] = 0;
+        s_take[tid] = 0;
     }
     __syncthreads();
 
@@ -620,7 +685,6 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         }
     }
 
-    int32_t *q = s_q + wv * kRing2;
     uint32_t *kx = s_kx + wv * kMfmaBins * 64;     // x key of bin a, pixel slot p: kx[a * 64 + p]
     uint16_t *cyb = s_cy + wv * kMfmaBins * 64;    // y code of bin b, pixel slot p: cyb[b * 64 + p]
 
@@ -658,7 +722,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     // keys plus the row's y key.  The row word 128 b is both the byte offset
     // of row b in the y-code array and the row's bits of the key.  The batch
     // list is read one entry ahead.
-    auto search = [&](int base, int nvalid) {
+    auto search = [&](const int32_t *grp, int nvalid) {
         __builtin_amdgcn_wave_barrier();
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + lane);
         const unsigned char *cyl = reinterpret_cast<const unsigned char *>(cyb + lane);
@@ -679,7 +743,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
             hb = hn;
         }
         if (lane < nvalid) {
-            const int pix = q[(base + lane) & (kRing2 - 1)];
+            const int pix = grp[lane];
             const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
             const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
             labels[pix] = k + 1;
@@ -689,44 +753,44 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    auto pixel_row = [&](int slot) { return emb + (size_t)q[slot & (kRing2 - 1)] * D; };
     auto background = [&](int p) {
         labels[p] = 0;
         if (score_map) score_map[p] = 0.0f;
     };
 
-    // Consume the queue 64 pixels (two tiles) at a time; the rows of the next
-    // tile are loaded before the current one is computed, also across groups
-    // and chunks.
-    ChunkFeed<T> feed;
-    feed.start(fg, npix, fg_thr, blockIdx.x * kWpb2 + wv, nw, lane);
-    int head = 0, tail = 0;
-    bool pend = false;                      // raw holds the tile at head
+    RoundScan<T, kWpb2, kRound2> rs;
+    rs.start(fg, npix, fg_thr, wv, lane);
     RawSlices<T, F> raw;
-    for (;;) {
-        tail = feed.template top_up<kRing2, 128>(q, head, tail, lane, background);
-        const int avail = tail - head;
-        if (avail < 64) break;
-        if (!pend) raw.load(pixel_row(head + ln), g);
-        RawSlices<T, F> cur = raw;
-        raw.load(pixel_row(head + 32 + ln), g);
-        codes(cur, 0);
-        cur = raw;
-        pend = avail >= 128;
-        if (pend) raw.load(pixel_row(head + 64 + ln), g);
-        codes(cur, 1);
-        search(head, 64);
-        head += 64;
-    }
-    if (tail > head) {
-        const int n = tail - head;
-        raw.load(pixel_row(head + (ln < n ? ln : 0)), g);
-        codes(raw, 0);
-        if (n > 32) {
-            raw.load(pixel_row(head + (32 + ln < n ? 32 + ln : 0)), g);
-            codes(raw, 1);
+    for (int r = 0; r < rs.nrounds; r++) {
+        const int par = r & 1;
+        if (tid == 0) {                  // the other parity's counters were last used in round r - 1
+            s_count[par ^ 1] = 0;
+            s_take[par ^ 1] = 0;
         }
-        search(head, n);
+        rs.template scan<true>(r, s_list, &s_count[par], lane, background);
+        rs.prefetch(r + 1, lane);
+        __syncthreads();
+        const int n = s_count[par], ngroups = (n + 63) >> 6;
+        // group j = list entries 64 j .. 64 j + 63; lane m of its half h reads
+        // entry 64 j + 32 h + m (entry 64 j past the end)
+        auto pixel_row = [&](int j, int h) {
+            const int i = 64 * j + 32 * h + ln;
+            return emb + (size_t)s_list[i < n ? i : 64 * j] * D;
+        };
+        int j = take_next(&s_take[par], lane);
+        if (j < ngroups) raw.load(pixel_row(j, 0), g);
+        while (j < ngroups) {
+            const int jn = take_next(&s_take[par], lane);
+            RawSlices<T, F> cur = raw;
+            raw.load(pixel_row(j, 1), g);
+            codes(cur, 0);
+            cur = raw;
+            if (jn < ngroups) raw.load(pixel_row(jn, 0), g);
+            codes(cur, 1);
+            search(s_list + 64 * j, min(64, n - 64 * j));
+            j = jn;
+        }
+        __syncthreads();                 // the list is rewritten in the next round
     }
     __syncthreads();
     for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)
