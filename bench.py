@@ -32,6 +32,37 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E peak, GB/s
 GOLDEN = os.path.join(ROOT, "tests", "golden", "configs.json")
+TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+STAGE_KERNEL = {"recover_vote": "k_vote_mfma", "assign_label": "k_assign_mfma"}
+
+
+def source_sha256():
+    """Hash of the library sources, as recorded with the profiler byte counts."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2609_16874_amd", "csrc", "*.hpp")) +
+                   glob.glob(os.path.join(ROOT, "paper_2609_16874_amd", "csrc", "*.hip")) +
+                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload_tag, stage):
+    """HBM bytes per launch of the stage's kernel from the committed profiler
+    counts (FETCH_SIZE and WRITE_SIZE scaled by a copy calibration), or None
+    when they are missing or were taken on different sources."""
+    try:
+        with open(TRAFFIC) as fh:
+            t = json.load(fh)
+        if t["source_sha256"] != source_sha256():
+            return None
+        return t["workloads"][workload_tag]["kernels"][STAGE_KERNEL[stage]]["bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def thresholds():
@@ -239,7 +270,8 @@ def main():
         "config": {"workload": spec.name, "frames_per_step": nfr, "H": spec.H, "W": spec.W, "D": spec.D,
                    "input_dtype": spec.dtype, "bins": spec.bins, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("16x640x640", dom),
                      "bytes_per_launch": round(bytes_[dom]), "avg_launch_ms": round(dom_ms, 5)},
         "stages_ms": {k: round(v, 5) for k, v in stages.items()},
         "literal_roofline_frac": round(bytes_["literal"] / (ms_step / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
