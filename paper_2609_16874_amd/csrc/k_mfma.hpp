@@ -358,10 +358,19 @@ __device__ __forceinline__ int take_next(int *counter, int lane)
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
 // the palette operands, the round's pixel list, and per wave the squared
 // norms of one tile.
+// Small per-workgroup state of the vote kernel, kept in the dynamic LDS
+// block after the tables (static LDS would be placed first and offset every
+// table lookup).
+struct VoteState {
+    PeakScratch ps;
+    int last;
+    int count[2], take[2];      // round list length, next tile (by round parity)
+};
+
 constexpr size_t kVoteLds(int wpb)
 {
     return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)kRound1 * kChunk * 4 +
-           (size_t)wpb * 64 * 4;
+           (size_t)wpb * 64 * 4 + sizeof(VoteState);
 }
 
 // Waves per SIMD the register allocation must allow: three for fp16 inputs
@@ -388,15 +397,17 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
     constexpr int kWpb = kVoteWpb<T, F>;
-    extern __shared__ __align__(16) unsigned char smem[];
+    // All LDS is static, so that table addresses are compile-time constants.
+    __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
     int32_t *s_list = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);           // [kRound1 * kChunk]
     int32_t *s_nrm = s_list + kRound1 * kChunk;                                       // [kWpb][64]
-    __shared__ PeakScratch ps;
-    __shared__ int s_last;
-    __shared__ int s_count[2], s_take[2];   // round list length, next tile (by round parity)
+    VoteState &st = *reinterpret_cast<VoteState *>(s_nrm + kWpb * 64);
+    PeakScratch &ps = st.ps;
+    int &s_last = st.last;
+    int *s_count = st.count, *s_take = st.take;
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -491,7 +502,9 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             axis_dot<T, KS, true>(Y, ph, pl, ah, al);
             weights(ah, al, 32, np1y, ey);
         }
-        if (nvalid < 32) {        // pixels past the end of the queue vote nothing
+        if (nvalid < 32) {        // pixels past the end of the list vote nothing
+            // (kept a real branch: only the last tile of a round is partial)
+            __asm__ volatile("" ::: "memory");
 #pragma unroll
             for (int r = 0; r < 16; r++)
                 if (acc_row(r, g) >= nvalid) ex[r] = 0u;
@@ -594,7 +607,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // LDS bytes of k_assign_mfma: code table, bin -> centroid table, counts,
 // candidate batches, and per wave a queue, x keys [32 bins][64 pixels] (u32)
 // and y codes [32 bins][64 pixels] (u16).
-constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
+constexpr size_t kAssignLds = 16 + (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
                               (size_t)(kMaxBatch + 1) * 20 + (size_t)kRound2 * kChunk * 4 +
                               (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
 
@@ -610,7 +623,8 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
 {
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
-    extern __shared__ __align__(16) unsigned char smem[];
+    // All LDS is static, so that table addresses are compile-time constants.
+    __shared__ __align__(16) unsigned char smem[kAssignLds];
     uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                           // [kCKeys]
     u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatch + 1]
     uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch + 1);           // [kMaxBatch + 1]
@@ -654,7 +668,9 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
 #pragma unroll
         for (int k = 0; k < kCKeys / 8 / kThreads; k++) reinterpret_cast<u32x4 *>(s_ct)[k * kThreads + tid] = w[k];
     }
-    __shared__ int s_count[2], s_take[2];   // round list length, next tile (by round parity)
+    // round list length, next group (by round parity), after the per-wave
+    // arrays (static LDS would offset every table lookup)
+    int *s_count = reinterpret_cast<int *>(s_cy + kWpb2 * kMfmaBins * 64), *s_take = s_count + 2;
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
         s_rank[i] = rank[i];
         s_cnt[i] = 0;

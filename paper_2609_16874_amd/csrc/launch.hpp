@@ -50,13 +50,13 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         constexpr int wpb = kVoteWpb<T, F>;
         const int64_t wgs = (chunks + wpb - 1) / wpb;
         const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), kVoteLds(wpb), stream, e, g, npix, fg_thr,
+        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), 0, stream, e, g, npix, fg_thr,
                            h->tb, Bw, Bh, h->hrep, h->hlast, cut, h->cap, po, h->ticket);
         mark(1);
         mark(2);
         const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), kAssignLds, stream, e, g, npix,
+        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, g, npix,
                            fg_thr, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
