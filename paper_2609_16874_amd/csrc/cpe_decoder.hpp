@@ -22,7 +22,7 @@ struct cpe_decoder {
     unsigned long long *hlast;           // [nb]
     int32_t *peaks;                      // [cap] a | b << 16
     int32_t *kinfo;                      // [0] = min(K, cap), [1] = K, [2] = candidate batches
-    uint32_t *bofs;                      // [kMaxBatch + 1][4] candidate batch column offsets
+    uint32_t *bofs;                      // [kMaxBatch + 1][4] candidate batch column offsets (padded list)
     uint32_t *bhdr;                      // [kMaxBatch + 1] candidate batch row words
     uint16_t *rank;                      // [32 * 32]
     uint32_t *ticket;                    // [32] completion counters of the vote kernel (0 between frames)

@@ -608,7 +608,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // candidate batches, and per wave a queue, x keys [32 bins][64 pixels] (u32)
 // and y codes [32 bins][64 pixels] (u16).
 constexpr size_t kAssignLds = 16 + (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                              (size_t)(kMaxBatch + 1) * 20 + (size_t)kRound2 * kChunk * 4 +
+                              (size_t)kMaxBatch * 20 + (size_t)kRound2 * kChunk * 4 +
                               (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
 
 template <typename T, int F>
@@ -626,9 +626,9 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kAssignLds];
     uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                           // [kCKeys]
-    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatch + 1]
-    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch + 1);           // [kMaxBatch + 1]
-    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch + 1);         // [32 * 32]
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatch]
+    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch);               // [kMaxBatch]
+    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch);             // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);  // [1024]
     int32_t *s_list = s_cnt + kMfmaBins * kMfmaBins;                               // [kRound2 * kChunk]
     uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_list + kRound2 * kChunk);      // [kWpb2][32][64]
@@ -653,9 +653,9 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         return;
     }
 
-    const int nbat = min(kinfo[2], kMaxBatch);
+    const int nbat = min(kinfo[2], kMaxBatch);      // a multiple of 4
     // The offsets are masked to the per-wave arrays' extents (columns and rows < 32).
-    for (int i = tid; i <= nbat; i += blockDim.x) {
+    for (int i = tid; i < nbat; i += blockDim.x) {
         s_bo[i] = (u32x4){bofs[4 * i], bofs[4 * i + 1], bofs[4 * i + 2], bofs[4 * i + 3]} & 0x1f00u;
         s_bh[i] = bhdr[i] & 0xf80u;
     }
@@ -743,20 +743,20 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + lane);
         const unsigned char *cyl = reinterpret_cast<const unsigned char *>(cyb + lane);
         uint32_t best = 0xffffffffu;
-        u32x4 o = s_bo[0];
-        uint32_t hb = s_bh[0];
-        for (int i = 0; i < nbat; i++) {
-            const u32x4 on = s_bo[i + 1];
-            const uint32_t hn = s_bh[i + 1];
-            const uint32_t v0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
-            const uint32_t v1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
-            const uint32_t v2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
-            const uint32_t v3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
-            const uint32_t cy = *reinterpret_cast<const uint16_t *>(cyl + hb);
-            const uint32_t m = min(min(v0, v1), min(v2, v3));
-            best = min(best, m + ((cy << 14) | hb));
-            o = on;
-            hb = hn;
+        // four batches per step: their 20 reads are in flight together
+        for (int i = 0; i < nbat; i += 4) {
+            const u32x4 hb = *reinterpret_cast<const u32x4 *>(s_bh + i);
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const u32x4 o = s_bo[i + u];
+                const uint32_t v0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
+                const uint32_t v1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
+                const uint32_t v2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
+                const uint32_t v3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+                const uint32_t cy = *reinterpret_cast<const uint16_t *>(cyl + hb[u]);
+                const uint32_t m = min(min(v0, v1), min(v2, v3));
+                best = min(best, m + ((cy << 14) | hb[u]));
+            }
         }
         if (lane < nvalid) {
             const int pix = grp[lane];

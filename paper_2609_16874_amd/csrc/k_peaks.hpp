@@ -18,8 +18,7 @@
 // of its 4 columns in the assignment kernel's [bin][64 pixels] x-key array,
 // and bhdr[i] = 128 b, which is both the byte offset of row b in its
 // [bin][64 pixels] 16-bit y-code array and the row's bits of the search key.
-// Entry nbat (one past the last) is zero, so a one-ahead prefetch stays
-// inside the list.
+// The list is padded to a multiple of 4 batches with copies of its last one.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -31,8 +30,8 @@ struct PeakOut {
     int32_t *num;                 // caller's K
     int32_t *peaks;               // [cap] a | b << 16
     int32_t *kinfo;               // [0] = min(K, cap), [1] = K, [2] = candidate batches
-    uint32_t *bofs;               // [kMaxBatch + 1][4] candidate batch column offsets
-    uint32_t *bhdr;               // [kMaxBatch + 1] candidate batch row words
+    uint32_t *bofs;               // [kMaxBatch][4] candidate batch column offsets
+    uint32_t *bhdr;               // [kMaxBatch] candidate batch row words
     uint16_t *rank;               // [32 * 32] centroid index of peak bin (a, b) at b * 32 + a
 };
 
@@ -175,11 +174,16 @@ __device__ __forceinline__ void peak_extract(unsigned long long *__restrict__ hr
                 bo[3] = o[3];
                 po.bhdr[start + j] = (uint32_t)b * 128u;
             }
-            if (b == 0) {
-                for (int s = 0; s < 4; s++) po.bofs[(size_t)total * 4 + s] = 0u;
-                po.bhdr[total] = 0u;
-                po.kinfo[2] = total;
+            // pad the list to a multiple of 4 with copies of the last batch (a
+            // repeated batch leaves every minimum unchanged)
+            const int padded = (total + 3) & ~3;
+            if (nbt > 0 && start + nbt == total) {
+                for (int e = total; e < padded; e++) {
+                    for (int s = 0; s < 4; s++) po.bofs[(size_t)e * 4 + s] = po.bofs[(size_t)(total - 1) * 4 + s];
+                    po.bhdr[e] = po.bhdr[total - 1];
+                }
             }
+            if (b == 0) po.kinfo[2] = padded;
         }
     }
     if (tid == 0) {
