@@ -363,6 +363,7 @@ __device__ __forceinline__ int take_next(int *counter, int lane)
 // table lookup).
 struct VoteState {
     PeakScratch ps;
+    int pk[max_peaks(kMfmaBins, kMfmaBins)];   // compacted peak bins of the last workgroup
     int last;
     int count[2], take[2];      // round list length, next tile (by round parity)
 };
@@ -597,7 +598,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     __syncthreads();
     if (!s_last) return;
     __threadfence();
-    peak_extract<2>(hrep, hlast, Bw, Bh, cut, cap, tb.cx, tb.cy, po, s_h, ps);
+    peak_extract<2>(hrep, hlast, Bw, Bh, cut, cap, tb.cx, tb.cy, po, s_h, st.pk, ps);
     if (tid <= kTicketGroups) __hip_atomic_store(ticket + tid, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 

@@ -67,7 +67,8 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         hipLaunchKernelGGL((k_vote_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb, Bw,
                            Bh, h->hrep);
         mark(1);
-        hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8, stream, h->hrep, h->hlast, Bw, Bh, cut,
+        hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, stream,
+                           h->hrep, h->hlast, Bw, Bh, cut,
                            h->cap, h->tb.cx, h->tb.cy, po);
         mark(2);
         const size_t fixed2 = tables + 16 + kCountCap * 4 + kCKeys * 2;
