@@ -247,8 +247,10 @@ __device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npi
     }
 }
 
-// Rounds.  Workgroup b owns the chunks b, b + G, b + 2G, ... (G = gridDim.x),
-// spread over the whole frame, and takes them in equal rounds of at most
+// Rounds.  The chunks form blocks of G = gridDim.x consecutive chunks;
+// workgroup b owns chunk (b - k) mod G of block k, k = 0, 1, ..., so that its
+// chunks are spread over the rows of the frame and, shifting by one chunk per
+// block, over its columns as well.  It takes them in equal rounds of at most
 // ROUND chunks.  In a round
 // every wave scans its share of the chunks and appends the participating
 // pixels to one list in LDS (a slot reservation per 64-pixel row); after a
@@ -273,7 +275,8 @@ struct RoundScan {
         fg_thr = thr;
         wv = wv_;
         nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
-        my_chunks = nchunks > (int)blockIdx.x ? (nchunks - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x : 0;
+        const int G = gridDim.x, full = nchunks / G, rem = nchunks % G;
+        my_chunks = full + ((((int)blockIdx.x - full) % G + G) % G < rem ? 1 : 0);
         nrounds = (my_chunks + ROUND - 1) / ROUND;
         per = nrounds ? (my_chunks + nrounds - 1) / nrounds : 0;   // <= ROUND
         prefetch(0, lane);
@@ -282,7 +285,8 @@ struct RoundScan {
     __device__ __forceinline__ int chunk(int r, int u) const
     {
         const int i = wv + u * WPB, k = r * per + i;
-        return (i < per && k < my_chunks) ? (int)blockIdx.x + k * (int)gridDim.x : -1;
+        const int G = gridDim.x;
+        return (i < per && k < my_chunks) ? k * G + ((((int)blockIdx.x - k) % G) + G) % G : -1;
     }
     __device__ __forceinline__ void prefetch(int r, int lane)
     {
