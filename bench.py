@@ -166,12 +166,13 @@ def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
     return dict(zip(native.STAGES, (acc / n).tolist()))
 
 
-def bench_config(cfg, steps, warmup, n_frames=None):
+def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=None):
     from paper_2609_16874_amd import native
-    th = thresholds()[str(cfg)]
-    spec, frames, embs, fgs = load_workload(cfg, n_frames)
+    th = th or thresholds()[str(cfg)]
+    spec, frames, embs, fgs = loaded or load_workload(cfg, n_frames)
     fx, fy = spec.freqs()
-    dec = native.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, spec.bins, spec.bins, th["capacity"])
+    nb = bins or spec.bins
+    dec = native.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, nb, nb, th["capacity"])
     outs = [dec.new_outputs() for _ in frames]
     ms_step = time_steps(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], steps, warmup)
     stages = stage_times(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], max(1, min(steps, 10)))
@@ -199,6 +200,38 @@ def cpu_baseline(cfg, frames, budget_s=15.0):
             "sample": f"frames 0-{done - 1} of the {spec.name} batch, single-threaded C oracle, {dt:.1f} s"}
 
 
+# The paper's optimised decoder latency for its 704x704, L = 4 maps on a Jetson
+# Orin Nano in fp32 (Table 1), by bin count: context only, other hardware.
+PAPER_TABLE1_MS = {8: 2.13, 16: 6.13, 32: 30.66, 64: 101.37, 80: 144.00}
+
+
+def sweep(steps, warmup):
+    """Bin-count sweep (Table 1's grids) on workload 5, the paper's own
+    decoder shape, and the resolution series of every workload at 32x32."""
+    from paper_2609_16874_amd import synth
+    with open(GOLDEN) as fh:
+        sw = json.load(fh)["sweep"]
+    out = {"bins_sweep": [], "resolution": []}
+    loaded = load_workload(5)
+    for b in synth.SWEEP_BINS:
+        th = sw[str(b)]
+        s, fr, ms, st, by, ws = bench_config(5, steps, warmup, bins=b, th=th, loaded=loaded)
+        out["bins_sweep"].append({"workload": s.name, "bins": b, "ms_per_frame": round(ms, 5),
+                                  "frames_per_s": round(1000.0 / ms, 1), "workspace_bytes": ws,
+                                  "path": "matrix-core" if b <= 32 else "generic",
+                                  "stages_ms": {k: round(v, 5) for k, v in st.items()},
+                                  "paper_ms_orin_nano_fp32": PAPER_TABLE1_MS[b]})
+    del loaded
+    for cfg in sorted(synth.CONFIGS):
+        s, fr, ms, st, by, ws = bench_config(cfg, steps, warmup)
+        nfr = len(fr)
+        out["resolution"].append({"workload": s.name, "pixels": s.H * s.W, "D": s.D, "dtype": s.dtype,
+                                  "ms_per_frame": round(ms / nfr, 5), "frames_per_s": round(nfr * 1000.0 / ms, 1),
+                                  "literal_roofline_frac": round(by["literal"] / (ms / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                  "workspace_bytes": ws})
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -210,6 +243,8 @@ def main():
                     help="time only this config (0-4) and print its per-stage line; for profiler runs")
     ap.add_argument("--copy-calibration", type=int, default=None, metavar="MIB",
                     help="time a plain device copy of MIB MiB instead (reference for profiler byte counters)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="bin-count sweep at the paper's 704x704 D=16 shape and the resolution series instead")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the decoder has no multi-GPU path (frames are independent; "
@@ -234,6 +269,9 @@ def main():
         ms = t0.elapsed_time(t1) / args.steps
         print(json.dumps({"copy_bytes": n, "ms_per_copy": round(ms, 5),
                           "gbs_read_plus_write": round(2 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
+        return
+    if args.sweep:
+        print(json.dumps(sweep(args.steps, args.warmup)), flush=True)
         return
     if args.only_config is not None:
         cfg = args.only_config

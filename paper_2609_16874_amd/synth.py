@@ -91,7 +91,14 @@ CONFIGS = {
                  kind="mixed", n_inst=(150, 150), radius=(4.0, 200.0), radius_law="rowdep"),
     4: FrameSpec("16x 640x640 D64 f16 10-100 mixed", 640, 640, 16, "f16", 640.0, 640.0, 0.1,
                  n_frames=16, kind="mixed", n_inst=(10, 100), radius=(10.0, 120.0)),
+    # the paper's own decoder shape: 616x616 input -> 704x704 maps, L = 4
+    # harmonics per axis (D = 16) in fp32; used for the bin-count sweep
+    5: FrameSpec("704x704 D16 f32 50 mixed", 704, 704, 4, "f32", 704.0, 704.0, 0.1,
+                 kind="mixed", n_inst=(50, 50), radius=(10.0, 120.0)),
 }
+
+# bin counts of the sweep on workload 5 (Table 1 of the paper)
+SWEEP_BINS = (8, 16, 32, 64, 80)
 
 
 def rng_for(config: int, *extra: int) -> np.random.Generator:

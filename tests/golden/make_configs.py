@@ -2,7 +2,8 @@
 
 For workload c the threshold is 0.10 x the largest vote mass of the CPU
 oracle's histogram on the calibration frame (seed [260916874, c, 999]), so
-that a peak must collect at least a tenth of the strongest bin's votes.  Only
+that a peak must collect at least a tenth of the strongest bin's votes; the
+bin-count sweep of workload 5 gets one threshold per grid the same way.  Only
 the generator and the oracle are called.  Run from the repository root:
 
     python -m tests.golden.make_configs
@@ -30,6 +31,16 @@ def main():
             "peak_threshold": FRACTION * hmax * 2.0 ** -30,
         }
         print(c, out["configs"][str(c)])
+    # workload 5 at every bin count of the sweep: its own calibration per grid
+    out["sweep"] = {}
+    f = synth.make_frame(5, calibration=True)
+    for b in synth.SWEEP_BINS:
+        r = oracle.decode_frame(f, bins=b, peak_threshold=0.0)
+        hmax = int(r["hist"].max())
+        out["sweep"][str(b)] = {"config": 5, "bins": b, "capacity": ((b + 1) // 2) ** 2,
+                                "calibration_max_vote_mass": hmax * 2.0 ** -30,
+                                "peak_threshold": FRACTION * hmax * 2.0 ** -30}
+        print("sweep", b, out["sweep"][str(b)])
     with open(OUT, "w") as fh:
         json.dump(out, fh, indent=1)
 

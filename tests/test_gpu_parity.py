@@ -89,6 +89,23 @@ def test_workload_parity(cfg):
     assert_parity(got, ref, th["capacity"])
 
 
+@pytest.mark.parametrize("bins", list(synth.SWEEP_BINS))
+def test_paper_shape_bin_sweep_parity(bins):
+    """The paper's own decoder shape (704x704, L = 4 harmonics, fp32) at every
+    bin count of its Table 1 sweep, with the thresholds calibrated per grid:
+    grids up to 32x32 take the matrix-core kernels, larger ones the generic
+    kernels and the stand-alone peak kernel."""
+    spec = synth.CONFIGS[5]
+    with open(GOLDEN) as fh:
+        th = json.load(fh)["sweep"][str(bins)]
+    f = synth.make_frame(5)
+    fx, fy = spec.freqs()
+    print(f"config 5 {spec.name} bins {bins}", flush=True)
+    got, ref = run_pair(f.emb, f.fg, fx, fy, bins, bins, th["capacity"], spec.fg_threshold, th["peak_threshold"])
+    assert ref["K"] >= 1
+    assert_parity(got, ref, th["capacity"])
+
+
 def test_workload4_batch_back_to_back():
     """16 frames decoded back to back on one handle and one stream (the
     launch sequence the benchmark times), each compared with the oracle."""
