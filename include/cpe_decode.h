@@ -129,6 +129,53 @@ cpe_status cpe_decode(cpe_decoder *h, hipStream_t stream, const void *emb, const
                       cpe_centroid *centroids, int32_t *num_centroids, int32_t *labels,
                       float *score_map);
 
+/* Options of cpe_decode_ex. */
+typedef struct {
+    float fg_threshold;     /* as in cpe_decode; unused when fg is NULL          */
+    int32_t reserved;       /* must be 0                                         */
+    double peak_threshold;  /* as in cpe_decode                                  */
+    double tau;             /* Eq8 mask threshold in distance units; +INFINITY:
+                               none (every participating pixel is labelled)     */
+} cpe_decode_options;
+
+/*
+ * cpe_decode with the two options of Section 3.1 that the foreground channel
+ * otherwise replaces:
+ *   fg == NULL   every pixel of the frame participates (the participating set
+ *                of Eq6 is the whole output grid); otherwise as cpe_decode.
+ *   opt->tau     Eq8: a participating pixel keeps the label of its nearest
+ *                candidate m (Eq7) only if that distance is below tau, the
+ *                distance being the assignment code sum D_m = c_x + c_y in
+ *                units of 1/4096 (test: D_m < 4096 tau, strict).  A pixel
+ *                that fails gets label 0 and score 0 and is not counted in
+ *                npix.  tau <= 0 labels nothing; +INFINITY is cpe_decode.
+ * The histogram and the centroid records do not depend on tau.
+ * Errors as cpe_decode; NaN or -INFINITY tau, a non-finite threshold or a
+ * nonzero reserved field is CPE_ERR_INVALID_ARG.
+ */
+cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg,
+                         int32_t H, int32_t W, const cpe_decode_options *opt,
+                         cpe_centroid *centroids, int32_t *num_centroids, int32_t *labels,
+                         float *score_map);
+
+/*
+ * Binary instance masks M^_m of Eq8 from a label map written by cpe_decode or
+ * cpe_decode_ex on this handle, asynchronously on `stream`:
+ *   masks[m][p] = 1 if labels[p] == first + m + 1, else 0,
+ * for m = 0 .. count-1 and p = 0 .. H*W-1, one byte per pixel, mask m at
+ * byte offset m*H*W.  Mask m belongs to centroid first+m, i.e. to bin
+ * (bin_x, bin_y) of that record; indices at or past min(K, cap) give empty
+ * masks.  (The paper preallocates one mask per histogram bin; placing the
+ * masks of this call at slot bin_y*B_w + bin_x gives that layout.)
+ *   labels  device [H][W] int32, 16-byte aligned (caller-owned)
+ *   masks   device [count][H][W] uint8, 16-byte aligned (caller-owned)
+ *   first   >= 0; count >= 1; first + count <= centroid_capacity
+ * Errors: CPE_ERR_INVALID_ARG for a bad argument (before any work is
+ * enqueued), CPE_ERR_HIP for a failed launch.
+ */
+cpe_status cpe_decode_masks(cpe_decoder *h, hipStream_t stream, const int32_t *labels, int32_t H, int32_t W,
+                            int32_t first, int32_t count, uint8_t *masks);
+
 /* Release a decoder (waits for nothing; the caller must have synchronised
  * the streams that used it).  NULL is a no-op. */
 cpe_status cpe_decode_destroy(cpe_decoder *h);

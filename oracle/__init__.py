@@ -11,6 +11,7 @@ from __future__ import annotations
 
 import contextlib
 import ctypes
+import math
 import os
 import subprocess
 
@@ -70,6 +71,10 @@ def _bind(lib):
     lib.cpe_oracle_decode.restype = i32
     lib.cpe_oracle_decode.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
                                       ctypes.c_float, ctypes.c_double, P, P, P, P, P, P, P, P, P]
+    lib.cpe_oracle_decode_ex.restype = i32
+    lib.cpe_oracle_decode_ex.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
+                                         ctypes.c_float, ctypes.c_double, ctypes.c_double,
+                                         P, P, P, P, P, P, P, P, P]
     lib.cpe_oracle_decode_real.restype = i32
     lib.cpe_oracle_decode_real.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
                                            ctypes.c_float, ctypes.c_double, P, P, P, P]
@@ -89,13 +94,15 @@ def _dtype_code(a: np.ndarray) -> int:
 
 
 def decode(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,
-           fg_threshold=0.5, peak_threshold=0.0, *, want_score=True, check=True):
+           fg_threshold=0.5, peak_threshold=0.0, *, tau=math.inf, want_score=True, check=True):
     """Canonical decode.  Returns a dict with centroids (structured array of
     length min(K, capacity)), K, labels [H][W] int32, score_map, hist
-    [bins_h][bins_w] uint64, pal_x, pal_y, weights, codes (bucket tables)."""
+    [bins_h][bins_w] uint64, pal_x, pal_y, weights, codes (bucket tables).
+    fg=None: every pixel participates; tau: the Eq8 mask threshold in
+    distance units (inf: none)."""
     lib = _load()
     emb = np.ascontiguousarray(emb)
-    fg = np.ascontiguousarray(fg, dtype=emb.dtype)
+    fg = None if fg is None else np.ascontiguousarray(fg, dtype=emb.dtype)
     H, W, D = emb.shape
     fx = np.ascontiguousarray(freq_x, dtype=np.float64)
     fy = np.ascontiguousarray(freq_y, dtype=np.float64)
@@ -111,10 +118,10 @@ def decode(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,
     pal_y = np.empty((bins_h, 2 * F), dtype=np.int16)
     wt = np.empty(W_KEYS, dtype=np.uint16)
     ct = np.empty(C_KEYS, dtype=np.uint16)
-    rc = lib.cpe_oracle_decode(H, W, D, _dtype_code(emb), _ptr(emb), _ptr(fg), _ptr(fx), _ptr(fy), F,
-                               bins_w, bins_h, capacity, float(fg_threshold), float(peak_threshold),
-                               _ptr(cents), _ptr(K), _ptr(labels), _ptr(score), _ptr(hist),
-                               _ptr(pal_x), _ptr(pal_y), _ptr(wt), _ptr(ct))
+    rc = lib.cpe_oracle_decode_ex(H, W, D, _dtype_code(emb), _ptr(emb), _ptr(fg), _ptr(fx), _ptr(fy), F,
+                                  bins_w, bins_h, capacity, float(fg_threshold), float(peak_threshold),
+                                  float(tau), _ptr(cents), _ptr(K), _ptr(labels), _ptr(score), _ptr(hist),
+                                  _ptr(pal_x), _ptr(pal_y), _ptr(wt), _ptr(ct))
     if rc != 0:
         if check:
             raise ValueError(f"oracle rejected the arguments (code {rc})")

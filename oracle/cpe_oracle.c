@@ -22,7 +22,8 @@
  *                 rint(4096 cos(w_k x_a)), fp64, stored as int16
  *   input         X = rintf(4096.0f * clamp(v, -1.5, 1.5)), fp32, where a
  *                 NaN channel clamps to -1.5
- *   participation p in S  <=>  (float)fg(p) > fg_threshold
+ *   participation p in S  <=>  (float)fg(p) > fg_threshold; with no fg
+ *                 channel every pixel is in S (the set of Section 3.1)
  *   distance      S_x = sum_c (X_c - P[a][c])^2 (exact integer); with
  *                 u = fl32(S+1) = 2^e (1 + f), 0 <= f < 1, the m-bit bucket
  *                 of S is key_m(S) = e 2^m + floor(f 2^m) (exponent and top
@@ -36,6 +37,9 @@
  *                 8-neighbour; listed in ascending b*B_w + a
  *   assignment    D_k = c_x(a_k) + c_y(b_k) (integer); the smallest k with
  *                 the minimal D_k wins; label = k+1, background 0
+ *   mask test     (Eq8) the winner m keeps the pixel only if its distance
+ *                 D_m / 4096 is below tau (tau = +inf keeps every pixel of
+ *                 S); a pixel that fails it gets label 0 and is not counted
  *   score map     expf(-D_m / 4096) for labelled pixels
  *
  * Pins (tests/test_oracle_*.py), each independent of this file's code:
@@ -48,7 +52,10 @@
  *   - noise-free frames whose centroids sit on bin centres decode to the
  *     generating centroids and the generating label map;
  *   - invariants: labels partition the foreground, counts sum to |S|,
- *     peaks pairwise non-adjacent, instance-order independence.
+ *     peaks pairwise non-adjacent, instance-order independence;
+ *   - the Eq8 mask threshold and the all-pixels mode: the exhaustive search
+ *     with tau on attained code sums, a noise-free frame where a tau of half
+ *     a code unit keeps exactly the instance pixels, and nesting in tau.
  * The whole pipeline against the paper's own decoder: parity unpinned (no
  * implementation or worked example is published).
  */
@@ -161,14 +168,14 @@ static int64_t peak_cut(double theta)
     return (int64_t)t;
 }
 
-static int check_args(int32_t H, int32_t W, int32_t D, int32_t dtype, const void *emb, const void *fg,
+static int check_args(int32_t H, int32_t W, int32_t D, int32_t dtype, const void *emb,
                       const double *fx, const double *fy, int32_t n_freq, int32_t bw, int32_t bh,
                       int32_t cap, float fg_thr, double peak_thr)
 {
     if (H < 1 || W < 1 || (int64_t)H * (int64_t)W > 2147483647LL) return CPE_ORACLE_EINVAL;
     if (n_freq < 1 || n_freq > 16 || D != 4 * n_freq) return CPE_ORACLE_EINVAL;
     if (dtype != 0 && dtype != 1) return CPE_ORACLE_EINVAL;
-    if (!emb || !fg || !fx || !fy) return CPE_ORACLE_EINVAL;
+    if (!emb || !fx || !fy) return CPE_ORACLE_EINVAL;
     if (bw < 1 || bw > 128 || bh < 1 || bh > 128 || cap < 1) return CPE_ORACLE_EINVAL;
     if (isnan(fg_thr) || isnan(peak_thr)) return CPE_ORACLE_EINVAL;
     return CPE_ORACLE_OK;
@@ -201,6 +208,12 @@ static int is_peak_f64(const double *h, int32_t bw, int32_t bh, int32_t a, int32
     return 1;
 }
 
+/* p in S: the foreground test, or every pixel when there is no fg channel */
+static int participates(const void *fg, int32_t dtype, size_t p, float fg_threshold)
+{
+    return !fg || load_value(fg, dtype, p) > fg_threshold;
+}
+
 int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       const void *emb, const void *fg,
                       const double *freq_x, const double *freq_y, int32_t n_freq,
@@ -210,9 +223,24 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       int32_t *labels, float *score_map,
                       uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out, uint16_t *ct_out)
 {
-    if (check_args(H, W, D, dtype, emb, fg, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
+    if (!fg) return CPE_ORACLE_EINVAL;
+    return cpe_oracle_decode_ex(H, W, D, dtype, emb, fg, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
+                                fg_threshold, peak_threshold, INFINITY, centroids, num_centroids, labels,
+                                score_map, hist, pal_x, pal_y, wt_out, ct_out);
+}
+
+int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
+                         const void *emb, const void *fg,
+                         const double *freq_x, const double *freq_y, int32_t n_freq,
+                         int32_t bins_w, int32_t bins_h, int32_t capacity,
+                         float fg_threshold, double peak_threshold, double tau,
+                         cpe_oracle_centroid *centroids, int32_t *num_centroids,
+                         int32_t *labels, float *score_map,
+                         uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out, uint16_t *ct_out)
+{
+    if (check_args(H, W, D, dtype, emb, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
                    fg_threshold, peak_threshold) != CPE_ORACLE_OK ||
-        !centroids || !num_centroids || !labels)
+        isnan(tau) || !centroids || !num_centroids || !labels)
         return CPE_ORACLE_EINVAL;
 
     const int32_t F = n_freq, twoF = 2 * n_freq;
@@ -236,7 +264,7 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
 
     /* histogram accumulation: H(a,b) = sum_{p in S} E_x(p,a) E_y(p,b) */
     for (size_t p = 0; p < npix; p++) {
-        if (!(load_value(fg, dtype, p) > fg_threshold)) continue;
+        if (!participates(fg, dtype, p, fg_threshold)) continue;
         for (int32_t c = 0; c < twoF; c++) {
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
             Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));
@@ -277,7 +305,7 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
     for (size_t p = 0; p < npix; p++) {
         labels[p] = 0;
         if (score_map) score_map[p] = 0.0f;
-        if (Kc == 0 || !(load_value(fg, dtype, p) > fg_threshold)) continue;
+        if (Kc == 0 || !participates(fg, dtype, p, fg_threshold)) continue;
         for (int32_t c = 0; c < twoF; c++) {
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
             Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));
@@ -293,6 +321,8 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                 best = k;
             }
         }
+        /* Eq8: the pixel joins mask m only if d(a_m, b_m) < tau */
+        if (!((double)best_d < 4096.0 * tau)) continue;
         labels[p] = best + 1;
         centroids[best].npix += 1;
         if (score_map) score_map[p] = expf(-((float)best_d * 0x1p-12f));
@@ -343,8 +373,8 @@ int cpe_oracle_decode_real(int32_t H, int32_t W, int32_t D, int32_t dtype,
                            double *hist, int32_t *peaks, int32_t *num_peaks,
                            int32_t *labels)
 {
-    if (check_args(H, W, D, dtype, emb, fg, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
-                   fg_threshold, peak_threshold) != CPE_ORACLE_OK ||
+    if (check_args(H, W, D, dtype, emb, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
+                   fg_threshold, peak_threshold) != CPE_ORACLE_OK || !fg ||
         !hist || !peaks || !num_peaks || !labels)
         return CPE_ORACLE_EINVAL;
     const int32_t F = n_freq, twoF = 2 * n_freq;

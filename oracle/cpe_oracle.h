@@ -66,6 +66,23 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
                       uint16_t *codes);
 
+/* The same with two of the paper's options:
+ *   fg   may be NULL: then every pixel participates (the participating set of
+ *        Section 3.1 is the whole output grid);
+ *   tau  the mask threshold of Eq8 in distance units: a pixel keeps the label
+ *        of its nearest candidate m only if D_m / 4096 < tau, where D_m is the
+ *        integer code sum; otherwise label 0, not counted.  +INFINITY keeps
+ *        every participating pixel (cpe_oracle_decode); NaN is rejected. */
+int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
+                         const void *emb, const void *fg,
+                         const double *freq_x, const double *freq_y, int32_t n_freq,
+                         int32_t bins_w, int32_t bins_h, int32_t capacity,
+                         float fg_threshold, double peak_threshold, double tau,
+                         cpe_oracle_centroid *centroids, int32_t *num_centroids,
+                         int32_t *labels, float *score_map,
+                         uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
+                         uint16_t *codes);
+
 /* Real-valued fp64 decoder (no quantisation, no threshold tau).  Outputs:
  * hist[bins_h*bins_w] (double), peak list (bin index b*bins_w+a, ascending)
  * in peaks[capacity] with *num_peaks = true count, labels[H*W]. */

@@ -70,6 +70,15 @@ template <typename T> __device__ __forceinline__ float load_scalar(const T *p);
 template <> __device__ __forceinline__ float load_scalar<float>(const float *p) { return *p; }
 template <> __device__ __forceinline__ float load_scalar<_Float16>(const _Float16 *p) { return (float)*p; }
 
+// Foreground value of pixel p.  Without a foreground channel (fg == nullptr,
+// a uniform branch) every pixel participates: +inf exceeds any finite
+// threshold.
+template <typename T>
+__device__ __forceinline__ float fg_value(const T *fg, int64_t p)
+{
+    return fg ? load_scalar<T>(fg + p) : __builtin_huge_valf();
+}
+
 // S = |X|^2 + |P|^2 - 2 X.P is exact modulo 2^32 and lies in [0, 2^32).
 __device__ __forceinline__ uint32_t axis_s(uint32_t nX, uint32_t nP, int32_t dot)
 {

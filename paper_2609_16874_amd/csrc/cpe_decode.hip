@@ -12,6 +12,9 @@
 //   peaks   local-maxima search and compaction (k_peaks);
 //   assign  nearest-candidate assignment, label and score write-out, pixel
 //           counts (k_assign_mfma / k_assign_generic).
+// For grids up to 32 x 32 the peak extraction runs at the end of the vote
+// launch, so a frame is two launches.  cpe_decode_masks expands a label map
+// into binary masks (masks.hip).
 
 #include <hip/hip_runtime.h>
 
@@ -38,6 +41,38 @@ long long peak_cut(double theta)
 }
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Eq8 on integer code sums D (distance x 4096): D / 4096 < tau  <=>
+// D < ceil(4096 tau).  Code sums stay below 2^18, so the saturated value
+// keeps every pixel.
+uint32_t tau_code(double tau)
+{
+    const double t = std::ceil(tau * 4096.0);
+    if (!(t > 0.0)) return 0u;
+    if (t >= 4294967295.0) return 0xffffffffu;
+    return (uint32_t)t;
+}
+
+cpe_status decode_frame(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg, int32_t H, int32_t W,
+                        float fg_threshold, double peak_threshold, double tau, cpe_centroid *centroids,
+                        int32_t *num_centroids, int32_t *labels, float *score_map)
+{
+    if (!h || !emb || !centroids || !num_centroids || !labels) return CPE_ERR_INVALID_ARG;
+    if (H != h->H || W != h->W) return CPE_ERR_INVALID_ARG;
+    const size_t esz = h->dtype == CPE_F32 ? 4 : 2;
+    if (!aligned(emb, 16) || (fg && !aligned(fg, esz)) || !aligned(labels, 16) || !aligned(centroids, 8) ||
+        !aligned(num_centroids, 4) || (score_map && !aligned(score_map, 4)))
+        return CPE_ERR_INVALID_ARG;
+    if (!std::isfinite(fg_threshold) || !std::isfinite(peak_threshold)) return CPE_ERR_INVALID_ARG;
+    if (std::isnan(tau) || tau == -INFINITY) return CPE_ERR_INVALID_ARG;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return CPE_ERR_HIP;
+    if (dev != h->device) return CPE_ERR_INVALID_ARG;
+    const FrameArgs fa{stream,    emb,           fg,     fg_threshold, peak_cut(peak_threshold),
+                       tau_code(tau), centroids, num_centroids, labels, score_map};
+    if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, fa) : launch_f32_hi(h, fa);
+    return h->F <= 8 ? launch_f16_lo(h, fa) : launch_f16_hi(h, fa);
+}
 
 // IEEE binary16 bit pattern of an integer with |v| <= 1024 (exact).
 uint16_t half_of_small_int(int v)
@@ -287,20 +322,32 @@ cpe_status cpe_decode(cpe_decoder *h, hipStream_t stream, const void *emb, const
                       float fg_threshold, double peak_threshold, cpe_centroid *centroids, int32_t *num_centroids,
                       int32_t *labels, float *score_map)
 {
-    if (!h || !emb || !fg || !centroids || !num_centroids || !labels) return CPE_ERR_INVALID_ARG;
+    if (!fg) return CPE_ERR_INVALID_ARG;
+    return decode_frame(h, stream, emb, fg, H, W, fg_threshold, peak_threshold, INFINITY, centroids, num_centroids,
+                        labels, score_map);
+}
+
+cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg, int32_t H, int32_t W,
+                         const cpe_decode_options *opt, cpe_centroid *centroids, int32_t *num_centroids,
+                         int32_t *labels, float *score_map)
+{
+    if (!opt || opt->reserved != 0) return CPE_ERR_INVALID_ARG;
+    // without a foreground channel the threshold is never read
+    const float fg_thr = fg ? opt->fg_threshold : 0.0f;
+    return decode_frame(h, stream, emb, fg, H, W, fg_thr, opt->peak_threshold, opt->tau, centroids, num_centroids,
+                        labels, score_map);
+}
+
+cpe_status cpe_decode_masks(cpe_decoder *h, hipStream_t stream, const int32_t *labels, int32_t H, int32_t W,
+                            int32_t first, int32_t count, uint8_t *masks)
+{
+    if (!h || !labels || !masks || !aligned(labels, 16) || !aligned(masks, 16)) return CPE_ERR_INVALID_ARG;
     if (H != h->H || W != h->W) return CPE_ERR_INVALID_ARG;
-    const size_t esz = h->dtype == CPE_F32 ? 4 : 2;
-    if (!aligned(emb, 16) || !aligned(fg, esz) || !aligned(labels, 16) || !aligned(centroids, 8) ||
-        !aligned(num_centroids, 4) || (score_map && !aligned(score_map, 4)))
-        return CPE_ERR_INVALID_ARG;
-    if (!std::isfinite(fg_threshold) || !std::isfinite(peak_threshold)) return CPE_ERR_INVALID_ARG;
+    if (first < 0 || count < 1 || (int64_t)first + count > h->cap) return CPE_ERR_INVALID_ARG;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess) return CPE_ERR_HIP;
     if (dev != h->device) return CPE_ERR_INVALID_ARG;
-    const FrameArgs fa{stream, emb, fg, fg_threshold, peak_cut(peak_threshold), centroids, num_centroids, labels,
-                       score_map};
-    if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, fa) : launch_f32_hi(h, fa);
-    return h->F <= 8 ? launch_f16_lo(h, fa) : launch_f16_hi(h, fa);
+    return launch_masks(stream, labels, (int64_t)H * W, first, count, masks);
 }
 
 cpe_status cpe_decode_destroy(cpe_decoder *h)

@@ -38,6 +38,7 @@ struct FrameArgs {
     const void *emb, *fg;
     float fg_thr;
     long long cut;               // floor(peak_threshold * 2^30), saturated
+    uint32_t tau_code;           // a pixel is labelled iff its code sum < tau_code (Eq8)
     cpe_centroid *cents;
     int32_t *num, *labels;
     float *score;
@@ -49,5 +50,9 @@ cpe_status launch_f32_lo(cpe_decoder *h, const FrameArgs &a);   // F = 1..8
 cpe_status launch_f32_hi(cpe_decoder *h, const FrameArgs &a);   // F = 9..16
 cpe_status launch_f16_lo(cpe_decoder *h, const FrameArgs &a);
 cpe_status launch_f16_hi(cpe_decoder *h, const FrameArgs &a);
+
+// Enqueue the binary masks of centroids first .. first+count-1 (masks.hip).
+cpe_status launch_masks(hipStream_t stream, const int32_t *labels, int64_t npix, int32_t first, int32_t count,
+                        uint8_t *masks);
 
 }  // namespace cpe

@@ -96,7 +96,7 @@ __global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb,
         if (tid == 0) *s_n = 0;
         __syncthreads();
         const int64_t p = tile * TP + tid;
-        if (p < npix && load_scalar<T>(fg + p) > fg_thr) {
+        if (p < npix && fg_value<T>(fg, p) > fg_thr) {
             int slot = atomicAdd(s_n, 1);
             s_list[slot] = (int32_t)p;
         }
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb,
 // ---------------------------------------------------------------------------
 template <typename T, int F>
 __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix,
-                                                float fg_thr, Tables tb, int32_t Bw, int32_t Bh,
+                                                float fg_thr, uint32_t tau_code, Tables tb, int32_t Bw, int32_t Bh,
                                                 const int32_t *__restrict__ peaks, const int32_t *__restrict__ kinfo,
                                                 cpe_centroid *__restrict__ cents, int32_t *__restrict__ labels,
                                                 float *__restrict__ score_map)
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
         __syncthreads();
         const int64_t p = tile * TP + tid;
         if (p < npix) {
-            const bool part = Kc > 0 && load_scalar<T>(fg + p) > fg_thr;
+            const bool part = Kc > 0 && fg_value<T>(fg, p) > fg_thr;
             if (part) {
                 int slot = atomicAdd(s_n, 1);
                 s_list[slot] = (int32_t)p;
@@ -226,12 +226,17 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
                     best = k;
                 }
             }
-            labels[pp] = best + 1;
-            if (score_map) score_map[pp] = expf(-((float)bd * 0x1p-12f));
-            if (best < kCountCap)
-                atomicAdd(s_cnt + best, 1);
-            else
-                atomicAdd(&cents[best].npix, 1);
+            if ((uint32_t)bd < tau_code) {     // Eq8 (tau_code = ceil(4096 tau))
+                labels[pp] = best + 1;
+                if (score_map) score_map[pp] = expf(-((float)bd * 0x1p-12f));
+                if (best < kCountCap)
+                    atomicAdd(s_cnt + best, 1);
+                else
+                    atomicAdd(&cents[best].npix, 1);
+            } else {
+                labels[pp] = 0;
+                if (score_map) score_map[pp] = 0.0f;
+            }
         }
         __syncthreads();
     }

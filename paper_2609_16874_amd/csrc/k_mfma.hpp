@@ -243,7 +243,7 @@ __device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npi
 #pragma unroll
     for (int i = 0; i < kChunkRows; i++) {
         const int p = c * kChunk + 64 * i + lane;
-        fv[i] = p < npix ? load_scalar<T>(fg + p) : 0.0f;
+        fv[i] = p < npix ? fg_value<T>(fg, p) : 0.0f;
     }
 }
 
@@ -618,7 +618,7 @@ constexpr size_t kAssignLds = 16 + (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 
 
 template <typename T, int F>
 __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const T *__restrict__ fg,
-                                                     int32_t npix, float fg_thr, Tables tb,
+                                                     int32_t npix, float fg_thr, uint32_t tau_code, Tables tb,
                                                      const uint32_t *__restrict__ bofs,
                                                      const uint32_t *__restrict__ bhdr,
                                                      const uint16_t *__restrict__ rank,
@@ -765,11 +765,16 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         }
         if (lane < nvalid) {
             const int pix = grp[lane];
-            const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
-            const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
-            labels[pix] = k + 1;
-            if (score_map) score_map[pix] = expf(-((float)(best >> 14) * 0x1p-12f));
-            atomicAdd(s_cnt + k, 1);
+            if ((best >> 14) < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
+                const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
+                const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
+                labels[pix] = k + 1;
+                if (score_map) score_map[pix] = expf(-((float)(best >> 14) * 0x1p-12f));
+                atomicAdd(s_cnt + k, 1);
+            } else {
+                labels[pix] = 0;
+                if (score_map) score_map[pix] = 0.0f;
+            }
         }
         __builtin_amdgcn_wave_barrier();
     };

@@ -57,7 +57,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
         hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, g, npix,
-                           fg_thr, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
+                           fg_thr, fa.tau_code, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
@@ -76,7 +76,8 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
-        hipLaunchKernelGGL((k_assign_generic<T, F>), dim3(grid2), dim3(tp2), lds2, stream, e, g, npix, fg_thr, h->tb,
+        hipLaunchKernelGGL((k_assign_generic<T, F>), dim3(grid2), dim3(tp2), lds2, stream, e, g, npix, fg_thr,
+                           fa.tau_code, h->tb,
                            Bw, Bh, h->peaks, h->kinfo, cents, labels, score);
     }
     mark(3);

@@ -8,6 +8,7 @@ the library has not been built this module raises; there is no fallback.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from typing import Optional
 
@@ -24,13 +25,19 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
                            ("score", "<f8"), ("npix", "<i4"), ("reserved", "<i4")])
 
 # Every entry point declared in include/cpe_decode.h.
-EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_destroy", "cpe_status_string",
-           "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
+EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
+           "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
            "cpe_decode_set_stage_events")
 STAGE_EVENTS = 4
 STAGES = ("recover_vote", "peaks", "assign_label")
 
 _lib = None
+
+
+class DecodeOptions(ctypes.Structure):
+    """cpe_decode_options (include/cpe_decode.h)."""
+    _fields_ = [("fg_threshold", ctypes.c_float), ("reserved", ctypes.c_int32),
+                ("peak_threshold", ctypes.c_double), ("tau", ctypes.c_double)]
 
 
 class CpeError(RuntimeError):
@@ -51,6 +58,10 @@ def library():
         lib.cpe_decode_create.argtypes = [ctypes.POINTER(P), i32, i32, i32, i32, P, P, i32, i32, i32, i32]
         lib.cpe_decode.restype = i32
         lib.cpe_decode.argtypes = [P, P, P, P, i32, i32, ctypes.c_float, ctypes.c_double, P, P, P, P]
+        lib.cpe_decode_ex.restype = i32
+        lib.cpe_decode_ex.argtypes = [P, P, P, P, i32, i32, ctypes.POINTER(DecodeOptions), P, P, P, P]
+        lib.cpe_decode_masks.restype = i32
+        lib.cpe_decode_masks.argtypes = [P, P, P, i32, i32, i32, i32, P]
         lib.cpe_decode_destroy.restype = i32
         lib.cpe_decode_destroy.argtypes = [P]
         lib.cpe_status_string.restype = ctypes.c_char_p
@@ -114,6 +125,22 @@ class Decoder:
                                   _ptr(labels), _ptr(score_map))
         return st
 
+    def decode_ex(self, emb, fg, fg_threshold: float, peak_threshold: float, tau: float, centroids, num_centroids,
+                  labels, score_map=None, stream=None, reserved: int = 0) -> int:
+        """cpe_decode_ex: ``fg`` may be None (every pixel participates);
+        ``tau`` is the Eq8 mask threshold (math.inf: none)."""
+        opt = DecodeOptions(float(fg_threshold), int(reserved), float(peak_threshold), float(tau))
+        return library().cpe_decode_ex(self._h, _stream_ptr(stream), _ptr(emb), _ptr(fg), self.H, self.W,
+                                       ctypes.byref(opt), _ptr(centroids), _ptr(num_centroids), _ptr(labels),
+                                       _ptr(score_map))
+
+    def masks(self, labels, first: int, count: int, masks, stream=None, H: Optional[int] = None,
+              W: Optional[int] = None) -> int:
+        """cpe_decode_masks: ``masks`` is a device uint8 tensor of count*H*W bytes."""
+        return library().cpe_decode_masks(self._h, _stream_ptr(stream), _ptr(labels),
+                                          self.H if H is None else H, self.W if W is None else W,
+                                          int(first), int(count), _ptr(masks))
+
     def histogram(self, out, stream=None) -> int:
         return library().cpe_decode_get_histogram(self._h, _stream_ptr(stream), _ptr(out))
 
@@ -159,12 +186,17 @@ class Decoder:
         }
         return out
 
-    def run(self, emb, fg, fg_threshold, peak_threshold, score=True, stream=None, outputs=None):
-        """Decode one frame, synchronise, and return host numpy results."""
+    def run(self, emb, fg, fg_threshold, peak_threshold, score=True, stream=None, outputs=None, tau=None):
+        """Decode one frame, synchronise, and return host numpy results
+        (cpe_decode_ex when ``tau`` is given or ``fg`` is None)."""
         import torch
         out = outputs or self.new_outputs(emb.device, score)
-        st = self.decode(emb, fg, fg_threshold, peak_threshold, out["centroids"], out["num_centroids"],
-                         out["labels"], out["score_map"], stream)
+        if tau is None and fg is not None:
+            st = self.decode(emb, fg, fg_threshold, peak_threshold, out["centroids"], out["num_centroids"],
+                             out["labels"], out["score_map"], stream)
+        else:
+            st = self.decode_ex(emb, fg, fg_threshold, peak_threshold, math.inf if tau is None else tau,
+                                out["centroids"], out["num_centroids"], out["labels"], out["score_map"], stream)
         if st != CPE_OK:
             raise CpeError(st, "cpe_decode")
         torch.cuda.synchronize()

@@ -16,6 +16,7 @@ that they can pin it:
 from __future__ import annotations
 
 import math
+from fractions import Fraction
 
 import numpy as np
 from scipy import ndimage
@@ -150,11 +151,14 @@ def bucket_range(key: int, m: int):
     return first - 1, stop - 2
 
 
-def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold):
+def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold, tau=math.inf, dist_out=None):
     """Exhaustive decode for tiny frames: every grid position is scored by a
     direct sum over the pixels, every bin is tested against its neighbours,
-    and every pixel scans every candidate.  Returns (hist[b][a] list of ints,
-    peaks [(a, b)], K, labels [H][W])."""
+    and every pixel scans every candidate.  fg=None: every pixel takes part
+    (Section 3.1); tau: Eq8, a pixel keeps its nearest candidate only if that
+    distance, as the exact rational code sum / 4096, is below tau.  Returns
+    (hist[b][a] list of ints, peaks [(a, b)], K, labels [H][W]); dist_out, a
+    dict, receives {(i, j): winning code sum}."""
     H, W, D = emb.shape
     F = len(fx)
     pal_x = [[int(np.rint(4096.0 * f(fx[k] * ((a + 1) * W / (bw + 1)))))
@@ -174,7 +178,7 @@ def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold
     pix = []
     for i in range(H):
         for j in range(W):
-            if float(np.float32(fg[i, j])) > _f32(fg_threshold):
+            if fg is None or float(np.float32(fg[i, j])) > _f32(fg_threshold):
                 X = [fixed(float(emb[i, j, c])) for c in range(2 * F)]
                 Y = [fixed(float(emb[i, j, 2 * F + c])) for c in range(2 * F)]
                 pix.append((i, j, X, Y))
@@ -202,5 +206,9 @@ def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold
             break
         ds = [c_of(s_of(X, pal_x[a])) + c_of(s_of(Y, pal_y[b])) for (a, b) in use]
         best = min(range(len(use)), key=lambda k: (ds[k], k))
+        if dist_out is not None:
+            dist_out[(i, j)] = ds[best]
+        if not Fraction(ds[best], 4096) < tau:
+            continue
         labels[i][j] = best + 1
     return hist, peaks, K, labels

@@ -41,6 +41,23 @@ def test_status_strings_and_null_handles():
     assert lib.cpe_decode_get_tables(None, None, None, None, None) == native.CPE_ERR_INVALID_ARG
     assert lib.cpe_decode_get_histogram(None, None, None) == native.CPE_ERR_INVALID_ARG
     assert lib.cpe_decode_workspace_bytes(None) == 0
+    opt = native.DecodeOptions(0.5, 0, 0.0, float("inf"))
+    assert lib.cpe_decode_ex(None, None, None, None, 4, 4, ctypes.byref(opt), None, None, None, None) == \
+        native.CPE_ERR_INVALID_ARG
+    assert lib.cpe_decode_masks(None, None, None, 4, 4, 0, 1, None) == native.CPE_ERR_INVALID_ARG
+
+
+def test_options_struct_layout():
+    """cpe_decode_options: float, int32, double, double -- 24 bytes, the
+    doubles at offsets 8 and 16."""
+    assert ctypes.sizeof(native.DecodeOptions) == 24
+    assert native.DecodeOptions.peak_threshold.offset == 8 and native.DecodeOptions.tau.offset == 16
+    text = open(os.path.join(ROOT, "include", "cpe_decode.h")).read()
+    body = re.search(r"typedef struct \{([^{}]*)\} cpe_decode_options;", text).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"(\w+)\s+(\w+);", body)
+    assert fields == [("float", "fg_threshold"), ("int32_t", "reserved"), ("double", "peak_threshold"),
+                      ("double", "tau")]
 
 
 @pytest.mark.parametrize("kw", [dict(H=0), dict(W=-1), dict(D=17), dict(n_freq=0), dict(n_freq=17, D=68),

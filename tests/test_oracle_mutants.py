@@ -44,8 +44,15 @@ MUTANTS = [
     ("tie goes to the last candidate", "if (dk < best_d) {", "if (dk <= best_d) {"),
     ("assignment ignores the y axis", "int32_t dk = cx[peak_a[k]] + cy[peak_b[k]];", "int32_t dk = cx[peak_a[k]];",
      "int32_t best_d = cx[peak_a[0]] + cy[peak_b[0]];", "int32_t best_d = cx[peak_a[0]];"),
-    ("background pixels vote", "if (!(load_value(fg, dtype, p) > fg_threshold)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]",
-     "if (!(load_value(fg, dtype, p) > -1e30f)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]"),
+    ("background pixels vote", "if (!participates(fg, dtype, p, fg_threshold)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]",
+     "if (!participates(fg, dtype, p, -1e30f)) continue;\n        for (int32_t c = 0; c < twoF; c++) {\n            X[c]"),
+    ("no-fg mode votes nothing", "return !fg || load_value(fg, dtype, p) > fg_threshold;", "return fg && load_value(fg, dtype, p) > fg_threshold;"),
+    ("mask threshold not strict", "if (!((double)best_d < 4096.0 * tau)) continue;", "if (!((double)best_d <= 4096.0 * tau)) continue;"),
+    ("mask threshold on a wrong scale", "if (!((double)best_d < 4096.0 * tau)) continue;", "if (!((double)best_d < 256.0 * tau)) continue;"),
+    ("mask threshold on the x distance only", "if (!((double)best_d < 4096.0 * tau)) continue;",
+     "if (!((double)cx[peak_a[best]] < 4096.0 * tau)) continue;"),
+    ("pixel over the mask threshold still counted", "if (!((double)best_d < 4096.0 * tau)) continue;\n        labels[p] = best + 1;\n        centroids[best].npix += 1;",
+     "if (!((double)best_d < 4096.0 * tau)) { centroids[best].npix += 1; continue; }\n        labels[p] = best + 1;\n        centroids[best].npix += 1;"),
     ("clamp too wide", "if (c > V_CLAMP) c = V_CLAMP;", "if (c > 1.6f) c = 1.6f;"),
 ]
 
@@ -66,6 +73,10 @@ PIN_CASES = [
     (pins.test_threshold_is_strict, ()),
     (pins.test_exact_tie_goes_to_lowest_index, ()),
     (pins.test_assignment_agrees_with_eq7_real_distances, (1,)),
+    (pins.test_mask_threshold_and_all_pixels_equal_exhaustive_search, (5, pins.np.float16, 3, 6, 6, 3, False, (0.7, 0.5))),
+    (pins.test_mask_threshold_and_all_pixels_equal_exhaustive_search, (6, pins.np.float32, 1, 4, 7, 8, False, (0.5, 0))),
+    (pins.test_mask_threshold_on_noise_free_frame_with_all_pixels, ()),
+    (pins.test_mask_threshold_nests, ()),
 ]
 
 

@@ -179,6 +179,105 @@ def test_oracle_equals_exhaustive_search(seed, dtype, F, bw, bh, cap):
 
 
 # --------------------------------------------------------------------------
+# Eq8 mask threshold and the all-pixels participation of Section 3.1
+# --------------------------------------------------------------------------
+def _tiny_frame(seed, dtype, F, H=7, W=9):
+    rng = np.random.default_rng(seed)
+    fx, fy = paper_freqs(H, W, F)
+    inst = rng.integers(0, 4, size=(H, W))
+    cx, cy = rng.uniform(0, W, 4), rng.uniform(0, H, 4)
+    emb = (synth.encode_positions(cx[inst], cy[inst], fx, fy) + 0.2 * rng.standard_normal((H, W, 4 * F))).astype(dtype)
+    fg = ((inst > 0) + 0.05 * rng.standard_normal((H, W))).astype(dtype)
+    return emb, fg, inst, fx, fy
+
+
+# tau = (q, off): the winning code sum at quantile q of the pixels, plus off,
+# over 4096; off = 0 puts pixels exactly on the threshold, where the strict
+# test of Eq8 decides
+@pytest.mark.parametrize("seed,dtype,F,bw,bh,cap,use_fg,tau", [
+    (4, np.float32, 2, 5, 4, 6, True, (0.3, 0.5)), (5, np.float16, 3, 6, 6, 3, False, (0.7, 0.5)),
+    (6, np.float32, 1, 4, 7, 8, False, (0.5, 0)), (7, np.float32, 2, 6, 5, 4, True, (0.4, 0)),
+    (8, np.float16, 2, 5, 5, 4, True, 0.0)])
+def test_mask_threshold_and_all_pixels_equal_exhaustive_search(seed, dtype, F, bw, bh, cap, use_fg, tau):
+    emb, fg, inst, fx, fy = _tiny_frame(seed, dtype, F)
+    fg = fg if use_fg else None
+    theta = 0.05 * (inst > 0).sum()
+    if isinstance(tau, tuple):
+        d = {}
+        refmath.brute_decode(emb, fg, fx, fy, bw, bh, cap, 0.5, theta, dist_out=d)
+        vals = sorted(d.values())
+        tau = (vals[int(tau[0] * len(vals))] + tau[1]) / 4096.0
+    hist, peaks, K, labels = refmath.brute_decode(emb, fg, fx, fy, bw, bh, cap, 0.5, theta, tau)
+    res = oracle.decode(emb, fg, fx, fy, bw, bh, cap, 0.5, theta, tau=tau)
+    assert np.array_equal(res["hist"], np.array(hist, dtype=np.uint64))
+    assert res["K"] == K
+    lab = np.array(labels, dtype=np.int32)
+    assert np.array_equal(res["labels"], lab)
+    assert np.array_equal(res["centroids"]["npix"], np.bincount(lab.ravel(), minlength=min(K, cap) + 1)[1:])
+
+
+def test_mask_threshold_on_noise_free_frame_with_all_pixels():
+    """Every pixel votes (no fg channel).  Instance pixels sit at distance 0
+    from their own bin; background pixels carry a zero embedding, at distance
+    sqrt(F) per axis from every bin (|gamma|^2 = F), so each adds about
+    e^(-2 sqrt F) to every bin: a threshold above that level plus half the
+    smallest instance finds exactly the instances.  A tau of half a code
+    unit then keeps exactly the instance pixels, and tau = 0 keeps nothing
+    (Eq8 is strict)."""
+    H = W = 96
+    bins, F = 16, 4
+    cells = [(3, 3), (11, 4), (3, 12), (12, 12), (8, 8)]
+    emb, fg, inst, fx, fy = _snapped_frame(H, W, bins, cells, half=5, F=F)
+    sizes = np.bincount(inst.ravel())
+    floor = sizes[0] * math.exp(-2.0 * math.sqrt(F)) * 1.02
+    theta = floor + 0.5 * sizes[1:].min()
+    want = sorted(cells, key=lambda ab: ab[1] * bins + ab[0])
+    rank = {ab: i + 1 for i, ab in enumerate(want)}
+    expect = np.zeros_like(inst)
+    for k, ab in enumerate(cells, start=1):
+        expect[inst == k] = rank[ab]
+    res = oracle.decode(emb, None, fx, fy, bins, bins, 64, 0.5, theta, tau=0.5 / 4096)
+    got = list(zip(res["centroids"]["bin_x"].tolist(), res["centroids"]["bin_y"].tolist()))
+    assert res["K"] == len(cells) and got == want
+    assert np.array_equal(res["labels"], expect)
+    assert np.array_equal(res["centroids"]["npix"], np.bincount(expect.ravel(), minlength=len(cells) + 1)[1:])
+    assert np.all(res["score_map"][expect > 0] == 1.0) and not res["score_map"][expect == 0].any()
+    # no threshold: every pixel is labelled, the instances as before
+    full = oracle.decode(emb, None, fx, fy, bins, bins, 64, 0.5, theta)
+    assert np.all(full["labels"] > 0) and np.array_equal(full["labels"][expect > 0], expect[expect > 0])
+    assert full["centroids"]["npix"].sum() == H * W
+    zero = oracle.decode(emb, None, fx, fy, bins, bins, 64, 0.5, theta, tau=0.0)
+    assert zero["K"] == len(cells) and not zero["labels"].any() and not zero["centroids"]["npix"].any()
+
+
+def test_mask_threshold_nests():
+    """Raising tau only adds pixels, each with its tau = inf label; the
+    histogram and the centroids do not depend on tau; counts follow labels;
+    and the kept pixels are those whose affinity e^-d (the paper's kernel
+    compares affinities with e^-tau) exceeds e^-tau, where d is read back
+    from the tau = inf score map."""
+    f = synth.make_frame(0)
+    base = oracle.decode_frame(f, peak_threshold=0.5)
+    lab0 = base["labels"]
+    d = np.full(lab0.shape, np.inf)
+    d[lab0 > 0] = -np.log(base["score_map"][lab0 > 0].astype(np.float64))
+    prev = np.zeros(lab0.shape, dtype=bool)
+    for tau in (0.0, 0.25, 0.5, 1.0, 2.0, 8.0):
+        r = oracle.decode_frame(f, peak_threshold=0.5, tau=tau)
+        assert np.array_equal(r["hist"], base["hist"]) and r["K"] == base["K"]
+        keep = r["labels"] > 0
+        assert np.all(prev <= keep) and np.all(keep <= (lab0 > 0))
+        assert np.array_equal(r["labels"][keep], lab0[keep])
+        assert np.array_equal(r["centroids"]["npix"],
+                              np.bincount(r["labels"].ravel(), minlength=len(r["centroids"]) + 1)[1:])
+        # away from the boundary (float rounding of expf) the sets agree
+        clear = np.abs(d - tau) > 1e-5
+        assert np.array_equal(keep[clear], (d < tau)[clear])
+        prev = keep
+    assert 0 < prev.sum() and prev.sum() <= (lab0 > 0).sum()
+
+
+# --------------------------------------------------------------------------
 # noise-free special case: exact recovery of the generating centroids
 # --------------------------------------------------------------------------
 def _snapped_frame(H, W, bins, cells, half, F=4):
