@@ -20,9 +20,6 @@ constexpr int kMaxF = 16;             // harmonics per axis
 constexpr int kMaxBins = 128;
 constexpr int kCountCap = 1024;       // centroids whose pixel counts are privatised in LDS
 constexpr int kMfmaBins = 32;         // bin grids up to 32 x 32 take the matrix-core path
-// Candidate batches of the matrix-core assignment: 4 peak columns of one row
-// each; a row holds at most 16 strict local maxima, so 32 rows need <= 128.
-constexpr int kMaxBatch = 128;
 
 typedef short v2s __attribute__((ext_vector_type(2)));
 

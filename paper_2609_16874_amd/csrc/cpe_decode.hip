@@ -5,16 +5,16 @@
 // distance-bucket tables in fp64 (once, at create), one device allocation
 // for all constants and scratch, and the launch sequence of cpe_decode.
 //
-// Three launches per frame on the caller's stream (launch.hpp), no
-// allocation, no host synchronisation, no host copy:
+// Launches per frame on the caller's stream (launch.hpp), no allocation, no
+// host synchronisation, no host copy:
 //   vote    per-pixel recovery + soft voting into replicated 64-bit histograms
 //           (k_vote_mfma for grids up to 32 x 32, k_vote_generic otherwise);
-//   peaks   local-maxima search and compaction (k_peaks);
+//   peaks   local-maxima search and compaction (k_peaks, larger grids only);
 //   assign  nearest-candidate assignment, label and score write-out, pixel
 //           counts (k_assign_mfma / k_assign_generic).
-// For grids up to 32 x 32 the peak extraction runs at the end of the vote
-// launch, so a frame is two launches.  cpe_decode_masks expands a label map
-// into binary masks (masks.hip).
+// For grids up to 32 x 32 every assignment workgroup extracts the peaks in
+// its prologue, so a frame is two launches.  cpe_decode_masks expands a
+// label map into binary masks (masks.hip).
 
 #include <hip/hip_runtime.h>
 
@@ -255,13 +255,12 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_npx = carve(np1x.size() * 4), o_npy = carve(np1y.size() * 4);
     const size_t o_pop = carve(pop.size() * 2);
     const size_t o_wpk = carve(wt_pk.size() * 4), o_cpm = carve(ct_pm.size() * 2);
-    const size_t o_hrep = carve((size_t)kReplicas * nb * 8);
+    const size_t o_hrep = carve((size_t)2 * kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
     const size_t o_kinfo = carve(16);
-    const size_t o_bofs = carve((size_t)(kMaxBatch + 1) * 16), o_bhdr = carve((size_t)(kMaxBatch + 1) * 4);
-    const size_t o_rank = carve(kMfmaBins * kMfmaBins * 2);
-    const size_t o_ticket = carve(4 * 32);
+    const size_t o_count = carve(16);
+    const size_t o_list = carve((size_t)H * W * 4);
     h->dev_bytes = off;
     if (hipMalloc(&h->dev, off) != hipSuccess) {
         delete h;
@@ -279,13 +278,10 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               up(o_npx, np1x.data(), np1x.size() * 4) && up(o_npy, np1y.data(), np1y.size() * 4) &&
               up(o_pop, pop.data(), pop.size() * 2) &&
               up(o_wpk, wt_pk.data(), wt_pk.size() * 4) && up(o_cpm, ct_pm.data(), ct_pm.size() * 2) &&
-              hipMemset(d + o_hrep, 0, (size_t)kReplicas * nb * 8) == hipSuccess &&
+              hipMemset(d + o_hrep, 0, (size_t)2 * kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
-              hipMemset(d + o_kinfo, 0, 16) == hipSuccess &&
-              hipMemset(d + o_bofs, 0, (size_t)(kMaxBatch + 1) * 16) == hipSuccess &&
-              hipMemset(d + o_bhdr, 0, (size_t)(kMaxBatch + 1) * 4) == hipSuccess &&
-              hipMemset(d + o_rank, 0, kMfmaBins * kMfmaBins * 2) == hipSuccess &&
-              hipMemset(d + o_ticket, 0, 4 * 32) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
+              hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, 16) == hipSuccess &&
+              hipDeviceSynchronize() == hipSuccess;
     if (!ok) {
         (void)hipFree(h->dev);
         delete h;
@@ -310,10 +306,9 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
     h->peaks = reinterpret_cast<int32_t *>(d + o_peaks);
     h->kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
-    h->bofs = reinterpret_cast<uint32_t *>(d + o_bofs);
-    h->bhdr = reinterpret_cast<uint32_t *>(d + o_bhdr);
-    h->rank = reinterpret_cast<uint16_t *>(d + o_rank);
-    h->ticket = reinterpret_cast<uint32_t *>(d + o_ticket);
+    h->count = reinterpret_cast<int32_t *>(d + o_count);
+    h->list = reinterpret_cast<int32_t *>(d + o_list);
+    h->parity = 0;
     *out = h;
     return CPE_OK;
 }

@@ -18,14 +18,15 @@ struct cpe_decoder {
     unsigned char *dev;                  // single device allocation
     size_t dev_bytes;
     cpe::Tables tb;
-    unsigned long long *hrep;            // [kReplicas][nb]
-    unsigned long long *hlast;           // [nb]
-    int32_t *peaks;                      // [cap] a | b << 16
-    int32_t *kinfo;                      // [0] = min(K, cap), [1] = K, [2] = candidate batches
-    uint32_t *bofs;                      // [kMaxBatch + 1][4] candidate batch column offsets (padded list)
-    uint32_t *bhdr;                      // [kMaxBatch + 1] candidate batch row words
-    uint16_t *rank;                      // [32 * 32]
-    uint32_t *ticket;                    // [32] completion counters of the vote kernel (0 between frames)
+    unsigned long long *hrep;            // [2][kReplicas][nb]: vote histograms by frame parity
+                                         //   (the generic path uses the first set only)
+    unsigned long long *hlast;           // [nb] summed histogram of the latest frame
+    int32_t *peaks;                      // [cap] a | b << 16 (generic path)
+    int32_t *kinfo;                      // [0] = min(K, cap), [1] = K (generic path)
+    int32_t *list;                       // [H * W] participating pixels of the current frame
+    int32_t *count;                      // [2] list lengths by frame parity (0 before use)
+    int parity;                          // histogram set and list counter of the next frame
+                                         //   (matrix-core path)
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;
 };

@@ -1,10 +1,12 @@
 // k_mfma.hpp -- matrix-core decoder kernels for bin grids up to 32 x 32.
 //
-// Both passes stream the frame in chunks of 512 pixels per wave: a wave
-// ballot-compacts the participating pixels of a whole chunk into a per-wave
-// queue in LDS (the foreground values of its next chunk are already being
-// fetched), then works through the queue in tiles of 32 pixels, issuing the
-// embedding loads of the next tile before it computes the current one.
+// Both passes stream the compact list of participating pixels written by
+// k_compact (or every pixel, when the frame has no foreground channel): the
+// list is cut into tiles of 32 consecutive entries, and wave w of the grid
+// takes tiles w, w + (waves in the grid), ..., always loading the embedding
+// rows of its next tile (and the list entries of the one after) before it
+// computes the current one.  Every tile but the last is full, and every wave
+// gets the same number of tiles to within one.
 //
 // Per-axis distances (Eq4/Eq10).  S = |X - P|^2 = |X|^2 + |P|^2 - 2 X.P,
 // where X.(-2P) is a dense [pixels x channels] x [channels x bins]
@@ -44,11 +46,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kChunk = 128;          // pixels scanned per chunk
-constexpr int kChunkRows = kChunk / 64;
 constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
-constexpr int kRound1 = 24;          // chunks per workgroup and round, at most: vote kernel
-constexpr int kRound2 = 32;          //   assignment kernel
 constexpr int kPopBytes = 2 * 2 * 2 * 64 * 16;   // palette operands of both axes, limbs and K-steps
 constexpr int kTicketGroups = 16;    // first level of the vote kernel's completion count
 
@@ -236,146 +234,32 @@ __device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t nx, uin
     return __float_as_uint((float)s1);
 }
 
-// Foreground values of chunk c, kChunkRows per lane.
-template <typename T>
-__device__ __forceinline__ void load_fg(const T *__restrict__ fg, int c, int npix, int lane, float (&fv)[kChunkRows])
-{
-#pragma unroll
-    for (int i = 0; i < kChunkRows; i++) {
-        const int p = c * kChunk + 64 * i + lane;
-        fv[i] = p < npix ? fg_value<T>(fg, p) : 0.0f;
-    }
-}
+// The list of participating pixels: entry i is list[i] (or pixel i when
+// there is no list).  Lanes past the end of the list take the entry `base`
+// of their tile or group, which is always valid (their votes are masked,
+// their labels not written).
+struct TileStream {
+    const int32_t *list;     // nullptr: entry i is pixel i
+    int n;                   // list length
 
-// Rounds.  The chunks form blocks of G = gridDim.x consecutive chunks;
-// workgroup b owns chunk (b - k) mod G of block k, k = 0, 1, ..., so that its
-// chunks are spread over the rows of the frame and, shifting by one chunk per
-// block, over its columns as well.  It takes them in equal rounds of at most
-// ROUND chunks.  In a round
-// every wave scans its share of the chunks and appends the participating
-// pixels to one list in LDS (a slot reservation per 64-pixel row); after a
-// barrier the waves take 32- or 64-pixel tiles of the list from a counter in
-// LDS, so that all of them finish within about one tile of each other however
-// the foreground is distributed and however the SIMDs favour older waves.
-// The foreground values of a wave's next-round chunks are loaded while the
-// current round is being processed.
-template <typename T, int WPB, int ROUND>
-struct RoundScan {
-    static constexpr int kPer = (ROUND + WPB - 1) / WPB;    // chunks per wave and round, at most
-    static constexpr int kList = ROUND * kChunk;            // participating pixels of a round, at most
-    const T *fg;
-    int npix, nchunks, my_chunks, nrounds, per, wv;
-    float fg_thr;
-    float fv[kPer][kChunkRows];             // foreground values of the wave's next chunks
-
-    __device__ __forceinline__ void start(const T *fg_, int npix_, float thr, int wv_, int lane)
+    __device__ __forceinline__ int entry(int i, int base) const
     {
-        fg = fg_;
-        npix = npix_;
-        fg_thr = thr;
-        wv = wv_;
-        nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
-        const int G = gridDim.x, full = nchunks / G, rem = nchunks % G;
-        my_chunks = full + ((((int)blockIdx.x - full) % G + G) % G < rem ? 1 : 0);
-        nrounds = (my_chunks + ROUND - 1) / ROUND;
-        per = nrounds ? (my_chunks + nrounds - 1) / nrounds : 0;   // <= ROUND
-        prefetch(0, lane);
-    }
-    // chunk scanned by this wave in round r, slot u (-1 if none)
-    __device__ __forceinline__ int chunk(int r, int u) const
-    {
-        const int i = wv + u * WPB, k = r * per + i;
-        const int G = gridDim.x;
-        return (i < per && k < my_chunks) ? k * G + ((((int)blockIdx.x - k) % G) + G) % G : -1;
-    }
-    __device__ __forceinline__ void prefetch(int r, int lane)
-    {
-#pragma unroll
-        for (int u = 0; u < kPer; u++) {
-            const int c = r < nrounds ? chunk(r, u) : -1;
-            if (c >= 0) {
-                load_fg(fg, c, npix, lane, fv[u]);
-            } else {
-#pragma unroll
-                for (int i = 0; i < kChunkRows; i++) fv[u][i] = 0.0f;
-            }
-        }
-    }
-    // Append this wave's participating pixels of round r to list[], counting
-    // in *count (LDS): one reservation per chunk (PER_CHUNK) or per 64-pixel
-    // row (fewer live registers).  `background(p)` runs for every other
-    // in-range pixel.
-    template <bool PER_CHUNK, typename BG>
-    __device__ __forceinline__ void scan(int r, int32_t *list, int *count, int lane, BG background)
-    {
-#pragma unroll
-        for (int u = 0; u < kPer; u++) {
-            const int c = chunk(r, u);
-            if (c < 0) continue;
-            if constexpr (PER_CHUNK) {
-                unsigned long long m[kChunkRows];
-                int total = 0;
-#pragma unroll
-                for (int i = 0; i < kChunkRows; i++) {
-                    const int p = c * kChunk + 64 * i + lane;
-                    const bool f = p < npix && fv[u][i] > fg_thr;
-                    if (p < npix && !f) background(p);
-                    m[i] = __ballot(f);
-                    total += __popcll(m[i]);
-                }
-                int base = 0;
-                if (lane == 0 && total) base = atomicAdd(count, total);
-                base = __builtin_amdgcn_readfirstlane(base);
-#pragma unroll
-                for (int i = 0; i < kChunkRows; i++) {
-                    if ((m[i] >> lane) & 1ull) list[base + lane_prefix(m[i])] = c * kChunk + 64 * i + lane;
-                    base += __popcll(m[i]);
-                }
-            } else {
-#pragma unroll
-                for (int i = 0; i < kChunkRows; i++) {
-                    const int p = c * kChunk + 64 * i + lane;
-                    const bool f = p < npix && fv[u][i] > fg_thr;
-                    if (p < npix && !f) background(p);
-                    const unsigned long long m = __ballot(f);
-                    int base = 0;
-                    if (lane == 0 && m) base = atomicAdd(count, __popcll(m));
-                    base = __builtin_amdgcn_readfirstlane(base);
-                    if (f) list[base + lane_prefix(m)] = p;
-                }
-            }
-        }
+        const int e = i < n ? i : base;
+        return list ? list[e] : e;
     }
 };
 
-// Next tile (or group) index of the round from an LDS counter, wave-uniform.
-__device__ __forceinline__ int take_next(int *counter, int lane)
-{
-    int k = 0;
-    if (lane == 0) k = atomicAdd(counter, 1);
-    return __builtin_amdgcn_readfirstlane(k);
-}
+// Number of participating pixels: |S| from the compaction, or every pixel.
+__device__ __forceinline__ int list_length(const int32_t *count, int npix) { return count ? *count : npix; }
 
 // ---------------------------------------------------------------------------
 // Pass 1: recovery + soft voting (+ the peak extraction in the last workgroup)
 // ---------------------------------------------------------------------------
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
-// the palette operands, the round's pixel list, and per wave the squared
-// norms of one tile.
-// Small per-workgroup state of the vote kernel, kept in the dynamic LDS
-// block after the tables (static LDS would be placed first and offset every
-// table lookup).
-struct VoteState {
-    PeakScratch ps;
-    int pk[max_peaks(kMfmaBins, kMfmaBins)];   // compacted peak bins of the last workgroup
-    int last;
-    int count[2], take[2];      // round list length, next tile (by round parity)
-};
-
+// the palette operands, and per wave the squared norms of one tile.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)kRound1 * kChunk * 4 +
-           (size_t)wpb * 64 * 4 + sizeof(VoteState);
+    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * 64 * 4;
 }
 
 // Waves per SIMD the register allocation must allow: three for fp16 inputs
@@ -390,14 +274,15 @@ constexpr int kVoteWaves = (sizeof(T) == 2 && (F <= 8 || F == 16)) ? 3 : 2;
 template <typename T, int F>
 constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 //
-// The workgroup that finishes last (a ticket counter, taken after a release
-// fence) runs the peak extraction on the summed replicas and resets the
-// counter for the next frame.
+// Every workgroup adds its histogram into one of the kReplicas vote
+// histograms `hrep` (zeroed beforehand); the assignment launch that follows
+// sums them and extracts the peaks.  Workgroup 0 also resets the pixel
+// counts of the centroid records, which the assignment launch accumulates.
 template <typename T, int F>
 __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
-    const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix, float fg_thr, Tables tb, int32_t Bw,
-    int32_t Bh, unsigned long long *__restrict__ hrep, unsigned long long *__restrict__ hlast, long long cut,
-    int32_t cap, PeakOut po, uint32_t *__restrict__ ticket)
+    const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ count, int32_t npix,
+    Tables tb, int32_t Bw, int32_t Bh, unsigned long long *__restrict__ hrep, cpe_centroid *__restrict__ cents,
+    int32_t cap)
 {
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
@@ -407,12 +292,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
-    int32_t *s_list = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);           // [kRound1 * kChunk]
-    int32_t *s_nrm = s_list + kRound1 * kChunk;                                       // [kWpb][64]
-    VoteState &st = *reinterpret_cast<VoteState *>(s_nrm + kWpb * 64);
-    PeakScratch &ps = st.ps;
-    int &s_last = st.last;
-    int *s_count = st.count, *s_take = st.take;
+    int32_t *s_nrm = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);            // [kWpb][64]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -430,10 +310,6 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             if (i < kN) reinterpret_cast<u32x4 *>(s_wt)[i] = w[k];
         }
         for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_h[i] = 0ull;
-        if (tid < 2) {
-            s_count[tid] = 0;
-            s_take[tid] = 0;
-        }
         for (int i = tid; i < kPopBytes / 16; i += kThreads)
             reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
     }
@@ -539,34 +415,27 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    RoundScan<T, kWpb, kRound1> rs;
-    rs.start(fg, npix, fg_thr, wv, lane);
+    // the wave's tiles: t = gw, gw + nw, ...
+    const int n = list_length(count, npix), ntiles = (n + 31) >> 5;
+    const int nw = gridDim.x * kWpb;
+    const TileStream ts{list, n};
+    int t = blockIdx.x * kWpb + wv;
     RawSlices<T, F> raw;
-    for (int r = 0; r < rs.nrounds; r++) {
-        const int par = r & 1;
-        if (tid == 0) {                  // the other parity's counters were last used in round r - 1
-            s_count[par ^ 1] = 0;
-            s_take[par ^ 1] = 0;
+    auto pixel = [&](int tt) { return ts.entry(32 * tt + ln, 32 * tt); };
+    int idx = 0;                                       // pixel of this lane in the tile after the next
+    if (t < ntiles) {
+        raw.load(emb + (size_t)pixel(t) * D, g);
+        if (t + nw < ntiles) idx = pixel(t + nw);
+    }
+    while (t < ntiles) {
+        const int tn = t + nw;
+        const RawSlices<T, F> cur = raw;
+        if (tn < ntiles) {
+            raw.load(emb + (size_t)idx * D, g);
+            if (tn + nw < ntiles) idx = pixel(tn + nw);
         }
-        rs.template scan<false>(r, s_list, &s_count[par], lane, [](int) {});
-        rs.prefetch(r + 1, lane);
-        __syncthreads();
-        const int n = s_count[par], ntiles = (n + 31) >> 5;
-        // lane m of a tile reads list entry 32 j + m (entry 32 j past the end)
-        auto pixel_row = [&](int j) {
-            const int i = 32 * j + ln;
-            return emb + (size_t)s_list[i < n ? i : 32 * j] * D;
-        };
-        int j = take_next(&s_take[par], lane);
-        if (j < ntiles) raw.load(pixel_row(j), g);
-        while (j < ntiles) {
-            const int jn = take_next(&s_take[par], lane);
-            const RawSlices<T, F> cur = raw;
-            if (jn < ntiles) raw.load(pixel_row(jn), g);
-            tile(cur, min(32, n - 32 * j));
-            j = jn;
-        }
-        __syncthreads();                 // the list is rewritten in the next round
+        tile(cur, min(32, n - 32 * t));
+        t = tn;
     }
     fold();
 
@@ -578,52 +447,35 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         const int b = i / kMfmaBins, a = i % kMfmaBins;
         if (a < Bw && b < Bh && s_h[i]) atomicAdd(dst + b * Bw + a, s_h[i]);
     }
-
-    // The last workgroup to finish extracts the peaks.  Every wave waits for
-    // its own histogram atomics; one release fence per workgroup then orders
-    // them before its count.  Counting is two-level (workgroup b counts in
-    // group b % kTicketGroups, the last of each group in the top counter), so
-    // that no counter is hit by more than about gridDim / kTicketGroups
-    // atomics.
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __syncthreads();
-    if (tid == 0) {
-        const int G = gridDim.x, k = blockIdx.x % kTicketGroups;
-        const int gsize = (G - k + kTicketGroups - 1) / kTicketGroups;
-        const int ngroups = G < kTicketGroups ? G : kTicketGroups;
-        bool last = false;
-        __threadfence();
-        if (atomicAdd(ticket + k, 1u) == (uint32_t)(gsize - 1)) {
-            __threadfence();
-            last = atomicAdd(ticket + kTicketGroups, 1u) == (uint32_t)(ngroups - 1);
-        }
-        s_last = last;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    peak_extract<2>(hrep, hlast, Bw, Bh, cut, cap, tb.cx, tb.cy, po, s_h, st.pk, ps);
-    if (tid <= kTicketGroups) __hip_atomic_store(ticket + tid, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (blockIdx.x == 0)
+        for (int k = tid; k < cap; k += blockDim.x) cents[k].npix = 0;
 }
 
 // ---------------------------------------------------------------------------
 // Pass 2: assignment + label write-out
 // ---------------------------------------------------------------------------
-// LDS bytes of k_assign_mfma: code table, bin -> centroid table, counts,
-// candidate batches, and per wave a queue, x keys [32 bins][64 pixels] (u32)
-// and y codes [32 bins][64 pixels] (u16).
-constexpr size_t kAssignLds = 16 + (size_t)kCKeys * 2 + kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                              (size_t)kMaxBatch * 20 + (size_t)kRound2 * kChunk * 4 +
-                              (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2);
+// LDS bytes of k_assign_mfma: code table, candidate batches, bin -> centroid
+// table, counts, per wave x keys [32 bins][64 pixels] (u32) and y codes
+// [32 bins][64 pixels] (u16), then the peak-extraction state.
+constexpr size_t kAssignLds = (size_t)kCKeys * 2 + (size_t)kMaxBatchLds * 20 + kMfmaBins * kMfmaBins * 2 +
+                              kMfmaBins * kMfmaBins * 4 +
+                              (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2) + sizeof(PeakLds);
 
+// Every workgroup first sums the vote histograms `hcur` of the vote launch
+// and extracts the peaks in LDS (identical in every workgroup); workgroup 0
+// writes the centroid records (all fields but the pixel count), K and the
+// summed histogram `hlast`, and the grid clears `hzero`, the histograms the
+// next frame's vote launch accumulates into.
 template <typename T, int F>
-__global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const T *__restrict__ fg,
-                                                     int32_t npix, float fg_thr, uint32_t tau_code, Tables tb,
-                                                     const uint32_t *__restrict__ bofs,
-                                                     const uint32_t *__restrict__ bhdr,
-                                                     const uint16_t *__restrict__ rank,
-                                                     const int32_t *__restrict__ kinfo,
-                                                     cpe_centroid *__restrict__ cents, int32_t *__restrict__ labels,
+__global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const int32_t *__restrict__ list,
+                                                     const int32_t *__restrict__ count, int32_t npix,
+                                                     uint32_t tau_code, Tables tb,
+                                                     const unsigned long long *__restrict__ hcur,
+                                                     unsigned long long *__restrict__ hzero,
+                                                     int32_t *__restrict__ count_next,
+                                                     unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
+                                                     long long cut, int32_t cap, cpe_centroid *__restrict__ cents,
+                                                     int32_t *__restrict__ num, int32_t *__restrict__ labels,
                                                      float *__restrict__ score_map)
 {
     constexpr int KS = AxisShape<F>::KS;
@@ -631,39 +483,20 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kAssignLds];
     uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                           // [kCKeys]
-    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatch]
-    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatch);               // [kMaxBatch]
-    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatch);             // [32 * 32]
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatchLds]
+    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatchLds);            // [kMaxBatchLds]
+    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatchLds);          // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);  // [1024]
-    int32_t *s_list = s_cnt + kMfmaBins * kMfmaBins;                               // [kRound2 * kChunk]
-    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_list + kRound2 * kChunk);      // [kWpb2][32][64]
+    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins);  // [kWpb2][32][64]
     uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
+    PeakLds &pl = *reinterpret_cast<PeakLds *>(s_cy + kWpb2 * kMfmaBins * 64);
+    // the summed histogram lives in the x-key arrays until the peaks are known
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_kx);
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
-    const int Kc = kinfo[0];
-    const int nchunks = (int)(((int64_t)npix + kChunk - 1) / kChunk);
-    const int nw = gridDim.x * kWpb2;
+    const int nb = Bw * Bh;
 
-    if (Kc == 0) {              // no centroid: every pixel is unlabelled
-        for (int c = blockIdx.x * kWpb2 + wv; c < nchunks; c += nw)
-#pragma unroll
-            for (int i = 0; i < kChunkRows; i++) {
-                const int p = c * kChunk + 64 * i + lane;
-                if (p < npix) {
-                    labels[p] = 0;
-                    if (score_map) score_map[p] = 0.0f;
-                }
-            }
-        return;
-    }
-
-    const int nbat = min(kinfo[2], kMaxBatch);      // a multiple of 4
-    // The offsets are masked to the per-wave arrays' extents (columns and rows < 32).
-    for (int i = tid; i < nbat; i += blockDim.x) {
-        s_bo[i] = (u32x4){bofs[4 * i], bofs[4 * i + 1], bofs[4 * i + 2], bofs[4 * i + 3]} & 0x1f00u;
-        s_bh[i] = bhdr[i] & 0xf80u;
-    }
     {
         constexpr int kThreads = kWpb2 * 64;
         u32x4 w[kCKeys / 8 / kThreads];
@@ -673,18 +506,42 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
 #pragma unroll
         for (int k = 0; k < kCKeys / 8 / kThreads; k++) reinterpret_cast<u32x4 *>(s_ct)[k * kThreads + tid] = w[k];
     }
-    // round list length, next group (by round parity), after the per-wave
-    // arrays (static LDS would offset every table lookup)
-    int *s_count = reinterpret_cast<int *>(s_cy + kWpb2 * kMfmaBins * 64), *s_take = s_count + 2;
-    for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
-        s_rank[i] = rank[i];
-        s_cnt[i] = 0;
+    for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) s_cnt[i] = 0;
+    peaks_lds(hcur, Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank);
+    const int Kc = pl.Kc;
+    if (blockIdx.x == 0) {
+        for (int k = tid; k < Kc; k += blockDim.x) {
+            const int i = pl.pk[k], a = i % Bw, b = i / Bw;
+            cpe_centroid *c = cents + k;    // npix was reset by the vote launch and is counted below
+            c->bin_x = a;
+            c->bin_y = b;
+            c->x = tb.cx[a];
+            c->y = tb.cy[b];
+            c->score = (double)s_h[i] * 0x1p-30;
+            c->reserved = 0;
+        }
+        for (int i = tid; i < nb; i += blockDim.x) hlast[i] = s_h[i];
+        if (tid == 0) {
+            *num = pl.K;
+            *count_next = 0;
+        }
     }
-    if (tid < 2) {
-        s_count[tid] = 0;
-        s_take[tid] = 0;
+    for (int i = blockIdx.x * blockDim.x + tid; i < kReplicas * nb; i += gridDim.x * blockDim.x) hzero[i] = 0ull;
+    __syncthreads();            // s_h is overwritten by the key arrays from here on
+
+    // the wave's groups of 64 list entries: j = gw, gw + nw, ...
+    const int n = list_length(count, npix), ngroups = (n + 63) >> 6;
+    const int nw = gridDim.x * kWpb2;
+    const TileStream ts{list, n};
+    if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
+        for (int i = (blockIdx.x * kWpb2 + wv) * 64 + lane; i < n; i += nw * 64) {
+            const int p = ts.entry(i, 0);
+            labels[p] = 0;
+            if (score_map) score_map[p] = 0.0f;
+        }
+        return;
     }
-    __syncthreads();
+    const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of 4
 
     f16x8 pxh[KS], pxl[KS], pyh[KS], pyl[KS];
 #pragma unroll
@@ -743,7 +600,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     // keys plus the row's y key.  The row word 128 b is both the byte offset
     // of row b in the y-code array and the row's bits of the key.  The batch
     // list is read one entry ahead.
-    auto search = [&](const int32_t *grp, int nvalid) {
+    auto search = [&](int pix, int nvalid) {
         __builtin_amdgcn_wave_barrier();
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + lane);
         const unsigned char *cyl = reinterpret_cast<const unsigned char *>(cyb + lane);
@@ -764,7 +621,6 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
             }
         }
         if (lane < nvalid) {
-            const int pix = grp[lane];
             if ((best >> 14) < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
                 const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
                 const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
@@ -779,44 +635,34 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    auto background = [&](int p) {
-        labels[p] = 0;
-        if (score_map) score_map[p] = 0.0f;
-    };
-
-    RoundScan<T, kWpb2, kRound2> rs;
-    rs.start(fg, npix, fg_thr, wv, lane);
+    // lane (m, h) of group j loads entry 64 j + 32 h' + m for both halves h'
+    // and labels entry 64 j + 32 h + m, i.e. slot lane
+    auto pixel = [&](int j, int h) { return ts.entry(64 * j + 32 * h + ln, 64 * j); };
+    int j = blockIdx.x * kWpb2 + wv;
     RawSlices<T, F> raw;
-    for (int r = 0; r < rs.nrounds; r++) {
-        const int par = r & 1;
-        if (tid == 0) {                  // the other parity's counters were last used in round r - 1
-            s_count[par ^ 1] = 0;
-            s_take[par ^ 1] = 0;
+    int ip0 = 0, ip1 = 0;
+    if (j < ngroups) {
+        ip0 = pixel(j, 0);
+        ip1 = pixel(j, 1);
+        raw.load(emb + (size_t)ip0 * D, g);
+    }
+    while (j < ngroups) {
+        const int jn = j + nw;
+        RawSlices<T, F> cur = raw;
+        raw.load(emb + (size_t)ip1 * D, g);
+        int np0 = 0, np1 = 0;
+        if (jn < ngroups) {
+            np0 = pixel(jn, 0);
+            np1 = pixel(jn, 1);
         }
-        rs.template scan<true>(r, s_list, &s_count[par], lane, background);
-        rs.prefetch(r + 1, lane);
-        __syncthreads();
-        const int n = s_count[par], ngroups = (n + 63) >> 6;
-        // group j = list entries 64 j .. 64 j + 63; lane m of its half h reads
-        // entry 64 j + 32 h + m (entry 64 j past the end)
-        auto pixel_row = [&](int j, int h) {
-            const int i = 64 * j + 32 * h + ln;
-            return emb + (size_t)s_list[i < n ? i : 64 * j] * D;
-        };
-        int j = take_next(&s_take[par], lane);
-        if (j < ngroups) raw.load(pixel_row(j, 0), g);
-        while (j < ngroups) {
-            const int jn = take_next(&s_take[par], lane);
-            RawSlices<T, F> cur = raw;
-            raw.load(pixel_row(j, 1), g);
-            codes(cur, 0);
-            cur = raw;
-            if (jn < ngroups) raw.load(pixel_row(jn, 0), g);
-            codes(cur, 1);
-            search(s_list + 64 * j, min(64, n - 64 * j));
-            j = jn;
-        }
-        __syncthreads();                 // the list is rewritten in the next round
+        codes(cur, 0);
+        cur = raw;
+        if (jn < ngroups) raw.load(emb + (size_t)np0 * D, g);
+        codes(cur, 1);
+        search(g ? ip1 : ip0, min(64, n - 64 * j));
+        ip0 = np0;
+        ip1 = np1;
+        j = jn;
     }
     __syncthreads();
     for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)

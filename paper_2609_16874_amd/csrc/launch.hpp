@@ -3,6 +3,7 @@
 #pragma once
 
 #include "cpe_decoder.hpp"
+#include "k_compact.hpp"
 #include "k_generic.hpp"
 #include "k_mfma.hpp"
 #include "k_peaks.hpp"
@@ -40,24 +41,44 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         if (h->stage_on) (void)hipEventRecord(h->stage_ev[i], stream);
     };
     const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;
-    const int64_t chunks = ((int64_t)npix + kChunk - 1) / kChunk;
     const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
 
-    PeakOut po{cents, num, h->peaks, h->kinfo, h->bofs, h->bhdr, h->rank};
     mark(0);
     if (mfma) {
-        // recovery + voting, and the peak extraction in the last workgroup
+        // the participating pixels as a compact list (every pixel when the
+        // frame has no foreground channel), recovery + voting into this
+        // frame's histograms, then the assignment launch, which extracts the
+        // peaks in its prologue and clears the other parity's histograms and
+        // list counter for the next frame
+        const int par = h->parity;
+        h->parity ^= 1;
+        unsigned long long *hcur = h->hrep + (size_t)par * kReplicas * nb;
+        unsigned long long *hnext = h->hrep + (size_t)(par ^ 1) * kReplicas * nb;
+        int32_t *list = g ? h->list : nullptr;
+        int32_t *count = g ? h->count + par : nullptr;
+        if (g) {
+            const int cgrid = (int)(((int64_t)npix + kCompactSpan - 1) / kCompactSpan);
+            if (((uintptr_t)g & 15u) == 0)
+                hipLaunchKernelGGL((k_compact<T, true>), dim3(cgrid), dim3(kCompactThreads), 0, stream, g, npix, fg_thr,
+                                   list, count, labels, score);
+            else
+                hipLaunchKernelGGL((k_compact<T, false>), dim3(cgrid), dim3(kCompactThreads), 0, stream, g, npix,
+                                   fg_thr, list, count, labels, score);
+        }
+        // grids: at most one workgroup per compute unit, no more waves than tiles
         constexpr int wpb = kVoteWpb<T, F>;
-        const int64_t wgs = (chunks + wpb - 1) / wpb;
+        const int64_t tiles = ((int64_t)npix + 31) / 32;
+        const int64_t wgs = (tiles + wpb - 1) / wpb;
         const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), 0, stream, e, g, npix, fg_thr,
-                           h->tb, Bw, Bh, h->hrep, h->hlast, cut, h->cap, po, h->ticket);
+        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), 0, stream, e, list, count, npix, h->tb, Bw,
+                           Bh, hcur, cents, h->cap);
         mark(1);
         mark(2);
-        const int64_t wgs2 = (chunks + kWpb2 - 1) / kWpb2;
+        const int64_t wgs2 = ((tiles + 1) / 2 + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, g, npix,
-                           fg_thr, fa.tau_code, h->tb, h->bofs, h->bhdr, h->rank, h->kinfo, cents, labels, score);
+        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, list, count, npix,
+                           fa.tau_code, h->tb, hcur, hnext, h->count + (par ^ 1), h->hlast, Bw, Bh, cut, h->cap, cents,
+                           num, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
@@ -67,9 +88,9 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         hipLaunchKernelGGL((k_vote_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb, Bw,
                            Bh, h->hrep);
         mark(1);
+        const PeakOut po{cents, num, h->peaks, h->kinfo};
         hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, stream,
-                           h->hrep, h->hlast, Bw, Bh, cut,
-                           h->cap, h->tb.cx, h->tb.cy, po);
+                           h->hrep, h->hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
         mark(2);
         const size_t fixed2 = tables + 16 + kCountCap * 4 + kCKeys * 2;
         const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
