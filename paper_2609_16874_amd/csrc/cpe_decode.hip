@@ -25,6 +25,7 @@
 #include <vector>
 
 #include "cpe_decoder.hpp"
+#include "k_compact.hpp"
 
 using namespace cpe;
 
@@ -259,8 +260,8 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
     const size_t o_kinfo = carve(16);
-    const size_t o_count = carve(16);
-    const size_t o_list = carve((size_t)H * W * 4);
+    const size_t o_count = carve((size_t)kMaxSlices * 4);
+    const size_t o_list = carve(((size_t)H * W + (size_t)slice_pixels((int64_t)H * W)) * 4);
     h->dev_bytes = off;
     if (hipMalloc(&h->dev, off) != hipSuccess) {
         delete h;
@@ -280,7 +281,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               up(o_wpk, wt_pk.data(), wt_pk.size() * 4) && up(o_cpm, ct_pm.data(), ct_pm.size() * 2) &&
               hipMemset(d + o_hrep, 0, (size_t)2 * kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
-              hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, 16) == hipSuccess &&
+              hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, (size_t)kMaxSlices * 4) == hipSuccess &&
               hipDeviceSynchronize() == hipSuccess;
     if (!ok) {
         (void)hipFree(h->dev);
@@ -306,7 +307,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
     h->peaks = reinterpret_cast<int32_t *>(d + o_peaks);
     h->kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
-    h->count = reinterpret_cast<int32_t *>(d + o_count);
+    h->counts = reinterpret_cast<int32_t *>(d + o_count);
     h->list = reinterpret_cast<int32_t *>(d + o_list);
     h->parity = 0;
     *out = h;

@@ -23,10 +23,9 @@ struct cpe_decoder {
     unsigned long long *hlast;           // [nb] summed histogram of the latest frame
     int32_t *peaks;                      // [cap] a | b << 16 (generic path)
     int32_t *kinfo;                      // [0] = min(K, cap), [1] = K (generic path)
-    int32_t *list;                       // [H * W] participating pixels of the current frame
-    int32_t *count;                      // [2] list lengths by frame parity (0 before use)
-    int parity;                          // histogram set and list counter of the next frame
-                                         //   (matrix-core path)
+    int32_t *list;                       // participating pixels of the current frame, in slices
+    int32_t *counts;                     // [kMaxSlices] entries per slice
+    int parity;                          // histogram set of the next frame (matrix-core path)
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;
 };

@@ -1,16 +1,16 @@
 // k_compact.hpp -- the participating set S of Eq6 as a compact pixel list.
 //
-// One launch per frame before the vote: every lane tests 8 consecutive
-// foreground values against the threshold, a wave prefix sum and one
-// global reservation per workgroup give each participating pixel its slot,
-// and its index is written to `list` (raster order within a workgroup's
-// 2048 pixels; workgroups in the order of their reservations).  The
-// non-participating pixels get their final outputs here: label 0 and, if a
-// score map is requested, score 0.  The vote and assignment launches then
-// stream equal shares of the list in full tiles, so their work does not
-// depend on where in the frame the foreground lies.
-//
-// `count` must be 0 before the launch; afterwards it holds |S|.
+// One launch per frame before the vote.  Workgroup s of the grid owns the
+// pixel range [s R, (s + 1) R) (R a multiple of 2048) and writes the indices
+// of its participating pixels, in raster order, to its slice list[s R ..]
+// and their number to counts[s]; every lane tests 8 consecutive foreground
+// values against the threshold and a wave prefix sum gives the slots.  No
+// atomics: the consumers concatenate the slices through the prefix sum of
+// the counts (slice_prefix / ListCursor).  The non-participating pixels get
+// their final outputs here: label 0 and, if a score map is requested,
+// score 0.  The vote and assignment launches then stream equal shares of
+// the list in full tiles, so their work does not depend on where in the
+// frame the foreground lies.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -19,92 +19,180 @@ namespace cpe {
 
 constexpr int kCompactThreads = 256;
 constexpr int kCompactPer = 8;                                   // pixels per lane
-constexpr int kCompactSpan = kCompactThreads * kCompactPer;      // pixels per workgroup
+constexpr int kCompactSpan = kCompactThreads * kCompactPer;      // pixels per workgroup and step
+constexpr int kMaxSlices = 256;                                  // workgroups of the compaction
 
-// VEC: the foreground plane is 16-byte aligned (fp16) / 32-byte aligned
-// (fp32), so a lane's 8 values are one or two vector loads.
+// Pixels per slice for a frame of npix pixels, and the number of slices.
+__host__ __device__ inline int slice_pixels(int64_t npix)
+{
+    const int64_t steps = (npix + (int64_t)kMaxSlices * kCompactSpan - 1) / ((int64_t)kMaxSlices * kCompactSpan);
+    return (int)(steps * kCompactSpan);
+}
+__host__ __device__ inline int slice_count(int64_t npix)
+{
+    const int64_t r = slice_pixels(npix);
+    return (int)((npix + r - 1) / r);
+}
+
+// VEC: the foreground plane is 16-byte aligned, so a lane's 8 values are one
+// (fp16) or two (fp32) vector loads.
 template <typename T, bool VEC>
 __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict__ fg, int32_t npix, float fg_thr,
-                                                             int32_t *__restrict__ list, int32_t *__restrict__ count,
+                                                             int32_t *__restrict__ list, int32_t *__restrict__ counts,
                                                              int32_t *__restrict__ labels, float *__restrict__ score)
 {
     __shared__ int s_wave[kCompactThreads / 64];
-    __shared__ int s_base;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int p0 = (blockIdx.x * kCompactThreads + tid) * kCompactPer;
+    const int R = slice_pixels(npix);
+    const int begin = blockIdx.x * R;
+    const int end = min(begin + R, npix);
+    int32_t *out = list + begin;
+    int base = 0;                                      // entries of the slice so far
+    const bool score_vec = score && ((uintptr_t)score & 15u) == 0;
 
-    float v[kCompactPer];
-    if (VEC && p0 + kCompactPer <= npix) {
-        if constexpr (sizeof(T) == 2) {
-            const uint4 w = *reinterpret_cast<const uint4 *>(fg + p0);
-            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+    for (int q0 = begin; q0 < end; q0 += kCompactSpan) {
+        const int p0 = q0 + tid * kCompactPer;
+        float v[kCompactPer];
+        if (VEC && p0 + kCompactPer <= end) {
+            if constexpr (sizeof(T) == 2) {
+                const uint4 w = *reinterpret_cast<const uint4 *>(fg + p0);
+                const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                v[2 * i] = half_bits_to_float(ww[i] & 0xffffu);
-                v[2 * i + 1] = half_bits_to_float(ww[i] >> 16);
+                for (int i = 0; i < 4; i++) {
+                    v[2 * i] = half_bits_to_float(ww[i] & 0xffffu);
+                    v[2 * i + 1] = half_bits_to_float(ww[i] >> 16);
+                }
+            } else {
+                const float4 a = *reinterpret_cast<const float4 *>(fg + p0);
+                const float4 b = *reinterpret_cast<const float4 *>(fg + p0 + 4);
+                v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+                v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
             }
         } else {
-            const float4 a = *reinterpret_cast<const float4 *>(fg + p0);
-            const float4 b = *reinterpret_cast<const float4 *>(fg + p0 + 4);
-            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+#pragma unroll
+            for (int i = 0; i < kCompactPer; i++) v[i] = p0 + i < end ? load_scalar<T>(fg + p0 + i) : 0.0f;
         }
-    } else {
+        uint32_t m = 0, valid = 0;
 #pragma unroll
-        for (int i = 0; i < kCompactPer; i++) v[i] = p0 + i < npix ? load_scalar<T>(fg + p0 + i) : 0.0f;
-    }
-    uint32_t m = 0, valid = 0;
-#pragma unroll
-    for (int i = 0; i < kCompactPer; i++) {
-        const bool in = p0 + i < npix;
-        valid |= (in ? 1u : 0u) << i;
-        m |= (in && v[i] > fg_thr ? 1u : 0u) << i;   // a NaN never exceeds the threshold
-    }
-    const int c = __popc(m);
-    int incl = c;                                      // inclusive prefix over the wave
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int t = __shfl_up(incl, d);
-        if (lane >= d) incl += t;
-    }
-    if (lane == 63) s_wave[wv] = incl;
-    __syncthreads();
-    if (tid == 0) {
-        int tot = 0;
-#pragma unroll
-        for (int w = 0; w < kCompactThreads / 64; w++) tot += s_wave[w];
-        s_base = tot ? atomicAdd(count, tot) : 0;
-    }
-    __syncthreads();
-    int off = s_base + incl - c;
-#pragma unroll
-    for (int w = 0; w < kCompactThreads / 64; w++) off += w < wv ? s_wave[w] : 0;
-#pragma unroll
-    for (int i = 0; i < kCompactPer; i++)
-        if ((m >> i) & 1u) list[off++] = p0 + i;
-
-    // outputs of the pixels outside S
-    const uint32_t bg = valid & ~m;
-    if (bg == 0xffu) {
-        const int4 z = {0, 0, 0, 0};
-        reinterpret_cast<int4 *>(labels + p0)[0] = z;
-        reinterpret_cast<int4 *>(labels + p0)[1] = z;
-        if (score && ((uintptr_t)score & 15u) == 0) {
-            const float4 zf = {0.0f, 0.0f, 0.0f, 0.0f};
-            reinterpret_cast<float4 *>(score + p0)[0] = zf;
-            reinterpret_cast<float4 *>(score + p0)[1] = zf;
-        } else if (score) {
-#pragma unroll
-            for (int i = 0; i < kCompactPer; i++) score[p0 + i] = 0.0f;
+        for (int i = 0; i < kCompactPer; i++) {
+            const bool in = p0 + i < end;
+            valid |= (in ? 1u : 0u) << i;
+            m |= (in && v[i] > fg_thr ? 1u : 0u) << i;   // a NaN never exceeds the threshold
         }
-    } else if (bg) {
+        const int c = __popc(m);
+        int incl = c;                                      // inclusive prefix over the wave
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int t = __shfl_up(incl, d);
+            if (lane >= d) incl += t;
+        }
+        if (lane == 63) s_wave[wv] = incl;
+        __syncthreads();
+        int off = base + incl - c, tot = 0;
+#pragma unroll
+        for (int w = 0; w < kCompactThreads / 64; w++) {
+            const int n = s_wave[w];
+            off += w < wv ? n : 0;
+            tot += n;
+        }
+        __syncthreads();                                   // s_wave is rewritten in the next step
+        base += tot;
 #pragma unroll
         for (int i = 0; i < kCompactPer; i++)
-            if ((bg >> i) & 1u) {
-                labels[p0 + i] = 0;
-                if (score) score[p0 + i] = 0.0f;
+            if ((m >> i) & 1u) out[off++] = p0 + i;
+
+        // outputs of the pixels outside S
+        const uint32_t bg = valid & ~m;
+        if (bg == 0xffu) {
+            const int4 z = {0, 0, 0, 0};
+            reinterpret_cast<int4 *>(labels + p0)[0] = z;
+            reinterpret_cast<int4 *>(labels + p0)[1] = z;
+            if (score_vec) {
+                const float4 zf = {0.0f, 0.0f, 0.0f, 0.0f};
+                reinterpret_cast<float4 *>(score + p0)[0] = zf;
+                reinterpret_cast<float4 *>(score + p0)[1] = zf;
+            } else if (score) {
+#pragma unroll
+                for (int i = 0; i < kCompactPer; i++) score[p0 + i] = 0.0f;
             }
+        } else if (bg) {
+#pragma unroll
+            for (int i = 0; i < kCompactPer; i++)
+                if ((bg >> i) & 1u) {
+                    labels[p0 + i] = 0;
+                    if (score) score[p0 + i] = 0.0f;
+                }
+        }
     }
+    if (tid == 0) counts[blockIdx.x] = base;
 }
+
+// Exclusive prefix sums s_pref[0 .. nslices] of the slice counts (LDS), by
+// the whole block (blockDim.x >= 64, a multiple of 64); s_pref[nslices] = |S|.
+__device__ __forceinline__ void slice_prefix(const int32_t *__restrict__ counts, int nslices, int *s_pref)
+{
+    const int tid = threadIdx.x;
+    if (tid < 64) {
+        // each lane sums 4 consecutive slices, then one wave scan
+        int c[kMaxSlices / 64], sum = 0;
+#pragma unroll
+        for (int k = 0; k < kMaxSlices / 64; k++) {
+            const int s = 4 * tid + k;
+            c[k] = s < nslices ? counts[s] : 0;
+            sum += c[k];
+        }
+        int incl = sum;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int t = __shfl_up(incl, d);
+            if (tid >= d) incl += t;
+        }
+        int run = incl - sum;
+#pragma unroll
+        for (int k = 0; k < kMaxSlices / 64; k++) {
+            const int s = 4 * tid + k;
+            if (s <= nslices) s_pref[s] = run;
+            run += c[k];
+        }
+        if (tid == 63) s_pref[nslices] = incl;
+    }
+    __syncthreads();
+}
+
+// The concatenated slices seen by one lane whose positions never decrease:
+// entry i is list[s R + i - pref[s]] for the slice s with pref[s] <= i <
+// pref[s + 1] (found by bisection once, then by stepping forward).  Without
+// a list (every pixel participates) entry i is pixel i.
+struct ListCursor {
+    const int32_t *list;
+    const int *pref;          // LDS, pref[0 .. nslices]
+    int R, s, lo, hi;
+
+    __device__ __forceinline__ void start(const int32_t *list_, const int *pref_, int nslices, int R_, int i)
+    {
+        list = list_;
+        pref = pref_;
+        R = R_;
+        if (!list) return;
+        int a = 0, b = nslices;   // pref[a] <= i < pref[b] for i < |S|
+        while (b - a > 1) {
+            const int m = (a + b) >> 1;
+            if (pref[m] <= i) a = m; else b = m;
+        }
+        s = a;
+        lo = pref[a];
+        hi = pref[a + 1];
+    }
+    __device__ __forceinline__ int pixel(int i)
+    {
+        if (!list) return i;
+        while (i >= hi) {
+            s++;
+            lo = hi;
+            hi = pref[s + 1];
+        }
+        return list[(size_t)s * R + (i - lo)];
+    }
+};
 
 }  // namespace cpe

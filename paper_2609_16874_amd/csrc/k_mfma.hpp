@@ -2,11 +2,11 @@
 //
 // Both passes stream the compact list of participating pixels written by
 // k_compact (or every pixel, when the frame has no foreground channel): the
-// list is cut into tiles of 32 consecutive entries, and wave w of the grid
-// takes tiles w, w + (waves in the grid), ..., always loading the embedding
-// rows of its next tile (and the list entries of the one after) before it
-// computes the current one.  Every tile but the last is full, and every wave
-// gets the same number of tiles to within one.
+// list is cut into tiles of 32 consecutive entries, and every wave of the
+// grid takes a contiguous run of tiles of the same length to within one,
+// always loading the embedding rows of its next tile (and the list entries
+// of the one after) before it computes the current one.  Every tile but the
+// last is full.
 //
 // Per-axis distances (Eq4/Eq10).  S = |X - P|^2 = |X|^2 + |P|^2 - 2 X.P,
 // where X.(-2P) is a dense [pixels x channels] x [channels x bins]
@@ -36,6 +36,7 @@
 #pragma once
 
 #include "cpe_common.hpp"
+#include "k_compact.hpp"
 #include "k_peaks.hpp"
 
 namespace cpe {
@@ -48,7 +49,6 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
 constexpr int kPopBytes = 2 * 2 * 2 * 64 * 16;   // palette operands of both axes, limbs and K-steps
-constexpr int kTicketGroups = 16;    // first level of the vote kernel's completion count
 
 template <int F>
 struct AxisShape {
@@ -234,23 +234,13 @@ __device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t nx, uin
     return __float_as_uint((float)s1);
 }
 
-// The list of participating pixels: entry i is list[i] (or pixel i when
-// there is no list).  Lanes past the end of the list take the entry `base`
-// of their tile or group, which is always valid (their votes are masked,
-// their labels not written).
-struct TileStream {
-    const int32_t *list;     // nullptr: entry i is pixel i
-    int n;                   // list length
-
-    __device__ __forceinline__ int entry(int i, int base) const
-    {
-        const int e = i < n ? i : base;
-        return list ? list[e] : e;
-    }
-};
-
-// Number of participating pixels: |S| from the compaction, or every pixel.
-__device__ __forceinline__ int list_length(const int32_t *count, int npix) { return count ? *count : npix; }
+// Tiles [first, last) of wave w of nw when ntiles tiles are shared out in
+// contiguous runs.
+__device__ __forceinline__ void wave_run(int ntiles, int w, int nw, int &first, int &last)
+{
+    first = (int)((int64_t)ntiles * w / nw);
+    last = (int)((int64_t)ntiles * (w + 1) / nw);
+}
 
 // ---------------------------------------------------------------------------
 // Pass 1: recovery + soft voting (+ the peak extraction in the last workgroup)
@@ -259,7 +249,7 @@ __device__ __forceinline__ int list_length(const int32_t *count, int npix) { ret
 // the palette operands, and per wave the squared norms of one tile.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * 64 * 4;
+    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4;
 }
 
 // Waves per SIMD the register allocation must allow: three for fp16 inputs
@@ -280,9 +270,9 @@ constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 // counts of the centroid records, which the assignment launch accumulates.
 template <typename T, int F>
 __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
-    const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ count, int32_t npix,
-    Tables tb, int32_t Bw, int32_t Bh, unsigned long long *__restrict__ hrep, cpe_centroid *__restrict__ cents,
-    int32_t cap)
+    const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ counts, int32_t nslices,
+    int32_t slice_px, int32_t npix, Tables tb, int32_t Bw, int32_t Bh, unsigned long long *__restrict__ hrep,
+    cpe_centroid *__restrict__ cents, int32_t cap)
 {
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
@@ -293,6 +283,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
     int32_t *s_nrm = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);            // [kWpb][64]
+    int *s_pref = s_nrm + kWpb * 64;                                                  // [kMaxSlices + 1]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -310,6 +301,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             if (i < kN) reinterpret_cast<u32x4 *>(s_wt)[i] = w[k];
         }
         for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_h[i] = 0ull;
+        if (list) slice_prefix(counts, nslices, s_pref);
         for (int i = tid; i < kPopBytes / 16; i += kThreads)
             reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
     }
@@ -415,27 +407,28 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // the wave's tiles: t = gw, gw + nw, ...
-    const int n = list_length(count, npix), ntiles = (n + 31) >> 5;
-    const int nw = gridDim.x * kWpb;
-    const TileStream ts{list, n};
-    int t = blockIdx.x * kWpb + wv;
+    // the wave's run of tiles
+    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
+    int t, tend;
+    wave_run(ntiles, blockIdx.x * kWpb + wv, gridDim.x * kWpb, t, tend);
+    ListCursor cur_list;
+    cur_list.start(list, s_pref, nslices, slice_px, 32 * t + ln < n ? 32 * t + ln : 0);
+    // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
+    auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
     RawSlices<T, F> raw;
-    auto pixel = [&](int tt) { return ts.entry(32 * tt + ln, 32 * tt); };
     int idx = 0;                                       // pixel of this lane in the tile after the next
-    if (t < ntiles) {
+    if (t < tend) {
         raw.load(emb + (size_t)pixel(t) * D, g);
-        if (t + nw < ntiles) idx = pixel(t + nw);
+        if (t + 1 < tend) idx = pixel(t + 1);
     }
-    while (t < ntiles) {
-        const int tn = t + nw;
+    while (t < tend) {
         const RawSlices<T, F> cur = raw;
-        if (tn < ntiles) {
+        if (t + 1 < tend) {
             raw.load(emb + (size_t)idx * D, g);
-            if (tn + nw < ntiles) idx = pixel(tn + nw);
+            if (t + 2 < tend) idx = pixel(t + 2);
         }
         tile(cur, min(32, n - 32 * t));
-        t = tn;
+        t++;
     }
     fold();
 
@@ -459,7 +452,8 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // [32 bins][64 pixels] (u16), then the peak-extraction state.
 constexpr size_t kAssignLds = (size_t)kCKeys * 2 + (size_t)kMaxBatchLds * 20 + kMfmaBins * kMfmaBins * 2 +
                               kMfmaBins * kMfmaBins * 4 +
-                              (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2) + sizeof(PeakLds);
+                              (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2) + sizeof(PeakLds) +
+                              (kMaxSlices + 1) * 4;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -468,11 +462,10 @@ constexpr size_t kAssignLds = (size_t)kCKeys * 2 + (size_t)kMaxBatchLds * 20 + k
 // next frame's vote launch accumulates into.
 template <typename T, int F>
 __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const int32_t *__restrict__ list,
-                                                     const int32_t *__restrict__ count, int32_t npix,
-                                                     uint32_t tau_code, Tables tb,
+                                                     const int32_t *__restrict__ counts, int32_t nslices,
+                                                     int32_t slice_px, int32_t npix, uint32_t tau_code, Tables tb,
                                                      const unsigned long long *__restrict__ hcur,
                                                      unsigned long long *__restrict__ hzero,
-                                                     int32_t *__restrict__ count_next,
                                                      unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
                                                      long long cut, int32_t cap, cpe_centroid *__restrict__ cents,
                                                      int32_t *__restrict__ num, int32_t *__restrict__ labels,
@@ -480,6 +473,8 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
 {
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
+    static_assert(kWpb2 * 64 == kPeakThreads, "the peak prologue takes two histogram slots per thread");
+    static_assert(kAssignLds <= 160 * 1024, "LDS of one compute unit");
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kAssignLds];
     uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                           // [kCKeys]
@@ -490,6 +485,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins);  // [kWpb2][32][64]
     uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
     PeakLds &pl = *reinterpret_cast<PeakLds *>(s_cy + kWpb2 * kMfmaBins * 64);
+    int *s_pref = reinterpret_cast<int *>(&pl + 1);                                 // [kMaxSlices + 1]
     // the summed histogram lives in the x-key arrays until the peaks are known
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_kx);
 
@@ -497,6 +493,8 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     const int g = lane >> 5, ln = lane & 31;
     const int nb = Bw * Bh;
 
+    PeakLoad pld;                                   // issued before the table staging
+    peaks_lds_load(hcur, Bw, Bh, pld);
     {
         constexpr int kThreads = kWpb2 * 64;
         u32x4 w[kCKeys / 8 / kThreads];
@@ -507,11 +505,12 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         for (int k = 0; k < kCKeys / 8 / kThreads; k++) reinterpret_cast<u32x4 *>(s_ct)[k * kThreads + tid] = w[k];
     }
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) s_cnt[i] = 0;
-    peaks_lds(hcur, Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank);
+    if (list) slice_prefix(counts, nslices, s_pref);
+    peaks_lds(pld, Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank);
     const int Kc = pl.Kc;
     if (blockIdx.x == 0) {
         for (int k = tid; k < Kc; k += blockDim.x) {
-            const int i = pl.pk[k], a = i % Bw, b = i / Bw;
+            const int i = pl.pk[k], a = i & 31, b = i >> 5;
             cpe_centroid *c = cents + k;    // npix was reset by the vote launch and is counted below
             c->bin_x = a;
             c->bin_y = b;
@@ -520,24 +519,26 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
             c->score = (double)s_h[i] * 0x1p-30;
             c->reserved = 0;
         }
-        for (int i = tid; i < nb; i += blockDim.x) hlast[i] = s_h[i];
-        if (tid == 0) {
-            *num = pl.K;
-            *count_next = 0;
-        }
+        for (int i = tid; i < nb; i += blockDim.x) hlast[i] = s_h[(i / Bw) * 32 + i % Bw];
+        if (tid == 0) *num = pl.K;
     }
     for (int i = blockIdx.x * blockDim.x + tid; i < kReplicas * nb; i += gridDim.x * blockDim.x) hzero[i] = 0ull;
     __syncthreads();            // s_h is overwritten by the key arrays from here on
 
-    // the wave's groups of 64 list entries: j = gw, gw + nw, ...
-    const int n = list_length(count, npix), ngroups = (n + 63) >> 6;
-    const int nw = gridDim.x * kWpb2;
-    const TileStream ts{list, n};
+    // the wave's run of groups of 64 list entries
+    const int n = list ? s_pref[nslices] : npix, ngroups = (n + 63) >> 6;
+    int j, jend;
+    wave_run(ngroups, blockIdx.x * kWpb2 + wv, gridDim.x * kWpb2, j, jend);
     if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
-        for (int i = (blockIdx.x * kWpb2 + wv) * 64 + lane; i < n; i += nw * 64) {
-            const int p = ts.entry(i, 0);
-            labels[p] = 0;
-            if (score_map) score_map[p] = 0.0f;
+        ListCursor c0;
+        c0.start(list, s_pref, nslices, slice_px, 64 * j + lane < n ? 64 * j + lane : 0);
+        for (; j < jend; j++) {
+            const int i = 64 * j + lane;
+            if (i < n) {
+                const int p = c0.pixel(i);
+                labels[p] = 0;
+                if (score_map) score_map[p] = 0.0f;
+            }
         }
         return;
     }
@@ -635,34 +636,37 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    // lane (m, h) of group j loads entry 64 j + 32 h' + m for both halves h'
-    // and labels entry 64 j + 32 h + m, i.e. slot lane
-    auto pixel = [&](int j, int h) { return ts.entry(64 * j + 32 * h + ln, 64 * j); };
-    int j = blockIdx.x * kWpb2 + wv;
+    // lane (m, h) of group jj loads entries 64 jj + m and 64 jj + 32 + m (the
+    // group's first entry past the end) and labels entry 64 jj + 32 h + m,
+    // i.e. slot lane; one list cursor per half
+    ListCursor lc0, lc1;
+    lc0.start(list, s_pref, nslices, slice_px, 64 * j + ln < n ? 64 * j + ln : 0);
+    lc1.start(list, s_pref, nslices, slice_px, 64 * j + 32 + ln < n ? 64 * j + 32 + ln : 0);
+    auto pixel0 = [&](int jj) { return lc0.pixel(64 * jj + ln < n ? 64 * jj + ln : 64 * jj); };
+    auto pixel1 = [&](int jj) { return lc1.pixel(64 * jj + 32 + ln < n ? 64 * jj + 32 + ln : 64 * jj); };
     RawSlices<T, F> raw;
     int ip0 = 0, ip1 = 0;
-    if (j < ngroups) {
-        ip0 = pixel(j, 0);
-        ip1 = pixel(j, 1);
+    if (j < jend) {
+        ip0 = pixel0(j);
+        ip1 = pixel1(j);
         raw.load(emb + (size_t)ip0 * D, g);
     }
-    while (j < ngroups) {
-        const int jn = j + nw;
+    while (j < jend) {
         RawSlices<T, F> cur = raw;
         raw.load(emb + (size_t)ip1 * D, g);
         int np0 = 0, np1 = 0;
-        if (jn < ngroups) {
-            np0 = pixel(jn, 0);
-            np1 = pixel(jn, 1);
+        if (j + 1 < jend) {
+            np0 = pixel0(j + 1);
+            np1 = pixel1(j + 1);
         }
         codes(cur, 0);
         cur = raw;
-        if (jn < ngroups) raw.load(emb + (size_t)np0 * D, g);
+        if (j + 1 < jend) raw.load(emb + (size_t)np0 * D, g);
         codes(cur, 1);
         search(g ? ip1 : ip0, min(64, n - 64 * j));
         ip0 = np0;
         ip1 = np1;
-        j = jn;
+        j++;
     }
     __syncthreads();
     for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)

@@ -113,62 +113,133 @@ __device__ __forceinline__ int compact_peaks(const unsigned long long *s_h, int 
 // ---------------------------------------------------------------------------
 // Grids up to 32 x 32: candidates in LDS, in the assignment kernel's prologue
 // ---------------------------------------------------------------------------
+// The histogram is held in a 32 x 32 slot layout, slot b * 32 + a, whose
+// order agrees with the bin order b * B_w + a.  A block of kPeakThreads
+// threads handles two slots per thread: t and t + kPeakThreads.
 constexpr int kLdsPeakBins = 32;
+constexpr int kPeakThreads = 512;
+constexpr int kMaxBatchLds = 128;   // <= 16 strict maxima per row of 32 -> <= 4 batches per row
 
 // LDS of peaks_lds (the summed histogram may alias any scratch the caller
 // does not need until the peaks are known).
 struct PeakLds {
-    CompactScratch cs;
+    int wave[2 * kPeakThreads / 64];  // per-wave counts of the two slot passes
     uint32_t rowmask[kLdsPeakBins];   // bit a of row b: (a, b) is one of the first min(K, cap) candidates
-    int nbt[kLdsPeakBins];            // batches of row b
     int K, Kc, nbat;
-    int pk[max_peaks(kLdsPeakBins, kLdsPeakBins)];
+    int pk[max_peaks(kLdsPeakBins, kLdsPeakBins)];   // candidate slots b * 32 + a, ascending
 };
 
-// Sum the kReplicas vote histograms `hsrc` (written by the previous launch)
-// into s_h, find and compact the candidates, and build in LDS the bin ->
-// candidate-index table s_rank [32 * 32] and the candidate batches s_bo /
-// s_bh (at most kMaxBatchLds, padded to a multiple of 4).  Every thread of
-// the block calls it; on return pl.K, pl.Kc, pl.nbat and pl.pk are set.
-constexpr int kMaxBatchLds = 128;   // <= 16 strict maxima per row of 32 -> <= 4 batches per row
-__device__ __forceinline__ void peaks_lds(const unsigned long long *__restrict__ hsrc, int Bw, int Bh, long long cut,
-                                          int cap, unsigned long long *s_h, PeakLds &pl, u32x4_pk *s_bo,
-                                          uint32_t *s_bh, uint16_t *s_rank)
+// The vote counts of this thread's two slots, summed over the kReplicas
+// histograms `hsrc` ([kReplicas][Bh][Bw], written by the previous launch).
+// Issued first, so that their latency overlaps the caller's table staging.
+struct PeakLoad {
+    unsigned long long v[2][kReplicas];
+};
+__device__ __forceinline__ void peaks_lds_load(const unsigned long long *__restrict__ hsrc, int Bw, int Bh,
+                                               PeakLoad &ld)
 {
-    const int tid = threadIdx.x, nb = Bw * Bh;
-    for (int i = tid; i < nb; i += blockDim.x) {
-        unsigned long long v[kReplicas];
+    const int nb = Bw * Bh;
 #pragma unroll
-        for (int r = 0; r < kReplicas; r++) v[r] = hsrc[(size_t)r * nb + i];
-        unsigned long long s = 0;
+    for (int u = 0; u < 2; u++) {
+        const int slot = u * kPeakThreads + (int)threadIdx.x, a = slot & 31, b = slot >> 5;
+        const bool in = a < Bw && b < Bh;
 #pragma unroll
-        for (int r = 0; r < kReplicas; r++) s += v[r];
-        s_h[i] = s;
+        for (int r = 0; r < kReplicas; r++) ld.v[u][r] = in ? hsrc[(size_t)r * nb + b * Bw + a] : 0ull;
+    }
+}
+
+// Strict 8-neighbour local maximum of slot (a, b) of s_h above `cut`;
+// out-of-range neighbours are ignored.
+__device__ __forceinline__ bool is_peak32(const unsigned long long *s_h, int a, int b, int Bw, int Bh, long long cut)
+{
+    const unsigned long long v = s_h[b * 32 + a];
+    bool f = a < Bw && b < Bh && (long long)v > cut;
+#pragma unroll
+    for (int db = -1; db <= 1; db++)
+#pragma unroll
+        for (int da = -1; da <= 1; da++) {
+            if (!da && !db) continue;
+            const int nb_ = b + db, na = a + da;
+            const bool in = nb_ >= 0 && nb_ < Bh && na >= 0 && na < Bw;
+            const unsigned long long w = s_h[in ? nb_ * 32 + na : b * 32 + a];   // self when out of range
+            f = f && (!in || v > w);
+        }
+    return f;
+}
+
+// From the loaded counts: the summed histogram s_h (32 x 32 slots), the
+// candidates compacted in ascending bin order (pl.pk), K and min(K, cap),
+// the bin -> candidate-index table s_rank [32 * 32] and the candidate
+// batches s_bo / s_bh (pl.nbat of them, a multiple of 4).  Called by every
+// thread of a block of kPeakThreads threads.
+__device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, long long cut, int cap,
+                                          unsigned long long *s_h, PeakLds &pl, u32x4_pk *s_bo, uint32_t *s_bh,
+                                          uint16_t *s_rank)
+{
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    constexpr int kWaves = kPeakThreads / 64;
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+        unsigned long long sum = 0;
+#pragma unroll
+        for (int r = 0; r < kReplicas; r++) sum += ld.v[u][r];
+        s_h[u * kPeakThreads + tid] = sum;
     }
     if (tid < kLdsPeakBins) pl.rowmask[tid] = 0u;
-    const int K = compact_peaks(s_h, Bw, Bh, cut, pl.pk, pl.cs, [&](int i, int pos) {
-        if (pos < cap) atomicOr(&pl.rowmask[i / Bw], 1u << (i % Bw));
-    });
-    const int Kc = K < cap ? K : cap;
-    for (int k = tid; k < Kc; k += blockDim.x) {
-        const int i = pl.pk[k];
-        s_rank[(i / Bw) * kLdsPeakBins + i % Bw] = (uint16_t)k;
-    }
-    // strict maxima are never horizontally adjacent: <= 16 per row, <= 4 batches
-    if (tid < kLdsPeakBins) pl.nbt[tid] = min((__popc(pl.rowmask[tid]) + 3) >> 2, kMaxBatchLds / kLdsPeakBins);
     __syncthreads();
-    if (tid < kLdsPeakBins) {
-        const int b = tid;
-        int start = 0, total = 0;
-        for (int r = 0; r < kLdsPeakBins; r++) {
-            const int n = pl.nbt[r];
-            start += r < b ? n : 0;
-            total += n;
+    bool flag[2];
+    unsigned long long mask[2];
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+        const int slot = u * kPeakThreads + tid;
+        flag[u] = is_peak32(s_h, slot & 31, slot >> 5, Bw, Bh, cut);
+        mask[u] = __ballot(flag[u]);
+    }
+    if (lane == 0) {
+        pl.wave[wid] = __popcll(mask[0]);
+        pl.wave[kWaves + wid] = __popcll(mask[1]);
+    }
+    __syncthreads();
+    int off0 = 0, off1 = 0, K = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; w++) {
+        const int n0 = pl.wave[w], n1 = pl.wave[kWaves + w];
+        off0 += w < wid ? n0 : 0;
+        off1 += n0 + (w < wid ? n1 : 0);
+        K += n0 + n1;
+    }
+    const int Kc = K < cap ? K : cap;
+#pragma unroll
+    for (int u = 0; u < 2; u++) {
+        if (flag[u]) {
+            const int slot = u * kPeakThreads + tid;
+            const int pos = (u ? off1 : off0) + lane_prefix(mask[u]);   // < max_peaks(32, 32)
+            pl.pk[pos] = slot;
+            if (pos < Kc) {
+                s_rank[slot] = (uint16_t)pos;
+                atomicOr(&pl.rowmask[slot >> 5], 1u << (slot & 31));
+            }
         }
-        uint32_t m = pl.rowmask[b], last = 0;
-        const int nbt = pl.nbt[b];
+    }
+    __syncthreads();
+    // batches: lane b of the first wave builds row b's (strict maxima are
+    // never horizontally adjacent: <= 16 per row, <= 4 batches)
+    if (tid < 64) {
+        const int b = tid;
+        uint32_t m = b < kLdsPeakBins ? pl.rowmask[b] : 0u;
+        const int nbt = (__popc(m) + 3) >> 2;
+        int incl = nbt;
+#pragma unroll
+        for (int d = 1; d < 32; d <<= 1) {
+            const int t = __shfl_up(incl, d);
+            if (lane >= d) incl += t;
+        }
+        const int start = incl - nbt, total = __shfl(incl, 31);
+        const int padded = (total + 3) & ~3;
+        uint32_t last = 0;
         u32x4_pk o = {0u, 0u, 0u, 0u};
         for (int j = 0; j < nbt; j++) {
+#pragma unroll
             for (int s4 = 0; s4 < 4; s4++) {
                 if (m) {
                     last = (uint32_t)__builtin_ctz(m) * 256u;
@@ -181,14 +252,12 @@ __device__ __forceinline__ void peaks_lds(const unsigned long long *__restrict__
         }
         // pad the list to a multiple of 4 with copies of the last batch (a
         // repeated batch leaves every minimum unchanged)
-        const int padded = (total + 3) & ~3;
-        if (nbt > 0 && start + nbt == total) {
+        if (nbt > 0 && start + nbt == total)
             for (int e = total; e < padded; e++) {
                 s_bo[e] = o;
                 s_bh[e] = (uint32_t)b * 128u;
             }
-        }
-        if (b == 0) {
+        if (tid == 0) {
             pl.K = K;
             pl.Kc = Kc;
             pl.nbat = padded;

@@ -55,30 +55,29 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         unsigned long long *hcur = h->hrep + (size_t)par * kReplicas * nb;
         unsigned long long *hnext = h->hrep + (size_t)(par ^ 1) * kReplicas * nb;
         int32_t *list = g ? h->list : nullptr;
-        int32_t *count = g ? h->count + par : nullptr;
+        const int nslices = slice_count(npix), slice_px = slice_pixels(npix);
         if (g) {
-            const int cgrid = (int)(((int64_t)npix + kCompactSpan - 1) / kCompactSpan);
             if (((uintptr_t)g & 15u) == 0)
-                hipLaunchKernelGGL((k_compact<T, true>), dim3(cgrid), dim3(kCompactThreads), 0, stream, g, npix, fg_thr,
-                                   list, count, labels, score);
+                hipLaunchKernelGGL((k_compact<T, true>), dim3(nslices), dim3(kCompactThreads), 0, stream, g, npix,
+                                   fg_thr, list, h->counts, labels, score);
             else
-                hipLaunchKernelGGL((k_compact<T, false>), dim3(cgrid), dim3(kCompactThreads), 0, stream, g, npix,
-                                   fg_thr, list, count, labels, score);
+                hipLaunchKernelGGL((k_compact<T, false>), dim3(nslices), dim3(kCompactThreads), 0, stream, g, npix,
+                                   fg_thr, list, h->counts, labels, score);
         }
         // grids: at most one workgroup per compute unit, no more waves than tiles
         constexpr int wpb = kVoteWpb<T, F>;
         const int64_t tiles = ((int64_t)npix + 31) / 32;
         const int64_t wgs = (tiles + wpb - 1) / wpb;
         const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), 0, stream, e, list, count, npix, h->tb, Bw,
-                           Bh, hcur, cents, h->cap);
+        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), 0, stream, e, list, h->counts, nslices,
+                           slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap);
         mark(1);
         mark(2);
         const int64_t wgs2 = ((tiles + 1) / 2 + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, list, count, npix,
-                           fa.tau_code, h->tb, hcur, hnext, h->count + (par ^ 1), h->hlast, Bw, Bh, cut, h->cap, cents,
-                           num, labels, score);
+        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, list, h->counts,
+                           nslices, slice_px, npix, fa.tau_code, h->tb, hcur, hnext, h->hlast, Bw, Bh, cut, h->cap,
+                           cents, num, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
