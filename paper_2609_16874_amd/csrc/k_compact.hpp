@@ -1,7 +1,7 @@
 // k_compact.hpp -- the participating set S of Eq6 as a compact pixel list.
 //
 // One launch per frame before the vote.  Workgroup s of the grid owns the
-// pixel range [s R, (s + 1) R) (R a multiple of 2048) and writes the indices
+// pixel range [s R, (s + 1) R) (R a multiple of 8192) and writes the indices
 // of its participating pixels, in raster order, to its slice list[s R ..]
 // and their number to counts[s]; every lane tests 8 consecutive foreground
 // values against the threshold and a wave prefix sum gives the slots.  No
@@ -17,7 +17,7 @@
 
 namespace cpe {
 
-constexpr int kCompactThreads = 256;
+constexpr int kCompactThreads = 1024;
 constexpr int kCompactPer = 8;                                   // pixels per lane
 constexpr int kCompactSpan = kCompactThreads * kCompactPer;      // pixels per workgroup and step
 constexpr int kMaxSlices = 256;                                  // workgroups of the compaction

@@ -2,11 +2,12 @@
 //
 // Both passes stream the compact list of participating pixels written by
 // k_compact (or every pixel, when the frame has no foreground channel): the
-// list is cut into tiles of 32 consecutive entries, and every wave of the
-// grid takes a contiguous run of tiles of the same length to within one,
-// always loading the embedding rows of its next tile (and the list entries
-// of the one after) before it computes the current one.  Every tile but the
-// last is full.
+// list is cut into tiles of 32 consecutive entries, every workgroup gets a
+// contiguous run of tiles of the same length to within one, and its waves
+// take the run's tiles one at a time from a counter in LDS (so that they
+// finish together however the SIMDs favour older waves), always loading the
+// embedding rows of the next tile (and the list entries of the one after)
+// before computing the current one.  Every tile but the last is full.
 //
 // Per-axis distances (Eq4/Eq10).  S = |X - P|^2 = |X|^2 + |P|^2 - 2 X.P,
 // where X.(-2P) is a dense [pixels x channels] x [channels x bins]
@@ -234,12 +235,20 @@ __device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t nx, uin
     return __float_as_uint((float)s1);
 }
 
-// Tiles [first, last) of wave w of nw when ntiles tiles are shared out in
-// contiguous runs.
-__device__ __forceinline__ void wave_run(int ntiles, int w, int nw, int &first, int &last)
+// Tiles [first, last) of workgroup b of nb when ntiles tiles are shared out
+// in contiguous runs.
+__device__ __forceinline__ void block_run(int ntiles, int b, int nb, int &first, int &last)
 {
-    first = (int)((int64_t)ntiles * w / nw);
-    last = (int)((int64_t)ntiles * (w + 1) / nw);
+    first = (int)((int64_t)ntiles * b / nb);
+    last = (int)((int64_t)ntiles * (b + 1) / nb);
+}
+
+// Next tile of the workgroup's run from the LDS counter (wave-uniform).
+__device__ __forceinline__ int take_tile(int *next, int lane)
+{
+    int k = 0;
+    if (lane == 0) k = atomicAdd(next, 1);
+    return __builtin_amdgcn_readfirstlane(k);
 }
 
 // ---------------------------------------------------------------------------
@@ -249,7 +258,8 @@ __device__ __forceinline__ void wave_run(int ntiles, int w, int nw, int &first, 
 // the palette operands, and per wave the squared norms of one tile.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4;
+    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
+           16;
 }
 
 // Waves per SIMD the register allocation must allow: three for fp16 inputs
@@ -284,6 +294,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
     int32_t *s_nrm = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);            // [kWpb][64]
     int *s_pref = s_nrm + kWpb * 64;                                                  // [kMaxSlices + 1]
+    int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -305,6 +316,11 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         for (int i = tid; i < kPopBytes / 16; i += kThreads)
             reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
     }
+    // the workgroup's run of tiles
+    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
+    int t, tend;
+    block_run(ntiles, blockIdx.x, gridDim.x, t, tend);
+    if (tid == 0) *s_next = t;
     __syncthreads();
     const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
 
@@ -407,28 +423,29 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // the wave's run of tiles
-    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
-    int t, tend;
-    wave_run(ntiles, blockIdx.x * kWpb + wv, gridDim.x * kWpb, t, tend);
+    t = take_tile(s_next, lane);
     ListCursor cur_list;
-    cur_list.start(list, s_pref, nslices, slice_px, 32 * t + ln < n ? 32 * t + ln : 0);
+    cur_list.start(list, s_pref, nslices, slice_px, t < tend && 32 * t + ln < n ? 32 * t + ln : 0);
     // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
     auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
     RawSlices<T, F> raw;
-    int idx = 0;                                       // pixel of this lane in the tile after the next
+    int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it
     if (t < tend) {
         raw.load(emb + (size_t)pixel(t) * D, g);
-        if (t + 1 < tend) idx = pixel(t + 1);
+        tn = take_tile(s_next, lane);
+        if (tn < tend) idx = pixel(tn);
     }
     while (t < tend) {
         const RawSlices<T, F> cur = raw;
-        if (t + 1 < tend) {
+        int tnn = tend;
+        if (tn < tend) {
             raw.load(emb + (size_t)idx * D, g);
-            if (t + 2 < tend) idx = pixel(t + 2);
+            tnn = take_tile(s_next, lane);
+            if (tnn < tend) idx = pixel(tnn);
         }
         tile(cur, min(32, n - 32 * t));
-        t++;
+        t = tn;
+        tn = tnn;
     }
     fold();
 
@@ -453,7 +470,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 constexpr size_t kAssignLds = (size_t)kCKeys * 2 + (size_t)kMaxBatchLds * 20 + kMfmaBins * kMfmaBins * 2 +
                               kMfmaBins * kMfmaBins * 4 +
                               (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2) + sizeof(PeakLds) +
-                              (kMaxSlices + 1) * 4;
+                              (kMaxSlices + 1) * 4 + 16;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -486,6 +503,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
     PeakLds &pl = *reinterpret_cast<PeakLds *>(s_cy + kWpb2 * kMfmaBins * 64);
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                 // [kMaxSlices + 1]
+    int *s_next = s_pref + kMaxSlices + 1;                                           // next group of the run
     // the summed histogram lives in the x-key arrays until the peaks are known
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_kx);
 
@@ -525,23 +543,22 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     for (int i = blockIdx.x * blockDim.x + tid; i < kReplicas * nb; i += gridDim.x * blockDim.x) hzero[i] = 0ull;
     __syncthreads();            // s_h is overwritten by the key arrays from here on
 
-    // the wave's run of groups of 64 list entries
+    // the workgroup's run of groups of 64 list entries
     const int n = list ? s_pref[nslices] : npix, ngroups = (n + 63) >> 6;
     int j, jend;
-    wave_run(ngroups, blockIdx.x * kWpb2 + wv, gridDim.x * kWpb2, j, jend);
+    block_run(ngroups, blockIdx.x, gridDim.x, j, jend);
     if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
         ListCursor c0;
-        c0.start(list, s_pref, nslices, slice_px, 64 * j + lane < n ? 64 * j + lane : 0);
-        for (; j < jend; j++) {
-            const int i = 64 * j + lane;
-            if (i < n) {
-                const int p = c0.pixel(i);
-                labels[p] = 0;
-                if (score_map) score_map[p] = 0.0f;
-            }
+        c0.start(list, s_pref, nslices, slice_px, 64 * j + tid < n ? 64 * j + tid : 0);
+        for (int i = 64 * j + tid; i < min(64 * jend, n); i += blockDim.x) {
+            const int p = c0.pixel(i);
+            labels[p] = 0;
+            if (score_map) score_map[p] = 0.0f;
         }
         return;
     }
+    if (tid == 0) *s_next = j;
+    __syncthreads();
     const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of 4
 
     f16x8 pxh[KS], pxl[KS], pyh[KS], pyl[KS];
@@ -639,9 +656,10 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     // lane (m, h) of group jj loads entries 64 jj + m and 64 jj + 32 + m (the
     // group's first entry past the end) and labels entry 64 jj + 32 h + m,
     // i.e. slot lane; one list cursor per half
+    j = take_tile(s_next, lane);
     ListCursor lc0, lc1;
-    lc0.start(list, s_pref, nslices, slice_px, 64 * j + ln < n ? 64 * j + ln : 0);
-    lc1.start(list, s_pref, nslices, slice_px, 64 * j + 32 + ln < n ? 64 * j + 32 + ln : 0);
+    lc0.start(list, s_pref, nslices, slice_px, j < jend && 64 * j + ln < n ? 64 * j + ln : 0);
+    lc1.start(list, s_pref, nslices, slice_px, j < jend && 64 * j + 32 + ln < n ? 64 * j + 32 + ln : 0);
     auto pixel0 = [&](int jj) { return lc0.pixel(64 * jj + ln < n ? 64 * jj + ln : 64 * jj); };
     auto pixel1 = [&](int jj) { return lc1.pixel(64 * jj + 32 + ln < n ? 64 * jj + 32 + ln : 64 * jj); };
     RawSlices<T, F> raw;
@@ -654,19 +672,20 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     while (j < jend) {
         RawSlices<T, F> cur = raw;
         raw.load(emb + (size_t)ip1 * D, g);
+        const int jn = take_tile(s_next, lane);
         int np0 = 0, np1 = 0;
-        if (j + 1 < jend) {
-            np0 = pixel0(j + 1);
-            np1 = pixel1(j + 1);
+        if (jn < jend) {
+            np0 = pixel0(jn);
+            np1 = pixel1(jn);
         }
         codes(cur, 0);
         cur = raw;
-        if (j + 1 < jend) raw.load(emb + (size_t)np0 * D, g);
+        if (jn < jend) raw.load(emb + (size_t)np0 * D, g);
         codes(cur, 1);
         search(g ? ip1 : ip0, min(64, n - 64 * j));
         ip0 = np0;
         ip1 = np1;
-        j++;
+        j = jn;
     }
     __syncthreads();
     for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)
