@@ -17,7 +17,8 @@
  *
  * Arithmetic.  All discrete decisions use a fixed-point arithmetic that any
  * correct implementation reproduces bit for bit:
- *   X = rint(4096 clamp(v, -1.5, 1.5)) per channel (a NaN clamps to -1.5);
+ *   X = 16 rint(256 clamp(v, -1.5, 1.5)) per channel (a NaN clamps to -1.5):
+ *   the input rounded to 1/256, in units of 1/4096;
  *   palettes P = rint(4096 gamma(bin centre)), bin centre (a+1) W/(B_w+1);
  *   S = |X - P|^2 exactly (integer);
  *   the bucket of S is the exponent and top m mantissa bits of fl32(S+1);

@@ -20,8 +20,10 @@
  *                 Eq9 with u = 2x/W - 1 and continuous pixel coordinates)
  *   palette       P[a][2k] = rint(4096 sin(w_k x_a)), P[a][2k+1] =
  *                 rint(4096 cos(w_k x_a)), fp64, stored as int16
- *   input         X = rintf(4096.0f * clamp(v, -1.5, 1.5)), fp32, where a
- *                 NaN channel clamps to -1.5
+ *   input         X = 16 rintf(256.0f * clamp(v, -1.5, 1.5)), fp32, where a
+ *                 NaN channel clamps to -1.5: the input rounded to 1/256
+ *                 (its error varies from pixel to pixel and averages out in
+ *                 the votes) in the palette's 1/4096 units
  *   participation p in S  <=>  (float)fg(p) > fg_threshold; with no fg
  *                 channel every pixel is in S (the set of Section 3.1)
  *   distance      S_x = sum_c (X_c - P[a][c])^2 (exact integer); with
@@ -65,7 +67,8 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define FIX_SCALE 4096.0f       /* input and palette fixed-point scale      */
+#define FIX_SCALE 4096.0f       /* palette and distance fixed-point scale    */
+#define IN_GRID 256.0f          /* inputs are rounded to multiples of 1/256  */
 #define V_CLAMP 1.5f            /* inputs are clamped to [-1.5, 1.5]         */
 #define W_MANT 8                /* mantissa bits of fl32(S+1): weight bucket */
 #define C_MANT 9                /* mantissa bits of fl32(S+1): code bucket   */
@@ -95,13 +98,14 @@ static float load_value(const void *base, int32_t dtype, size_t index)
     return half_to_float(((const uint16_t *)base)[index]);
 }
 
-/* Input to fixed point: clamp to [-1.5, 1.5] (NaN -> -1.5), scale, round. */
+/* Input to fixed point: clamp to [-1.5, 1.5] (NaN -> -1.5), round to the
+ * nearest multiple of 1/256, express in units of 1/4096. */
 static int32_t to_fixed(float v)
 {
     float c = v;
     if (isnan(c) || c < -V_CLAMP) c = -V_CLAMP;
     if (c > V_CLAMP) c = V_CLAMP;
-    return (int32_t)rintf(FIX_SCALE * c);
+    return (int32_t)(FIX_SCALE / IN_GRID) * (int32_t)rintf(IN_GRID * c);
 }
 
 /* m-bit distance bucket of an exact squared distance S: the exponent and

@@ -16,8 +16,9 @@
  *   counts (mask-aggregation paragraph).
  *
  * Two arithmetic modes:
- *   cpe_oracle_decode       canonical fixed-point arithmetic: integer inputs
- *                           and palettes (x4096), exact integer squared
+ *   cpe_oracle_decode       canonical fixed-point arithmetic: inputs rounded
+ *                           to 1/256 and palettes to 1/4096, both in units of
+ *                           1/4096, exact integer squared
  *                           distances, distance buckets given by the
  *                           exponent and top mantissa bits of fl32(S+1) with
  *                           tables of 2^15 e^-d weights (8-bit buckets) and

@@ -45,12 +45,13 @@ struct Tables {
     const uint16_t *ct_pm;    // [kCKeys] code at LDS position ((e + 31) & 31) * 512 + t
 };
 
-// Input to fixed point: rint(4096 clamp(v, -1.5, 1.5)); a NaN clamps to -1.5
+// Input to fixed point: 16 rint(256 clamp(v, -1.5, 1.5)), the input on a
+// 1/256 grid in the palette's units of 1/4096; a NaN clamps to -1.5
 // (fmaxf/fminf return the non-NaN operand).
 __device__ __forceinline__ int32_t to_fixed(float v)
 {
     const float c = fminf(fmaxf(v, -1.5f), 1.5f);
-    return (int32_t)rintf(c * 4096.0f);
+    return 16 * (int32_t)rintf(c * 256.0f);
 }
 
 __device__ __forceinline__ int32_t pack2(int32_t lo, int32_t hi)

@@ -9,14 +9,17 @@
 // embedding rows of the next tile (and the list entries of the one after)
 // before computing the current one.  Every tile but the last is full.
 //
-// Per-axis distances (Eq4/Eq10).  S = |X - P|^2 = |X|^2 + |P|^2 - 2 X.P,
-// where X.(-2P) is a dense [pixels x channels] x [channels x bins]
-// contraction: v_mfma_f32_32x32x16_f16 with X as fp16 (for fp16 inputs every
-// clamped, scaled, rounded value is exactly representable; fp32 inputs add
-// the residual X - fp16(X) as a second operand) against -2P split into two
-// fp16 limbs, -2P = 128 hi + lo with |hi|, |lo| <= 64.  Every partial sum is
-// an integer below 2^24 in magnitude, so both fp32 accumulators are exact
-// and S is assembled exactly in 32-bit integer arithmetic.
+// Per-axis distances (Eq4/Eq10).  With the input on its 1/256 grid,
+// X = 16 Xr (Xr = rint(256 clamp(v, -1.5, 1.5)), |Xr| <= 384, exact in fp16)
+// and the palette limbs -2P = 128 hi + lo (|hi|, |lo| <= 64, exact in fp16),
+// S + 1 = 256 |Xr|^2 + (|P|^2 + 1) + 16 (128 Xr.hi + Xr.lo).  The two dot
+// products are dense [pixels x channels] x [channels x bins] contractions:
+// v_mfma_f32_32x32x16_f16 accumulating onto 1.5 * 2^23, where every partial
+// sum (at most 32 * 384 * 64 < 2^22 in magnitude) stays in the binade of unit
+// spacing, so the accumulator's bit pattern minus 0x4B400000 is the exact
+// integer: S + 1 follows from the two bit patterns with two shift-adds and
+// one add, modulo 2^32 (S + 1 < 2^32).  |Xr|^2 <= 32 * 384^2 < 2^24 is an
+// exact fp32 dot product of the fp16 operands.
 //
 // Pass 1, k_vote_mfma (recovery + soft voting, Eq5/Eq6/Eq11).  With pixels
 // as the MFMA rows, the distance result leaves in each lane one bin and 16
@@ -57,44 +60,37 @@ struct AxisShape {
     static constexpr int KS = (C + 15) / 16;    // MFMA K-steps of 16 channels
 };
 
-// Scale, clamp and round a pair of fp16 inputs to fixed-point integers (kept
-// as fp16, exact) and accumulate their squares.  Scaling first is exact (a
-// power of two; overflow gives +-inf, which the clamp maps like any value
-// beyond 1.5), and it lets the clamp see a canonical operand: a NaN becomes
-// -6144 because max returns the non-NaN operand.
-__device__ __forceinline__ f16x2 fix_pair_f16(f16x2 v, int32_t &n2)
+// The fp32 value 1.5 * 2^23 (bit pattern 0x4B400000) onto which the limb
+// accumulators are summed.
+constexpr float kMagic = 12582912.0f;
+constexpr uint32_t kMagicBits = 0x4B400000u;
+
+// Round a pair of fp16 inputs to the 1/256 grid, clamped to [-1.5, 1.5]:
+// Xr = rint(256 v) as fp16, and accumulate Xr^2 (exact in fp32).  The
+// rounding is one fused multiply-add onto 1536: for |256 v| <= 512 the sum
+// lies in [1024, 2048], where fp16 spacing is 1, so it is rounded to the
+// nearest integer, ties to even (1536 is even); larger magnitudes (and
+// overflow to +-inf) leave that range and are clamped to 1536 +- 384 like
+// any value beyond 1.5.  A NaN clamps to 1536 - 384 (max returns the
+// non-NaN operand), i.e. to -1.5.
+__device__ __forceinline__ f16x2 fix_pair_f16(f16x2 v, float &n2)
 {
-    const f16x2 lo = {(_Float16)-6144.0f, (_Float16)-6144.0f}, hi = {(_Float16)6144.0f, (_Float16)6144.0f};
-    v = v * (f16x2){(_Float16)4096.0f, (_Float16)4096.0f};
-    v = __builtin_elementwise_max(v, lo);
-    v = __builtin_elementwise_min(v, hi);
-    f16x2 r;
-    r[0] = __builtin_rintf16(v[0]);
-    r[1] = __builtin_rintf16(v[1]);
-    const v2s si = {(short)r[0], (short)r[1]};
-    n2 = __builtin_amdgcn_sdot2(si, si, n2, false);
+    const f16x2 k256 = {(_Float16)256.0f, (_Float16)256.0f}, k1536 = {(_Float16)1536.0f, (_Float16)1536.0f};
+    const f16x2 lo = {(_Float16)1152.0f, (_Float16)1152.0f}, hi = {(_Float16)1920.0f, (_Float16)1920.0f};
+    f16x2 r = __builtin_elementwise_fma(v, k256, k1536);
+    r = __builtin_elementwise_max(r, lo);
+    r = __builtin_elementwise_min(r, hi);
+    r = r - k1536;
+    n2 = __builtin_amdgcn_fdot2(r, r, n2, false);
     return r;
 }
 
-// fp32 input: X = rint(4096 clamp(v, -1.5, 1.5)) may exceed fp16's 11-bit
-// significand, so it is fed to the matrix cores as fp16(X) plus the exact
-// residual X - fp16(X) (|residual| <= 2), both accumulated into the same sums.
-__device__ __forceinline__ void fix_f32(float v, _Float16 &main, _Float16 &rest, short &si)
+// fp32 input: Xr = rint(256 clamp(v, -1.5, 1.5)) (a NaN clamps to -1.5, as
+// fmaxf returns the non-NaN operand), exact in fp16.
+__device__ __forceinline__ _Float16 fix_f32(float v)
 {
-    const float t = rintf(fminf(fmaxf(v * 4096.0f, -6144.0f), 6144.0f));
-    si = (short)t;
-    main = (_Float16)t;
-    rest = (_Float16)(t - (float)main);
+    return (_Float16)rintf(fminf(fmaxf(v * 256.0f, -384.0f), 384.0f));
 }
-
-// Fixed-point channel values of one lane's operand slice.  For fp16 inputs
-// every value is exact in fp16 and `rest` stays zero.
-struct Fix8 {
-    f16x8 main, rest;
-};
-
-template <typename T>
-constexpr bool kNeedsRest = sizeof(T) == 4;
 
 // Raw input words of one lane's operand slices: for each axis and K-step j
 // the 8 channels [16 j + 8 g, 16 j + 8 g + 8) of one pixel (channels past 2F
@@ -144,13 +140,11 @@ struct RawSlices {
             }
     }
 
-    // Fixed-point operands of one axis and its partial squared norm.
-    __device__ __forceinline__ void convert(int ax, Fix8 (&X)[KS], int32_t &n2) const
+    // Rounded operands of one axis and its partial |Xr|^2.
+    __device__ __forceinline__ void convert(int ax, f16x8 (&X)[KS], float &n2) const
     {
 #pragma unroll
         for (int j = 0; j < KS; j++) {
-            Fix8 &out = X[j];
-            out.rest = (f16x8){};
             if constexpr (kVecH) {
                 u32x4 res;
 #pragma unroll
@@ -163,20 +157,15 @@ struct RawSlices {
                     __builtin_memcpy(&o, &r, 4);
                     res[q] = o;
                 }
-                out.main = __builtin_bit_cast(f16x8, res);
+                X[j] = __builtin_bit_cast(f16x8, res);
             } else {
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
-                    short s0, s1;
-                    _Float16 m0, m1, r0, r1;
-                    fix_f32(__uint_as_float(w[ax][j][2 * q]), m0, r0, s0);
-                    fix_f32(__uint_as_float(w[ax][j][2 * q + 1]), m1, r1, s1);
-                    out.main[2 * q] = m0;
-                    out.main[2 * q + 1] = m1;
-                    out.rest[2 * q] = r0;
-                    out.rest[2 * q + 1] = r1;
-                    const v2s si = {s0, s1};
-                    n2 = __builtin_amdgcn_sdot2(si, si, n2, false);
+                    const f16x2 r = {fix_f32(__uint_as_float(w[ax][j][2 * q])),
+                                     fix_f32(__uint_as_float(w[ax][j][2 * q + 1]))};
+                    X[j][2 * q] = r[0];
+                    X[j][2 * q + 1] = r[1];
+                    n2 = __builtin_amdgcn_fdot2(r, r, n2, false);
                 }
             }
         }
@@ -199,40 +188,41 @@ __device__ __forceinline__ f32x16 mfma16(f16x8 a, f16x8 b, f32x16 c)
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-// -2 X.P of one axis as two limb accumulators (exact integers in fp32).
+// Xr.hi and Xr.lo of one axis, accumulated onto kMagic (see above).
 // PIX_ROWS: pixels are the MFMA rows (pass 1) or its columns (pass 2).
-template <typename T, int KS, bool PIX_ROWS>
-__device__ __forceinline__ void axis_dot(const Fix8 (&X)[KS], const f16x8 (&ph)[KS], const f16x8 (&pl)[KS],
+template <int KS, bool PIX_ROWS>
+__device__ __forceinline__ void axis_dot(const f16x8 (&X)[KS], const f16x8 (&ph)[KS], const f16x8 (&pl)[KS],
                                          f32x16 &ah, f32x16 &al)
 {
-    ah = (f32x16){};
-    al = (f32x16){};
+    const f32x16 m = {kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic,
+                      kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic};
+    ah = m;
+    al = m;
 #pragma unroll
     for (int j = 0; j < KS; j++) {
         if constexpr (PIX_ROWS) {
-            ah = mfma16(X[j].main, ph[j], ah);
-            al = mfma16(X[j].main, pl[j], al);
-            if constexpr (kNeedsRest<T>) {
-                ah = mfma16(X[j].rest, ph[j], ah);
-                al = mfma16(X[j].rest, pl[j], al);
-            }
+            ah = mfma16(X[j], ph[j], ah);
+            al = mfma16(X[j], pl[j], al);
         } else {
-            ah = mfma16(ph[j], X[j].main, ah);
-            al = mfma16(pl[j], X[j].main, al);
-            if constexpr (kNeedsRest<T>) {
-                ah = mfma16(ph[j], X[j].rest, ah);
-                al = mfma16(pl[j], X[j].rest, al);
-            }
+            ah = mfma16(ph[j], X[j], ah);
+            al = mfma16(pl[j], X[j], al);
         }
     }
 }
 
-// Bits of fl32(S + 1) from the two limb accumulators of -2 X.P, |X|^2 and
-// |P|^2 + 1 (the integer sum is exact modulo 2^32 and S + 1 < 2^32).
-__device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t nx, uint32_t np1)
+// Bits of fl32(S + 1) from the two limb accumulators and c = 256 |Xr|^2 +
+// |P|^2 + 1 - 2064 * 0x4B400000 (mod 2^32): S + 1 = 16 (128 bits(ah) +
+// bits(al)) + c exactly, modulo 2^32, and S + 1 < 2^32.
+__device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t c)
 {
-    const uint32_t s1 = (uint32_t)((int32_t)ah * 128 + (int32_t)al) + nx + np1;
-    return __float_as_uint((float)s1);
+    const uint32_t t = (__float_as_uint(ah) << 7) + __float_as_uint(al);
+    return __float_as_uint((float)((t << 4) + c));
+}
+
+// The pixel's part of c: 256 |Xr|^2 - 2064 * 0x4B400000 (mod 2^32).
+__device__ __forceinline__ uint32_t pixel_const(float n2)
+{
+    return ((uint32_t)n2 << 8) - 2064u * kMagicBits;
 }
 
 // Tiles [first, last) of workgroup b of nb when ntiles tiles are shared out
@@ -343,30 +333,33 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // Packed weight limbs of the 16 (pixel, bin) results of one axis.
+    // Packed weight limbs of the 16 (pixel, bin) results of one axis; nrm
+    // holds the pixels' constants (pixel_const), np1 = |P|^2 + 1 of the bin.
     auto weights = [&](const f32x16 &ah, const f32x16 &al, int nbase, uint32_t np1, uint32_t (&e)[16]) {
 #pragma unroll
         for (int r4 = 0; r4 < 4; r4++) {
-            const i32x4 n4 = *reinterpret_cast<const i32x4 *>(nrm + nbase + 8 * r4 + 4 * g);
+            const u32x4 n4 = *reinterpret_cast<const u32x4 *>(nrm + nbase + 8 * r4 + 4 * g);
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 const int r = 4 * r4 + i;
-                e[r] = s_wt[(s1_bits(ah[r], al[r], (uint32_t)n4[i], np1) >> 15) & (kWKeys - 1)];
+                e[r] = s_wt[(s1_bits(ah[r], al[r], n4[i] + np1) >> 15) & (kWKeys - 1)];
             }
         }
     };
 
-    // One tile of up to 32 pixels (queue slot m = lane & 31) from prefetched input.
-    auto tile = [&](const RawSlices<T, F> &raw, int nvalid) {
-        int32_t n2x = 0, n2y = 0;
-        Fix8 X[KS], Y[KS];
+    // One tile of up to 32 pixels (queue slot m = lane & 31) from prefetched
+    // input; `next` reuses the input registers once they are converted.
+    auto tile = [&](RawSlices<T, F> &raw, int nvalid, auto next) {
+        float n2x = 0.0f, n2y = 0.0f;
+        f16x8 X[KS], Y[KS];
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
+        next();
         n2x += __shfl_xor(n2x, 32);
         n2y += __shfl_xor(n2y, 32);
         if (g == 0) {
-            nrm[ln] = n2x;
-            nrm[32 + ln] = n2y;
+            nrm[ln] = pixel_const(n2x);
+            nrm[32 + ln] = pixel_const(n2y);
         }
         uint32_t ex[16], ey[16];
         {
@@ -377,7 +370,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
                 pl[j] = palette_operand(s_pop, 0, 1, j, lane);
             }
             f32x16 ah, al;
-            axis_dot<T, KS, true>(X, ph, pl, ah, al);
+            axis_dot<KS, true>(X, ph, pl, ah, al);
             weights(ah, al, 0, np1x, ex);
         }
         {
@@ -388,7 +381,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
                 pl[j] = palette_operand(s_pop, 1, 1, j, lane);
             }
             f32x16 ah, al;
-            axis_dot<T, KS, true>(Y, ph, pl, ah, al);
+            axis_dot<KS, true>(Y, ph, pl, ah, al);
             weights(ah, al, 32, np1y, ey);
         }
         if (nvalid < 32) {        // pixels past the end of the list vote nothing
@@ -428,6 +421,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     cur_list.start(list, s_pref, nslices, slice_px, t < tend && 32 * t + ln < n ? 32 * t + ln : 0);
     // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
     auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
+    // the next tile's rows are loaded as soon as the current ones are converted
     RawSlices<T, F> raw;
     int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it
     if (t < tend) {
@@ -436,14 +430,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         if (tn < tend) idx = pixel(tn);
     }
     while (t < tend) {
-        const RawSlices<T, F> cur = raw;
         int tnn = tend;
-        if (tn < tend) {
-            raw.load(emb + (size_t)idx * D, g);
-            tnn = take_tile(s_next, lane);
-            if (tnn < tend) idx = pixel(tnn);
-        }
-        tile(cur, min(32, n - 32 * t));
+        tile(raw, min(32, n - 32 * t), [&]() {
+            if (tn < tend) {
+                raw.load(emb + (size_t)idx * D, g);
+                tnn = take_tile(s_next, lane);
+                if (tnn < tend) idx = pixel(tnn);
+            }
+        });
         t = tn;
         tn = tnn;
     }
@@ -585,31 +579,32 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     uint16_t *cyb = s_cy + wv * kMfmaBins * 64;    // y code of bin b, pixel slot p: cyb[b * 64 + p]
 
     // Keys of one tile of 32 pixels (pixel slots 32 h + (lane & 31)).
-    auto codes = [&](const RawSlices<T, F> &raw, int h) {
+    auto codes = [&](RawSlices<T, F> &raw, int h, auto next) {
         const int slot = 32 * h + ln;
-        int32_t n2x = 0, n2y = 0;
-        Fix8 X[KS], Y[KS];
+        float n2x = 0.0f, n2y = 0.0f;
+        f16x8 X[KS], Y[KS];
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
-        n2x += __shfl_xor(n2x, 32);
-        n2y += __shfl_xor(n2y, 32);
+        next();
+        const uint32_t cx = pixel_const(n2x + __shfl_xor(n2x, 32));
+        const uint32_t cy = pixel_const(n2y + __shfl_xor(n2y, 32));
         {
             f32x16 ah, al;
-            axis_dot<T, KS, false>(X, pxh, pxl, ah, al);
+            axis_dot<KS, false>(X, pxh, pxl, ah, al);
 #pragma unroll
             for (int r = 0; r < 16; r++) {
-                const uint32_t code = s_ct[(s1_bits(ah[r], al[r], (uint32_t)n2x, npx[r]) >> 14) & (kCKeys - 1)];
+                const uint32_t code = s_ct[(s1_bits(ah[r], al[r], cx + npx[r]) >> 14) & (kCKeys - 1)];
                 const int a = acc_row(r, g);
                 kx[a * 64 + slot] = (code << 14) | (uint32_t)a;
             }
         }
         {
             f32x16 ah, al;
-            axis_dot<T, KS, false>(Y, pyh, pyl, ah, al);
+            axis_dot<KS, false>(Y, pyh, pyl, ah, al);
 #pragma unroll
             for (int r = 0; r < 16; r++)
                 cyb[acc_row(r, g) * 64 + slot] =
-                    s_ct[(s1_bits(ah[r], al[r], (uint32_t)n2y, npy[r]) >> 14) & (kCKeys - 1)];
+                    s_ct[(s1_bits(ah[r], al[r], cy + npy[r]) >> 14) & (kCKeys - 1)];
         }
     };
 
@@ -662,6 +657,7 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     lc1.start(list, s_pref, nslices, slice_px, j < jend && 64 * j + 32 + ln < n ? 64 * j + 32 + ln : 0);
     auto pixel0 = [&](int jj) { return lc0.pixel(64 * jj + ln < n ? 64 * jj + ln : 64 * jj); };
     auto pixel1 = [&](int jj) { return lc1.pixel(64 * jj + 32 + ln < n ? 64 * jj + 32 + ln : 64 * jj); };
+    // a half's rows are loaded as soon as the previous half is converted
     RawSlices<T, F> raw;
     int ip0 = 0, ip1 = 0;
     if (j < jend) {
@@ -670,18 +666,16 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         raw.load(emb + (size_t)ip0 * D, g);
     }
     while (j < jend) {
-        RawSlices<T, F> cur = raw;
-        raw.load(emb + (size_t)ip1 * D, g);
         const int jn = take_tile(s_next, lane);
         int np0 = 0, np1 = 0;
         if (jn < jend) {
             np0 = pixel0(jn);
             np1 = pixel1(jn);
         }
-        codes(cur, 0);
-        cur = raw;
-        if (jn < jend) raw.load(emb + (size_t)np0 * D, g);
-        codes(cur, 1);
+        codes(raw, 0, [&]() { raw.load(emb + (size_t)ip1 * D, g); });
+        codes(raw, 1, [&]() {
+            if (jn < jend) raw.load(emb + (size_t)np0 * D, g);
+        });
         search(g ? ip1 : ip0, min(64, n - 64 * j));
         ip0 = np0;
         ip1 = np1;

@@ -62,13 +62,13 @@ def quant_bound(ex, ey, twoF):
     """Bound on |H_canonical * 2^-30 - H_real| per bin, as [b][a].
 
     Per pixel and axis the canonical distance differs from the real one by
-    (i) input and palette rounding to 1/4096 per channel: at most
-    sqrt(2F) 2^-12 (triangle inequality, no clamping);
+    (i) input rounding to 1/256 and palette rounding to 1/4096 per channel:
+    at most sqrt(2F) (2^-9 + 2^-13) (triangle inequality, no clamping);
     (ii) the 8-bit weight bucket: fl32(S+1) falls in [L, L(1+2^-8)) and the
     bucket centre S_mid+1 is within a factor e^(2^-9 + 2^-23) of S+1, so its
     square root is within e^(2^-10 + 2^-24) of sqrt(S+1); replacing S+1 by S
     moves sqrt by at most 1, i.e. 2^-12 in embedding units, on each side.
-    Hence |d~ - d| <= delta(d) = sqrt(2F) 2^-12 + 2^-11 + 2^-10 (d + 0.01).
+    Hence |d~ - d| <= delta(d) = sqrt(2F) (2^-9 + 2^-13) + 2^-11 + 2^-10 (d + 0.01).
     The weight table rounds 2^15 e^-d~ to an integer (2^-16 absolute), so per
     axis eps = e^-d (e^delta(d) - 1) + 2^-16 bounds |q/2^15 - e^-d|, and for
     a product of two weights the error is at most
@@ -76,7 +76,7 @@ def quant_bound(ex, ey, twoF):
     """
     def eps(e):
         d = -np.log(np.maximum(e, 1e-300))
-        delta = math.sqrt(twoF) * 2.0 ** -12 + 2.0 ** -11 + 2.0 ** -10 * (d + 0.01) + 1e-9
+        delta = math.sqrt(twoF) * (2.0 ** -9 + 2.0 ** -13) + 2.0 ** -11 + 2.0 ** -10 * (d + 0.01) + 1e-9
         return e * np.expm1(delta) + 2.0 ** -16
 
     epx, epy = eps(ex), eps(ey)
@@ -105,13 +105,14 @@ def _f32(x):
 
 
 def fixed(v: float) -> int:
-    """rint(4096 clamp(v, -1.5, 1.5)) in binary32, NaN clamping to -1.5."""
+    """16 rint(256 clamp(v, -1.5, 1.5)) in binary32 (the input on a 1/256 grid,
+    in units of 1/4096), NaN clamping to -1.5."""
     c = np.float32(v)
     if np.isnan(c) or c < np.float32(-1.5):
         c = np.float32(-1.5)
     if c > np.float32(1.5):
         c = np.float32(1.5)
-    return int(np.rint(np.float32(4096.0) * c))
+    return 16 * int(np.rint(np.float32(256.0) * c))
 
 
 def dist_key(S: int, m: int) -> int:

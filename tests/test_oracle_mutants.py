@@ -54,6 +54,10 @@ MUTANTS = [
     ("pixel over the mask threshold still counted", "if (!((double)best_d < 4096.0 * tau)) continue;\n        labels[p] = best + 1;\n        centroids[best].npix += 1;",
      "if (!((double)best_d < 4096.0 * tau)) { centroids[best].npix += 1; continue; }\n        labels[p] = best + 1;\n        centroids[best].npix += 1;"),
     ("clamp too wide", "if (c > V_CLAMP) c = V_CLAMP;", "if (c > 1.6f) c = 1.6f;"),
+    ("input read on the palette's 1/4096 grid", "return (int32_t)(FIX_SCALE / IN_GRID) * (int32_t)rintf(IN_GRID * c);",
+     "return (int32_t)rintf(FIX_SCALE * c);"),
+    ("input truncated instead of rounded", "return (int32_t)(FIX_SCALE / IN_GRID) * (int32_t)rintf(IN_GRID * c);",
+     "return (int32_t)(FIX_SCALE / IN_GRID) * (int32_t)truncf(IN_GRID * c);"),
 ]
 
 PIN_CASES = [

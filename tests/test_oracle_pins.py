@@ -217,13 +217,13 @@ def test_mask_threshold_and_all_pixels_equal_exhaustive_search(seed, dtype, F, b
 
 
 def test_mask_threshold_on_noise_free_frame_with_all_pixels():
-    """Every pixel votes (no fg channel).  Instance pixels sit at distance 0
-    from their own bin; background pixels carry a zero embedding, at distance
-    sqrt(F) per axis from every bin (|gamma|^2 = F), so each adds about
-    e^(-2 sqrt F) to every bin: a threshold above that level plus half the
-    smallest instance finds exactly the instances.  A tau of half a code
-    unit then keeps exactly the instance pixels, and tau = 0 keeps nothing
-    (Eq8 is strict)."""
+    """Every pixel votes (no fg channel).  Instance pixels sit within
+    snap_distance(F) of their own bin; background pixels carry a zero
+    embedding, at distance sqrt(F) per axis from every bin (|gamma|^2 = F),
+    so each adds about e^(-2 sqrt F) to every bin: a threshold above that
+    level plus half the smallest instance finds exactly the instances.  A
+    tau just above twice the snap distance then keeps exactly the instance
+    pixels, and tau = 0 keeps nothing (Eq8 is strict)."""
     H = W = 96
     bins, F = 16, 4
     cells = [(3, 3), (11, 4), (3, 12), (12, 12), (8, 8)]
@@ -236,12 +236,15 @@ def test_mask_threshold_on_noise_free_frame_with_all_pixels():
     expect = np.zeros_like(inst)
     for k, ab in enumerate(cells, start=1):
         expect[inst == k] = rank[ab]
-    res = oracle.decode(emb, None, fx, fy, bins, bins, 64, 0.5, theta, tau=0.5 / 4096)
+    tau = 2.0 * snap_distance(F) * (1 + 2.0 ** -9) + 3.0 / 4096     # code rounding: <= 1 unit per axis
+    assert tau < math.sqrt(F)
+    res = oracle.decode(emb, None, fx, fy, bins, bins, 64, 0.5, theta, tau=tau)
     got = list(zip(res["centroids"]["bin_x"].tolist(), res["centroids"]["bin_y"].tolist()))
     assert res["K"] == len(cells) and got == want
     assert np.array_equal(res["labels"], expect)
     assert np.array_equal(res["centroids"]["npix"], np.bincount(expect.ravel(), minlength=len(cells) + 1)[1:])
-    assert np.all(res["score_map"][expect > 0] == 1.0) and not res["score_map"][expect == 0].any()
+    assert np.all(res["score_map"][expect > 0] >= np.float32(math.exp(-tau)))
+    assert not res["score_map"][expect == 0].any()
     # no threshold: every pixel is labelled, the instances as before
     full = oracle.decode(emb, None, fx, fy, bins, bins, 64, 0.5, theta)
     assert np.all(full["labels"] > 0) and np.array_equal(full["labels"][expect > 0], expect[expect > 0])
@@ -280,10 +283,17 @@ def test_mask_threshold_nests():
 # --------------------------------------------------------------------------
 # noise-free special case: exact recovery of the generating centroids
 # --------------------------------------------------------------------------
+def snap_distance(F):
+    """Largest canonical distance between the fp32 encoding of a bin centre,
+    read on the 1/256 input grid (<= 8 units of 1/4096 per channel), and that
+    bin's palette entry (rounded to 1/4096, <= 1/2 unit): sqrt(2F) 8.5/4096."""
+    return math.sqrt(2 * F) * 8.5 / 4096
+
+
 def _snapped_frame(H, W, bins, cells, half, F=4):
     """Square instances centred on chosen bin centres; the embedding is the
-    encoding of that exact bin centre, so every instance pixel has distance 0
-    to its own bin."""
+    encoding of that exact bin centre, so every instance pixel is within
+    snap_distance(F) of its own bin."""
     fx, fy = paper_freqs(H, W, F)
     xa = refmath.bin_centres(bins, W)
     yb = refmath.bin_centres(bins, H)
@@ -322,10 +332,12 @@ def test_noise_free_decodes_generating_centroids_and_labels(order):
         expect[inst == k] = rank[ab]
     assert np.array_equal(res["labels"], expect)
     assert np.array_equal(res["centroids"]["npix"], np.bincount(expect.ravel(), minlength=len(cells) + 1)[1:])
-    # zero distance means weight 2^15 on both axes: score >= |Omega_k|
+    # a distance of at most snap_distance per axis weighs at least
+    # e^-snap_distance (up to the table's rounding): score >= |Omega_k| e^-2d
+    w = math.exp(-2.0 * snap_distance(4) * (1 + 2.0 ** -8)) - 2.0 ** -14
     for c in res["centroids"]:
         k = [kk for kk, ab in enumerate(cells, start=1) if ab == (c["bin_x"], c["bin_y"])][0]
-        assert c["score"] >= sizes[k - 1]
+        assert c["score"] >= sizes[k - 1] * w
 
 
 # --------------------------------------------------------------------------
