@@ -91,6 +91,21 @@ __device__ __forceinline__ int dist_key(uint32_t s)
     return (int)(bits >> (23 - M)) - (127 << M);
 }
 
+// Inclusive prefix sum of x over the 64 lanes of a wave with DPP moves:
+// shifts by 1, 2, 4, 8 within each row of 16 lanes, then the last lane of
+// row 0 added to row 1 (and of row 2 to row 3), then the last lane of row 1
+// added to rows 2 and 3.  Every lane must be active.
+__device__ __forceinline__ int wave_incl_sum(int x)
+{
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+    return x;
+}
+
 __device__ __forceinline__ int lane_prefix(unsigned long long mask)
 {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));

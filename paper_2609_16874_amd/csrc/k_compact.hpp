@@ -4,7 +4,8 @@
 // pixel range [s R, (s + 1) R) (R a multiple of 8192) and writes the indices
 // of its participating pixels, in raster order, to its slice list[s R ..]
 // and their number to counts[s]; every lane tests 8 consecutive foreground
-// values against the threshold and a wave prefix sum gives the slots.  No
+// values against the threshold, a wave prefix sum gives the slots, and each
+// step's entries are gathered in LDS and stored as one contiguous run.  No
 // atomics: the consumers concatenate the slices through the prefix sum of
 // the counts (slice_prefix / ListCursor).  The non-participating pixels get
 // their final outputs here: label 0 and, if a score map is requested,
@@ -42,6 +43,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict
                                                              int32_t *__restrict__ labels, float *__restrict__ score)
 {
     __shared__ int s_wave[kCompactThreads / 64];
+    __shared__ int32_t s_out[kCompactSpan];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int R = slice_pixels(npix);
     const int begin = blockIdx.x * R;
@@ -80,26 +82,22 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict
             m |= (in && v[i] > fg_thr ? 1u : 0u) << i;   // a NaN never exceeds the threshold
         }
         const int c = __popc(m);
-        int incl = c;                                      // inclusive prefix over the wave
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int t = __shfl_up(incl, d);
-            if (lane >= d) incl += t;
-        }
+        const int incl = wave_incl_sum(c);
         if (lane == 63) s_wave[wv] = incl;
         __syncthreads();
-        int off = base + incl - c, tot = 0;
+        int off = incl - c, tot = 0;
 #pragma unroll
         for (int w = 0; w < kCompactThreads / 64; w++) {
             const int n = s_wave[w];
             off += w < wv ? n : 0;
             tot += n;
         }
-        __syncthreads();                                   // s_wave is rewritten in the next step
-        base += tot;
 #pragma unroll
         for (int i = 0; i < kCompactPer; i++)
-            if ((m >> i) & 1u) out[off++] = p0 + i;
+            if ((m >> i) & 1u) s_out[off++] = p0 + i;
+        __syncthreads();                                   // s_wave and s_out are rewritten in the next step
+        for (int i = tid; i < tot; i += kCompactThreads) out[base + i] = s_out[i];
+        base += tot;
 
         // outputs of the pixels outside S
         const uint32_t bg = valid & ~m;
