@@ -51,7 +51,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWpb2 = 8;             // waves per workgroup of the assignment kernel
+constexpr int kWpb2 = 12;            // waves per workgroup of the assignment kernel (3 per SIMD)
 constexpr int kPopBytes = 2 * 2 * 2 * 64 * 16;   // palette operands of both axes, limbs and K-steps
 
 template <int F>
@@ -458,48 +458,57 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // ---------------------------------------------------------------------------
 // Pass 2: assignment + label write-out
 // ---------------------------------------------------------------------------
-// LDS bytes of k_assign_mfma: code table, candidate batches, bin -> centroid
-// table, counts, per wave x keys [32 bins][64 pixels] (u32) and y codes
-// [32 bins][64 pixels] (u16), then the peak-extraction state.
-constexpr size_t kAssignLds = (size_t)kCKeys * 2 + (size_t)kMaxBatchLds * 20 + kMfmaBins * kMfmaBins * 2 +
-                              kMfmaBins * kMfmaBins * 4 +
-                              (size_t)kWpb2 * (kMfmaBins * 64 * 4 + kMfmaBins * 64 * 2) + sizeof(PeakLds) +
-                              (kMaxSlices + 1) * 4 + 16;
+// LDS bytes of k_assign_mfma: code table, palette operands, bin constants,
+// candidate batches, bin -> centroid table, counts, per wave x keys and y
+// keys [32 bins][32 pixels] (u32), then the peak-extraction state.
+constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
+                              kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
+                              (size_t)kWpb2 * 2 * kMfmaBins * 32 * 4 + sizeof(PeakLds) + (kMaxSlices + 1) * 4 + 16;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
 // writes the centroid records (all fields but the pixel count), K and the
 // summed histogram `hlast`, and the grid clears `hzero`, the histograms the
 // next frame's vote launch accumulates into.
+//
+// Then, per tile of 32 pixels, the distance codes of both axes (palette as
+// the MFMA rows, so that each lane holds one pixel and 16 bins) go to LDS
+// as search keys: x key (c_x << 14) | a and y key (c_y << 14) | 128 b, laid
+// out [bin][32 pixels] so that lane m reads pixel m's key of any bin at a
+// fixed stride.  The candidate search walks the batches of 4 columns of one
+// row; the two halves of the wave take alternate batches for the same 32
+// pixels and combine their minima at the end.  The minimum of
+// x key + y key is ((c_x + c_y) << 14) | (128 b + a): the smallest code sum
+// and, on ties, the lowest bin index, i.e. the lowest centroid index.
 template <typename T, int F>
-__global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, const int32_t *__restrict__ list,
-                                                     const int32_t *__restrict__ counts, int32_t nslices,
-                                                     int32_t slice_px, int32_t npix, uint32_t tau_code, Tables tb,
-                                                     const unsigned long long *__restrict__ hcur,
-                                                     unsigned long long *__restrict__ hzero,
-                                                     unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
-                                                     long long cut, int32_t cap, cpe_centroid *__restrict__ cents,
-                                                     int32_t *__restrict__ num, int32_t *__restrict__ labels,
-                                                     float *__restrict__ score_map)
+__global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb2 / 4))) void k_assign_mfma(
+    const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ counts,
+    int32_t nslices, int32_t slice_px, int32_t npix, uint32_t tau_code, Tables tb,
+    const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hzero,
+    unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
+    cpe_centroid *__restrict__ cents, int32_t *__restrict__ num, int32_t *__restrict__ labels,
+    float *__restrict__ score_map)
 {
     constexpr int KS = AxisShape<F>::KS;
     constexpr int D = 4 * F;
-    static_assert(kWpb2 * 64 == kPeakThreads, "the peak prologue takes two histogram slots per thread");
+    constexpr int kThreads = kWpb2 * 64;
+    static_assert(kThreads >= kPeakThreads, "the peak prologue takes two histogram slots per thread");
     static_assert(kAssignLds <= 160 * 1024, "LDS of one compute unit");
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kAssignLds];
-    uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                           // [kCKeys]
-    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_ct + kCKeys);                        // [kMaxBatchLds]
-    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatchLds);            // [kMaxBatchLds]
-    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatchLds);          // [32 * 32]
-    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);  // [1024]
-    uint32_t *s_kx = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins);  // [kWpb2][32][64]
-    uint16_t *s_cy = reinterpret_cast<uint16_t *>(s_kx + kWpb2 * kMfmaBins * 64); // [kWpb2][32][64]
-    PeakLds &pl = *reinterpret_cast<PeakLds *>(s_cy + kWpb2 * kMfmaBins * 64);
-    int *s_pref = reinterpret_cast<int *>(&pl + 1);                                 // [kMaxSlices + 1]
-    int *s_next = s_pref + kMaxSlices + 1;                                           // next group of the run
-    // the summed histogram lives in the x-key arrays until the peaks are known
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_kx);
+    uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                            // [kCKeys]
+    uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_ct + kCKeys);                  // palette operands
+    uint32_t *s_np = s_pop + kPopBytes / 4;                                          // [2][32] |P|^2 + 1
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_np + 2 * kMfmaBins);                 // [kMaxBatchLds]
+    uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatchLds);             // [kMaxBatchLds]
+    uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatchLds);           // [32 * 32]
+    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);   // [1024]
+    uint32_t *s_keys = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins); // [kWpb2][2][32][32]
+    PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * 32);
+    int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
+    int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
+    // the summed histogram lives in the key arrays until the peaks are known
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_keys);
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -508,20 +517,28 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
     PeakLoad pld;                                   // issued before the table staging
     peaks_lds_load(hcur, Bw, Bh, pld);
     {
-        constexpr int kThreads = kWpb2 * 64;
-        u32x4 w[kCKeys / 8 / kThreads];
+        constexpr int kN = kCKeys / 8, kPer = (kN + kThreads - 1) / kThreads;
+        u32x4 w[kPer];
 #pragma unroll
-        for (int k = 0; k < kCKeys / 8 / kThreads; k++)
-            w[k] = reinterpret_cast<const u32x4 *>(tb.ct_pm)[k * kThreads + tid];
+        for (int k = 0; k < kPer; k++) {
+            const int i = k * kThreads + tid;
+            w[k] = reinterpret_cast<const u32x4 *>(tb.ct_pm)[i < kN ? i : 0];
+        }
 #pragma unroll
-        for (int k = 0; k < kCKeys / 8 / kThreads; k++) reinterpret_cast<u32x4 *>(s_ct)[k * kThreads + tid] = w[k];
+        for (int k = 0; k < kPer; k++) {
+            const int i = k * kThreads + tid;
+            if (i < kN) reinterpret_cast<u32x4 *>(s_ct)[i] = w[k];
+        }
+        for (int i = tid; i < kPopBytes / 16; i += kThreads)
+            reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
+        if (tid < 2 * kMfmaBins) s_np[tid] = tid < kMfmaBins ? tb.np1_x[tid] : tb.np1_y[tid - kMfmaBins];
     }
-    for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) s_cnt[i] = 0;
+    for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_cnt[i] = 0;
     if (list) slice_prefix(counts, nslices, s_pref);
     peaks_lds(pld, Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank);
     const int Kc = pl.Kc;
     if (blockIdx.x == 0) {
-        for (int k = tid; k < Kc; k += blockDim.x) {
+        for (int k = tid; k < Kc; k += kThreads) {
             const int i = pl.pk[k], a = i & 31, b = i >> 5;
             cpe_centroid *c = cents + k;    // npix was reset by the vote launch and is counted below
             c->bin_x = a;
@@ -531,109 +548,91 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
             c->score = (double)s_h[i] * 0x1p-30;
             c->reserved = 0;
         }
-        for (int i = tid; i < nb; i += blockDim.x) hlast[i] = s_h[(i / Bw) * 32 + i % Bw];
+        for (int i = tid; i < nb; i += kThreads) hlast[i] = s_h[(i / Bw) * 32 + i % Bw];
         if (tid == 0) *num = pl.K;
     }
-    for (int i = blockIdx.x * blockDim.x + tid; i < kReplicas * nb; i += gridDim.x * blockDim.x) hzero[i] = 0ull;
-    __syncthreads();            // s_h is overwritten by the key arrays from here on
+    for (int i = blockIdx.x * kThreads + tid; i < kReplicas * nb; i += gridDim.x * kThreads) hzero[i] = 0ull;
 
-    // the workgroup's run of groups of 64 list entries
-    const int n = list ? s_pref[nslices] : npix, ngroups = (n + 63) >> 6;
-    int j, jend;
-    block_run(ngroups, blockIdx.x, gridDim.x, j, jend);
+    // the workgroup's run of tiles of 32 list entries
+    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
+    int t, tend;
+    block_run(ntiles, blockIdx.x, gridDim.x, t, tend);
     if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
         ListCursor c0;
-        c0.start(list, s_pref, nslices, slice_px, 64 * j + tid < n ? 64 * j + tid : 0);
-        for (int i = 64 * j + tid; i < min(64 * jend, n); i += blockDim.x) {
+        c0.start(list, s_pref, nslices, slice_px, 32 * t + tid < n ? 32 * t + tid : 0);
+        for (int i = 32 * t + tid; i < min(32 * tend, n); i += kThreads) {
             const int p = c0.pixel(i);
             labels[p] = 0;
             if (score_map) score_map[p] = 0.0f;
         }
         return;
     }
-    if (tid == 0) *s_next = j;
-    __syncthreads();
-    const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of 4
+    if (tid == 0) *s_next = t;
+    __syncthreads();            // s_h is overwritten by the key arrays from here on
+    const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of kBatchPad
 
-    f16x8 pxh[KS], pxl[KS], pyh[KS], pyl[KS];
-#pragma unroll
-    for (int j = 0; j < KS; j++) {
-        pxh[j] = palette_operand(tb.pop, 0, 0, j, lane);
-        pxl[j] = palette_operand(tb.pop, 0, 1, j, lane);
-        pyh[j] = palette_operand(tb.pop, 1, 0, j, lane);
-        pyl[j] = palette_operand(tb.pop, 1, 1, j, lane);
-    }
-    uint32_t npx[16], npy[16];
-#pragma unroll
-    for (int r4 = 0; r4 < 4; r4++) {
-        const u32x4 vx = *reinterpret_cast<const u32x4 *>(tb.np1_x + 8 * r4 + 4 * g);
-        const u32x4 vy = *reinterpret_cast<const u32x4 *>(tb.np1_y + 8 * r4 + 4 * g);
-#pragma unroll
-        for (int i = 0; i < 4; i++) {
-            npx[4 * r4 + i] = vx[i];
-            npy[4 * r4 + i] = vy[i];
-        }
-    }
+    uint32_t *kx = s_keys + wv * 2 * kMfmaBins * 32;   // x key of bin a, pixel m: kx[a * 32 + m]
+    uint32_t *ky = kx + kMfmaBins * 32;                // y key of bin b, pixel m: ky[b * 32 + m]
 
-    uint32_t *kx = s_kx + wv * kMfmaBins * 64;     // x key of bin a, pixel slot p: kx[a * 64 + p]
-    uint16_t *cyb = s_cy + wv * kMfmaBins * 64;    // y code of bin b, pixel slot p: cyb[b * 64 + p]
-
-    // Keys of one tile of 32 pixels (pixel slots 32 h + (lane & 31)).
-    auto codes = [&](RawSlices<T, F> &raw, int h, auto next) {
-        const int slot = 32 * h + ln;
+    // Keys of one tile (pixel m = lane & 31; this lane's 16 bins of each
+    // axis); `next` reuses the input registers once they are converted.
+    auto codes = [&](RawSlices<T, F> &raw, auto next) {
         float n2x = 0.0f, n2y = 0.0f;
         f16x8 X[KS], Y[KS];
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
         next();
-        const uint32_t cx = pixel_const(n2x + __shfl_xor(n2x, 32));
-        const uint32_t cy = pixel_const(n2y + __shfl_xor(n2y, 32));
-        {
-            f32x16 ah, al;
-            axis_dot<KS, false>(X, pxh, pxl, ah, al);
+        const uint32_t cxp = pixel_const(n2x + __shfl_xor(n2x, 32));
+        const uint32_t cyp = pixel_const(n2y + __shfl_xor(n2y, 32));
 #pragma unroll
-            for (int r = 0; r < 16; r++) {
-                const uint32_t code = s_ct[(s1_bits(ah[r], al[r], cx + npx[r]) >> 14) & (kCKeys - 1)];
-                const int a = acc_row(r, g);
-                kx[a * 64 + slot] = (code << 14) | (uint32_t)a;
+        for (int ax = 0; ax < 2; ax++) {
+            f16x8 ph[KS], pl_[KS];
+#pragma unroll
+            for (int j = 0; j < KS; j++) {
+                ph[j] = palette_operand(s_pop, ax, 0, j, lane);
+                pl_[j] = palette_operand(s_pop, ax, 1, j, lane);
             }
-        }
-        {
             f32x16 ah, al;
-            axis_dot<KS, false>(Y, pyh, pyl, ah, al);
+            axis_dot<KS, false>(ax ? Y : X, ph, pl_, ah, al);
+            const uint32_t cp = ax ? cyp : cxp;
+            uint32_t *dst = ax ? ky : kx;
 #pragma unroll
-            for (int r = 0; r < 16; r++)
-                cyb[acc_row(r, g) * 64 + slot] =
-                    s_ct[(s1_bits(ah[r], al[r], cy + npy[r]) >> 14) & (kCKeys - 1)];
+            for (int r4 = 0; r4 < 4; r4++) {
+                const u32x4 np = *reinterpret_cast<const u32x4 *>(s_np + ax * kMfmaBins + 8 * r4 + 4 * g);
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int r = 4 * r4 + i, bin = acc_row(r, g);
+                    const uint32_t code = s_ct[(s1_bits(ah[r], al[r], cp + np[i]) >> 14) & (kCKeys - 1)];
+                    dst[bin * 32 + ln] = (code << 14) | (uint32_t)(ax ? 128 * bin : bin);
+                }
+            }
         }
     };
 
-    // Candidate search for the pixels in queue slots base .. base + nvalid - 1
-    // (lane p: slot p of the key arrays): per batch, the smallest of its 4 x
-    // keys plus the row's y key.  The row word 128 b is both the byte offset
-    // of row b in the y-code array and the row's bits of the key.  The batch
-    // list is read one entry ahead.
+    // Candidate search for the pixel of lane m: this half of the wave takes
+    // batches g, g + 2, ... (8 batches, 4 per half, read per step), then the
+    // halves combine; lanes of half 0 write the labels of valid pixels.
     auto search = [&](int pix, int nvalid) {
         __builtin_amdgcn_wave_barrier();
-        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + lane);
-        const unsigned char *cyl = reinterpret_cast<const unsigned char *>(cyb + lane);
+        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
+        const unsigned char *kyl = reinterpret_cast<const unsigned char *>(ky + ln);
         uint32_t best = 0xffffffffu;
-        // four batches per step: their 20 reads are in flight together
-        for (int i = 0; i < nbat; i += 4) {
-            const u32x4 hb = *reinterpret_cast<const u32x4 *>(s_bh + i);
+        for (int i = 0; i < nbat; i += kBatchPad) {
 #pragma unroll
-            for (int u = 0; u < 4; u++) {
-                const u32x4 o = s_bo[i + u];
+            for (int u = 0; u < kBatchPad / 2; u++) {
+                const int bi = i + 2 * u + g;
+                const u32x4 o = s_bo[bi];
+                const uint32_t hb = s_bh[bi];
                 const uint32_t v0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
                 const uint32_t v1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
                 const uint32_t v2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
                 const uint32_t v3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
-                const uint32_t cy = *reinterpret_cast<const uint16_t *>(cyl + hb[u]);
-                const uint32_t m = min(min(v0, v1), min(v2, v3));
-                best = min(best, m + ((cy << 14) | hb[u]));
+                const uint32_t yk = *reinterpret_cast<const uint32_t *>(kyl + hb);
+                best = min(best, min(min(v0, v1), min(v2, v3)) + yk);
             }
         }
-        if (lane < nvalid) {
+        best = min(best, (uint32_t)__shfl_xor((int)best, 32));
+        if (g == 0 && ln < nvalid) {
             if ((best >> 14) < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
                 const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
                 const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
@@ -648,41 +647,37 @@ __global__ __launch_bounds__(512) void k_assign_mfma(const T *__restrict__ emb, 
         __builtin_amdgcn_wave_barrier();
     };
 
-    // lane (m, h) of group jj loads entries 64 jj + m and 64 jj + 32 + m (the
-    // group's first entry past the end) and labels entry 64 jj + 32 h + m,
-    // i.e. slot lane; one list cursor per half
-    j = take_tile(s_next, lane);
-    ListCursor lc0, lc1;
-    lc0.start(list, s_pref, nslices, slice_px, j < jend && 64 * j + ln < n ? 64 * j + ln : 0);
-    lc1.start(list, s_pref, nslices, slice_px, j < jend && 64 * j + 32 + ln < n ? 64 * j + 32 + ln : 0);
-    auto pixel0 = [&](int jj) { return lc0.pixel(64 * jj + ln < n ? 64 * jj + ln : 64 * jj); };
-    auto pixel1 = [&](int jj) { return lc1.pixel(64 * jj + 32 + ln < n ? 64 * jj + 32 + ln : 64 * jj); };
-    // a half's rows are loaded as soon as the previous half is converted
+    // the next tile's rows are loaded as soon as the current ones are converted
+    t = take_tile(s_next, lane);
+    ListCursor cur_list;
+    cur_list.start(list, s_pref, nslices, slice_px, t < tend && 32 * t + ln < n ? 32 * t + ln : 0);
+    // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
+    auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
     RawSlices<T, F> raw;
-    int ip0 = 0, ip1 = 0;
-    if (j < jend) {
-        ip0 = pixel0(j);
-        ip1 = pixel1(j);
-        raw.load(emb + (size_t)ip0 * D, g);
+    int tn = tend, ip = 0, ipn = 0;                     // next tile; this lane's pixel in this / the next tile
+    if (t < tend) {
+        ip = pixel(t);
+        raw.load(emb + (size_t)ip * D, g);
+        tn = take_tile(s_next, lane);
+        if (tn < tend) ipn = pixel(tn);
     }
-    while (j < jend) {
-        const int jn = take_tile(s_next, lane);
-        int np0 = 0, np1 = 0;
-        if (jn < jend) {
-            np0 = pixel0(jn);
-            np1 = pixel1(jn);
-        }
-        codes(raw, 0, [&]() { raw.load(emb + (size_t)ip1 * D, g); });
-        codes(raw, 1, [&]() {
-            if (jn < jend) raw.load(emb + (size_t)np0 * D, g);
+    while (t < tend) {
+        int tnn = tend, ipnn = 0;
+        codes(raw, [&]() {
+            if (tn < tend) {
+                raw.load(emb + (size_t)ipn * D, g);
+                tnn = take_tile(s_next, lane);
+                if (tnn < tend) ipnn = pixel(tnn);
+            }
         });
-        search(g ? ip1 : ip0, min(64, n - 64 * j));
-        ip0 = np0;
-        ip1 = np1;
-        j = jn;
+        search(ip, min(32, n - 32 * t));
+        t = tn;
+        tn = tnn;
+        ip = ipn;
+        ipn = ipnn;
     }
     __syncthreads();
-    for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += blockDim.x)
+    for (int i = tid; i < Kc && i < kMfmaBins * kMfmaBins; i += kThreads)
         if (s_cnt[i]) atomicAdd(&cents[i].npix, s_cnt[i]);
 }
 

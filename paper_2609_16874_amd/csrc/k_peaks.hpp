@@ -17,10 +17,10 @@
 // Candidate batches.  The first min(K, cap) candidates are grouped by row b
 // into batches of 4 columns (a row's last batch repeats its last column,
 // which leaves a minimum unchanged).  Batch i is bo[i] = the byte offsets
-// a * 256 of its 4 columns in the assignment kernel's [bin][64 pixels] x-key
+// a * 128 of its 4 columns in the assignment kernel's [bin][32 pixels] x-key
 // array, and bh[i] = 128 b, which is both the byte offset of row b in its
-// [bin][64 pixels] 16-bit y-code array and the row's bits of the search key.
-// The list is padded to a multiple of 4 batches with copies of its last one.
+// [bin][32 pixels] y-key array and the row's bits of the search key.  The
+// list is padded to a multiple of 8 batches with copies of its last one.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -114,16 +114,17 @@ __device__ __forceinline__ int compact_peaks(const unsigned long long *s_h, int 
 // Grids up to 32 x 32: candidates in LDS, in the assignment kernel's prologue
 // ---------------------------------------------------------------------------
 // The histogram is held in a 32 x 32 slot layout, slot b * 32 + a, whose
-// order agrees with the bin order b * B_w + a.  A block of kPeakThreads
-// threads handles two slots per thread: t and t + kPeakThreads.
+// order agrees with the bin order b * B_w + a.  The first kPeakThreads
+// threads of the block own two slots each: t and t + kPeakThreads.
 constexpr int kLdsPeakBins = 32;
 constexpr int kPeakThreads = 512;
 constexpr int kMaxBatchLds = 128;   // <= 16 strict maxima per row of 32 -> <= 4 batches per row
+constexpr int kBatchPad = 8;        // the batch list is padded to a multiple of this
 
 // LDS of peaks_lds (the summed histogram may alias any scratch the caller
 // does not need until the peaks are known).
 struct PeakLds {
-    int wave[2 * kPeakThreads / 64];  // per-wave counts of the two slot passes
+    int wave[2 * kPeakThreads / 64];  // per-wave counts of the two slot passes (slot-owning waves)
     uint32_t rowmask[kLdsPeakBins];   // bit a of row b: (a, b) is one of the first min(K, cap) candidates
     int K, Kc, nbat;
     int pk[max_peaks(kLdsPeakBins, kLdsPeakBins)];   // candidate slots b * 32 + a, ascending
@@ -142,7 +143,7 @@ __device__ __forceinline__ void peaks_lds_load(const unsigned long long *__restr
 #pragma unroll
     for (int u = 0; u < 2; u++) {
         const int slot = u * kPeakThreads + (int)threadIdx.x, a = slot & 31, b = slot >> 5;
-        const bool in = a < Bw && b < Bh;
+        const bool in = (int)threadIdx.x < kPeakThreads && a < Bw && b < Bh;
 #pragma unroll
         for (int r = 0; r < kReplicas; r++) ld.v[u][r] = in ? hsrc[(size_t)r * nb + b * Bw + a] : 0ull;
     }
@@ -170,20 +171,23 @@ __device__ __forceinline__ bool is_peak32(const unsigned long long *s_h, int a, 
 // From the loaded counts: the summed histogram s_h (32 x 32 slots), the
 // candidates compacted in ascending bin order (pl.pk), K and min(K, cap),
 // the bin -> candidate-index table s_rank [32 * 32] and the candidate
-// batches s_bo / s_bh (pl.nbat of them, a multiple of 4).  Called by every
-// thread of a block of kPeakThreads threads.
+// batches s_bo / s_bh (pl.nbat of them, a multiple of kBatchPad).  Called by
+// every thread of a block of at least kPeakThreads threads.
 __device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, long long cut, int cap,
                                           unsigned long long *s_h, PeakLds &pl, u32x4_pk *s_bo, uint32_t *s_bh,
                                           uint16_t *s_rank)
 {
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     constexpr int kWaves = kPeakThreads / 64;
+    const bool own = tid < kPeakThreads;            // wave-uniform
+    if (own) {
 #pragma unroll
-    for (int u = 0; u < 2; u++) {
-        unsigned long long sum = 0;
+        for (int u = 0; u < 2; u++) {
+            unsigned long long sum = 0;
 #pragma unroll
-        for (int r = 0; r < kReplicas; r++) sum += ld.v[u][r];
-        s_h[u * kPeakThreads + tid] = sum;
+            for (int r = 0; r < kReplicas; r++) sum += ld.v[u][r];
+            s_h[u * kPeakThreads + tid] = sum;
+        }
     }
     if (tid < kLdsPeakBins) pl.rowmask[tid] = 0u;
     __syncthreads();
@@ -192,10 +196,10 @@ __device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, lo
 #pragma unroll
     for (int u = 0; u < 2; u++) {
         const int slot = u * kPeakThreads + tid;
-        flag[u] = is_peak32(s_h, slot & 31, slot >> 5, Bw, Bh, cut);
+        flag[u] = own && is_peak32(s_h, slot & 31, slot >> 5, Bw, Bh, cut);
         mask[u] = __ballot(flag[u]);
     }
-    if (lane == 0) {
+    if (own && lane == 0) {
         pl.wave[wid] = __popcll(mask[0]);
         pl.wave[kWaves + wid] = __popcll(mask[1]);
     }
@@ -235,14 +239,14 @@ __device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, lo
             if (lane >= d) incl += t;
         }
         const int start = incl - nbt, total = __shfl(incl, 31);
-        const int padded = (total + 3) & ~3;
+        const int padded = (total + kBatchPad - 1) & ~(kBatchPad - 1);
         uint32_t last = 0;
         u32x4_pk o = {0u, 0u, 0u, 0u};
         for (int j = 0; j < nbt; j++) {
 #pragma unroll
             for (int s4 = 0; s4 < 4; s4++) {
                 if (m) {
-                    last = (uint32_t)__builtin_ctz(m) * 256u;
+                    last = (uint32_t)__builtin_ctz(m) * 128u;
                     m &= m - 1u;
                 }
                 o[s4] = last;
@@ -250,8 +254,8 @@ __device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, lo
             s_bo[start + j] = o;
             s_bh[start + j] = (uint32_t)b * 128u;
         }
-        // pad the list to a multiple of 4 with copies of the last batch (a
-        // repeated batch leaves every minimum unchanged)
+        // pad the list with copies of the last batch (a repeated batch leaves
+        // every minimum unchanged)
         if (nbt > 0 && start + nbt == total)
             for (int e = total; e < padded; e++) {
                 s_bo[e] = o;

@@ -11,7 +11,7 @@
 namespace cpe {
 
 // Grid caps of the matrix-core kernels: one resident vote workgroup (8 or 12
-// waves) and one assignment workgroup of 8 waves per compute unit.
+// waves) and one assignment workgroup of 12 waves per compute unit.
 constexpr int64_t kVoteGrid = 256;
 constexpr int64_t kAssignGrid = 256;
 
@@ -73,7 +73,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
                            slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap);
         mark(1);
         mark(2);
-        const int64_t wgs2 = ((tiles + 1) / 2 + kWpb2 - 1) / kWpb2;
+        const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
         hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, list, h->counts,
                            nslices, slice_px, npix, fa.tau_code, h->tb, hcur, hnext, h->hlast, Bw, Bh, cut, h->cap,
