@@ -9,8 +9,8 @@ Inputs are resident in HBM before timing starts.  Prints one JSON line:
   value        decoded frames per second (whole job, one GPU)
   ms_per_step  wall time of one 16-frame step (hipEvents around K steps)
   roofline     the dominant kernel's algorithmic bytes per launch divided by
-               its average launch duration (hipEvents recorded by the
-               library between its launches), against 8 TB/s HBM
+               its average duration (start and end events recorded by the
+               kernel's own dispatch), against 8 TB/s HBM
   cpu_baseline the plain single-threaded CPU oracle on a bounded sample of
                the same frames (reported, not a target)
   extra        the 640x640 single frame and the 1024x2048 frame, with the
@@ -33,7 +33,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E peak, GB/s
 GOLDEN = os.path.join(ROOT, "tests", "golden", "configs.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
-STAGE_KERNEL = {"recover_vote": "k_vote_mfma", "assign_label": "k_assign_mfma"}
+STAGE_KERNEL = {"compact": "k_compact", "recover_vote": "k_vote_mfma", "assign_label": "k_assign_mfma"}
 
 
 def source_sha256():
@@ -115,9 +115,10 @@ def frame_bytes(spec, frame):
     nfg = int((frame.fg.astype(np.float32) > np.float32(spec.fg_threshold)).sum())
     return {
         "literal": npx * spec.D * es + 4 * npx,
-        "recover_vote": npx * es + nfg * spec.D * es,
+        "compact": npx * es + 4 * nfg + 4 * (npx - nfg),
+        "recover_vote": 4 * nfg + nfg * spec.D * es,
         "peaks": 0,
-        "assign_label": npx * es + nfg * spec.D * es + 4 * npx,
+        "assign_label": 4 * nfg + nfg * spec.D * es + 4 * nfg,
         "n_fg": nfg,
     }
 
@@ -148,22 +149,23 @@ def time_steps(dec, embs, fgs, outs, fg_thr, theta, steps, warmup):
 
 
 def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
-    """Average per-kernel duration over reps x frames, from the events the
-    library records between its launches."""
+    """Average duration of each of the frame's three kernels over reps x
+    frames, from the start and end events their dispatches record."""
     from paper_2609_16874_amd import native
+    names = native.stage_names(dec.bins_w, dec.bins_h)
     ev = HipEvents(native.STAGE_EVENTS)
     assert dec.set_stage_events(ev.ev) == 0
-    acc = np.zeros(len(native.STAGES))
+    acc = np.zeros(len(names))
     n = 0
     for _ in range(reps):
         for i in range(len(embs)):
             o = outs[i]
             assert dec.decode(embs[i], fgs[i], fg_thr, theta, o["centroids"], o["num_centroids"], o["labels"]) == 0
-            acc += [ev.elapsed_ms(k, k + 1) for k in range(len(native.STAGES))]
+            acc += [ev.elapsed_ms(2 * k, 2 * k + 1) for k in range(len(names))]
             n += 1
     dec.set_stage_events(None)
     ev.close()
-    return dict(zip(native.STAGES, (acc / n).tolist()))
+    return dict(zip(names, (acc / n).tolist()))
 
 
 def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=None):

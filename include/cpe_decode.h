@@ -207,13 +207,18 @@ size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
 
 /*
  * Profiling: when `events` is non-NULL, every later cpe_decode on this handle
- * records events[0] before its first kernel and events[i+1] after its i-th
- * kernel, on the decode's stream, so that hipEventElapsedTime gives the
- * duration of each stage (recovery+voting, peak extraction, assignment).
- * `n_events` must be CPE_STAGE_EVENTS; the caller owns the events and must
- * keep them alive while set.  NULL switches the recording off.
+ * launches its i-th kernel (i = 0, 1, 2) so that the dispatch itself records
+ * events[2i] when the kernel starts and events[2i+1] when it ends, on the
+ * decode's stream; hipEventElapsedTime(events[2i], events[2i+1]) is then that
+ * kernel's duration.  Grids up to 32 x 32 bins: 0 = compaction of the
+ * participating pixels, 1 = recovery + voting, 2 = peak extraction +
+ * assignment (without a foreground channel launch 0 is skipped and its two
+ * events are recorded back to back).  Larger grids: 0 = recovery + voting,
+ * 1 = peak extraction, 2 = assignment.  `n_events` must be CPE_STAGE_EVENTS;
+ * the caller owns the events and must keep them alive while set.  NULL
+ * switches the recording off.
  */
-#define CPE_STAGE_EVENTS 4
+#define CPE_STAGE_EVENTS 6
 cpe_status cpe_decode_set_stage_events(cpe_decoder *h, hipEvent_t *events, int32_t n_events);
 
 #ifdef __cplusplus

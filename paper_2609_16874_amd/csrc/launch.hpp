@@ -2,6 +2,8 @@
 // type and harmonic count by the launch_*.hip translation units.
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include "cpe_decoder.hpp"
 #include "k_compact.hpp"
 #include "k_generic.hpp"
@@ -37,13 +39,24 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
     const int npix = h->H * h->W;
     const T *e = static_cast<const T *>(emb);
     const T *g = static_cast<const T *>(fg);
-    auto mark = [&](int i) {
-        if (h->stage_on) (void)hipEventRecord(h->stage_ev[i], stream);
+    // Launch i of the frame; with stage events on, the dispatch itself
+    // records events 2i and 2i + 1 at the kernel's start and end.
+    auto launch = [&](int i, auto kernel, dim3 grid, dim3 block, size_t lds, auto... args) {
+        if (h->stage_on)
+            hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, stream, h->stage_ev[2 * i],
+                                  h->stage_ev[2 * i + 1], 0u, args...);
+        else
+            hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
+    };
+    auto skip = [&](int i) {           // a launch this frame does not need: its events coincide
+        if (h->stage_on) {
+            (void)hipEventRecord(h->stage_ev[2 * i], stream);
+            (void)hipEventRecord(h->stage_ev[2 * i + 1], stream);
+        }
     };
     const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;
     const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
 
-    mark(0);
     if (mfma) {
         // the participating pixels as a compact list (every pixel when the
         // frame has no foreground channel), recovery + voting into this
@@ -56,51 +69,44 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         unsigned long long *hnext = h->hrep + (size_t)(par ^ 1) * kReplicas * nb;
         int32_t *list = g ? h->list : nullptr;
         const int nslices = slice_count(npix), slice_px = slice_pixels(npix);
-        if (g) {
-            if (((uintptr_t)g & 15u) == 0)
-                hipLaunchKernelGGL((k_compact<T, true>), dim3(nslices), dim3(kCompactThreads), 0, stream, g, npix,
-                                   fg_thr, list, h->counts, labels, score);
-            else
-                hipLaunchKernelGGL((k_compact<T, false>), dim3(nslices), dim3(kCompactThreads), 0, stream, g, npix,
-                                   fg_thr, list, h->counts, labels, score);
-        }
+        if (!g)
+            skip(0);
+        else if (((uintptr_t)g & 15u) == 0)
+            launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, h->counts,
+                   labels, score);
+        else
+            launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, h->counts,
+                   labels, score);
         // grids: at most one workgroup per compute unit, no more waves than tiles
         constexpr int wpb = kVoteWpb<T, F>;
         const int64_t tiles = ((int64_t)npix + 31) / 32;
         const int64_t wgs = (tiles + wpb - 1) / wpb;
         const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        hipLaunchKernelGGL((k_vote_mfma<T, F>), dim3(grid), dim3(wpb * 64), 0, stream, e, list, h->counts, nslices,
-                           slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap);
-        mark(1);
-        mark(2);
+        launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, (const int32_t *)list,
+               (const int32_t *)h->counts, nslices, slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap);
         const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        hipLaunchKernelGGL((k_assign_mfma<T, F>), dim3(grid2), dim3(kWpb2 * 64), 0, stream, e, list, h->counts,
-                           nslices, slice_px, npix, fa.tau_code, h->tb, hcur, hnext, h->hlast, Bw, Bh, cut, h->cap,
-                           cents, num, labels, score);
+        launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, (const int32_t *)list,
+               (const int32_t *)h->counts, nslices, slice_px, npix, fa.tau_code, h->tb,
+               (const unsigned long long *)hcur, hnext, h->hlast, Bw, Bh, cut, h->cap, cents, num, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
         const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 2;
         const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
         const int grid = (int)(tiles < 1024 ? tiles : 1024);
-        hipLaunchKernelGGL((k_vote_generic<T, F>), dim3(grid), dim3(tp), lds, stream, e, g, npix, fg_thr, h->tb, Bw,
-                           Bh, h->hrep);
-        mark(1);
+        launch(0, k_vote_generic<T, F>, dim3(grid), dim3(tp), lds, e, g, npix, fg_thr, h->tb, Bw, Bh, h->hrep);
         const PeakOut po{cents, num, h->peaks, h->kinfo};
-        hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, stream,
-                           h->hrep, h->hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
-        mark(2);
+        launch(1, k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, h->hrep, h->hlast,
+               Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
         const size_t fixed2 = tables + 16 + kCountCap * 4 + kCKeys * 2;
         const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
         const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
-        hipLaunchKernelGGL((k_assign_generic<T, F>), dim3(grid2), dim3(tp2), lds2, stream, e, g, npix, fg_thr,
-                           fa.tau_code, h->tb,
-                           Bw, Bh, h->peaks, h->kinfo, cents, labels, score);
+        launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, g, npix, fg_thr, fa.tau_code, h->tb, Bw, Bh,
+               (const int32_t *)h->peaks, (const int32_t *)h->kinfo, cents, labels, score);
     }
-    mark(3);
     return hipGetLastError() == hipSuccess ? CPE_OK : CPE_ERR_HIP;
 }
 

@@ -28,8 +28,15 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
            "cpe_decode_set_stage_events")
-STAGE_EVENTS = 4
-STAGES = ("recover_vote", "peaks", "assign_label")
+STAGE_EVENTS = 6
+MFMA_BINS = 32
+
+
+def stage_names(bins_w: int, bins_h: int):
+    """Names of the three launches of a frame, as timed by the stage events."""
+    if bins_w <= MFMA_BINS and bins_h <= MFMA_BINS:
+        return ("compact", "recover_vote", "assign_label")
+    return ("recover_vote", "peaks", "assign_label")
 
 _lib = None
 
@@ -156,7 +163,8 @@ class Decoder:
         return pal_x, pal_y, wt, ct
 
     def set_stage_events(self, events) -> int:
-        """``events``: a ctypes array of CPE_STAGE_EVENTS hipEvent_t handles, or None."""
+        """``events``: a ctypes array of CPE_STAGE_EVENTS hipEvent_t handles, or
+        None; events 2i and 2i+1 bracket launch i of every later decode."""
         if events is None:
             return library().cpe_decode_set_stage_events(self._h, None, 0)
         return library().cpe_decode_set_stage_events(self._h, ctypes.cast(events, ctypes.c_void_p), len(events))
