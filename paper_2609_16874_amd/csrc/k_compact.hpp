@@ -125,61 +125,74 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict
     if (tid == 0) counts[blockIdx.x] = base;
 }
 
-// Exclusive prefix sums s_pref[0 .. nslices] of the slice counts (LDS), by
-// the whole block (blockDim.x >= 64, a multiple of 64); s_pref[nslices] = |S|.
-__device__ __forceinline__ void slice_prefix(const int32_t *__restrict__ counts, int nslices, int *s_pref)
+// Exclusive prefix sums s_pref[0 .. nslices] of the slice counts (LDS),
+// s_pref[nslices] = |S|, by the first wave: slice_load issues the loads
+// (lane l holds slices 4 l .. 4 l + 3), slice_scan writes the sums.  Split
+// so that the caller can issue its other loads in between; the caller's
+// barrier publishes s_pref.
+struct SliceLoad {
+    int c[kMaxSlices / 64];
+};
+__device__ __forceinline__ void slice_load(const int32_t *__restrict__ counts, int nslices, SliceLoad &sl)
 {
     const int tid = threadIdx.x;
     if (tid < 64) {
-        // each lane sums 4 consecutive slices, then one wave scan
-        int c[kMaxSlices / 64], sum = 0;
 #pragma unroll
         for (int k = 0; k < kMaxSlices / 64; k++) {
             const int s = 4 * tid + k;
-            c[k] = s < nslices ? counts[s] : 0;
-            sum += c[k];
+            sl.c[k] = s < nslices ? counts[s] : 0;
         }
-        int incl = sum;
+    }
+}
+__device__ __forceinline__ void slice_scan(const SliceLoad &sl, int nslices, int *s_pref)
+{
+    const int tid = threadIdx.x;
+    if (tid < 64) {
+        int sum = 0;
 #pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int t = __shfl_up(incl, d);
-            if (tid >= d) incl += t;
-        }
+        for (int k = 0; k < kMaxSlices / 64; k++) sum += sl.c[k];
+        const int incl = wave_incl_sum(sum);
         int run = incl - sum;
 #pragma unroll
         for (int k = 0; k < kMaxSlices / 64; k++) {
             const int s = 4 * tid + k;
             if (s <= nslices) s_pref[s] = run;
-            run += c[k];
+            run += sl.c[k];
         }
+        // the lanes' slices end at kMaxSlices - 1: the total for nslices == kMaxSlices
         if (tid == 63) s_pref[nslices] = incl;
     }
-    __syncthreads();
 }
 
 // The concatenated slices seen by one lane whose positions never decrease:
 // entry i is list[s R + i - pref[s]] for the slice s with pref[s] <= i <
-// pref[s + 1] (found by bisection once, then by stepping forward).  Without
-// a list (every pixel participates) entry i is pixel i.
+// pref[s + 1].  start() locates the slice of a wave-uniform position i0 (no
+// larger than any position the lane asks for) by counting the prefix sums
+// <= i0 with ballots; pixel() then steps forward.  Without a list (every
+// pixel participates) entry i is pixel i.
 struct ListCursor {
     const int32_t *list;
     const int *pref;          // LDS, pref[0 .. nslices]
     int R, s, lo, hi;
 
-    __device__ __forceinline__ void start(const int32_t *list_, const int *pref_, int nslices, int R_, int i)
+    // Called by every lane of the wave; i0 < pref[nslices] unless the lane
+    // asks for no entry.
+    __device__ __forceinline__ void start(const int32_t *list_, const int *pref_, int nslices, int R_, int i0)
     {
         list = list_;
         pref = pref_;
         R = R_;
         if (!list) return;
-        int a = 0, b = nslices;   // pref[a] <= i < pref[b] for i < |S|
-        while (b - a > 1) {
-            const int m = (a + b) >> 1;
-            if (pref[m] <= i) a = m; else b = m;
+        const int lane = threadIdx.x & 63;
+        int cnt = 0;              // slices s < nslices with pref[s] <= i0 (pref is non-decreasing)
+#pragma unroll
+        for (int k = 0; k < kMaxSlices / 64; k++) {
+            const int q = 64 * k + lane;
+            cnt += __popcll(__ballot(q < nslices && pref[q] <= i0));
         }
-        s = a;
-        lo = pref[a];
-        hi = pref[a + 1];
+        s = cnt > 0 ? cnt - 1 : 0;
+        lo = pref[s];
+        hi = pref[s + 1];
     }
     __device__ __forceinline__ int pixel(int i)
     {

@@ -233,22 +233,29 @@ __device__ __forceinline__ void block_run(int ntiles, int b, int nb, int &first,
     last = (int)((int64_t)ntiles * (b + 1) / nb);
 }
 
-// Next tile of the workgroup's run from the LDS counter (wave-uniform).
-__device__ __forceinline__ int take_tile(int *next, int lane)
+// Tiles of a workgroup's run: wave w starts with tile first + w, later
+// tiles come from an LDS counter (zeroed before the run) in taking order,
+// tile first + waves + k for the k-th taker (wave-uniform).
+__device__ __forceinline__ int take_tile(int *next, int lane, int first, int waves)
 {
     int k = 0;
     if (lane == 0) k = atomicAdd(next, 1);
-    return __builtin_amdgcn_readfirstlane(k);
+    return first + waves + __builtin_amdgcn_readfirstlane(k);
 }
 
 // ---------------------------------------------------------------------------
 // Pass 1: recovery + soft voting (+ the peak extraction in the last workgroup)
 // ---------------------------------------------------------------------------
+// Row stride (in 64-bit words) of the vote kernel's LDS histogram: one word
+// of padding per row puts the 32 rows that one fold instruction touches
+// (lanes = y bins, fixed x bin) into distinct banks.
+constexpr int kHStride = kMfmaBins + 1;
+
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
 // the palette operands, and per wave the squared norms of one tile.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kMfmaBins * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
+    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
            16;
 }
 
@@ -280,14 +287,16 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32 * 32], b * 32 + a
-    uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kMfmaBins);     // palette operands
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32][kHStride], b * kHStride + a
+    uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kHStride);      // palette operands
     int32_t *s_nrm = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);            // [kWpb][64]
     int *s_pref = s_nrm + kWpb * 64;                                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
+    SliceLoad sl;
+    if (list) slice_load(counts, nslices, sl);
     {
         constexpr int kThreads = kWpb * 64, kN = kWKeys / 4, kPer = (kN + kThreads - 1) / kThreads;
         u32x4 w[kPer];
@@ -301,17 +310,17 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             const int i = k * kThreads + tid;
             if (i < kN) reinterpret_cast<u32x4 *>(s_wt)[i] = w[k];
         }
-        for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_h[i] = 0ull;
-        if (list) slice_prefix(counts, nslices, s_pref);
+        for (int i = tid; i < kMfmaBins * kHStride; i += kThreads) s_h[i] = 0ull;
         for (int i = tid; i < kPopBytes / 16; i += kThreads)
             reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
+        if (tid == 0) *s_next = 0;
+        if (list) slice_scan(sl, nslices, s_pref);
     }
+    __syncthreads();
     // the workgroup's run of tiles
     const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
-    int t, tend;
-    block_run(ntiles, blockIdx.x, gridDim.x, t, tend);
-    if (tid == 0) *s_next = t;
-    __syncthreads();
+    int t0, tend;
+    block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
     const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
 
     int32_t *nrm = s_nrm + wv * 64;
@@ -326,7 +335,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             const unsigned long long v = ((unsigned long long)(uint32_t)acc2[r] << 16) +
                                          ((unsigned long long)(uint32_t)acc1[r] << 8) +
                                          (unsigned long long)(uint32_t)acc0[r];
-            atomicAdd(&s_h[ln * kMfmaBins + acc_row(r, g)], v);
+            atomicAdd(&s_h[ln * kHStride + acc_row(r, g)], v);
             acc2[r] = 0.0f;
             acc1[r] = 0.0f;
             acc0[r] = 0.0f;
@@ -416,9 +425,9 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    t = take_tile(s_next, lane);
+    int t = t0 + wv;
     ListCursor cur_list;
-    cur_list.start(list, s_pref, nslices, slice_px, t < tend && 32 * t + ln < n ? 32 * t + ln : 0);
+    cur_list.start(list, s_pref, nslices, slice_px, t < tend ? 32 * t : 0);
     // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
     auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
     // the next tile's rows are loaded as soon as the current ones are converted
@@ -426,7 +435,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it
     if (t < tend) {
         raw.load(emb + (size_t)pixel(t) * D, g);
-        tn = take_tile(s_next, lane);
+        tn = take_tile(s_next, lane, t0, kWpb);
         if (tn < tend) idx = pixel(tn);
     }
     while (t < tend) {
@@ -434,7 +443,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         tile(raw, min(32, n - 32 * t), [&]() {
             if (tn < tend) {
                 raw.load(emb + (size_t)idx * D, g);
-                tnn = take_tile(s_next, lane);
+                tnn = take_tile(s_next, lane, t0, kWpb);
                 if (tnn < tend) idx = pixel(tnn);
             }
         });
@@ -449,7 +458,8 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     unsigned long long *dst = hrep + (size_t)(blockIdx.x % kReplicas) * nb;
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
         const int b = i / kMfmaBins, a = i % kMfmaBins;
-        if (a < Bw && b < Bh && s_h[i]) atomicAdd(dst + b * Bw + a, s_h[i]);
+        const unsigned long long v = s_h[b * kHStride + a];
+        if (a < Bw && b < Bh && v) atomicAdd(dst + b * Bw + a, v);
     }
     if (blockIdx.x == 0)
         for (int k = tid; k < cap; k += blockDim.x) cents[k].npix = 0;
@@ -516,6 +526,8 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
 
     PeakLoad pld;                                   // issued before the table staging
     peaks_lds_load(hcur, Bw, Bh, pld);
+    SliceLoad sl;
+    if (list) slice_load(counts, nslices, sl);
     {
         constexpr int kN = kCKeys / 8, kPer = (kN + kThreads - 1) / kThreads;
         u32x4 w[kPer];
@@ -534,8 +546,26 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         if (tid < 2 * kMfmaBins) s_np[tid] = tid < kMfmaBins ? tb.np1_x[tid] : tb.np1_y[tid - kMfmaBins];
     }
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_cnt[i] = 0;
-    if (list) slice_prefix(counts, nslices, s_pref);
-    peaks_lds(pld, Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank);
+    if (tid == 0) *s_next = 0;
+    peaks_lds_sum(pld, s_h, pl);
+    if (list) slice_scan(sl, nslices, s_pref);
+    __syncthreads();
+
+    // the workgroup's run of tiles of 32 list entries; the first tile's list
+    // entries and rows are loaded while the peaks are extracted
+    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
+    int t0, tend;
+    block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
+    int t = t0 + wv;
+    ListCursor cur_list;
+    cur_list.start(list, s_pref, nslices, slice_px, t < tend ? 32 * t : 0);
+    // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
+    auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
+    RawSlices<T, F> raw;
+    int ip = t < tend ? pixel(t) : 0;                   // this lane's pixel in this tile
+    peaks_lds_find(Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank, [&]() {
+        if (t < tend) raw.load(emb + (size_t)ip * D, g);
+    });
     const int Kc = pl.Kc;
     if (blockIdx.x == 0) {
         for (int k = tid; k < Kc; k += kThreads) {
@@ -553,22 +583,16 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     }
     for (int i = blockIdx.x * kThreads + tid; i < kReplicas * nb; i += gridDim.x * kThreads) hzero[i] = 0ull;
 
-    // the workgroup's run of tiles of 32 list entries
-    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
-    int t, tend;
-    block_run(ntiles, blockIdx.x, gridDim.x, t, tend);
     if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
         ListCursor c0;
-        c0.start(list, s_pref, nslices, slice_px, 32 * t + tid < n ? 32 * t + tid : 0);
-        for (int i = 32 * t + tid; i < min(32 * tend, n); i += kThreads) {
+        c0.start(list, s_pref, nslices, slice_px, 32 * t0 + 64 * wv < n ? 32 * t0 + 64 * wv : 0);
+        for (int i = 32 * t0 + tid; i < min(32 * tend, n); i += kThreads) {
             const int p = c0.pixel(i);
             labels[p] = 0;
             if (score_map) score_map[p] = 0.0f;
         }
         return;
     }
-    if (tid == 0) *s_next = t;
-    __syncthreads();            // s_h is overwritten by the key arrays from here on
     const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of kBatchPad
 
     uint32_t *kx = s_keys + wv * 2 * kMfmaBins * 32;   // x key of bin a, pixel m: kx[a * 32 + m]
@@ -648,17 +672,9 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     };
 
     // the next tile's rows are loaded as soon as the current ones are converted
-    t = take_tile(s_next, lane);
-    ListCursor cur_list;
-    cur_list.start(list, s_pref, nslices, slice_px, t < tend && 32 * t + ln < n ? 32 * t + ln : 0);
-    // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
-    auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
-    RawSlices<T, F> raw;
-    int tn = tend, ip = 0, ipn = 0;                     // next tile; this lane's pixel in this / the next tile
+    int tn = tend, ipn = 0;                             // next tile; this lane's pixel in it
     if (t < tend) {
-        ip = pixel(t);
-        raw.load(emb + (size_t)ip * D, g);
-        tn = take_tile(s_next, lane);
+        tn = take_tile(s_next, lane, t0, kWpb2);
         if (tn < tend) ipn = pixel(tn);
     }
     while (t < tend) {
@@ -666,7 +682,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         codes(raw, [&]() {
             if (tn < tend) {
                 raw.load(emb + (size_t)ipn * D, g);
-                tnn = take_tile(s_next, lane);
+                tnn = take_tile(s_next, lane, t0, kWpb2);
                 if (tnn < tend) ipnn = pixel(tnn);
             }
         });

@@ -168,19 +168,19 @@ __device__ __forceinline__ bool is_peak32(const unsigned long long *s_h, int a, 
     return f;
 }
 
-// From the loaded counts: the summed histogram s_h (32 x 32 slots), the
-// candidates compacted in ascending bin order (pl.pk), K and min(K, cap),
-// the bin -> candidate-index table s_rank [32 * 32] and the candidate
-// batches s_bo / s_bh (pl.nbat of them, a multiple of kBatchPad).  Called by
-// every thread of a block of at least kPeakThreads threads.
-__device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, long long cut, int cap,
-                                          unsigned long long *s_h, PeakLds &pl, u32x4_pk *s_bo, uint32_t *s_bh,
-                                          uint16_t *s_rank)
+// The extraction in two parts, called by every thread of a block of at
+// least kPeakThreads threads.  peaks_lds_sum stores the summed histogram
+// s_h (32 x 32 slots) from the loaded counts; after a barrier of the
+// caller's, peaks_lds_find compacts the candidates in ascending bin order
+// (pl.pk) and writes K and min(K, cap), the bin -> candidate-index table
+// s_rank [32 * 32] and the candidate batches s_bo / s_bh (pl.nbat of them, a
+// multiple of kBatchPad).  `mid` runs between its first and second barrier
+// (the caller's independent work, e.g. loads whose latency the extraction
+// hides).
+__device__ __forceinline__ void peaks_lds_sum(const PeakLoad &ld, unsigned long long *s_h, PeakLds &pl)
 {
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    constexpr int kWaves = kPeakThreads / 64;
-    const bool own = tid < kPeakThreads;            // wave-uniform
-    if (own) {
+    const int tid = threadIdx.x;
+    if (tid < kPeakThreads) {
 #pragma unroll
         for (int u = 0; u < 2; u++) {
             unsigned long long sum = 0;
@@ -190,7 +190,15 @@ __device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, lo
         }
     }
     if (tid < kLdsPeakBins) pl.rowmask[tid] = 0u;
-    __syncthreads();
+}
+template <typename Mid>
+__device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, int cap, const unsigned long long *s_h,
+                                               PeakLds &pl, u32x4_pk *s_bo, uint32_t *s_bh, uint16_t *s_rank,
+                                               Mid mid)
+{
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    constexpr int kWaves = kPeakThreads / 64;
+    const bool own = tid < kPeakThreads;            // wave-uniform
     bool flag[2];
     unsigned long long mask[2];
 #pragma unroll
@@ -204,6 +212,7 @@ __device__ __forceinline__ void peaks_lds(const PeakLoad &ld, int Bw, int Bh, lo
         pl.wave[kWaves + wid] = __popcll(mask[1]);
     }
     __syncthreads();
+    mid();
     int off0 = 0, off1 = 0, K = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; w++) {
