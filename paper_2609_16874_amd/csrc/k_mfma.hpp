@@ -31,12 +31,13 @@
 // histogram in LDS.
 //
 // Pass 2, k_assign_mfma (assignment, Eq7, and label write-out).  With the
-// palette as MFMA rows each lane holds one pixel and 16 bins; the distance
-// codes go through LDS, transposed so that one lane serves one pixel, and
-// the candidate search walks the peak kernel's batches of 4 columns of one
-// row: the key (c_x + c_y) * 2^14 + (128 b + a) is minimised over the peaks,
-// which selects the smallest code sum and, on ties, the lowest bin index,
-// i.e. the lowest centroid index.
+// palette as MFMA rows each lane holds one pixel and 16 bins; the codes go
+// to LDS as the high halves of search keys whose low halves hold the bin
+// index, laid out so that one lane serves one pixel, and the candidate
+// search walks the batches of 4 columns of one row: the key
+// (c_x + c_y) * 2^16 + (128 b + a) is minimised over the peaks, which
+// selects the smallest code sum and, on ties, the lowest bin index, i.e. the
+// lowest centroid index.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -188,16 +189,13 @@ __device__ __forceinline__ f32x16 mfma16(f16x8 a, f16x8 b, f32x16 c)
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-// Xr.hi and Xr.lo of one axis, accumulated onto kMagic (see above).
+// Xr.hi and Xr.lo of one axis, accumulated onto the starting values ah, al
+// (kMagic plus the pixel's part, see below).
 // PIX_ROWS: pixels are the MFMA rows (pass 1) or its columns (pass 2).
 template <int KS, bool PIX_ROWS>
 __device__ __forceinline__ void axis_dot(const f16x8 (&X)[KS], const f16x8 (&ph)[KS], const f16x8 (&pl)[KS],
                                          f32x16 &ah, f32x16 &al)
 {
-    const f32x16 m = {kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic,
-                      kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic, kMagic};
-    ah = m;
-    al = m;
 #pragma unroll
     for (int j = 0; j < KS; j++) {
         if constexpr (PIX_ROWS) {
@@ -210,19 +208,50 @@ __device__ __forceinline__ void axis_dot(const f16x8 (&X)[KS], const f16x8 (&ph)
     }
 }
 
-// Bits of fl32(S + 1) from the two limb accumulators and c = 256 |Xr|^2 +
-// |P|^2 + 1 - 2064 * 0x4B400000 (mod 2^32): S + 1 = 16 (128 bits(ah) +
-// bits(al)) + c exactly, modulo 2^32, and S + 1 < 2^32.
+// S + 1 = 2048 A + 16 L + 256 |Xr|^2 + |P|^2 + 1 with A = Xr.hi and L =
+// Xr.lo.  The pixel's part 256 |Xr|^2 = 2048 (|Xr|^2 >> 3) + 16 (16 (|Xr|^2
+// & 7)) starts the two accumulators: ah = kMagic + (|Xr|^2 >> 3) + A and
+// al = kMagic + 16 (|Xr|^2 & 7) + L, both integers within 2^22 of kMagic,
+// so exact in fp32 and bits(ah) = 0x4B400000 + their offset.  Then
+// S + 1 = 2048 bits(ah) + 16 bits(al) + c (mod 2^32) with the bin's
+// constant c = |P|^2 + 1 - 2064 * 0x4B400000, and S + 1 < 2^32.
+struct PixelInit {
+    uint32_t a, l;    // bit patterns of the starting values of ah and al
+};
+__device__ __forceinline__ PixelInit pixel_init(float n2)
+{
+    const uint32_t u = (uint32_t)n2;    // |Xr|^2 <= 32 * 384^2, exact in fp32
+    return {kMagicBits + (u >> 3), kMagicBits + ((u & 7u) << 4)};
+}
+__device__ __forceinline__ uint32_t bin_const(uint32_t np1) { return np1 - 2064u * kMagicBits; }
+
+// Bits of fl32(S + 1) from the two accumulators and the remaining constant
+// (the bin's constant, plus 256 |Xr|^2 when both accumulators start at
+// kMagic), as
+// two shift-and-add instructions: the empty asm makes the first sum opaque,
+// which keeps the compiler from forming two shifts and a three-way add.
+// (The instructions themselves stay compiler-generated: the accumulators
+// are MFMA results, and only the compiler inserts the wait states a read of
+// them needs.)
 __device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t c)
 {
-    const uint32_t t = (__float_as_uint(ah) << 7) + __float_as_uint(al);
-    return __float_as_uint((float)((t << 4) + c));
+    uint32_t t = (__float_as_uint(al) << 4) + c;
+    asm("" : "+v"(t));
+    return __float_as_uint((float)((__float_as_uint(ah) << 11) + t));
 }
 
-// The pixel's part of c: 256 |Xr|^2 - 2064 * 0x4B400000 (mod 2^32).
-__device__ __forceinline__ uint32_t pixel_const(float n2)
+// Starting values of one accumulator for the 16 pixels (rows acc_row(r, g))
+// of a lane in group g, from a per-wave LDS array indexed by pixel.
+__device__ __forceinline__ f32x16 row_init(const uint32_t *a, int g)
 {
-    return ((uint32_t)n2 << 8) - 2064u * kMagicBits;
+    f32x16 v;
+#pragma unroll
+    for (int r4 = 0; r4 < 4; r4++) {
+        const u32x4 w = *reinterpret_cast<const u32x4 *>(a + 8 * r4 + 4 * g);
+#pragma unroll
+        for (int i = 0; i < 4; i++) v[4 * r4 + i] = __uint_as_float(w[i]);
+    }
+    return v;
 }
 
 // Tiles [first, last) of workgroup b of nb when ntiles tiles are shared out
@@ -252,10 +281,11 @@ __device__ __forceinline__ int take_tile(int *next, int lane, int first, int wav
 constexpr int kHStride = kMfmaBins + 1;
 
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
-// the palette operands, and per wave the squared norms of one tile.
+// the palette operands, and per wave the accumulator starting values of one
+// tile's pixels.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
+    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 128 * 4 + (kMaxSlices + 1) * 4 +
            16;
 }
 
@@ -289,8 +319,8 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32][kHStride], b * kHStride + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kHStride);      // palette operands
-    int32_t *s_nrm = reinterpret_cast<int32_t *>(s_pop + kPopBytes / 4);            // [kWpb][64]
-    int *s_pref = s_nrm + kWpb * 64;                                                  // [kMaxSlices + 1]
+    uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][4][32]
+    int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 128);                       // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -321,9 +351,10 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
     int t0, tend;
     block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
-    const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
+    const uint32_t cbx = bin_const(tb.np1_x[ln]), cby = bin_const(tb.np1_y[ln]);
 
-    int32_t *nrm = s_nrm + wv * 64;
+    // this wave's starting values: [0] x ah, [1] x al, [2] y ah, [3] y al, by pixel
+    uint32_t *ini = s_ini + wv * 128;
     f32x16 acc2 = {}, acc1 = {}, acc0 = {};
     int ntile = 0;
 
@@ -342,18 +373,11 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // Packed weight limbs of the 16 (pixel, bin) results of one axis; nrm
-    // holds the pixels' constants (pixel_const), np1 = |P|^2 + 1 of the bin.
-    auto weights = [&](const f32x16 &ah, const f32x16 &al, int nbase, uint32_t np1, uint32_t (&e)[16]) {
+    // Packed weight limbs of the 16 (pixel, bin) results of one axis; cb is
+    // the bin's constant (bin_const).
+    auto weights = [&](const f32x16 &ah, const f32x16 &al, uint32_t cb, uint32_t (&e)[16]) {
 #pragma unroll
-        for (int r4 = 0; r4 < 4; r4++) {
-            const u32x4 n4 = *reinterpret_cast<const u32x4 *>(nrm + nbase + 8 * r4 + 4 * g);
-#pragma unroll
-            for (int i = 0; i < 4; i++) {
-                const int r = 4 * r4 + i;
-                e[r] = s_wt[(s1_bits(ah[r], al[r], n4[i] + np1) >> 15) & (kWKeys - 1)];
-            }
-        }
+        for (int r = 0; r < 16; r++) e[r] = s_wt[(s1_bits(ah[r], al[r], cb) >> 15) & (kWKeys - 1)];
     };
 
     // One tile of up to 32 pixels (queue slot m = lane & 31) from prefetched
@@ -367,8 +391,11 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         n2x += __shfl_xor(n2x, 32);
         n2y += __shfl_xor(n2y, 32);
         if (g == 0) {
-            nrm[ln] = pixel_const(n2x);
-            nrm[32 + ln] = pixel_const(n2y);
+            const PixelInit ix = pixel_init(n2x), iy = pixel_init(n2y);
+            ini[ln] = ix.a;
+            ini[32 + ln] = ix.l;
+            ini[64 + ln] = iy.a;
+            ini[96 + ln] = iy.l;
         }
         uint32_t ex[16], ey[16];
         {
@@ -378,9 +405,9 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
                 ph[j] = palette_operand(s_pop, 0, 0, j, lane);
                 pl[j] = palette_operand(s_pop, 0, 1, j, lane);
             }
-            f32x16 ah, al;
+            f32x16 ah = row_init(ini, g), al = row_init(ini + 32, g);
             axis_dot<KS, true>(X, ph, pl, ah, al);
-            weights(ah, al, 0, np1x, ex);
+            weights(ah, al, cbx, ex);
         }
         {
             f16x8 ph[KS], pl[KS];
@@ -389,9 +416,9 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
                 ph[j] = palette_operand(s_pop, 1, 0, j, lane);
                 pl[j] = palette_operand(s_pop, 1, 1, j, lane);
             }
-            f32x16 ah, al;
+            f32x16 ah = row_init(ini + 64, g), al = row_init(ini + 96, g);
             axis_dot<KS, true>(Y, ph, pl, ah, al);
-            weights(ah, al, 32, np1y, ey);
+            weights(ah, al, cby, ey);
         }
         if (nvalid < 32) {        // pixels past the end of the list vote nothing
             // (kept a real branch: only the last tile of a round is partial)
@@ -470,10 +497,10 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // ---------------------------------------------------------------------------
 // LDS bytes of k_assign_mfma: code table, palette operands, bin constants,
 // candidate batches, bin -> centroid table, counts, per wave x keys and y
-// keys [32 bins][32 pixels] (u32), then the peak-extraction state.
+// keys [32 bins][kKeyStride] (u32), then the peak-extraction state.
 constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
                               kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                              (size_t)kWpb2 * 2 * kMfmaBins * 32 * 4 + sizeof(PeakLds) + (kMaxSlices + 1) * 4 + 16;
+                              (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) + (kMaxSlices + 1) * 4 + 16;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -482,14 +509,17 @@ constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins * 4
 // next frame's vote launch accumulates into.
 //
 // Then, per tile of 32 pixels, the distance codes of both axes (palette as
-// the MFMA rows, so that each lane holds one pixel and 16 bins) go to LDS
-// as search keys: x key (c_x << 14) | a and y key (c_y << 14) | 128 b, laid
-// out [bin][32 pixels] so that lane m reads pixel m's key of any bin at a
-// fixed stride.  The candidate search walks the batches of 4 columns of one
-// row; the two halves of the wave take alternate batches for the same 32
-// pixels and combine their minima at the end.  The minimum of
-// x key + y key is ((c_x + c_y) << 14) | (128 b + a): the smallest code sum
-// and, on ties, the lowest bin index, i.e. the lowest centroid index.
+// the MFMA rows, so that each lane holds one pixel and 16 bins) go to LDS as
+// search keys: x key (c_x << 16) | a and y key (c_y << 16) | 128 b, laid out
+// [bin][kKeyStride] so that lane m reads pixel m's key of any bin at a fixed
+// stride.  The low halves are written once; per tile only the codes are
+// stored, as 16-bit writes.  The candidate search walks the batches of 4
+// columns of one row; the two halves of the wave take alternate batches for
+// the same 32 pixels and combine their minima at the end.  The sum of an
+// x key and a y key is ((c_x + c_y) << 16) | (128 b + a), taken with
+// unsigned saturation: codes are below 2^16 but a sum of two may not be.
+// The minimum is exact unless every candidate saturates (all code sums of
+// the pixel at least 2^16); such a pixel is searched again in 64 bits.
 template <typename T, int F>
 __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb2 / 4))) void k_assign_mfma(
     const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ counts,
@@ -508,13 +538,13 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     __shared__ __align__(16) unsigned char smem[kAssignLds];
     uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                            // [kCKeys]
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_ct + kCKeys);                  // palette operands
-    uint32_t *s_np = s_pop + kPopBytes / 4;                                          // [2][32] |P|^2 + 1
-    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_np + 2 * kMfmaBins);                 // [kMaxBatchLds]
+    uint32_t *s_cb = s_pop + kPopBytes / 4;                                          // [2][32] bin_const
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_cb + 2 * kMfmaBins);                 // [kMaxBatchLds]
     uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatchLds);             // [kMaxBatchLds]
     uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatchLds);           // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);   // [1024]
-    uint32_t *s_keys = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins); // [kWpb2][2][32][32]
-    PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * 32);
+    uint32_t *s_keys = reinterpret_cast<uint32_t *>(s_cnt + kMfmaBins * kMfmaBins); // [kWpb2][2][32][kKeyStride]
+    PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * kKeyStride);
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
     // the summed histogram lives in the key arrays until the peaks are known
@@ -543,7 +573,8 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         }
         for (int i = tid; i < kPopBytes / 16; i += kThreads)
             reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
-        if (tid < 2 * kMfmaBins) s_np[tid] = tid < kMfmaBins ? tb.np1_x[tid] : tb.np1_y[tid - kMfmaBins];
+        if (tid < 2 * kMfmaBins)
+            s_cb[tid] = bin_const(tid < kMfmaBins ? tb.np1_x[tid] : tb.np1_y[tid - kMfmaBins]);
     }
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_cnt[i] = 0;
     if (tid == 0) *s_next = 0;
@@ -595,39 +626,59 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     }
     const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of kBatchPad
 
-    uint32_t *kx = s_keys + wv * 2 * kMfmaBins * 32;   // x key of bin a, pixel m: kx[a * 32 + m]
-    uint32_t *ky = kx + kMfmaBins * 32;                // y key of bin b, pixel m: ky[b * 32 + m]
+    uint32_t *kx = s_keys + wv * 2 * kMfmaBins * kKeyStride;   // x key of bin a, pixel m: kx[a * kKeyStride + m]
+    uint32_t *ky = kx + kMfmaBins * kKeyStride;                // y key of bin b, pixel m: ky[b * kKeyStride + m]
+    // low halves of the keys: a for the x keys of column a, 128 b for the y
+    // keys of row b (workgroup 0 reads the summed histogram, which these
+    // arrays overwrite, until its records are written)
+    if (blockIdx.x == 0) __syncthreads();
+    for (int i = lane; i < 2 * kMfmaBins * kKeyStride; i += 64) {
+        const int row = i / kKeyStride;
+        kx[i] = row < kMfmaBins ? (uint32_t)row : 128u * (uint32_t)(row - kMfmaBins);
+    }
 
-    // Keys of one tile (pixel m = lane & 31; this lane's 16 bins of each
-    // axis); `next` reuses the input registers once they are converted.
+    // the palette operands stay in registers for the whole run
+    f16x8 pop_h[2][KS], pop_l[2][KS];
+#pragma unroll
+    for (int ax = 0; ax < 2; ax++)
+#pragma unroll
+        for (int j = 0; j < KS; j++) {
+            pop_h[ax][j] = palette_operand(s_pop, ax, 0, j, lane);
+            pop_l[ax][j] = palette_operand(s_pop, ax, 1, j, lane);
+        }
+
+    // Codes of one tile into the keys' high halves (pixel m = lane & 31; this
+    // lane's 16 bins acc_row(r, g) of each axis); `next` reuses the input
+    // registers once they are converted.
     auto codes = [&](RawSlices<T, F> &raw, auto next) {
         float n2x = 0.0f, n2y = 0.0f;
         f16x8 X[KS], Y[KS];
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
         next();
-        const uint32_t cxp = pixel_const(n2x + __shfl_xor(n2x, 32));
-        const uint32_t cyp = pixel_const(n2y + __shfl_xor(n2y, 32));
+        // the pixel's part of the constant: 256 |Xr|^2, the accumulators
+        // starting at kMagic (one starting value shared by all four)
+        const uint32_t npx = (uint32_t)(n2x + __shfl_xor(n2x, 32)) << 8;
+        const uint32_t npy = (uint32_t)(n2y + __shfl_xor(n2y, 32)) << 8;
 #pragma unroll
         for (int ax = 0; ax < 2; ax++) {
-            f16x8 ph[KS], pl_[KS];
-#pragma unroll
-            for (int j = 0; j < KS; j++) {
-                ph[j] = palette_operand(s_pop, ax, 0, j, lane);
-                pl_[j] = palette_operand(s_pop, ax, 1, j, lane);
-            }
             f32x16 ah, al;
-            axis_dot<KS, false>(ax ? Y : X, ph, pl_, ah, al);
-            const uint32_t cp = ax ? cyp : cxp;
-            uint32_t *dst = ax ? ky : kx;
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                ah[r] = kMagic;
+                al[r] = kMagic;
+            }
+            axis_dot<KS, false>(ax ? Y : X, pop_h[ax], pop_l[ax], ah, al);
+            const uint32_t np = ax ? npy : npx;
+            // high half of key (bin acc_row(r, g), pixel ln)
+            uint16_t *dst = reinterpret_cast<uint16_t *>((ax ? ky : kx) + 4 * g * kKeyStride + ln) + 1;
 #pragma unroll
             for (int r4 = 0; r4 < 4; r4++) {
-                const u32x4 np = *reinterpret_cast<const u32x4 *>(s_np + ax * kMfmaBins + 8 * r4 + 4 * g);
+                const u32x4 cb = *reinterpret_cast<const u32x4 *>(s_cb + ax * kMfmaBins + 8 * r4 + 4 * g);
 #pragma unroll
                 for (int i = 0; i < 4; i++) {
-                    const int r = 4 * r4 + i, bin = acc_row(r, g);
-                    const uint32_t code = s_ct[(s1_bits(ah[r], al[r], cp + np[i]) >> 14) & (kCKeys - 1)];
-                    dst[bin * 32 + ln] = (code << 14) | (uint32_t)(ax ? 128 * bin : bin);
+                    const int r = 4 * r4 + i;
+                    dst[2 * kKeyStride * (8 * r4 + i)] = s_ct[(s1_bits(ah[r], al[r], np + cb[i]) >> 14) & (kCKeys - 1)];
                 }
             }
         }
@@ -652,16 +703,29 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
                 const uint32_t v2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
                 const uint32_t v3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
                 const uint32_t yk = *reinterpret_cast<const uint32_t *>(kyl + hb);
-                best = min(best, min(min(v0, v1), min(v2, v3)) + yk);
+                best = min(best, __builtin_elementwise_add_sat((uint32_t)min(min(v0, v1), min(v2, v3)), yk));
             }
         }
         best = min(best, (uint32_t)__shfl_xor((int)best, 32));
+        uint32_t sum = best >> 16, idx = best & 0xffffu;   // code sum and 128 b + a of the winner
+        if (best == 0xffffffffu) {   // every sum saturated: all batches again, in 64 bits
+            unsigned long long b64 = ~0ull;
+            for (int bi = 0; bi < nbat; bi++) {
+                const u32x4 o = s_bo[bi];
+                const unsigned long long yk = *reinterpret_cast<const uint32_t *>(kyl + s_bh[bi]);
+#pragma unroll
+                for (int q = 0; q < 4; q++)
+                    b64 = min(b64, (unsigned long long)*reinterpret_cast<const uint32_t *>(kxl + o[q]) + yk);
+            }
+            sum = (uint32_t)(b64 >> 16);
+            idx = (uint32_t)b64 & 0xffffu;
+        }
         if (g == 0 && ln < nvalid) {
-            if ((best >> 14) < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
-                const int a = (int)(best & 31u), b = (int)((best >> 7) & 31u);
+            if (sum < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
+                const int a = (int)(idx & 31u), b = (int)((idx >> 7) & 31u);
                 const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
                 labels[pix] = k + 1;
-                if (score_map) score_map[pix] = expf(-((float)(best >> 14) * 0x1p-12f));
+                if (score_map) score_map[pix] = expf(-((float)sum * 0x1p-12f));
                 atomicAdd(s_cnt + k, 1);
             } else {
                 labels[pix] = 0;

@@ -120,6 +120,7 @@ constexpr int kLdsPeakBins = 32;
 constexpr int kPeakThreads = 512;
 constexpr int kMaxBatchLds = 128;   // <= 16 strict maxima per row of 32 -> <= 4 batches per row
 constexpr int kBatchPad = 8;        // the batch list is padded to a multiple of this
+constexpr int kKeyStride = 32;      // words per bin row of the assignment kernel's key arrays
 
 // LDS of peaks_lds (the summed histogram may alias any scratch the caller
 // does not need until the peaks are known).
@@ -255,20 +256,20 @@ __device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, in
 #pragma unroll
             for (int s4 = 0; s4 < 4; s4++) {
                 if (m) {
-                    last = (uint32_t)__builtin_ctz(m) * 128u;
+                    last = (uint32_t)__builtin_ctz(m) * (4u * kKeyStride);
                     m &= m - 1u;
                 }
                 o[s4] = last;
             }
             s_bo[start + j] = o;
-            s_bh[start + j] = (uint32_t)b * 128u;
+            s_bh[start + j] = (uint32_t)b * (4u * kKeyStride);
         }
         // pad the list with copies of the last batch (a repeated batch leaves
         // every minimum unchanged)
         if (nbt > 0 && start + nbt == total)
             for (int e = total; e < padded; e++) {
                 s_bo[e] = o;
-                s_bh[e] = (uint32_t)b * 128u;
+                s_bh[e] = (uint32_t)b * (4u * kKeyStride);
             }
         if (tid == 0) {
             pl.K = K;
