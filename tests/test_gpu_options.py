@@ -220,3 +220,26 @@ def test_option_and_mask_argument_errors():
     assert dec.masks(lab, 0, cap, m) == 0
     torch.cuda.synchronize()
     dec.close()
+
+
+def test_far_pixels_with_saturating_code_sums():
+    """Foreground pixels whose every x + y code sum is at least 2^16 (the
+    32-bit search keys saturate and the kernel searches them again in 64
+    bits): labels, counts and scores equal the oracle's, with no mask
+    threshold and with tau on either side of some of their sums."""
+    from tests import farframe
+    emb, fg, fx, fy, theta, far = farframe.make()
+    dec = native().Decoder(farframe.H, farframe.W, farframe.F, "f32", fx, fy, farframe.BINS, farframe.BINS,
+                           farframe.CAP)
+    for tau in (math.inf, 20.0, 100.0):
+        print(f"far pixels tau {tau}", flush=True)
+        ref = oracle.decode(emb, fg, fx, fy, farframe.BINS, farframe.BINS, farframe.CAP, 0.5, theta, tau=tau)
+        if tau == math.inf:
+            sums = farframe.candidate_code_sums(ref, emb, farframe.F)
+            assert sums[far].min() >= 2 ** 16
+        got = run_ex(dec, emb, fg, 0.5, theta, tau)
+        assert_parity(got, ref, farframe.CAP)
+        if tau == 20.0:     # some far pixels below tau, some above
+            lab = got["labels"].reshape(-1)[far]
+            assert 0 < int((lab > 0).sum()) < len(far)
+    dec.close()

@@ -504,3 +504,23 @@ def test_assignment_agrees_with_eq7_real_distances(cfg):
     bad = np.nonzero(got != real)[0]
     gap = D[bad, got[bad] - 1] - D[bad, real[bad] - 1]
     assert np.all(gap < 0.02 * (1 + D[bad, real[bad] - 1])), gap.max()
+
+
+def test_far_pixels_take_the_exact_argmin():
+    """Pixels whose every candidate code sum is at least 2^16: the label is
+    the lowest (code sum, 128 b + a) over the candidates (Eq7 with the
+    lowest-index tie rule), by brute force over the oracle's own tables."""
+    from tests import farframe
+    emb, fg, fx, fy, theta, far = farframe.make()
+    ref = oracle.decode(emb, fg, fx, fy, farframe.BINS, farframe.BINS, farframe.CAP, 0.5, theta)
+    sums = farframe.candidate_code_sums(ref, emb, farframe.F)
+    assert ref["K"] >= 2 and sums[far].min() >= 2 ** 16
+    idx = 128 * ref["centroids"]["bin_y"].astype(np.int64) + ref["centroids"]["bin_x"].astype(np.int64)
+    key = sums * 4096 + idx[None, :]
+    want = key.argmin(1) + 1
+    lab = ref["labels"].reshape(-1)
+    assert np.array_equal(lab[far], want[far])
+    assert len(set(lab[far].tolist())) >= 3          # several different winners among them
+    # and the score is e^-(winning code sum / 4096)
+    np.testing.assert_allclose(ref["score_map"].reshape(-1)[far],
+                               np.exp(-sums[far].min(1) / 4096.0).astype(np.float32), rtol=1e-6)
