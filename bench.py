@@ -185,21 +185,23 @@ def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=N
     return spec, frames, ms_step, stages, mean_bytes, ws
 
 
-def cpu_baseline(cfg, frames, budget_s=15.0):
+def cpu_baseline(cfg, frames, budget_s=12.0):
+    """The oracle on the step's frames in order, cycling through them until
+    about budget_s seconds of CPU work are done."""
     import oracle
     th = thresholds()[str(cfg)]
     spec = frames[0].spec
     fx, fy = spec.freqs()
     done, t0 = 0, time.perf_counter()
-    for f in frames:
+    while time.perf_counter() - t0 < budget_s:
+        f = frames[done % len(frames)]
         oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
                       th["peak_threshold"], want_score=False)
         done += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
     dt = time.perf_counter() - t0
     return {"value": done / dt, "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "sample": f"frames 0-{done - 1} of the {spec.name} batch, single-threaded C oracle, {dt:.1f} s"}
+            "sample": f"{done} decodes cycling through the {len(frames)} frames of the {spec.name} batch, "
+                      f"single-threaded C oracle, {dt:.1f} s"}
 
 
 # The paper's optimised decoder latency for its 704x704, L = 4 maps on a Jetson
