@@ -498,9 +498,13 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // LDS bytes of k_assign_mfma: code table, palette operands, bin constants,
 // candidate batches, bin -> centroid table, counts, per wave x keys and y
 // keys [32 bins][kKeyStride] (u32), then the peak-extraction state.
-constexpr size_t kAssignLds = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
-                              kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                              (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) + (kMaxSlices + 1) * 4 + 16;
+constexpr size_t kAssignLdsCore = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
+                                  kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
+                                  (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
+                                  (kMaxSlices + 1) * 4 + 16;
+// then, 16-byte aligned, per wave the 32 search results of a tile
+constexpr size_t kBestOff = (kAssignLdsCore + 15) & ~(size_t)15;
+constexpr size_t kAssignLds = kBestOff + (size_t)kWpb2 * 32 * 4;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -547,6 +551,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * kKeyStride);
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
+    uint32_t *s_best = reinterpret_cast<uint32_t *>(smem + kBestOff);                 // [kWpb2][32]
     // the summed histogram lives in the key arrays until the peaks are known
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_keys);
 
@@ -684,29 +689,47 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         }
     };
 
-    // Candidate search for the pixel of lane m: this half of the wave takes
-    // batches g, g + 2, ... (8 batches, 4 per half, read per step), then the
-    // halves combine; lanes of half 0 write the labels of valid pixels.
+    // Candidate search.  Lane l serves the four pixels 4 q .. 4 q + 3
+    // (q = l & 7) for the batches j, j + 8, ... (j = l >> 3): one 16-byte
+    // read fetches a column's keys of its four pixels, so each address
+    // computation and each read serve four pixels.  The eight lanes of a
+    // pixel quad then combine their minima, and lane m takes pixel m's
+    // result through LDS; lanes of half 0 write the labels of valid pixels.
+    uint32_t *best_w = s_best + wv * 32;
     auto search = [&](int pix, int nvalid) {
         __builtin_amdgcn_wave_barrier();
+        const int q = lane & 7, j0 = lane >> 3;
+        const unsigned char *kxq = reinterpret_cast<const unsigned char *>(kx + 4 * q);
+        const unsigned char *kyq = reinterpret_cast<const unsigned char *>(ky + 4 * q);
+        uint32_t b4[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+#pragma unroll 2
+        for (int bi = j0; bi < nbat; bi += 8) {     // nbat is a multiple of 8: the same count for every lane
+            const u32x4 o = s_bo[bi];
+            const uint32_t hb = s_bh[bi];
+            const u32x4 v0 = *reinterpret_cast<const u32x4 *>(kxq + o.x);
+            const u32x4 v1 = *reinterpret_cast<const u32x4 *>(kxq + o.y);
+            const u32x4 v2 = *reinterpret_cast<const u32x4 *>(kxq + o.z);
+            const u32x4 v3 = *reinterpret_cast<const u32x4 *>(kxq + o.w);
+            const u32x4 yk = *reinterpret_cast<const u32x4 *>(kyq + hb);
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+                b4[e] = min(b4[e], __builtin_elementwise_add_sat((uint32_t)min(min(v0[e], v1[e]), min(v2[e], v3[e])),
+                                                                 yk[e]));
+        }
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            b4[e] = min(b4[e], (uint32_t)__shfl_xor((int)b4[e], 8));
+            b4[e] = min(b4[e], (uint32_t)__shfl_xor((int)b4[e], 16));
+            b4[e] = min(b4[e], (uint32_t)__shfl_xor((int)b4[e], 32));
+        }
+        if (lane < 8) {
+            const u32x4 w4 = {b4[0], b4[1], b4[2], b4[3]};
+            *reinterpret_cast<u32x4 *>(best_w + 4 * q) = w4;
+        }
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t best = best_w[ln];
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
         const unsigned char *kyl = reinterpret_cast<const unsigned char *>(ky + ln);
-        uint32_t best = 0xffffffffu;
-        for (int i = 0; i < nbat; i += kBatchPad) {
-#pragma unroll
-            for (int u = 0; u < kBatchPad / 2; u++) {
-                const int bi = i + 2 * u + g;
-                const u32x4 o = s_bo[bi];
-                const uint32_t hb = s_bh[bi];
-                const uint32_t v0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
-                const uint32_t v1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
-                const uint32_t v2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
-                const uint32_t v3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
-                const uint32_t yk = *reinterpret_cast<const uint32_t *>(kyl + hb);
-                best = min(best, __builtin_elementwise_add_sat((uint32_t)min(min(v0, v1), min(v2, v3)), yk));
-            }
-        }
-        best = min(best, (uint32_t)__shfl_xor((int)best, 32));
         uint32_t sum = best >> 16, idx = best & 0xffffu;   // code sum and 128 b + a of the winner
         if (best == 0xffffffffu) {   // every sum saturated: all batches again, in 64 bits
             unsigned long long b64 = ~0ull;
@@ -714,8 +737,8 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
                 const u32x4 o = s_bo[bi];
                 const unsigned long long yk = *reinterpret_cast<const uint32_t *>(kyl + s_bh[bi]);
 #pragma unroll
-                for (int q = 0; q < 4; q++)
-                    b64 = min(b64, (unsigned long long)*reinterpret_cast<const uint32_t *>(kxl + o[q]) + yk);
+                for (int c = 0; c < 4; c++)
+                    b64 = min(b64, (unsigned long long)*reinterpret_cast<const uint32_t *>(kxl + o[c]) + yk);
             }
             sum = (uint32_t)(b64 >> 16);
             idx = (uint32_t)b64 & 0xffffu;
