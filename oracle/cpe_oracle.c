@@ -177,7 +177,11 @@ static int check_args(int32_t H, int32_t W, int32_t D, int32_t dtype, const void
                       int32_t cap, float fg_thr, double peak_thr)
 {
     if (H < 1 || W < 1 || (int64_t)H * (int64_t)W > 2147483647LL) return CPE_ORACLE_EINVAL;
-    if (n_freq < 1 || n_freq > 16 || D != 4 * n_freq) return CPE_ORACLE_EINVAL;
+    /* D channels per pixel: the x block [0, D/2) and the y block [D/2, D),
+     * each (sin, cos) pairs of ascending harmonics (Eq2, Eq3); the decoder
+     * uses the first 2 n_freq channels of each block (D > 4 n_freq: only the
+     * low harmonics, those a coarse bin grid resolves) */
+    if (n_freq < 1 || n_freq > 16 || D < 4 * n_freq || D % 2 != 0) return CPE_ORACLE_EINVAL;
     if (dtype != 0 && dtype != 1) return CPE_ORACLE_EINVAL;
     if (!emb || !fx || !fy) return CPE_ORACLE_EINVAL;
     if (bw < 1 || bw > 128 || bh < 1 || bh > 128 || cap < 1) return CPE_ORACLE_EINVAL;
@@ -247,7 +251,7 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
         isnan(tau) || !centroids || !num_centroids || !labels)
         return CPE_ORACLE_EINVAL;
 
-    const int32_t F = n_freq, twoF = 2 * n_freq;
+    const int32_t F = n_freq, twoF = 2 * n_freq, yoff = D / 2;
     const size_t npix = (size_t)H * (size_t)W;
     const int32_t nbins = bins_w * bins_h;
 
@@ -271,7 +275,7 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
         if (!participates(fg, dtype, p, fg_threshold)) continue;
         for (int32_t c = 0; c < twoF; c++) {
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
-            Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));
+            Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c)));
         }
         axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);
         axis_profile(Y, Ph, bins_h, twoF, wt, ct, qy, NULL);
@@ -312,7 +316,7 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
         if (Kc == 0 || !participates(fg, dtype, p, fg_threshold)) continue;
         for (int32_t c = 0; c < twoF; c++) {
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
-            Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));
+            Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c)));
         }
         axis_profile(X, Pw, bins_w, twoF, wt, ct, NULL, cx);
         axis_profile(Y, Ph, bins_h, twoF, wt, ct, NULL, cy);
@@ -381,7 +385,7 @@ int cpe_oracle_decode_real(int32_t H, int32_t W, int32_t D, int32_t dtype,
                    fg_threshold, peak_threshold) != CPE_ORACLE_OK || !fg ||
         !hist || !peaks || !num_peaks || !labels)
         return CPE_ORACLE_EINVAL;
-    const int32_t F = n_freq, twoF = 2 * n_freq;
+    const int32_t F = n_freq, twoF = 2 * n_freq, yoff = D / 2;
     const size_t npix = (size_t)H * (size_t)W;
     const int32_t nbins = bins_w * bins_h;
     double *Pw = malloc(sizeof(double) * bins_w * twoF), *Ph = malloc(sizeof(double) * bins_h * twoF);
@@ -396,7 +400,7 @@ int cpe_oracle_decode_real(int32_t H, int32_t W, int32_t D, int32_t dtype,
         if (!(load_value(fg, dtype, p) > fg_threshold)) continue;
         for (int32_t c = 0; c < twoF; c++) {
             vx[c] = (double)load_value(emb, dtype, p * (size_t)D + (size_t)c);
-            vy[c] = (double)load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c));
+            vy[c] = (double)load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c));
         }
         real_distances(vx, Pw, bins_w, twoF, dx);
         real_distances(vy, Ph, bins_h, twoF, dy);
@@ -416,7 +420,7 @@ int cpe_oracle_decode_real(int32_t H, int32_t W, int32_t D, int32_t dtype,
         if (Kc == 0 || !(load_value(fg, dtype, p) > fg_threshold)) continue;
         for (int32_t c = 0; c < twoF; c++) {
             vx[c] = (double)load_value(emb, dtype, p * (size_t)D + (size_t)c);
-            vy[c] = (double)load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c));
+            vy[c] = (double)load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c));
         }
         real_distances(vx, Pw, bins_w, twoF, dx);
         real_distances(vy, Ph, bins_h, twoF, dy);

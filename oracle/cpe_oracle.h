@@ -52,7 +52,10 @@ typedef struct {
 #define CPE_ORACLE_EINVAL 1
 
 /* dtype: 0 = float32, 1 = float16 (IEEE binary16 bit patterns).
- * emb: [H][W][D] channels-last, D = 4*n_freq; fg: [H][W]; both host memory.
+ * emb: [H][W][D] channels-last, D >= 4*n_freq and even: the x block is
+ * channels [0, D/2), the y block [D/2, D), each (sin, cos) pairs of ascending
+ * harmonics; the first 2*n_freq channels of each block are decoded (with
+ * D > 4*n_freq only the low harmonics).  fg: [H][W]; both host memory.
  * Outputs (host): centroids[capacity], *num_centroids (true count K),
  * labels[H*W]; optional (may be NULL): score_map[H*W], hist[bins_h*bins_w]
  * (row-major [b][a]), pal_x[bins_w*2F], pal_y[bins_h*2F], weights[8192]

@@ -25,8 +25,11 @@ MUTANTS = [
      "double centre = ((double)(a) * (double)extent) / (double)(n + 1);\n        for (int32_t k = 0; k < F; k++) {\n            double phase"),
     ("sin/cos swapped", "pal[a * 2 * F + 2 * k] = (int16_t)rint(4096.0 * sin(phase));",
      "pal[a * 2 * F + 2 * k] = (int16_t)rint(4096.0 * cos(phase));"),
-    ("y block read from x channels", "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(twoF + c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);",
+    ("y block read from x channels", "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);",
      "Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(c)));\n        }\n        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);"),
+    ("y block taken right after the decoded x channels",
+     "twoF = 2 * n_freq, yoff = D / 2;\n    const size_t npix = (size_t)H * (size_t)W;\n    const int32_t nbins = bins_w * bins_h;\n\n    int16_t *Pw",
+     "twoF = 2 * n_freq, yoff = twoF;\n    const size_t npix = (size_t)H * (size_t)W;\n    const int32_t nbins = bins_w * bins_h;\n\n    int16_t *Pw"),
     ("x palette used for y", "axis_profile(Y, Ph, bins_h, twoF, wt, ct, qy, NULL);", "axis_profile(Y, Pw, bins_h, twoF, wt, ct, qy, NULL);"),
     ("weight e^-2d", "wt[key] = (uint16_t)rint(32768.0 * exp(-key_distance(key, W_MANT)));",
      "wt[key] = (uint16_t)rint(32768.0 * exp(-2.0 * key_distance(key, W_MANT)));"),
@@ -81,6 +84,7 @@ PIN_CASES = [
     (pins.test_mask_threshold_and_all_pixels_equal_exhaustive_search, (6, pins.np.float32, 1, 4, 7, 8, False, (0.5, 0))),
     (pins.test_mask_threshold_on_noise_free_frame_with_all_pixels, ()),
     (pins.test_mask_threshold_nests, ()),
+    (pins.test_low_harmonics_equal_decoding_the_sliced_encoding, (0, 4)),
 ]
 
 

@@ -427,6 +427,47 @@ def test_argument_errors():
         args.update(kw)
         assert oracle.decode(emb, fg, fx, fy, check=False, **args)["rc"] == 1
     assert oracle.decode(emb[..., :12], fg, fx, fy, 4, 4, 4, 0.5, 0.0, check=False)["rc"] == 1
+    # more channels than 4 n_freq are allowed (low harmonics only), an odd count is not
+    assert oracle.decode(np.zeros((4, 4, 18), np.float32), fg, fx, fy, 4, 4, 4, 0.5, 0.0, check=False)["rc"] == 0
+    assert oracle.decode(np.zeros((4, 4, 17), np.float32), fg, fx, fy, 4, 4, 4, 0.5, 0.0, check=False)["rc"] == 1
+
+
+# --------------------------------------------------------------------------
+# Low harmonics of a longer encoding (the "resolved harmonics" decode)
+# --------------------------------------------------------------------------
+def low_harmonic_channels(emb, F_used):
+    """The channels of the first F_used harmonics of each axis block of a
+    [H][W][D] embedding (x block first, then y, each (sin, cos) pairs of
+    ascending harmonics, Eq2/Eq3), as a [H][W][4 F_used] array."""
+    half = emb.shape[-1] // 2
+    return np.concatenate([emb[..., :2 * F_used], emb[..., half:half + 2 * F_used]], axis=-1)
+
+
+@pytest.mark.parametrize("cfg,F_used", [(0, 1), (0, 3), (0, 4), (0, 8), (2, 4)])
+def test_low_harmonics_equal_decoding_the_sliced_encoding(cfg, F_used):
+    """Decoding a D-channel map with its first F' harmonics is, by definition,
+    decoding the map cut down to those 4 F' channels (Eq9/Eq10 compare each
+    axis block with palettes of the same harmonics)."""
+    f = synth.make_frame(cfg)
+    if cfg == 2:      # a 128 x 160 window keeps the full-size frame's instances and layout
+        emb, fg = f.emb[256:384, 240:400], f.fg[256:384, 240:400]
+        H, W = emb.shape[:2]
+        fx = np.array([2.0 * math.pi * 2 ** k / 640 for k in range(f.spec.n_freq)])
+        fy = fx.copy()
+    else:
+        emb, fg = f.emb, f.fg
+        H, W = emb.shape[:2]
+        fx, fy = f.spec.freqs()
+    fx, fy = fx[:F_used], fy[:F_used]
+    bins = 16
+    theta = 0.02 * H * W / 1024
+    full = oracle.decode(emb, fg, fx, fy, bins, bins, 64, 0.5, theta)
+    cut = oracle.decode(low_harmonic_channels(emb, F_used), fg, fx, fy, bins, bins, 64, 0.5, theta)
+    assert full["K"] == cut["K"]
+    assert np.array_equal(full["hist"], cut["hist"])
+    assert np.array_equal(full["centroids"], cut["centroids"])
+    assert np.array_equal(full["labels"], cut["labels"])
+    assert full["K"] > 0
 
 
 def test_clamp_saturates():
