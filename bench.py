@@ -168,19 +168,48 @@ def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
     return dict(zip(names, (acc / n).tolist()))
 
 
-def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=None):
+def panoptic_quality(labels, inst):
+    """PQ of a decoded label map against the generating instance map (0 =
+    background in both): segments match when their IoU exceeds 0.5 (then
+    uniquely); PQ = sum of matched IoUs / (TP + FP/2 + FN/2).  Host-side
+    evaluation of the outputs on a synthetic frame, outside any timing."""
+    labels = np.asarray(labels, dtype=np.int64)
+    inst = np.asarray(inst, dtype=np.int64)
+    K, N = int(labels.max()), int(inst.max())
+    m = (inst > 0) | (labels > 0)
+    cnt = np.bincount(inst[m] * (K + 1) + labels[m], minlength=(N + 1) * (K + 1)).reshape(N + 1, K + 1)
+    inter = cnt[1:, 1:].astype(np.float64)
+    ia, la = cnt[1:, :].sum(1), cnt[:, 1:].sum(0)
+    iou = inter / np.maximum(ia[:, None] + la[None, :] - inter, 1)
+    tp = iou > 0.5
+    ntp = int(tp.sum())
+    nfn, nfp = int((ia > 0).sum()) - ntp, int((la > 0).sum()) - ntp
+    return {"pq": round(float(iou[tp].sum()) / max(ntp + 0.5 * nfp + 0.5 * nfn, 1e-9), 4),
+            "tp": ntp, "fp": nfp, "fn": nfn}
+
+
+def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=None, n_used=None, quality=False):
+    """Time workload cfg; n_used: decode only the first n_used harmonics of
+    the same embedding (the resolved-harmonics decode).  quality: also the
+    PQ of each frame's labels against its instance map."""
     from paper_2609_16874_amd import native
     th = th or thresholds()[str(cfg)]
     spec, frames, embs, fgs = loaded or load_workload(cfg, n_frames)
     fx, fy = spec.freqs()
+    nf = n_used or spec.n_freq
     nb = bins or spec.bins
-    dec = native.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, nb, nb, th["capacity"])
+    dec = native.Decoder(spec.H, spec.W, nf, spec.dtype, fx[:nf], fy[:nf], nb, nb, th.get("capacity"), D=spec.D)
     outs = [dec.new_outputs() for _ in frames]
     ms_step = time_steps(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], steps, warmup)
     stages = stage_times(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], max(1, min(steps, 10)))
     fb = [frame_bytes(spec, f) for f in frames]
     mean_bytes = {k: float(np.mean([b[k] for b in fb])) for k in fb[0]}
     ws = dec.workspace_bytes()
+    if quality:
+        q = [dict(panoptic_quality(o["labels"].cpu().numpy(), f.inst), K=int(o["num_centroids"].item()),
+                  instances=int(f.kept.sum())) for o, f in zip(outs, frames)]
+        mean_bytes["quality"] = q[0] if len(q) == 1 else {"pq_mean": round(float(np.mean([x["pq"] for x in q])), 4),
+                                                          "K_mean": float(np.mean([x["K"] for x in q]))}
     dec.close()
     return spec, frames, ms_step, stages, mean_bytes, ws
 
@@ -321,14 +350,30 @@ def main():
         "workspace_bytes": ws,
     }
     if not args.no_extra:
+        from paper_2609_16874_amd import harmonics
+        with open(GOLDEN) as fh:
+            resolved = json.load(fh)["resolved"]
         extra = {}
         for cfg in (2, 3):
-            s, fr, ms, st, b, _ = bench_config(cfg, max(1, args.steps // 2), max(1, args.warmup // 2))
+            loaded = load_workload(cfg)
+            s, fr, ms, st, b, _ = bench_config(cfg, max(1, args.steps // 2), max(1, args.warmup // 2),
+                                               loaded=loaded, quality=True)
             extra[f"cfg{cfg}"] = {"workload": s.name, "ms_per_frame": round(ms, 5), "frames_per_s": round(1000 / ms, 1),
                                   "literal_bytes": int(b["literal"]),
                                   "literal_roofline_frac": round(b["literal"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                                  "stages_ms": {k: round(v, 5) for k, v in st.items()}}
-            del fr
+                                  "stages_ms": {k: round(v, 5) for k, v in st.items()},
+                                  "quality_vs_instances": b["quality"]}
+            # the same frame decoded with only the harmonics the 32x32 grid resolves
+            fx, fy = s.freqs()
+            n = harmonics.resolved_pair(fx, fy, s.W, s.H, s.bins, s.bins)
+            th = dict(resolved[str(cfg)], capacity=thresholds()[str(cfg)]["capacity"])
+            s, fr, ms, st, b, _ = bench_config(cfg, max(1, args.steps // 2), max(1, args.warmup // 2), th=th,
+                                               loaded=loaded, n_used=n, quality=True)
+            extra[f"cfg{cfg}_resolved"] = {"workload": s.name, "harmonics_decoded": n,
+                                           "ms_per_frame": round(ms, 5), "frames_per_s": round(1000 / ms, 1),
+                                           "stages_ms": {k: round(v, 5) for k, v in st.items()},
+                                           "quality_vs_instances": b["quality"]}
+            del fr, loaded
         result["extra"] = extra
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(4, frames)

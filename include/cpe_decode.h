@@ -30,8 +30,10 @@
  * axes adds 1.0).
  *
  * Layouts (all row-major, channels last):
- *   emb    [H][W][D], D = 4F: channels [0,2F) encode x, [2F,4F) encode y;
- *          within a block channel 2k = sin(w_k p), 2k+1 = cos(w_k p)
+ *   emb    [H][W][D]: channels [0,D/2) encode x, [D/2,D) encode y; within a
+ *          block channel 2k = sin(w_k p), 2k+1 = cos(w_k p).  The decoder
+ *          reads the first 2F channels of each block (F = n_freq; D = 4F
+ *          reads them all)
  *   fg     [H][W], same dtype as emb; a pixel participates iff fg > threshold
  *   labels [H][W] int32
  *   score  [H][W] float (optional): expf(-(c_x + c_y)/4096) of the assigned
@@ -85,16 +87,24 @@ typedef struct {
 typedef struct cpe_decoder cpe_decoder;
 
 /*
- * Build a decoder for frames of H x W pixels with D = 4*n_freq channels.
+ * Build a decoder for frames of H x W pixels with D channels, decoding the
+ * first n_freq harmonics of each axis.
  * Section 3.2 (Eq9): the palettes P_w, P_h are the encodings of the bin
  * centres and are computed here once, on the host in fp64, then kept on the
  * device with the weight table ("preloaded ... without recomputing").
  *   out          receives the handle (set to NULL on failure)
  *   H, W         frame size, H*W <= 2^31-1
- *   D            channels per pixel, must equal 4*n_freq
+ *   D            channels per pixel: the x block is channels [0, D/2), the y
+ *                block [D/2, D), each (sin, cos) pairs of ascending harmonics
+ *                (Eq2, Eq3).  D = 4*n_freq decodes every harmonic.  D >
+ *                4*n_freq decodes only the first n_freq of each block (the
+ *                harmonics a coarse bin grid resolves; the palettes of Eq9 are
+ *                built for those); then D must be even and each block 16-byte
+ *                aligned (D * element size a multiple of 32), else
+ *                CPE_ERR_UNSUPPORTED.  D < 4*n_freq or odd: CPE_ERR_INVALID_ARG
  *   dtype        element type of emb and fg
  *   freq_x/y     host arrays of n_freq angular frequencies in rad/pixel
- *                (harmonic k of the x and y encodings), copied
+ *                (harmonic k of the x and y encodings, k < n_freq), copied
  *   n_freq       1..16
  *   bins_w/h     1..128 histogram bins along x / y
  *   centroid_capacity  >= 1 and <= bins_w*bins_h; the number of centroid

@@ -43,6 +43,9 @@ __device__ __forceinline__ int32_t dot_pk(const int32_t (&x)[F], const int32_t *
     return acc;
 }
 
+// Alignment of a pixel's axis blocks in the layout with D = 4F channels; a
+// longer encoding (D > 4F) has 16-byte aligned rows and y blocks, which
+// satisfies the same bounds.
 template <typename T, int F>
 struct PixelLayout {
     static constexpr int kRowBytes = 4 * F * (int)sizeof(T);
@@ -54,7 +57,8 @@ struct PixelLayout {
 // S1 + S2: recovery and soft voting
 // ---------------------------------------------------------------------------
 template <typename T, int F>
-__global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix,
+__global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb, int32_t dstride, int32_t yoff,
+                                              const T *__restrict__ fg, int32_t npix,
                                               float fg_thr, Tables tb, int32_t Bw, int32_t Bh,
                                               unsigned long long *__restrict__ hrep)
 {
@@ -103,10 +107,10 @@ __global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb,
         __syncthreads();
         const int n = *s_n;
         if (tid < n) {
-            const T *row = emb + (size_t)s_list[tid] * (4 * F);
+            const T *row = emb + (size_t)s_list[tid] * dstride;
             int32_t xk[F], yk[F];
             load_block<T, F, L::kAlignX>(row, xk);
-            load_block<T, F, L::kAlignY>(row + 2 * F, yk);
+            load_block<T, F, L::kAlignY>(row + yoff, yk);
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
             for (int a = 0; a < Bw; a++)
@@ -158,7 +162,8 @@ __global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb,
 // S4 + S5: assignment, label write-out, counts
 // ---------------------------------------------------------------------------
 template <typename T, int F>
-__global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ emb, const T *__restrict__ fg, int32_t npix,
+__global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ emb, int32_t dstride, int32_t yoff,
+                                                const T *__restrict__ fg, int32_t npix,
                                                 float fg_thr, uint32_t tau_code, Tables tb, int32_t Bw, int32_t Bh,
                                                 const int32_t *__restrict__ peaks, const int32_t *__restrict__ kinfo,
                                                 cpe_centroid *__restrict__ cents, int32_t *__restrict__ labels,
@@ -205,10 +210,10 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
         const int n = *s_n;
         if (tid < n) {
             const int32_t pp = s_list[tid];
-            const T *row = emb + (size_t)pp * (4 * F);
+            const T *row = emb + (size_t)pp * dstride;
             int32_t xk[F], yk[F];
             load_block<T, F, L::kAlignX>(row, xk);
-            load_block<T, F, L::kAlignY>(row + 2 * F, yk);
+            load_block<T, F, L::kAlignY>(row + yoff, yk);
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
             for (int a = 0; a < Bw; a++)

@@ -94,44 +94,46 @@ __device__ __forceinline__ _Float16 fix_f32(float v)
 }
 
 // Raw input words of one lane's operand slices: for each axis and K-step j
-// the 8 channels [16 j + 8 g, 16 j + 8 g + 8) of one pixel (channels past 2F
-// read as 0).  Loaded one tile ahead of their use.
+// the 8 channels [16 j + 8 g, 16 j + 8 g + 8) of one pixel's axis block
+// (channels past 2F read as 0).  Loaded one tile ahead of their use.
 template <typename T, int F>
 struct RawSlices {
     static constexpr int C = 2 * F;
     static constexpr int KS = AxisShape<F>::KS;
-    static constexpr bool kVecH = sizeof(T) == 2 && C % 16 == 0;   // 16-byte fp16 slices
-    static constexpr bool kVecF = sizeof(T) == 4 && C % 16 == 0;   // 32-byte fp32 slices
-    static constexpr int kWords = kVecH ? 4 : 8;
+    static constexpr bool kH = sizeof(T) == 2;
+    // 16-byte aligned vector slices: whole K-steps, or a single 8-channel
+    // slice per axis (F = 4) that the lanes of half 0 load
+    static constexpr bool kVec = C % 16 == 0 || C == 8;
+    static constexpr int kWords = (kH && kVec) ? 4 : 8;
     uint32_t w[2][KS][kWords];
 
-    // `row` = first channel of the pixel; the host guarantees 16-byte
-    // alignment of the embedding, so with 2F a multiple of 16 every slice is
-    // 16-byte aligned.
-    __device__ __forceinline__ void load(const T *__restrict__ row, int g)
+    // `row` = first channel of the pixel, `yoff` = first channel of its y
+    // block.  The host guarantees that every vector slice is 16-byte aligned
+    // (16-byte aligned embedding; 2F a multiple of 16, or 2F = 8 with the
+    // row and the y block 16-byte aligned).
+    __device__ __forceinline__ void load(const T *__restrict__ row, int yoff, int g)
     {
 #pragma unroll
         for (int ax = 0; ax < 2; ax++)
 #pragma unroll
             for (int j = 0; j < KS; j++) {
-                const T *blk = row + ax * C + 16 * j + 8 * g;
-                if constexpr (kVecH) {
-                    const u32x4 v = *reinterpret_cast<const u32x4 *>(__builtin_assume_aligned(blk, 16));
-                    w[ax][j][0] = v.x;
-                    w[ax][j][1] = v.y;
-                    w[ax][j][2] = v.z;
-                    w[ax][j][3] = v.w;
-                } else if constexpr (kVecF) {
-                    const float4 *p = reinterpret_cast<const float4 *>(__builtin_assume_aligned(blk, 16));
-                    const float4 a = p[0], b = p[1];
-                    w[ax][j][0] = __float_as_uint(a.x);
-                    w[ax][j][1] = __float_as_uint(a.y);
-                    w[ax][j][2] = __float_as_uint(a.z);
-                    w[ax][j][3] = __float_as_uint(a.w);
-                    w[ax][j][4] = __float_as_uint(b.x);
-                    w[ax][j][5] = __float_as_uint(b.y);
-                    w[ax][j][6] = __float_as_uint(b.z);
-                    w[ax][j][7] = __float_as_uint(b.w);
+                const T *blk = row + ax * yoff + 16 * j + 8 * g;
+                if constexpr (kVec) {
+                    // C == 8: the slice of half 1 lies past the block; it reads
+                    // the half-0 slice (in bounds) and keeps zeros
+                    const bool on = C % 16 == 0 || g == 0;
+                    const T *src = on ? blk : row + ax * yoff + 16 * j;
+                    if constexpr (kH) {
+                        const u32x4 v = *reinterpret_cast<const u32x4 *>(__builtin_assume_aligned(src, 16));
+#pragma unroll
+                        for (int q = 0; q < 4; q++) w[ax][j][q] = on ? v[q] : 0u;
+                    } else {
+                        const float4 *p = reinterpret_cast<const float4 *>(__builtin_assume_aligned(src, 16));
+                        const float4 a = p[0], b = p[1];
+                        const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+                        for (int q = 0; q < 8; q++) w[ax][j][q] = on ? __float_as_uint(f[q]) : 0u;
+                    }
                 } else {
 #pragma unroll
                     for (int s = 0; s < 8; s++)
@@ -146,7 +148,7 @@ struct RawSlices {
     {
 #pragma unroll
         for (int j = 0; j < KS; j++) {
-            if constexpr (kVecH) {
+            if constexpr (kH && kVec) {
                 u32x4 res;
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
@@ -307,12 +309,12 @@ constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 // counts of the centroid records, which the assignment launch accumulates.
 template <typename T, int F>
 __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
-    const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ counts, int32_t nslices,
-    int32_t slice_px, int32_t npix, Tables tb, int32_t Bw, int32_t Bh, unsigned long long *__restrict__ hrep,
+    const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
+    const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, Tables tb, int32_t Bw,
+    int32_t Bh, unsigned long long *__restrict__ hrep,
     cpe_centroid *__restrict__ cents, int32_t cap)
 {
     constexpr int KS = AxisShape<F>::KS;
-    constexpr int D = 4 * F;
     constexpr int kWpb = kVoteWpb<T, F>;
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
@@ -461,7 +463,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     RawSlices<T, F> raw;
     int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it
     if (t < tend) {
-        raw.load(emb + (size_t)pixel(t) * D, g);
+        raw.load(emb + (size_t)pixel(t) * dstride, yoff, g);
         tn = take_tile(s_next, lane, t0, kWpb);
         if (tn < tend) idx = pixel(tn);
     }
@@ -469,7 +471,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         int tnn = tend;
         tile(raw, min(32, n - 32 * t), [&]() {
             if (tn < tend) {
-                raw.load(emb + (size_t)idx * D, g);
+                raw.load(emb + (size_t)idx * dstride, yoff, g);
                 tnn = take_tile(s_next, lane, t0, kWpb);
                 if (tnn < tend) idx = pixel(tnn);
             }
@@ -526,15 +528,14 @@ constexpr size_t kAssignLds = kBestOff + (size_t)kWpb2 * 32 * 4;
 // the pixel at least 2^16); such a pixel is searched again in 64 bits.
 template <typename T, int F>
 __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb2 / 4))) void k_assign_mfma(
-    const T *__restrict__ emb, const int32_t *__restrict__ list, const int32_t *__restrict__ counts,
-    int32_t nslices, int32_t slice_px, int32_t npix, uint32_t tau_code, Tables tb,
+    const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
+    const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, uint32_t tau_code, Tables tb,
     const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hzero,
     unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
     cpe_centroid *__restrict__ cents, int32_t *__restrict__ num, int32_t *__restrict__ labels,
     float *__restrict__ score_map)
 {
     constexpr int KS = AxisShape<F>::KS;
-    constexpr int D = 4 * F;
     constexpr int kThreads = kWpb2 * 64;
     static_assert(kThreads >= kPeakThreads, "the peak prologue takes two histogram slots per thread");
     static_assert(kAssignLds <= 160 * 1024, "LDS of one compute unit");
@@ -600,7 +601,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     RawSlices<T, F> raw;
     int ip = t < tend ? pixel(t) : 0;                   // this lane's pixel in this tile
     peaks_lds_find(Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank, [&]() {
-        if (t < tend) raw.load(emb + (size_t)ip * D, g);
+        if (t < tend) raw.load(emb + (size_t)ip * dstride, yoff, g);
     });
     const int Kc = pl.Kc;
     if (blockIdx.x == 0) {
@@ -768,7 +769,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         int tnn = tend, ipnn = 0;
         codes(raw, [&]() {
             if (tn < tend) {
-                raw.load(emb + (size_t)ipn * D, g);
+                raw.load(emb + (size_t)ipn * dstride, yoff, g);
                 tnn = take_tile(s_next, lane, t0, kWpb2);
                 if (tnn < tend) ipnn = pixel(tnn);
             }

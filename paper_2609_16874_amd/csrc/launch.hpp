@@ -38,6 +38,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
     const int Bw = h->bins_w, Bh = h->bins_h, nb = Bw * Bh;
     const int npix = h->H * h->W;
     const T *e = static_cast<const T *>(emb);
+    const int32_t dstride = h->D, yoff = h->D / 2;     // channels per pixel; first channel of the y block
     const T *g = static_cast<const T *>(fg);
     // Launch i of the frame; with stage events on, the dispatch itself
     // records events 2i and 2i + 1 at the kernel's start and end.
@@ -82,11 +83,11 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const int64_t tiles = ((int64_t)npix + 31) / 32;
         const int64_t wgs = (tiles + wpb - 1) / wpb;
         const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, (const int32_t *)list,
+        launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
                (const int32_t *)h->counts, nslices, slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap);
         const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, (const int32_t *)list,
+        launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
                (const int32_t *)h->counts, nslices, slice_px, npix, fa.tau_code, h->tb,
                (const unsigned long long *)hcur, hnext, h->hlast, Bw, Bh, cut, h->cap, cents, num, labels, score);
     } else {
@@ -95,7 +96,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 2;
         const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
         const int grid = (int)(tiles < 1024 ? tiles : 1024);
-        launch(0, k_vote_generic<T, F>, dim3(grid), dim3(tp), lds, e, g, npix, fg_thr, h->tb, Bw, Bh, h->hrep);
+        launch(0, k_vote_generic<T, F>, dim3(grid), dim3(tp), lds, e, dstride, yoff, g, npix, fg_thr, h->tb, Bw, Bh, h->hrep);
         const PeakOut po{cents, num, h->peaks, h->kinfo};
         launch(1, k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, h->hrep, h->hlast,
                Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
@@ -104,7 +105,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
-        launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, g, npix, fg_thr, fa.tau_code, h->tb, Bw, Bh,
+        launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, dstride, yoff, g, npix, fg_thr, fa.tau_code, h->tb, Bw, Bh,
                (const int32_t *)h->peaks, (const int32_t *)h->kinfo, cents, labels, score);
     }
     return hipGetLastError() == hipSuccess ? CPE_OK : CPE_ERR_HIP;

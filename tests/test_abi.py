@@ -75,3 +75,21 @@ def test_create_rejects_bad_arguments(kw):
                                a["n_freq"], a["bins_w"], a["bins_h"], a["cap"])
     assert st == native.CPE_ERR_INVALID_ARG
     assert h.value is None
+
+
+@pytest.mark.parametrize("D,dtype,n_freq,expect", [
+    (12, 0, 4, "invalid"),        # fewer channels than 4 n_freq
+    (18, 0, 4, "unsupported"),    # f32, 72-byte rows: the y block starts 36 bytes in
+    (20, 1, 4, "unsupported"),    # f16, 40-byte rows: the y block starts 20 bytes in
+    (35, 0, 4, "invalid"),        # odd channel count
+])
+def test_create_rejects_unaligned_longer_encodings(D, dtype, n_freq, expect):
+    """A longer encoding (D > 4 n_freq, low harmonics only) must split into
+    two 16-byte aligned axis blocks; these checks run before any device call."""
+    lib = native.library()
+    fx = np.ones(n_freq)
+    h = ctypes.c_void_p(123)
+    st = lib.cpe_decode_create(ctypes.byref(h), 16, 16, D, dtype, fx.ctypes.data, fx.ctypes.data, n_freq, 8, 8, 16)
+    want = native.CPE_ERR_INVALID_ARG if expect == "invalid" else native.CPE_ERR_UNSUPPORTED
+    assert st == want
+    assert h.value is None

@@ -1,0 +1,77 @@
+"""GPU parity of the resolved-harmonics decode, through the C ABI.
+
+The embedding keeps all its channels (D = 4 x the encoding's harmonics) and
+the decoder is built for its first n harmonics only: the matrix-core kernels
+read the 8-channel slices of n = 4 as 16-byte vectors from each axis block,
+n = 2 and n = 1 take the scalar path, n = 8 of a 16-harmonic encoding reads
+whole blocks at a y offset of D/2, and a 48 x 48 grid takes the generic
+kernels.  Thresholds: the frozen resolved-decode thresholds for the
+workloads' own grids, 0.1 x the oracle's largest vote mass otherwise.
+Bit-exact on histogram, records, K and labels; the score map within 1e-5
+relative.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_16874_amd import harmonics, synth
+from tests.test_gpu_parity import assert_parity, gpu_decode, native
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "configs.json")
+
+
+def resolved_thresholds():
+    with open(GOLDEN) as fh:
+        return json.load(fh)["resolved"]
+
+
+# (workload, harmonics decoded or None for the resolved count, bins or None for its own grid)
+CASES = [(2, None, None), (3, None, None), (4, None, None), (1, None, None), (0, None, None),
+         (3, 8, None), (0, 2, None), (1, 1, None), (2, None, 48)]
+
+
+@pytest.mark.parametrize("cfg,n_used,bins", CASES)
+def test_resolved_harmonics_parity(cfg, n_used, bins):
+    f = synth.make_frame(cfg)
+    spec = f.spec
+    fx, fy = spec.freqs()
+    b = bins or spec.bins
+    n = n_used or harmonics.resolved_pair(fx, fy, spec.W, spec.H, b, b)
+    fx, fy = fx[:n], fy[:n]
+    if n_used is None and bins is None:
+        theta = resolved_thresholds()[str(cfg)]["peak_threshold"]
+        assert resolved_thresholds()[str(cfg)]["n_freq"] == n
+    else:
+        probe = oracle.decode(f.emb, f.fg, fx, fy, b, b, None, spec.fg_threshold, 0.0, want_score=False)
+        theta = 0.1 * float(probe["hist"].max()) * 2.0 ** -30
+    print(f"resolved parity: workload {cfg}, {n} of {spec.n_freq} harmonics, {b}x{b} bins", flush=True)
+    ref = oracle.decode(f.emb, f.fg, fx, fy, b, b, None, spec.fg_threshold, theta)
+    dec = native().Decoder(spec.H, spec.W, n, spec.dtype, fx, fy, b, b, D=spec.D)
+    try:
+        got = gpu_decode(dec, f.emb, f.fg, spec.fg_threshold, theta)
+        assert_parity(got, ref, dec.capacity)
+        assert ref["K"] > 0
+    finally:
+        dec.close()
+
+
+def test_full_count_equals_the_standard_decode():
+    """Building the decoder with every harmonic and an explicit D = 4F is the
+    standard decode."""
+    f = synth.make_frame(1)
+    spec = f.spec
+    fx, fy = spec.freqs()
+    with open(GOLDEN) as fh:
+        theta = json.load(fh)["configs"]["1"]["peak_threshold"]
+    ref = oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, None, spec.fg_threshold, theta)
+    dec = native().Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, spec.bins, spec.bins, D=spec.D)
+    try:
+        assert_parity(gpu_decode(dec, f.emb, f.fg, spec.fg_threshold, theta), ref, dec.capacity)
+    finally:
+        dec.close()
