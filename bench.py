@@ -233,6 +233,45 @@ def cpu_baseline(cfg, frames, budget_s=12.0):
                       f"single-threaded C oracle, {dt:.1f} s"}
 
 
+def naive_ablation(cfg, reps=3):
+    """The per-tuple ablation (cpe_decode_naive: per-(pixel, bin) float
+    atomics and per-(pixel, candidate) aggregation, Table 3's "Naive") on
+    frame 0 of workload cfg, timed like a step, beside the decoder on the same
+    frame; and how many histogram bins differ bit for bit between two of its
+    runs (float atomics add in a different order each time)."""
+    import torch
+    from paper_2609_16874_amd import native
+    th = thresholds()[str(cfg)]
+    spec, frames, embs, fgs = load_workload(cfg, 1)
+    fx, fy = spec.freqs()
+    dec = native.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, spec.bins, spec.bins, th["capacity"])
+    o = dec.new_outputs()
+    hist = torch.empty((spec.bins, spec.bins), dtype=torch.float32, device="cuda")
+
+    def run():
+        st = dec.decode_naive(embs[0], fgs[0], spec.fg_threshold, th["peak_threshold"], o["centroids"],
+                              o["num_centroids"], o["labels"], hist)
+        if st != 0:
+            raise RuntimeError(f"cpe_decode_naive failed with status {st}")
+
+    run()
+    torch.cuda.synchronize()
+    first = hist.clone()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        run()
+    t1.record()
+    torch.cuda.synchronize()
+    naive_ms = t0.elapsed_time(t1) / reps
+    differ = int((hist.view(torch.int32) != first.view(torch.int32)).sum().item())
+    opt_ms = time_steps(dec, embs, fgs, [dec.new_outputs()], spec.fg_threshold, th["peak_threshold"], 10, 3)
+    dec.close()
+    return {"workload": spec.name, "naive_ms_per_frame": round(naive_ms, 3), "decoder_ms_per_frame": round(opt_ms, 5),
+            "naive_over_decoder": round(naive_ms / opt_ms, 1), "hist_bins_differing_between_naive_runs": differ,
+            "bins": spec.bins * spec.bins}
+
+
 # The paper's optimised decoder latency for its 704x704, L = 4 maps on a Jetson
 # Orin Nano in fp32 (Table 1), by bin count: context only, other hardware.
 PAPER_TABLE1_MS = {8: 2.13, 16: 6.13, 32: 30.66, 64: 101.37, 80: 144.00}
@@ -374,6 +413,9 @@ def main():
                                            "stages_ms": {k: round(v, 5) for k, v in st.items()},
                                            "quality_vs_instances": b["quality"]}
             del fr, loaded
+        # Table 3's naive-vs-optimised contrast on this GPU: the paper's own
+        # shape (704x704, L = 4) and a 640x640 D = 64 frame
+        extra["naive_ablation"] = [naive_ablation(5), naive_ablation(2)]
         result["extra"] = extra
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(4, frames)

@@ -231,6 +231,35 @@ size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
 #define CPE_STAGE_EVENTS 6
 cpe_status cpe_decode_set_stage_events(cpe_decoder *h, hipEvent_t *events, int32_t n_events);
 
+/*
+ * Ablation, not the decoder: the per-tuple GPU decoder of the prior work the
+ * paper compares against (Section 3.2 "Histogram Accumulation" and "Mask
+ * Aggregation"; Table 3, "Naive"), with the real-valued definition of
+ * Section 3.1 in fp32 and no quantisation:
+ *   votes   one thread per (pixel, bin) tuple computes both distances to the
+ *           real palettes gamma(bin centre) and adds e^-d_x e^-d_y to
+ *           H(a, b) with a float atomicAdd (Eq4, Eq6).  The addition order,
+ *           and so the last bits of H, differ from run to run;
+ *   peaks   strict 8-neighbour maxima with H > peak_threshold, in bin order;
+ *   labels  one thread per (pixel, candidate) tuple recomputes the affinity
+ *           e^-d_x e^-d_y; each pixel takes the largest, lowest index on
+ *           equal affinities (Eq7); counts in the records.
+ * Same handle and arguments as cpe_decode (fg required; emb and fg aligned
+ * to their element size, labels to 4 bytes; peak_threshold in vote-mass
+ * units, H itself here), plus
+ *   hist   device [B_h][B_w] float: receives H, or NULL.
+ * The records' score is H(a_k, b_k).  Results agree with the real-valued
+ * definition (fp64) to fp32 rounding; near-equal distances and near-equal
+ * neighbouring bins may decide differently, and repeated calls may differ
+ * in those decisions.  The first call allocates the ablation's workspace
+ * (real palettes, histogram, peak list, one 64-bit key per pixel), freed by
+ * cpe_decode_destroy; the call is otherwise asynchronous on `stream`.  Not
+ * for use with cpe_decode on overlapping streams.
+ */
+cpe_status cpe_decode_naive(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg,
+                            int32_t H, int32_t W, float fg_threshold, double peak_threshold,
+                            cpe_centroid *centroids, int32_t *num_centroids, int32_t *labels, float *hist);
+
 #ifdef __cplusplus
 }
 #endif

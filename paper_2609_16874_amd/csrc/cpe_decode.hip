@@ -170,6 +170,19 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     std::vector<float> cx, cy;
     palette(bins_w, W, freq_x, h->pal_x, cx);
     palette(bins_h, H, freq_y, h->pal_y, cy);
+    // the same encodings unquantised, in fp32 (the per-tuple ablation)
+    auto real_palette = [&](int n, int extent, const double *freq, std::vector<float> &pal) {
+        pal.assign((size_t)n * twoF, 0.0f);
+        for (int a = 0; a < n; a++) {
+            const double c = ((double)(a + 1) * (double)extent) / (double)(n + 1);
+            for (int k = 0; k < F; k++) {
+                pal[(size_t)a * twoF + 2 * k] = (float)std::sin(freq[k] * c);
+                pal[(size_t)a * twoF + 2 * k + 1] = (float)std::cos(freq[k] * c);
+            }
+        }
+    };
+    real_palette(bins_w, W, freq_x, h->palf_x);
+    real_palette(bins_h, H, freq_y, h->palf_y);
 
     // bucket tables: weight 2^15 e^-d (8-bit buckets), code 4096 d (9-bit
     // buckets), d taken at the bucket centre of fl32(S+1)
@@ -351,7 +364,8 @@ cpe_status cpe_decode_masks(cpe_decoder *h, hipStream_t stream, const int32_t *l
 cpe_status cpe_decode_destroy(cpe_decoder *h)
 {
     if (!h) return CPE_OK;
-    const hipError_t e = hipFree(h->dev);
+    hipError_t e = hipFree(h->dev);
+    if (h->naive && hipFree(h->naive) != hipSuccess) e = hipErrorUnknown;
     delete h;
     return e == hipSuccess ? CPE_OK : CPE_ERR_HIP;
 }

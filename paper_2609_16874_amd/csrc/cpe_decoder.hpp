@@ -28,6 +28,11 @@ struct cpe_decoder {
     int parity;                          // histogram set of the next frame (matrix-core path)
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;
+    // per-tuple ablation (cpe_decode_naive): real palettes gamma(bin centre)
+    // in fp32, [bins][2F], and its device workspace, allocated on first use
+    std::vector<float> palf_x, palf_y;
+    unsigned char *naive = nullptr;
+    size_t naive_bytes = 0;
 };
 
 namespace cpe {

@@ -27,7 +27,7 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 # Every entry point declared in include/cpe_decode.h.
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
-           "cpe_decode_set_stage_events")
+           "cpe_decode_set_stage_events", "cpe_decode_naive")
 STAGE_EVENTS = 6
 MFMA_BINS = 32
 
@@ -81,6 +81,8 @@ def library():
         lib.cpe_decode_workspace_bytes.argtypes = [P]
         lib.cpe_decode_set_stage_events.restype = i32
         lib.cpe_decode_set_stage_events.argtypes = [P, P, i32]
+        lib.cpe_decode_naive.restype = i32
+        lib.cpe_decode_naive.argtypes = [P, P, P, P, i32, i32, ctypes.c_float, ctypes.c_double, P, P, P, P]
         _lib = lib
     return _lib
 
@@ -147,6 +149,14 @@ class Decoder:
         return library().cpe_decode_masks(self._h, _stream_ptr(stream), _ptr(labels),
                                           self.H if H is None else H, self.W if W is None else W,
                                           int(first), int(count), _ptr(masks))
+
+    def decode_naive(self, emb, fg, fg_threshold: float, peak_threshold: float, centroids, num_centroids, labels,
+                     hist=None, stream=None) -> int:
+        """cpe_decode_naive (the per-tuple ablation): ``hist`` is a device
+        float32 [bins_h][bins_w] tensor or None."""
+        return library().cpe_decode_naive(self._h, _stream_ptr(stream), _ptr(emb), _ptr(fg), self.H, self.W,
+                                          float(fg_threshold), float(peak_threshold), _ptr(centroids),
+                                          _ptr(num_centroids), _ptr(labels), _ptr(hist))
 
     def histogram(self, out, stream=None) -> int:
         return library().cpe_decode_get_histogram(self._h, _stream_ptr(stream), _ptr(out))
