@@ -504,9 +504,11 @@ constexpr size_t kAssignLdsCore = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins
                                   kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
                                   (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
                                   (kMaxSlices + 1) * 4 + 16;
-// then, 16-byte aligned, per wave the 32 search results of a tile
+// then, 16-byte aligned, per wave the 32 search results of a tile, and the
+// summed vote histogram (32 x 32 slots)
 constexpr size_t kBestOff = (kAssignLdsCore + 15) & ~(size_t)15;
-constexpr size_t kAssignLds = kBestOff + (size_t)kWpb2 * 32 * 4;
+constexpr size_t kSumOff = kBestOff + (size_t)kWpb2 * 32 * 4;
+constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -553,8 +555,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
     uint32_t *s_best = reinterpret_cast<uint32_t *>(smem + kBestOff);                 // [kWpb2][32]
-    // the summed histogram lives in the key arrays until the peaks are known
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_keys);
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem + kSumOff);  // [32 * 32] summed votes
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -562,6 +563,22 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
 
     PeakLoad pld;                                   // issued before the table staging
     peaks_lds_load(hcur, Bw, Bh, pld);
+    // This wave's search keys, [bin][kKeyStride] per axis: x key of bin a,
+    // pixel m at kx[a * kKeyStride + m], y key of bin b at ky[...]; their
+    // low halves (a for x keys, 128 b for y keys) are written here, while
+    // the loads are in flight, and the codes fill the high halves per tile.
+    uint32_t *kx = s_keys + wv * 2 * kMfmaBins * kKeyStride;
+    uint32_t *ky = kx + kMfmaBins * kKeyStride;
+    {
+        constexpr int kVecPerRow = kKeyStride / 4;
+#pragma unroll
+        for (int i = lane; i < 2 * kMfmaBins * kVecPerRow; i += 64) {
+            const int row = i / kVecPerRow;          // a power-of-two division: a shift
+            const uint32_t v = row < kMfmaBins ? (uint32_t)row : 128u * (uint32_t)(row - kMfmaBins);
+            const u32x4 v4 = {v, v, v, v};
+            reinterpret_cast<u32x4 *>(kx)[i] = v4;
+        }
+    }
     SliceLoad sl;
     if (list) slice_load(counts, nslices, sl);
     {
@@ -632,16 +649,6 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     }
     const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of kBatchPad
 
-    uint32_t *kx = s_keys + wv * 2 * kMfmaBins * kKeyStride;   // x key of bin a, pixel m: kx[a * kKeyStride + m]
-    uint32_t *ky = kx + kMfmaBins * kKeyStride;                // y key of bin b, pixel m: ky[b * kKeyStride + m]
-    // low halves of the keys: a for the x keys of column a, 128 b for the y
-    // keys of row b (workgroup 0 reads the summed histogram, which these
-    // arrays overwrite, until its records are written)
-    if (blockIdx.x == 0) __syncthreads();
-    for (int i = lane; i < 2 * kMfmaBins * kKeyStride; i += 64) {
-        const int row = i / kKeyStride;
-        kx[i] = row < kMfmaBins ? (uint32_t)row : 128u * (uint32_t)(row - kMfmaBins);
-    }
 
     // the palette operands stay in registers for the whole run
     f16x8 pop_h[2][KS], pop_l[2][KS];

@@ -242,13 +242,8 @@ __device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, in
         const int b = tid;
         uint32_t m = b < kLdsPeakBins ? pl.rowmask[b] : 0u;
         const int nbt = (__popc(m) + 3) >> 2;
-        int incl = nbt;
-#pragma unroll
-        for (int d = 1; d < 32; d <<= 1) {
-            const int t = __shfl_up(incl, d);
-            if (lane >= d) incl += t;
-        }
-        const int start = incl - nbt, total = __shfl(incl, 31);
+        const int incl = wave_incl_sum(nbt);      // the whole first wave is active here
+        const int start = incl - nbt, total = __builtin_amdgcn_readlane(incl, 31);
         const int padded = (total + kBatchPad - 1) & ~(kBatchPad - 1);
         uint32_t last = 0;
         u32x4_pk o = {0u, 0u, 0u, 0u};
