@@ -329,6 +329,9 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     const int g = lane >> 5, ln = lane & 31;
     SliceLoad sl;
     if (list) slice_load(counts, nslices, sl);
+    // the bin constants of this lane's bin (loaded with the tables, not after
+    // the barrier, where they would cost a memory round trip of their own)
+    const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
     {
         constexpr int kThreads = kWpb * 64, kN = kWKeys / 4, kPer = (kN + kThreads - 1) / kThreads;
         u32x4 w[kPer];
@@ -353,7 +356,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
     int t0, tend;
     block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
-    const uint32_t cbx = bin_const(tb.np1_x[ln]), cby = bin_const(tb.np1_y[ln]);
+    const uint32_t cbx = bin_const(np1x), cby = bin_const(np1y);
 
     // this wave's starting values: [0] x ah, [1] x al, [2] y ah, [3] y al, by pixel
     uint32_t *ini = s_ini + wv * 128;
