@@ -30,13 +30,16 @@
 // as at most 256 pixels are summed, after which they are added into a 64-bit
 // histogram in LDS.
 //
-// Pass 2, k_assign_mfma (assignment, Eq7, and label write-out).  With the
-// palette as MFMA rows each lane holds one pixel and 16 bins; the codes go
-// to LDS as the high halves of search keys whose low halves hold the bin
-// index, laid out so that one lane serves one pixel, and the candidate
-// search walks the batches of 4 columns of one row: the key
-// (c_x + c_y) * 2^16 + (128 b + a) is minimised over the peaks, which
-// selects the smallest code sum and, on ties, the lowest bin index, i.e. the
+// Pass 2, k_assign_mfma (assignment, Eq7, and label write-out).  Only the
+// candidate columns and rows are needed: they are numbered in ascending
+// order (slots), the MFMA rows are the slots' palette entries, each lane
+// holds one pixel and 16 slots, and codes are computed for the groups of 8
+// slots that hold candidates.  The codes go to LDS as the high halves of
+// search keys whose low halves hold the slot index, laid out so that one lane
+// serves one pixel, and the candidate search walks the batches of 4 columns
+// of one row: the key (c_x + c_y) * 2^16 + (128 row slot + column slot) is
+// minimised over the peaks, which selects the smallest code sum and, on
+// ties, the lowest (row, column) -- slots keep the bins' order -- i.e. the
 // lowest centroid index.
 #pragma once
 
@@ -503,7 +506,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // LDS bytes of k_assign_mfma: code table, palette operands, bin constants,
 // candidate batches, bin -> centroid table, counts, per wave x keys and y
 // keys [32 bins][kKeyStride] (u32), then the peak-extraction state.
-constexpr size_t kAssignLdsCore = (size_t)kCKeys * 2 + kPopBytes + 2 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
+constexpr size_t kAssignLdsCore = (size_t)kCKeys * 2 + kPopBytes + 4 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
                                   kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
                                   (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
                                   (kMaxSlices + 1) * 4 + 16;
@@ -519,15 +522,15 @@ constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 // summed histogram `hlast`, and the grid clears `hzero`, the histograms the
 // next frame's vote launch accumulates into.
 //
-// Then, per tile of 32 pixels, the distance codes of both axes (palette as
-// the MFMA rows, so that each lane holds one pixel and 16 bins) go to LDS as
-// search keys: x key (c_x << 16) | a and y key (c_y << 16) | 128 b, laid out
-// [bin][kKeyStride] so that lane m reads pixel m's key of any bin at a fixed
-// stride.  The low halves are written once; per tile only the codes are
-// stored, as 16-bit writes.  The candidate search walks the batches of 4
-// columns of one row; the two halves of the wave take alternate batches for
-// the same 32 pixels and combine their minima at the end.  The sum of an
-// x key and a y key is ((c_x + c_y) << 16) | (128 b + a), taken with
+// Then, per tile of 32 pixels, the distance codes of both axes for the
+// candidate slots (palette entries of the slots' bins as the MFMA rows, so
+// that each lane holds one pixel and 16 slots) go to LDS as search keys:
+// x key (c_x << 16) | column slot and y key (c_y << 16) | 128 row slot, laid
+// out [slot][kKeyStride] so that lane m reads pixel m's key of any slot at a
+// fixed stride.  The low halves are written once; per tile only the codes
+// are stored, as 16-bit writes.  The candidate search walks the batches of 4
+// columns of one row (see the search below).  The sum of an x key and a y
+// key is ((c_x + c_y) << 16) | (128 row slot + column slot), taken with
 // unsigned saturation: codes are below 2^16 but a sum of two may not be.
 // The minimum is exact unless every candidate saturates (all code sums of
 // the pixel at least 2^16); such a pixel is searched again in 64 bits.
@@ -548,8 +551,9 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     __shared__ __align__(16) unsigned char smem[kAssignLds];
     uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                            // [kCKeys]
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_ct + kCKeys);                  // palette operands
-    uint32_t *s_cb = s_pop + kPopBytes / 4;                                          // [2][32] bin_const
-    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_cb + 2 * kMfmaBins);                 // [kMaxBatchLds]
+    uint32_t *s_cb = s_pop + kPopBytes / 4;                                          // [2][32] bin_const by bin
+    uint32_t *s_cbs = s_cb + 2 * kMfmaBins;                                           // [2][32] by slot
+    u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_cbs + 2 * kMfmaBins);                // [kMaxBatchLds]
     uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatchLds);             // [kMaxBatchLds]
     uint16_t *s_rank = reinterpret_cast<uint16_t *>(s_bh + kMaxBatchLds);           // [32 * 32]
     int32_t *s_cnt = reinterpret_cast<int32_t *>(s_rank + kMfmaBins * kMfmaBins);   // [1024]
@@ -620,7 +624,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
     RawSlices<T, F> raw;
     int ip = t < tend ? pixel(t) : 0;                   // this lane's pixel in this tile
-    peaks_lds_find(Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank, [&]() {
+    peaks_lds_find(Bw, Bh, cut, cap, s_h, pl, s_bo, s_bh, s_rank, s_cb, s_cbs, [&]() {
         if (t < tend) raw.load(emb + (size_t)ip * dstride, yoff, g);
     });
     const int Kc = pl.Kc;
@@ -653,15 +657,20 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of kBatchPad
 
 
-    // the palette operands stay in registers for the whole run
+    // The MFMA rows are the candidate slots: the palette operands of slot j's
+    // bin, gathered once and kept in registers for the whole run; codes are
+    // computed only for the groups of 8 slots that hold candidates.
+    const int nslot[2] = {__builtin_amdgcn_readfirstlane(pl.ncol), __builtin_amdgcn_readfirstlane(pl.nrow)};
     f16x8 pop_h[2][KS], pop_l[2][KS];
 #pragma unroll
-    for (int ax = 0; ax < 2; ax++)
+    for (int ax = 0; ax < 2; ax++) {
+        const int bin = ax ? pl.rowbin[ln] : pl.colbin[ln];
 #pragma unroll
         for (int j = 0; j < KS; j++) {
-            pop_h[ax][j] = palette_operand(s_pop, ax, 0, j, lane);
-            pop_l[ax][j] = palette_operand(s_pop, ax, 1, j, lane);
+            pop_h[ax][j] = palette_operand(s_pop, ax, 0, j, g * 32 + bin);
+            pop_l[ax][j] = palette_operand(s_pop, ax, 1, j, g * 32 + bin);
         }
+    }
 
     // Codes of one tile into the keys' high halves (pixel m = lane & 31; this
     // lane's 16 bins acc_row(r, g) of each axis); `next` reuses the input
@@ -686,11 +695,12 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
             }
             axis_dot<KS, false>(ax ? Y : X, pop_h[ax], pop_l[ax], ah, al);
             const uint32_t np = ax ? npy : npx;
-            // high half of key (bin acc_row(r, g), pixel ln)
+            // high half of key (slot acc_row(r, g), pixel ln)
             uint16_t *dst = reinterpret_cast<uint16_t *>((ax ? ky : kx) + 4 * g * kKeyStride + ln) + 1;
 #pragma unroll
             for (int r4 = 0; r4 < 4; r4++) {
-                const u32x4 cb = *reinterpret_cast<const u32x4 *>(s_cb + ax * kMfmaBins + 8 * r4 + 4 * g);
+                if (8 * r4 >= nslot[ax]) break;      // wave-uniform: no candidate in slots 8 r4 ..
+                const u32x4 cb = *reinterpret_cast<const u32x4 *>(s_cbs + ax * kMfmaBins + 8 * r4 + 4 * g);
 #pragma unroll
                 for (int i = 0; i < 4; i++) {
                     const int r = 4 * r4 + i;
@@ -741,7 +751,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         const uint32_t best = best_w[ln];
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
         const unsigned char *kyl = reinterpret_cast<const unsigned char *>(ky + ln);
-        uint32_t sum = best >> 16, idx = best & 0xffffu;   // code sum and 128 b + a of the winner
+        uint32_t sum = best >> 16, idx = best & 0xffffu;   // code sum and 128 (row slot) + column slot
         if (best == 0xffffffffu) {   // every sum saturated: all batches again, in 64 bits
             unsigned long long b64 = ~0ull;
             for (int bi = 0; bi < nbat; bi++) {
@@ -756,7 +766,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         }
         if (g == 0 && ln < nvalid) {
             if (sum < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
-                const int a = (int)(idx & 31u), b = (int)((idx >> 7) & 31u);
+                const int a = pl.colbin[idx & 31u], b = pl.rowbin[(idx >> 7) & 31u];
                 const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
                 labels[pix] = k + 1;
                 if (score_map) score_map[pix] = expf(-((float)sum * 0x1p-12f));

@@ -127,7 +127,11 @@ constexpr int kKeyStride = 32;      // words per bin row of the assignment kerne
 struct PeakLds {
     int wave[2 * kPeakThreads / 64];  // per-wave counts of the two slot passes (slot-owning waves)
     uint32_t rowmask[kLdsPeakBins];   // bit a of row b: (a, b) is one of the first min(K, cap) candidates
+    uint32_t colmask;                 // bit a: column a holds one of them
     int K, Kc, nbat;
+    int ncol, nrow;                   // candidate columns and rows
+    uint8_t colbin[kLdsPeakBins];     // column of column slot j (ascending; 0 past ncol)
+    uint8_t rowbin[kLdsPeakBins];     // row of row slot j (ascending; 0 past nrow)
     int pk[max_peaks(kLdsPeakBins, kLdsPeakBins)];   // candidate slots b * 32 + a, ascending
 };
 
@@ -174,8 +178,9 @@ __device__ __forceinline__ bool is_peak32(const unsigned long long *s_h, int a, 
 // s_h (32 x 32 slots) from the loaded counts; after a barrier of the
 // caller's, peaks_lds_find compacts the candidates in ascending bin order
 // (pl.pk) and writes K and min(K, cap), the bin -> candidate-index table
-// s_rank [32 * 32] and the candidate batches s_bo / s_bh (pl.nbat of them, a
-// multiple of kBatchPad).  `mid` runs between its first and second barrier
+// s_rank [32 * 32], the column and row slots (pl.ncol, pl.nrow, pl.colbin,
+// pl.rowbin, and the bin constants by slot s_cbs) and the candidate batches
+// s_bo / s_bh in slot offsets (pl.nbat of them, a multiple of kBatchPad).  `mid` runs between its first and second barrier
 // (the caller's independent work, e.g. loads whose latency the extraction
 // hides).
 __device__ __forceinline__ void peaks_lds_sum(const PeakLoad &ld, unsigned long long *s_h, PeakLds &pl)
@@ -191,11 +196,12 @@ __device__ __forceinline__ void peaks_lds_sum(const PeakLoad &ld, unsigned long 
         }
     }
     if (tid < kLdsPeakBins) pl.rowmask[tid] = 0u;
+    if (tid == 0) pl.colmask = 0u;
 }
 template <typename Mid>
 __device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, int cap, const unsigned long long *s_h,
                                                PeakLds &pl, u32x4_pk *s_bo, uint32_t *s_bh, uint16_t *s_rank,
-                                               Mid mid)
+                                               const uint32_t *s_cb, uint32_t *s_cbs, Mid mid)
 {
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     constexpr int kWaves = kPeakThreads / 64;
@@ -232,44 +238,70 @@ __device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, in
             if (pos < Kc) {
                 s_rank[slot] = (uint16_t)pos;
                 atomicOr(&pl.rowmask[slot >> 5], 1u << (slot & 31));
+                atomicOr(&pl.colmask, 1u << (slot & 31));
             }
         }
     }
     __syncthreads();
-    // batches: lane b of the first wave builds row b's (strict maxima are
-    // never horizontally adjacent: <= 16 per row, <= 4 batches)
+    // Slots: the candidate columns and rows, each numbered in ascending
+    // order; the assignment computes codes for slots only, and its key
+    // arrays, batches and bin constants are indexed by slot.  Lane j of the
+    // first wave numbers column j and row j and scatters them (and their
+    // bin constants, s_cb [2][32] by bin -> s_cbs [2][32] by slot).
+    // Batches: lane b builds row b's (strict maxima are never horizontally
+    // adjacent: <= 16 per row, <= 4 batches), as slot byte offsets.
     if (tid < 64) {
         const int b = tid;
         uint32_t m = b < kLdsPeakBins ? pl.rowmask[b] : 0u;
+        const uint32_t cm = pl.colmask;
+        const unsigned long long rows = __ballot(m != 0u);
+        const int rslot = lane_prefix(rows);                         // slot of row b if it holds candidates
+        if (b < kLdsPeakBins) {
+            pl.colbin[b] = 0;
+            pl.rowbin[b] = 0;
+        }
+        if (b < kLdsPeakBins && ((cm >> b) & 1u)) {
+            const int cs = __popc(cm & ((1u << b) - 1u));
+            pl.colbin[cs] = (uint8_t)b;
+            s_cbs[cs] = s_cb[b];
+        }
+        if (m) {
+            pl.rowbin[rslot] = (uint8_t)b;
+            s_cbs[kLdsPeakBins + rslot] = s_cb[kLdsPeakBins + b];
+        }
         const int nbt = (__popc(m) + 3) >> 2;
         const int incl = wave_incl_sum(nbt);      // the whole first wave is active here
         const int start = incl - nbt, total = __builtin_amdgcn_readlane(incl, 31);
         const int padded = (total + kBatchPad - 1) & ~(kBatchPad - 1);
+        const uint32_t hb = (uint32_t)rslot * (4u * kKeyStride);
         uint32_t last = 0;
         u32x4_pk o = {0u, 0u, 0u, 0u};
         for (int j = 0; j < nbt; j++) {
 #pragma unroll
             for (int s4 = 0; s4 < 4; s4++) {
                 if (m) {
-                    last = (uint32_t)__builtin_ctz(m) * (4u * kKeyStride);
+                    const int a = __builtin_ctz(m);
+                    last = (uint32_t)__popc(cm & ((1u << a) - 1u)) * (4u * kKeyStride);
                     m &= m - 1u;
                 }
                 o[s4] = last;
             }
             s_bo[start + j] = o;
-            s_bh[start + j] = (uint32_t)b * (4u * kKeyStride);
+            s_bh[start + j] = hb;
         }
         // pad the list with copies of the last batch (a repeated batch leaves
         // every minimum unchanged)
         if (nbt > 0 && start + nbt == total)
             for (int e = total; e < padded; e++) {
                 s_bo[e] = o;
-                s_bh[e] = (uint32_t)b * (4u * kKeyStride);
+                s_bh[e] = hb;
             }
         if (tid == 0) {
             pl.K = K;
             pl.Kc = Kc;
             pl.nbat = padded;
+            pl.ncol = __popc(cm);
+            pl.nrow = __popcll(rows);
         }
     }
     __syncthreads();
