@@ -148,6 +148,54 @@ def time_steps(dec, embs, fgs, outs, fg_thr, theta, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
+def step_latency(dec, embs, fgs, outs, fg_thr, theta, steps=100, warmup=10):
+    """Per-frame latency distribution: each of `steps` steps (one decode per
+    frame of the workload, back to back) bracketed by its own pair of events,
+    after `warmup` untimed steps; ms per frame = step time / frames."""
+    import torch
+    nfr = len(embs)
+
+    def step():
+        for i in range(nfr):
+            o = outs[i]
+            assert dec.decode(embs[i], fgs[i], fg_thr, theta, o["centroids"], o["num_centroids"], o["labels"]) == 0
+
+    for _ in range(warmup):
+        step()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record()
+        step()
+        b.record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev]) / nfr
+    return {"steps": steps, "warmup": warmup, "mean": round(float(t.mean()), 5), "std": round(float(t.std()), 5),
+            "min": round(float(t.min()), 5), "p50": round(float(np.percentile(t, 50)), 5),
+            "p99": round(float(np.percentile(t, 99)), 5)}
+
+
+def copy_bandwidth(mib=256, reps=10):
+    """GB/s (bytes read + bytes written) of a plain device-to-device copy on
+    this GPU, the box's practical HBM ceiling beside the 8 TB/s peak."""
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del src, dst
+    return 2 * n / (ms * 1e-3) / 1e9
+
+
 def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
     """Average duration of each of the frame's three kernels over reps x
     frames, from the start and end events their dispatches record."""
@@ -202,6 +250,7 @@ def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=N
     outs = [dec.new_outputs() for _ in frames]
     ms_step = time_steps(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], steps, warmup)
     stages = stage_times(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"], max(1, min(steps, 10)))
+    bench_config.latency = step_latency(dec, embs, fgs, outs, spec.fg_threshold, th["peak_threshold"])
     fb = [frame_bytes(spec, f) for f in frames]
     mean_bytes = {k: float(np.mean([b[k] for b in fb])) for k in fb[0]}
     ws = dec.workspace_bytes()
@@ -228,7 +277,15 @@ def cpu_baseline(cfg, frames, budget_s=12.0):
                       th["peak_threshold"], want_score=False)
         done += 1
     dt = time.perf_counter() - t0
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), model)
+    except OSError:
+        pass
     return {"value": done / dt, "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "host_cpu": model, "host_cores_available": len(os.sched_getaffinity(0)),
+            "host_cores_total": os.cpu_count(),
             "sample": f"{done} decodes cycling through the {len(frames)} frames of the {spec.name} batch, "
                       f"single-threaded C oracle, {dt:.1f} s"}
 
@@ -353,16 +410,21 @@ def main():
                           "frames_per_s": round(nfr * 1000 / ms, 1), "literal_bytes": int(b["literal"]),
                           "literal_roofline_frac": round(b["literal"] / (ms / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "n_fg": int(b["n_fg"]), "stages_ms": {k: round(v, 5) for k, v in st.items()},
+                          "ms_per_frame_stats": bench_config.latency,
                           "host_enqueue_us_per_frame": round(time_steps.host_us_per_call, 2),
                           "workspace_bytes": ws}), flush=True)
         return
 
     spec, frames, ms_step, stages, bytes_, ws = bench_config(4, args.steps, args.warmup)
+    latency = bench_config.latency
+    copy_gbs = copy_bandwidth()
     nfr = len(frames)
     fps = nfr * 1000.0 / ms_step
     dom = max(stages, key=stages.get)
     dom_ms = stages[dom]
     achieved = bytes_[dom] / (dom_ms * 1e-3) / 1e9
+    traffic = measured_traffic("16x640x640", dom)
+    literal_gbs = bytes_["literal"] / (ms_step / nfr * 1e-3) / 1e9
     result = {
         "metric": "decoded frames/sec at 640x640 D=64",
         "value": round(fps, 2),
@@ -381,10 +443,14 @@ def main():
                    "input_dtype": spec.dtype, "bins": spec.bins, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("16x640x640", dom),
+                     "traffic": traffic,
+                     "traffic_gbs": None if traffic is None else round(traffic / (dom_ms * 1e-3) / 1e9, 1),
                      "bytes_per_launch": round(bytes_[dom]), "avg_launch_ms": round(dom_ms, 5)},
         "stages_ms": {k: round(v, 5) for k, v in stages.items()},
-        "literal_roofline_frac": round(bytes_["literal"] / (ms_step / nfr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "ms_per_frame_stats": latency,
+        "literal_roofline_frac": round(literal_gbs / HBM_PEAK_GBS, 4),
+        "copy_gbs": round(copy_gbs, 1),
+        "literal_frac_of_copy": round(literal_gbs / copy_gbs, 4),
         "host_enqueue_us_per_frame": round(time_steps.host_us_per_call, 2),
         "workspace_bytes": ws,
     }
@@ -400,6 +466,8 @@ def main():
             extra[f"cfg{cfg}"] = {"workload": s.name, "ms_per_frame": round(ms, 5), "frames_per_s": round(1000 / ms, 1),
                                   "literal_bytes": int(b["literal"]),
                                   "literal_roofline_frac": round(b["literal"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                  "literal_frac_of_copy": round(b["literal"] / (ms * 1e-3) / 1e9 / copy_gbs, 4),
+                                  "ms_per_frame_stats": bench_config.latency,
                                   "stages_ms": {k: round(v, 5) for k, v in st.items()},
                                   "quality_vs_instances": b["quality"]}
             # the same frame decoded with only the harmonics the 32x32 grid resolves
