@@ -270,13 +270,18 @@ def cpu_baseline(cfg, frames, budget_s=12.0):
     th = thresholds()[str(cfg)]
     spec = frames[0].spec
     fx, fy = spec.freqs()
-    done, t0 = 0, time.perf_counter()
-    while time.perf_counter() - t0 < budget_s:
-        f = frames[done % len(frames)]
-        oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
-                      th["peak_threshold"], want_score=False)
-        done += 1
-    dt = time.perf_counter() - t0
+    avail = sorted(os.sched_getaffinity(0))
+    os.sched_setaffinity(0, {avail[0]})    # one core, as a single-threaded baseline
+    try:
+        done, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < budget_s:
+            f = frames[done % len(frames)]
+            oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
+                          th["peak_threshold"], want_score=False)
+            done += 1
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, set(avail))
     model = "unknown"
     try:
         with open("/proc/cpuinfo") as fh:
@@ -284,7 +289,7 @@ def cpu_baseline(cfg, frames, budget_s=12.0):
     except OSError:
         pass
     return {"value": done / dt, "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "host_cpu": model, "host_cores_available": len(os.sched_getaffinity(0)),
+            "pinned_core": avail[0], "host_cpu": model, "host_cores_available": len(avail),
             "host_cores_total": os.cpu_count(),
             "sample": f"{done} decodes cycling through the {len(frames)} frames of the {spec.name} batch, "
                       f"single-threaded C oracle, {dt:.1f} s"}
