@@ -381,8 +381,9 @@ def main():
                     help="bin-count sweep at the paper's 704x704 D=16 shape and the resolution series instead")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: the decoder has no multi-GPU path (frames are independent; "
-              "see the sharding note in DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the decoder has no multi-GPU path (frames are independent "
+              "and would shard across GPUs without communication; one GPU's throughput is what is measured)",
+              file=sys.stderr)
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
