@@ -93,7 +93,7 @@ typedef struct cpe_decoder cpe_decoder;
  * centres and are computed here once, on the host in fp64, then kept on the
  * device with the weight table ("preloaded ... without recomputing").
  *   out          receives the handle (set to NULL on failure)
- *   H, W         frame size, H*W <= 2^31-1
+ *   H, W         frame size, H*W <= 2^31 - 2^23 (2,139,095,040 pixels)
  *   D            channels per pixel: the x block is channels [0, D/2), the y
  *                block [D/2, D), each (sin, cos) pairs of ascending harmonics
  *                (Eq2, Eq3).  D = 4*n_freq decodes every harmonic.  D >

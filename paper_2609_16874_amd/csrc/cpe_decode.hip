@@ -126,7 +126,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
 {
     if (!out) return CPE_ERR_INVALID_ARG;
     *out = nullptr;
-    if (H < 1 || W < 1 || (int64_t)H * W > 2147483647LL) return CPE_ERR_INVALID_ARG;
+    if (H < 1 || W < 1 || (int64_t)H * W > kMaxPixels) return CPE_ERR_INVALID_ARG;
     if (n_freq < 1 || n_freq > kMaxF || D < 4 * n_freq || D % 2 != 0 || D > 1 << 16) return CPE_ERR_INVALID_ARG;
     if (dtype != CPE_F32 && dtype != CPE_F16) return CPE_ERR_INVALID_ARG;
     // a longer encoding (low harmonics only) is read as two 16-byte aligned blocks

@@ -22,6 +22,10 @@ constexpr int kCompactThreads = 1024;
 constexpr int kCompactPer = 8;                                   // pixels per lane
 constexpr int kCompactSpan = kCompactThreads * kCompactPer;      // pixels per workgroup and step
 constexpr int kMaxSlices = 256;                                  // workgroups of the compaction
+// Largest frame: every slice end (at most one slice, 2^23 pixels, past the
+// frame) and every tile offset then stays below 2^31, so pixel and list
+// positions are int32 throughout.
+constexpr int64_t kMaxPixels = (1LL << 31) - (1LL << 23);
 
 // Pixels per slice for a frame of npix pixels, and the number of slices.
 __host__ __device__ inline int slice_pixels(int64_t npix)
@@ -47,7 +51,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int R = slice_pixels(npix);
     const int begin = blockIdx.x * R;
-    const int end = min(begin + R, npix);
+    const int end = (int)min((int64_t)begin + R, (int64_t)npix);
     int32_t *out = list + begin;
     int base = 0;                                      // entries of the slice so far
     const bool score_vec = score && ((uintptr_t)score & 15u) == 0;

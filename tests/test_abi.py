@@ -62,7 +62,7 @@ def test_options_struct_layout():
 
 @pytest.mark.parametrize("kw", [dict(H=0), dict(W=-1), dict(D=17), dict(n_freq=0), dict(n_freq=17, D=68),
                                 dict(dtype=7), dict(bins_w=0), dict(bins_h=129), dict(cap=0), dict(cap=10 ** 6),
-                                dict(H=65536, W=65536), dict(freq_nan=True)])
+                                dict(H=65536, W=65536), dict(H=32768, W=65281), dict(freq_nan=True)])
 def test_create_rejects_bad_arguments(kw):
     lib = native.library()
     a = dict(H=16, W=16, D=16, dtype=0, n_freq=4, bins_w=8, bins_h=8, cap=16)
