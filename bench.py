@@ -177,7 +177,7 @@ def step_latency(dec, embs, fgs, outs, fg_thr, theta, steps=100, warmup=10):
 
 def copy_bandwidth(mib=256, reps=10):
     """GB/s (bytes read + bytes written) of a plain device-to-device copy on
-    this GPU, the box's practical HBM ceiling beside the 8 TB/s peak."""
+    this GPU: its practical HBM ceiling beside the 8 TB/s peak."""
     import torch
     n = mib << 20
     src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
