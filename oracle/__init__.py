@@ -26,7 +26,6 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 assert CENTROID_DTYPE.itemsize == 32
 
 W_KEYS = 8192          # weight buckets: 32 binades x 2^8 mantissa steps of fl32(S+1)
-C_KEYS = 16384         # code buckets: 32 binades x 2^9 mantissa steps
 
 _lib = None
 
@@ -70,11 +69,11 @@ def _bind(lib):
     i32 = ctypes.c_int32
     lib.cpe_oracle_decode.restype = i32
     lib.cpe_oracle_decode.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
-                                      ctypes.c_float, ctypes.c_double, P, P, P, P, P, P, P, P, P]
+                                      ctypes.c_float, ctypes.c_double, P, P, P, P, P, P, P, P]
     lib.cpe_oracle_decode_ex.restype = i32
     lib.cpe_oracle_decode_ex.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
                                          ctypes.c_float, ctypes.c_double, ctypes.c_double,
-                                         P, P, P, P, P, P, P, P, P]
+                                         P, P, P, P, P, P, P, P]
     lib.cpe_oracle_decode_real.restype = i32
     lib.cpe_oracle_decode_real.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, i32, i32, i32,
                                            ctypes.c_float, ctypes.c_double, P, P, P, P]
@@ -97,7 +96,7 @@ def decode(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,
            fg_threshold=0.5, peak_threshold=0.0, *, tau=math.inf, want_score=True, check=True):
     """Canonical decode.  Returns a dict with centroids (structured array of
     length min(K, capacity)), K, labels [H][W] int32, score_map, hist
-    [bins_h][bins_w] uint64, pal_x, pal_y, weights, codes (bucket tables).
+    [bins_h][bins_w] uint64, pal_x, pal_y, weights (the weight buckets).
     fg=None: every pixel participates; tau: the Eq8 mask threshold in
     distance units (inf: none)."""
     lib = _load()
@@ -117,18 +116,17 @@ def decode(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,
     pal_x = np.empty((bins_w, 2 * F), dtype=np.int16)
     pal_y = np.empty((bins_h, 2 * F), dtype=np.int16)
     wt = np.empty(W_KEYS, dtype=np.uint16)
-    ct = np.empty(C_KEYS, dtype=np.uint16)
     rc = lib.cpe_oracle_decode_ex(H, W, D, _dtype_code(emb), _ptr(emb), _ptr(fg), _ptr(fx), _ptr(fy), F,
                                   bins_w, bins_h, capacity, float(fg_threshold), float(peak_threshold),
                                   float(tau), _ptr(cents), _ptr(K), _ptr(labels), _ptr(score), _ptr(hist),
-                                  _ptr(pal_x), _ptr(pal_y), _ptr(wt), _ptr(ct))
+                                  _ptr(pal_x), _ptr(pal_y), _ptr(wt))
     if rc != 0:
         if check:
             raise ValueError(f"oracle rejected the arguments (code {rc})")
         return {"rc": rc}
     k = int(K[0])
     return {"rc": 0, "K": k, "centroids": cents[:min(k, capacity)].copy(), "labels": labels,
-            "score_map": score, "hist": hist, "pal_x": pal_x, "pal_y": pal_y, "weights": wt, "codes": ct}
+            "score_map": score, "hist": hist, "pal_x": pal_x, "pal_y": pal_y, "weights": wt}
 
 
 def decode_real(emb, fg, freq_x, freq_y, bins_w=32, bins_h=32, capacity=None,

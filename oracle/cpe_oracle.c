@@ -3,15 +3,16 @@
  *
  * TEST INFRASTRUCTURE ONLY (see cpe_oracle.h).  Single-threaded, no SIMD, no
  * blocking, no reordering beyond what each step's definition states.  Built
- * with gcc -O2 and without -ffast-math so that rintf/(float) casts are
- * the IEEE round-to-nearest-even operations the canonical arithmetic names.
+ * with gcc -O2 and without -ffast-math so that rintf, sqrtf and the (float)
+ * casts are the IEEE round-to-nearest-even operations the canonical
+ * arithmetic names.
  *
  * The steps follow Section 3 of the paper in its own order:
  *   palettes (Eq9)                     -> build_palette()
  *   per-axis distances, weights        -> axis_profile()      (Eq4, Eq5, Eq10)
  *   vote histogram                     -> accumulate over S   (Eq6, Eq11)
  *   local-maxima search                -> is_peak()           (LMS paragraph)
- *   assignment and counts              -> assign()            (Eq7, mask
+ *   assignment and counts              -> assignment loop     (Eq7, mask
  *                                                              aggregation)
  *
  * Canonical arithmetic (the reading adopted where the paper fixes no
@@ -20,44 +21,51 @@
  *                 Eq9 with u = 2x/W - 1 and continuous pixel coordinates)
  *   palette       P[a][2k] = rint(4096 sin(w_k x_a)), P[a][2k+1] =
  *                 rint(4096 cos(w_k x_a)), fp64, stored as int16
- *   input         X = 16 rintf(256.0f * clamp(v, -1.5, 1.5)), fp32, where a
- *                 NaN channel clamps to -1.5: the input rounded to 1/256
- *                 (its error varies from pixel to pixel and averages out in
- *                 the votes) in the palette's 1/4096 units
+ *   input         X = rintf(4096.0f * clamp(v, -1.5, 1.5)) in fp32 (a NaN
+ *                 channel clamps to -1.5): the input on the palette's grid
+ *                 of 1/4096
  *   participation p in S  <=>  (float)fg(p) > fg_threshold; with no fg
  *                 channel every pixel is in S (the set of Section 3.1)
- *   distance      S_x = sum_c (X_c - P[a][c])^2 (exact integer); with
- *                 u = fl32(S+1) = 2^e (1 + f), 0 <= f < 1, the m-bit bucket
- *                 of S is key_m(S) = e 2^m + floor(f 2^m) (exponent and top
- *                 m mantissa bits of u), its centre distance
- *                 d~_m(key) = sqrt(2^e (1 + (t+0.5)/2^m) - 1)/4096, t =
- *                 key mod 2^m (0 for the bucket of S = 0)
- *   weight        q = WT[key_8(S)] = rint(2^15 e^{-d~_8})    (Eq5/Eq10)
- *   code          c = CT[key_9(S)] = rint(4096 d~_9)         (distance, 1/4096)
+ *   distance      S_x = sum_c (X_c - P[a][c])^2 (exact integer, < 2^32)
+ *   weight        with u = fl32(S+1) = 2^e (1 + f), 0 <= f < 1, the 8-bit
+ *                 bucket of S is key(S) = e 2^8 + floor(f 2^8) (exponent and
+ *                 top 8 mantissa bits of u); q = WT[key] = rint(2^15 e^-d~),
+ *                 d~ = sqrt(2^e (1 + (t+0.5)/2^8) - 1)/4096 the distance at
+ *                 the bucket centre, t = key mod 2^8 (0 for S = 0)  (Eq5/Eq10)
  *   votes         H[b][a] = sum_{p in S} q_x(p,a) q_y(p,b)  (exact uint64)
  *   peaks         H[b][a] > floor(theta_peak 2^30) and > every in-range
  *                 8-neighbour; listed in ascending b*B_w + a
- *   assignment    D_k = c_x(a_k) + c_y(b_k) (integer); the smallest k with
- *                 the minimal D_k wins; label = k+1, background 0
- *   mask test     (Eq8) the winner m keeps the pixel only if its distance
- *                 D_m / 4096 is below tau (tau = +inf keeps every pixel of
- *                 S); a pixel that fails it gets label 0 and is not counted
- *   score map     expf(-D_m / 4096) for labelled pixels
+ *   distance      r = sqrtf(fl32(S)), the correctly rounded binary32 square
+ *   (Eq7)         root of S rounded to binary32: the Euclidean distance in
+ *                 units of 1/4096
+ *   assignment    D_k = r_x(a_k) + r_y(b_k), the exact sum (representable in
+ *                 binary64); the smallest k with the minimal D_k wins;
+ *                 label = k+1, background 0
+ *   mask test     (Eq8) the winner m keeps the pixel only if D_m < 4096 tau
+ *                 (binary64 compare; tau = +inf keeps every pixel of S); a
+ *                 pixel that fails it gets label 0 and is not counted
+ *   score map     expf(-(float)(D_m / 4096)) for labelled pixels
  *
  * Pins (tests/test_oracle_*.py), each independent of this file's code:
- *   - bucket tables against e^-d and 256 d over each bucket's exact range;
- *     palette sin^2+cos^2 = 1 and its values against gamma at the centres;
+ *   - weight buckets against e^-d over each bucket's exact range; palette
+ *     sin^2+cos^2 = 1 and its values against gamma at the centres;
  *   - the vote histogram against the paper's matrix form E_x^T E_y in fp64
  *     (numpy), within the quantisation error bound;
  *   - brute force on tiny frames: exhaustive scan of every grid position for
- *     the peaks and every candidate for each pixel's assignment;
+ *     the peaks and every candidate for each pixel's assignment, with exact
+ *     rational sums of the square roots;
  *   - noise-free frames whose centroids sit on bin centres decode to the
  *     generating centroids and the generating label map;
  *   - invariants: labels partition the foreground, counts sum to |S|,
  *     peaks pairwise non-adjacent, instance-order independence;
- *   - the Eq8 mask threshold and the all-pixels mode: the exhaustive search
- *     with tau on attained code sums, a noise-free frame where a tau of half
- *     a code unit keeps exactly the instance pixels, and nesting in tau.
+ *   - the assignment against Eq7 evaluated in fp64 on the unquantised input
+ *     (at most 0.1 % of the foreground differs on the 256x256, 640x640 and
+ *     1024x2048 workloads, all of them near-ties);
+ *   - the Eq8 mask threshold and the all-pixels mode: the exhaustive search,
+ *     a noise-free frame where a small tau keeps exactly the instance
+ *     pixels, and nesting in tau;
+ *   - the fp64 real-valued mode: its histogram against E_x^T E_y, its peaks
+ *     against a library maximum filter, its labels against a numpy argmin.
  * The whole pipeline against the paper's own decoder: parity unpinned (no
  * implementation or worked example is published).
  */
@@ -67,13 +75,10 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define FIX_SCALE 4096.0f       /* palette and distance fixed-point scale    */
-#define IN_GRID 256.0f          /* inputs are rounded to multiples of 1/256  */
+#define FIX_SCALE 4096.0f       /* input, palette and distance fixed point   */
 #define V_CLAMP 1.5f            /* inputs are clamped to [-1.5, 1.5]         */
 #define W_MANT 8                /* mantissa bits of fl32(S+1): weight bucket */
-#define C_MANT 9                /* mantissa bits of fl32(S+1): code bucket   */
 #define W_KEYS (32 << W_MANT)   /* 32 binades of S+1 in [1, 2^32)            */
-#define C_KEYS (32 << C_MANT)
 
 /* IEEE binary16 -> binary32, exact (every half is a float). */
 static float half_to_float(uint16_t h)
@@ -99,13 +104,13 @@ static float load_value(const void *base, int32_t dtype, size_t index)
 }
 
 /* Input to fixed point: clamp to [-1.5, 1.5] (NaN -> -1.5), round to the
- * nearest multiple of 1/256, express in units of 1/4096. */
+ * nearest multiple of 1/4096 (ties to even), in units of 1/4096. */
 static int32_t to_fixed(float v)
 {
     float c = v;
     if (isnan(c) || c < -V_CLAMP) c = -V_CLAMP;
     if (c > V_CLAMP) c = V_CLAMP;
-    return (int32_t)(FIX_SCALE / IN_GRID) * (int32_t)rintf(IN_GRID * c);
+    return (int32_t)rintf(FIX_SCALE * c);
 }
 
 /* m-bit distance bucket of an exact squared distance S: the exponent and
@@ -140,18 +145,17 @@ static void build_palette(int32_t n, int32_t extent, const double *freq, int32_t
     }
 }
 
-/* Eq5 weights e^-d of the 8-bit buckets and distance codes of the 9-bit
- * buckets. */
-static void build_tables(uint16_t *wt, uint16_t *ct)
+/* Eq5 weights e^-d of the 8-bit buckets. */
+static void build_weights(uint16_t *wt)
 {
     for (int32_t key = 0; key < W_KEYS; key++) wt[key] = (uint16_t)rint(32768.0 * exp(-key_distance(key, W_MANT)));
-    for (int32_t key = 0; key < C_KEYS; key++) ct[key] = (uint16_t)rint(4096.0 * key_distance(key, C_MANT));
 }
 
-/* Eq4/Eq10 for one axis of one pixel: distance bucket of every palette
- * entry, giving its vote weight q[a] and distance code c[a]. */
+/* Eq4/Eq10 for one axis of one pixel: the exact squared distance S to every
+ * palette entry, giving its vote weight q[a] (from the bucket of S) and its
+ * distance r[a] = sqrtf(fl32(S)) in units of 1/4096. */
 static void axis_profile(const int32_t *X, const int16_t *pal, int32_t n, int32_t twoF,
-                         const uint16_t *wt, const uint16_t *ct, uint32_t *q, int32_t *c)
+                         const uint16_t *wt, uint32_t *q, float *r)
 {
     for (int32_t a = 0; a < n; a++) {
         uint64_t s = 0;
@@ -160,7 +164,7 @@ static void axis_profile(const int32_t *X, const int16_t *pal, int32_t n, int32_
             s += (uint64_t)(diff * diff);
         }
         if (q) q[a] = wt[dist_key((uint32_t)s, W_MANT)];
-        if (c) c[a] = ct[dist_key((uint32_t)s, C_MANT)];
+        if (r) r[a] = sqrtf((float)(uint32_t)s);
     }
 }
 
@@ -229,12 +233,12 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       float fg_threshold, double peak_threshold,
                       cpe_oracle_centroid *centroids, int32_t *num_centroids,
                       int32_t *labels, float *score_map,
-                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out, uint16_t *ct_out)
+                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out)
 {
     if (!fg) return CPE_ORACLE_EINVAL;
     return cpe_oracle_decode_ex(H, W, D, dtype, emb, fg, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
                                 fg_threshold, peak_threshold, INFINITY, centroids, num_centroids, labels,
-                                score_map, hist, pal_x, pal_y, wt_out, ct_out);
+                                score_map, hist, pal_x, pal_y, wt_out);
 }
 
 int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
@@ -244,7 +248,7 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
                          float fg_threshold, double peak_threshold, double tau,
                          cpe_oracle_centroid *centroids, int32_t *num_centroids,
                          int32_t *labels, float *score_map,
-                         uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out, uint16_t *ct_out)
+                         uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *wt_out)
 {
     if (check_args(H, W, D, dtype, emb, freq_x, freq_y, n_freq, bins_w, bins_h, capacity,
                    fg_threshold, peak_threshold) != CPE_ORACLE_OK ||
@@ -257,18 +261,18 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
 
     int16_t *Pw = malloc(sizeof(int16_t) * bins_w * twoF);
     int16_t *Ph = malloc(sizeof(int16_t) * bins_h * twoF);
-    uint16_t *wt = malloc(sizeof(uint16_t) * W_KEYS), *ct = malloc(sizeof(uint16_t) * C_KEYS);
+    uint16_t *wt = malloc(sizeof(uint16_t) * W_KEYS);
     uint64_t *Hv = calloc((size_t)nbins, sizeof(uint64_t));
     int32_t *X = malloc(sizeof(int32_t) * twoF);
     int32_t *Y = malloc(sizeof(int32_t) * twoF);
-    int32_t *cx = malloc(sizeof(int32_t) * bins_w), *cy = malloc(sizeof(int32_t) * bins_h);
+    float *rx = malloc(sizeof(float) * bins_w), *ry = malloc(sizeof(float) * bins_h);
     uint32_t *qx = malloc(sizeof(uint32_t) * bins_w), *qy = malloc(sizeof(uint32_t) * bins_h);
     int32_t *peak_a = malloc(sizeof(int32_t) * nbins), *peak_b = malloc(sizeof(int32_t) * nbins);
 
-    /* palettes, preloaded once (Section 3.2, Eq9), and the bucket tables */
+    /* palettes, preloaded once (Section 3.2, Eq9), and the weight buckets */
     build_palette(bins_w, W, freq_x, F, Pw);
     build_palette(bins_h, H, freq_y, F, Ph);
-    build_tables(wt, ct);
+    build_weights(wt);
 
     /* histogram accumulation: H(a,b) = sum_{p in S} E_x(p,a) E_y(p,b) */
     for (size_t p = 0; p < npix; p++) {
@@ -277,8 +281,8 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
             Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c)));
         }
-        axis_profile(X, Pw, bins_w, twoF, wt, ct, qx, NULL);
-        axis_profile(Y, Ph, bins_h, twoF, wt, ct, qy, NULL);
+        axis_profile(X, Pw, bins_w, twoF, wt, qx, NULL);
+        axis_profile(Y, Ph, bins_h, twoF, wt, qy, NULL);
         for (int32_t b = 0; b < bins_h; b++)
             for (int32_t a = 0; a < bins_w; a++)
                 Hv[b * bins_w + a] += (uint64_t)qx[a] * (uint64_t)qy[b];
@@ -309,7 +313,9 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
         c->reserved = 0;
     }
 
-    /* assignment (Eq7): nearest candidate in the encoded space */
+    /* assignment (Eq7): nearest candidate in the encoded space, d_x + d_y
+     * summed exactly (two binary32 values always have an exact binary64
+     * sum) */
     for (size_t p = 0; p < npix; p++) {
         labels[p] = 0;
         if (score_map) score_map[p] = 0.0f;
@@ -318,32 +324,31 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
             X[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)c));
             Y[c] = to_fixed(load_value(emb, dtype, p * (size_t)D + (size_t)(yoff + c)));
         }
-        axis_profile(X, Pw, bins_w, twoF, wt, ct, NULL, cx);
-        axis_profile(Y, Ph, bins_h, twoF, wt, ct, NULL, cy);
+        axis_profile(X, Pw, bins_w, twoF, wt, NULL, rx);
+        axis_profile(Y, Ph, bins_h, twoF, wt, NULL, ry);
         int32_t best = 0;
-        int32_t best_d = cx[peak_a[0]] + cy[peak_b[0]];
+        double best_d = (double)rx[peak_a[0]] + (double)ry[peak_b[0]];
         for (int32_t k = 1; k < Kc; k++) {
-            int32_t dk = cx[peak_a[k]] + cy[peak_b[k]];
+            double dk = (double)rx[peak_a[k]] + (double)ry[peak_b[k]];
             if (dk < best_d) {
                 best_d = dk;
                 best = k;
             }
         }
         /* Eq8: the pixel joins mask m only if d(a_m, b_m) < tau */
-        if (!((double)best_d < 4096.0 * tau)) continue;
+        if (!(best_d < 4096.0 * tau)) continue;
         labels[p] = best + 1;
         centroids[best].npix += 1;
-        if (score_map) score_map[p] = expf(-((float)best_d * 0x1p-12f));
+        if (score_map) score_map[p] = expf(-(float)(best_d * 0x1p-12));
     }
 
     if (hist) memcpy(hist, Hv, sizeof(uint64_t) * (size_t)nbins);
     if (pal_x) memcpy(pal_x, Pw, sizeof(int16_t) * bins_w * twoF);
     if (pal_y) memcpy(pal_y, Ph, sizeof(int16_t) * bins_h * twoF);
     if (wt_out) memcpy(wt_out, wt, sizeof(uint16_t) * W_KEYS);
-    if (ct_out) memcpy(ct_out, ct, sizeof(uint16_t) * C_KEYS);
 
-    free(Pw); free(Ph); free(wt); free(ct); free(Hv); free(X); free(Y);
-    free(cx); free(cy); free(qx); free(qy); free(peak_a); free(peak_b);
+    free(Pw); free(Ph); free(wt); free(Hv); free(X); free(Y);
+    free(rx); free(ry); free(qx); free(qy); free(peak_a); free(peak_b);
     return CPE_ORACLE_OK;
 }
 

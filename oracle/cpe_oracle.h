@@ -16,16 +16,15 @@
  *   counts (mask-aggregation paragraph).
  *
  * Two arithmetic modes:
- *   cpe_oracle_decode       canonical fixed-point arithmetic: inputs rounded
- *                           to 1/256 and palettes to 1/4096, both in units of
- *                           1/4096, exact integer squared
- *                           distances, distance buckets given by the
- *                           exponent and top mantissa bits of fl32(S+1) with
- *                           tables of 2^15 e^-d weights (8-bit buckets) and
- *                           1/4096 distance codes (9-bit buckets), exact
- *                           64-bit vote sums, integer distance sums for the
- *                           assignment.  Every discrete decision
- *                           is reproducible bit for bit by any correct
+ *   cpe_oracle_decode       canonical fixed-point arithmetic: inputs and
+ *                           palettes rounded to 1/4096, exact integer
+ *                           squared distances S, vote weights 2^15 e^-d of
+ *                           the bucket given by the exponent and top 8
+ *                           mantissa bits of fl32(S+1), exact 64-bit vote
+ *                           sums; for the assignment the correctly rounded
+ *                           binary32 distances sqrtf(fl32(S)) of both axes,
+ *                           summed exactly.  Every discrete decision is
+ *                           reproducible bit for bit by any correct
  *                           implementation.
  *   cpe_oracle_decode_real  the real-valued definition in fp64 with no
  *                           quantisation (diagnostic only).
@@ -59,7 +58,7 @@ typedef struct {
  * Outputs (host): centroids[capacity], *num_centroids (true count K),
  * labels[H*W]; optional (may be NULL): score_map[H*W], hist[bins_h*bins_w]
  * (row-major [b][a]), pal_x[bins_w*2F], pal_y[bins_h*2F], weights[8192]
- * (indexed by the 8-bit bucket), codes[16384] (indexed by the 9-bit bucket). */
+ * (indexed by the 8-bit bucket). */
 int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       const void *emb, const void *fg,
                       const double *freq_x, const double *freq_y, int32_t n_freq,
@@ -67,15 +66,15 @@ int cpe_oracle_decode(int32_t H, int32_t W, int32_t D, int32_t dtype,
                       float fg_threshold, double peak_threshold,
                       cpe_oracle_centroid *centroids, int32_t *num_centroids,
                       int32_t *labels, float *score_map,
-                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
-                      uint16_t *codes);
+                      uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights);
 
 /* The same with two of the paper's options:
  *   fg   may be NULL: then every pixel participates (the participating set of
  *        Section 3.1 is the whole output grid);
  *   tau  the mask threshold of Eq8 in distance units: a pixel keeps the label
- *        of its nearest candidate m only if D_m / 4096 < tau, where D_m is the
- *        integer code sum; otherwise label 0, not counted.  +INFINITY keeps
+ *        of its nearest candidate m only if D_m < 4096 tau, where D_m =
+ *        sqrtf(S_x) + sqrtf(S_y) (exact sum) is its distance in units of
+ *        1/4096; otherwise label 0, not counted.  +INFINITY keeps
  *        every participating pixel (cpe_oracle_decode); NaN is rejected. */
 int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
                          const void *emb, const void *fg,
@@ -84,8 +83,7 @@ int cpe_oracle_decode_ex(int32_t H, int32_t W, int32_t D, int32_t dtype,
                          float fg_threshold, double peak_threshold, double tau,
                          cpe_oracle_centroid *centroids, int32_t *num_centroids,
                          int32_t *labels, float *score_map,
-                         uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
-                         uint16_t *codes);
+                         uint64_t *hist, int16_t *pal_x, int16_t *pal_y, uint16_t *weights);
 
 /* Real-valued fp64 decoder (no quantisation, no threshold tau).  Outputs:
  * hist[bins_h*bins_w] (double), peak list (bin index b*bins_w+a, ascending)

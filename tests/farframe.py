@@ -3,9 +3,10 @@
 Two instances (left and right halves of a 40 x 48 frame, 16 harmonics per
 axis, fp32) plus 40 pixels whose every channel sits at the clamp bound
 +-1.5, pointing away from the candidates' palette entries (half of them with
-some channels flipped).  Every x + y code sum of those pixels is at least
-2^16, the range where the GPU's 32-bit search keys saturate; the winner is
-still the Eq7 argmin (smallest code sum, then lowest bin index).
+some channels flipped).  Their squared distances reach far above 2^24, where
+rounding S to binary32 loses integer precision; the winner is still the Eq7
+argmin (smallest exact sum of the two axis distances, then the lowest
+candidate index).
 """
 import math
 
@@ -18,23 +19,22 @@ H, W, F = 40, 48, 16
 BINS, CAP = 32, 64
 
 
-def candidate_code_sums(ref, emb, nf):
-    """[pixels][K] x + y code sums of every candidate, from the oracle's
-    palettes and code table: input on its 1/256 grid in 1/4096 units, the
-    code of bucket(fl32(S + 1)) (exponent and top 9 mantissa bits)."""
+def candidate_distance_sums(ref, emb, nf):
+    """[pixels][K] Eq7 distance sums of every candidate in units of 1/4096,
+    from the oracle's palettes: input on the 1/4096 grid (clamped to
+    +-1.5), S exact, r = the float32 square root of S rounded to float32,
+    r_x + r_y summed exactly in float64; and per pixel the largest S."""
     v = np.clip(emb.reshape(-1, 4 * nf).astype(np.float32), -1.5, 1.5)
-    X = 16 * np.rint(np.float32(256.0) * v).astype(np.int64)
-    ct = ref["codes"].astype(np.int64)
+    X = np.rint(np.float32(4096.0) * v).astype(np.int64)
 
-    def codes(Xa, P):
+    def dist(Xa, P):
         S = ((Xa[:, None, :] - P[None].astype(np.int64)) ** 2).sum(-1)
-        bits = (S + 1).astype(np.float32).view(np.uint32).astype(np.int64)
-        return ct[(bits >> 14) - (127 << 9)]
+        return np.sqrt(S.astype(np.float32)).astype(np.float64), S.max(1)
 
-    cx = codes(X[:, :2 * nf], ref["pal_x"])
-    cy = codes(X[:, 2 * nf:], ref["pal_y"])
+    rx, sx = dist(X[:, :2 * nf], ref["pal_x"])
+    ry, sy = dist(X[:, 2 * nf:], ref["pal_y"])
     A, B = ref["centroids"]["bin_x"], ref["centroids"]["bin_y"]
-    return cx[:, A] + cy[:, B]
+    return rx[:, A] + ry[:, B], np.maximum(sx, sy)
 
 
 def make():

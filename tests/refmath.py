@@ -11,7 +11,8 @@ that they can pin it:
 * ``strict_local_maxima``: the local-maxima search of Section 3.2 via
   ``scipy.ndimage.maximum_filter`` with a ring footprint;
 * ``brute_decode``: pure-Python loops over every grid position and every
-  candidate, for tiny frames only.
+  candidate, for tiny frames only;
+* ``real_labels``: Eq7 by a numpy argmin of fp64 distance sums, in chunks.
 """
 from __future__ import annotations
 
@@ -62,13 +63,13 @@ def quant_bound(ex, ey, twoF):
     """Bound on |H_canonical * 2^-30 - H_real| per bin, as [b][a].
 
     Per pixel and axis the canonical distance differs from the real one by
-    (i) input rounding to 1/256 and palette rounding to 1/4096 per channel:
-    at most sqrt(2F) (2^-9 + 2^-13) (triangle inequality, no clamping);
+    (i) input and palette rounding to 1/4096 per channel: at most
+    sqrt(2F) (2^-13 + 2^-13) (triangle inequality, no clamping);
     (ii) the 8-bit weight bucket: fl32(S+1) falls in [L, L(1+2^-8)) and the
     bucket centre S_mid+1 is within a factor e^(2^-9 + 2^-23) of S+1, so its
     square root is within e^(2^-10 + 2^-24) of sqrt(S+1); replacing S+1 by S
     moves sqrt by at most 1, i.e. 2^-12 in embedding units, on each side.
-    Hence |d~ - d| <= delta(d) = sqrt(2F) (2^-9 + 2^-13) + 2^-11 + 2^-10 (d + 0.01).
+    Hence |d~ - d| <= delta(d) = sqrt(2F) 2^-12 + 2^-11 + 2^-10 (d + 0.01).
     The weight table rounds 2^15 e^-d~ to an integer (2^-16 absolute), so per
     axis eps = e^-d (e^delta(d) - 1) + 2^-16 bounds |q/2^15 - e^-d|, and for
     a product of two weights the error is at most
@@ -76,7 +77,7 @@ def quant_bound(ex, ey, twoF):
     """
     def eps(e):
         d = -np.log(np.maximum(e, 1e-300))
-        delta = math.sqrt(twoF) * (2.0 ** -9 + 2.0 ** -13) + 2.0 ** -11 + 2.0 ** -10 * (d + 0.01) + 1e-9
+        delta = math.sqrt(twoF) * 2.0 ** -12 + 2.0 ** -11 + 2.0 ** -10 * (d + 0.01) + 1e-9
         return e * np.expm1(delta) + 2.0 ** -16
 
     epx, epy = eps(ex), eps(ey)
@@ -97,7 +98,7 @@ def strict_local_maxima(h: np.ndarray, cut) -> np.ndarray:
 # --------------------------------------------------------------------------
 # pure-Python brute force for tiny frames (canonical arithmetic written out)
 # --------------------------------------------------------------------------
-W_MANT, C_MANT = 8, 9
+W_MANT = 8
 
 
 def _f32(x):
@@ -105,14 +106,21 @@ def _f32(x):
 
 
 def fixed(v: float) -> int:
-    """16 rint(256 clamp(v, -1.5, 1.5)) in binary32 (the input on a 1/256 grid,
-    in units of 1/4096), NaN clamping to -1.5."""
+    """rint(4096 clamp(v, -1.5, 1.5)) in binary32 (the input on the
+    palette's 1/4096 grid, in units of 1/4096), NaN clamping to -1.5."""
     c = np.float32(v)
     if np.isnan(c) or c < np.float32(-1.5):
         c = np.float32(-1.5)
     if c > np.float32(1.5):
         c = np.float32(1.5)
-    return 16 * int(np.rint(np.float32(256.0) * c))
+    return int(np.rint(np.float32(4096.0) * c))
+
+
+def root(S: int) -> Fraction:
+    """The Eq4 distance of an exact squared distance S, in units of 1/4096:
+    S rounded to binary32, then its correctly rounded binary32 square root
+    (numpy's float32 sqrt is the IEEE operation), as an exact rational."""
+    return Fraction(float(np.sqrt(np.float32(S))))
 
 
 def dist_key(S: int, m: int) -> int:
@@ -155,11 +163,12 @@ def bucket_range(key: int, m: int):
 def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold, tau=math.inf, dist_out=None):
     """Exhaustive decode for tiny frames: every grid position is scored by a
     direct sum over the pixels, every bin is tested against its neighbours,
-    and every pixel scans every candidate.  fg=None: every pixel takes part
-    (Section 3.1); tau: Eq8, a pixel keeps its nearest candidate only if that
-    distance, as the exact rational code sum / 4096, is below tau.  Returns
-    (hist[b][a] list of ints, peaks [(a, b)], K, labels [H][W]); dist_out, a
-    dict, receives {(i, j): winning code sum}."""
+    and every pixel scans every candidate with the exact rational sum of its
+    two axis distances.  fg=None: every pixel takes part (Section 3.1); tau:
+    Eq8, a pixel keeps its nearest candidate only if that distance sum / 4096
+    is below tau (exact rationals).  Returns (hist[b][a] list of ints, peaks
+    [(a, b)], K, labels [H][W]); dist_out, a dict, receives {(i, j): winning
+    distance sum in units of 1/4096, as a float (exact)}."""
     H, W, D = emb.shape
     F = len(fx)
     pal_x = [[int(np.rint(4096.0 * f(fx[k] * ((a + 1) * W / (bw + 1)))))
@@ -173,8 +182,6 @@ def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold
     def q_of(S):
         return int(np.rint(32768.0 * math.exp(-key_distance(dist_key(S, W_MANT), W_MANT))))
 
-    def c_of(S):
-        return int(np.rint(4096.0 * key_distance(dist_key(S, C_MANT), C_MANT)))
 
     pix = []
     for i in range(H):
@@ -205,11 +212,44 @@ def brute_decode(emb, fg, fx, fy, bw, bh, capacity, fg_threshold, peak_threshold
     for (i, j, X, Y) in pix:
         if not use:
             break
-        ds = [c_of(s_of(X, pal_x[a])) + c_of(s_of(Y, pal_y[b])) for (a, b) in use]
+        ds = [root(s_of(X, pal_x[a])) + root(s_of(Y, pal_y[b])) for (a, b) in use]
         best = min(range(len(use)), key=lambda k: (ds[k], k))
         if dist_out is not None:
-            dist_out[(i, j)] = ds[best]
-        if not Fraction(ds[best], 4096) < tau:
+            dist_out[(i, j)] = float(ds[best])
+        if not (math.isinf(tau) and tau > 0) and not ds[best] / 4096 < Fraction(tau):
             continue
         labels[i][j] = best + 1
     return hist, peaks, K, labels
+
+
+def real_labels(emb, fg, fx, fy, bw, bh, bins_x, bins_y, fg_threshold=0.5, chunk=200000):
+    """Eq7 on the unquantised input in fp64: for every participating pixel
+    the index (1-based) of the candidate (bins_x[k], bins_y[k]) with the
+    smallest d_x + d_y, numpy argmin (first index on ties), in chunks of
+    pixels.  Distances via |v - p|^2 = |v|^2 + |p|^2 - 2 v.p (fp64 matmul).
+    Returns (labels of the participating pixels, their selection mask, and
+    per pixel the gap between its two smallest distance sums)."""
+    H, W, D = emb.shape
+    F = len(fx)
+    half = D // 2
+    sel = fg.astype(np.float32).reshape(-1) > np.float32(fg_threshold)
+    flat = emb.reshape(-1, D)
+    px, py = palettes_real(H, W, fx, fy, bw, bh)
+    idx = np.nonzero(sel)[0]
+    lab = np.empty(len(idx), np.int64)
+    gap = np.empty(len(idx), np.float64)
+    a = np.asarray(bins_x)
+    b = np.asarray(bins_y)
+    for s in range(0, len(idx), chunk):
+        v = flat[idx[s:s + chunk]].astype(np.float64)
+        vx, vy = v[:, :2 * F], v[:, half:half + 2 * F]
+        dx = np.sqrt(np.maximum((vx ** 2).sum(1)[:, None] + (px ** 2).sum(1)[None] - 2.0 * vx @ px.T, 0.0))
+        dy = np.sqrt(np.maximum((vy ** 2).sum(1)[:, None] + (py ** 2).sum(1)[None] - 2.0 * vy @ py.T, 0.0))
+        Dk = dx[:, a] + dy[:, b]
+        lab[s:s + chunk] = Dk.argmin(1) + 1
+        if Dk.shape[1] > 1:
+            part = np.partition(Dk, 1, axis=1)
+            gap[s:s + chunk] = part[:, 1] - part[:, 0]
+        else:
+            gap[s:s + chunk] = np.inf
+    return lab, sel, gap
