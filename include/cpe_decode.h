@@ -17,15 +17,16 @@
  *
  * Arithmetic.  All discrete decisions use a fixed-point arithmetic that any
  * correct implementation reproduces bit for bit:
- *   X = 16 rint(256 clamp(v, -1.5, 1.5)) per channel (a NaN clamps to -1.5):
- *   the input rounded to 1/256, in units of 1/4096;
+ *   X = rint(4096 clamp(v, -1.5, 1.5)) per channel (a NaN clamps to -1.5):
+ *   the input on a grid of 1/4096, in units of 1/4096;
  *   palettes P = rint(4096 gamma(bin centre)), bin centre (a+1) W/(B_w+1);
  *   S = |X - P|^2 exactly (integer);
- *   the bucket of S is the exponent and top m mantissa bits of fl32(S+1);
- *   vote weight = rint(2^15 e^-d) and assignment code = rint(4096 d), with d
- *   the distance at the centre of the 8-bit (weight) or 9-bit (code) bucket;
- *   votes are exact 64-bit sums; a pixel goes to the centroid with the
- *   smallest code sum c_x + c_y, lowest index on ties.
+ *   vote weight = rint(2^15 e^-d), d the distance at the centre of the
+ *   bucket of S given by the exponent and top 8 mantissa bits of fl32(S+1);
+ *   votes are exact 64-bit sums;
+ *   assignment distance r = sqrtf(fl32(S)), the correctly rounded binary32
+ *   square root (units of 1/4096); a pixel goes to the centroid with the
+ *   smallest exact sum r_x + r_y, lowest index on ties.
  * Vote masses are reported as H * 2^-30 (so a pixel at distance 0 on both
  * axes adds 1.0).
  *
@@ -36,8 +37,8 @@
  *          reads them all)
  *   fg     [H][W], same dtype as emb; a pixel participates iff fg > threshold
  *   labels [H][W] int32
- *   score  [H][W] float (optional): expf(-(c_x + c_y)/4096) of the assigned
- *          centroid, 0 on unlabelled pixels
+ *   score  [H][W] float (optional): expf(-(float)((r_x + r_y)/4096)) of the
+ *          assigned centroid, 0 on unlabelled pixels
  *
  * Ownership.  The caller owns every buffer passed to cpe_decode (device
  * memory).  The handle owns the palettes, the table and all scratch; they
@@ -90,8 +91,8 @@ typedef struct cpe_decoder cpe_decoder;
  * Build a decoder for frames of H x W pixels with D channels, decoding the
  * first n_freq harmonics of each axis.
  * Section 3.2 (Eq9): the palettes P_w, P_h are the encodings of the bin
- * centres and are computed here once, on the host in fp64, then kept on the
- * device with the weight table ("preloaded ... without recomputing").
+ * centres; they are computed here once, on the host in fp64, and stay on the
+ * device with the weight table for every later frame.
  *   out          receives the handle (set to NULL on failure)
  *   H, W         frame size, H*W <= 2^31 - 2^23 (2,139,095,040 pixels)
  *   D            channels per pixel: the x block is channels [0, D/2), the y
@@ -156,8 +157,9 @@ typedef struct {
  *                of Eq6 is the whole output grid); otherwise as cpe_decode.
  *   opt->tau     Eq8: a participating pixel keeps the label of its nearest
  *                candidate m (Eq7) only if that distance is below tau, the
- *                distance being the assignment code sum D_m = c_x + c_y in
- *                units of 1/4096 (test: D_m < 4096 tau, strict).  A pixel
+ *                distance being the exact sum D_m = r_x + r_y of the two axis
+ *                distances in units of 1/4096 (test: D_m < 4096 tau in
+ *                binary64, strict).  A pixel
  *                that fails gets label 0 and score 0 and is not counted in
  *                npix.  tau <= 0 labels nothing; +INFINITY is cpe_decode.
  * The histogram and the centroid records do not depend on tau.
@@ -198,11 +200,9 @@ const char *cpe_status_string(cpe_status s);
  * Inspection (tests and profiling).  Host copies of the constants built by
  * cpe_decode_create: pal_x [bins_w][2F] and pal_y [bins_h][2F] int16 (Eq9
  * palettes x4096, rounded), weights [8192] uint16 (2^15 e^-d per 8-bit
- * bucket), codes [16384] uint16 (4096 d per 9-bit bucket).  Any pointer may
- * be NULL.
+ * bucket).  Any pointer may be NULL.
  */
-cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
-                                 uint16_t *codes);
+cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *weights);
 
 /*
  * Enqueue on `stream` a device-to-device copy of the vote histogram of the
@@ -211,6 +211,16 @@ cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *
  * q_x(a) q_y(b).
  */
 cpe_status cpe_decode_get_histogram(cpe_decoder *h, hipStream_t stream, uint64_t *hist);
+
+/*
+ * Self-check (tests): enqueue on `stream` a comparison of the square root the
+ * assignment uses (the hardware square root plus a rounding correction) with
+ * the IEEE correctly rounded sqrtf on every binary32 value it can receive
+ * (0 and every float in [1, 2^32)); the device uint64 *mismatches (8-byte
+ * aligned, caller-owned) receives the number of differing results, 0 when
+ * the assignment's distances are exactly those of Eq4 as defined above.
+ */
+cpe_status cpe_check_sqrt(hipStream_t stream, unsigned long long *mismatches);
 
 /* Bytes of device memory the handle holds (constants + scratch). */
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h);

@@ -12,14 +12,13 @@
 namespace cpe {
 
 constexpr int kWMant = 8;             // weight bucket: top 8 mantissa bits of fl32(S+1)
-constexpr int kCMant = 9;             // code bucket: top 9 mantissa bits
 constexpr int kWKeys = 32 << kWMant;  // 8192 weight buckets (32 binades)
-constexpr int kCKeys = 32 << kCMant;  // 16384 code buckets
 constexpr int kReplicas = 4;          // replicated global histograms (spread of the atomics)
 constexpr int kMaxF = 16;             // harmonics per axis
 constexpr int kMaxBins = 128;
 constexpr int kCountCap = 1024;       // centroids whose pixel counts are privatised in LDS
 constexpr int kMfmaBins = 32;         // bin grids up to 32 x 32 take the matrix-core path
+constexpr int kPopKinds = 3;          // int8 palette operand kinds per axis (AxisOp in k_mfma.hpp)
 
 typedef short v2s __attribute__((ext_vector_type(2)));
 
@@ -30,28 +29,69 @@ struct Tables {
     const uint32_t *n2_x;     // [Bw] sum of squared palette entries
     const uint32_t *n2_y;     // [Bh]
     const uint16_t *wt;       // [kWKeys] 2^15 e^-d per 8-bit bucket (bucket order)
-    const uint16_t *ct;       // [kCKeys] 4096 d per 9-bit bucket (bucket order)
     const float *cx;          // [Bw] bin centres (pixels)
     const float *cy;          // [Bh]
     // matrix-core path (bins <= 32)
-    const int8_t *qx;         // [2][32][32]: limbs (hi, lo) of -2 P_w[bin][ch], -2P = 128 hi + lo
-    const int8_t *qy;         // [2][32][32]
     const uint32_t *np1_x;    // [32] |P_w[bin]|^2 + 1 (1 for padded bins)
     const uint32_t *np1_y;    // [32]
-    const uint32_t *pop;      // [axis][limb][K-step j][64 lanes][4 words]: the fp16 palette operand
-                              //   of lane l (bin l & 31, channels 16 j + 8 (l >> 5) + 0..7)
+    const uint32_t *pop;      // [axis][kind][64 lanes][4 words]: the int8 palette operand of lane l
+                              //   (bin l & 31, K slots 16 (l >> 5) .. + 15); see k_mfma.hpp
     const uint32_t *wt_pk;    // [kWKeys] weight as two fp16 limbs (q & 255) | (q >> 8) << 16,
                               //          at LDS position ((e + 31) & 31) * 256 + t
-    const uint16_t *ct_pm;    // [kCKeys] code at LDS position ((e + 31) & 31) * 512 + t
 };
 
-// Input to fixed point: 16 rint(256 clamp(v, -1.5, 1.5)), the input on a
-// 1/256 grid in the palette's units of 1/4096; a NaN clamps to -1.5
-// (fmaxf/fminf return the non-NaN operand).
+// Input to fixed point: rint(4096 clamp(v, -1.5, 1.5)), the input on the
+// palette's grid of 1/4096; a NaN clamps to -1.5 (fmaxf/fminf return the
+// non-NaN operand).
 __device__ __forceinline__ int32_t to_fixed(float v)
 {
     const float c = fminf(fmaxf(v, -1.5f), 1.5f);
-    return 16 * (int32_t)rintf(c * 256.0f);
+    return (int32_t)rintf(c * 4096.0f);
+}
+
+// The Eq4 distance in units of 1/4096: the correctly rounded binary32 square
+// root of x = fl32(S) (0 or at least 1).  The hardware square root is within
+// one unit in the last place; the neighbours s - u and s + u of its result s
+// are tested against x with exact residuals: x - s (s - u) is a multiple of
+// u^2 and differs from x - (s - u/2)^2 by u^2/4, so its sign is that of x
+// against the lower midpoint, and likewise x - s (s + u) for the upper
+// midpoint (no midpoint is a root of a binary32 value).  For x = 0 both
+// tests fail and 0 is returned.
+__device__ __forceinline__ float sqrt_cr(float x)
+{
+    const float s = __builtin_amdgcn_sqrtf(x);
+    const float sd = __uint_as_float(__float_as_uint(s) - 1u);
+    const float su = __uint_as_float(__float_as_uint(s) + 1u);
+    const float rd = __builtin_fmaf(-sd, s, x);
+    const float ru = __builtin_fmaf(-su, s, x);
+    float r = rd <= 0.0f ? sd : s;
+    r = ru > 0.0f ? su : r;
+    return r;
+}
+
+// Search key of an x distance r = sqrt_cr(fl32(S)) and its column slot:
+// (bits(r) - 0x3F7FFFFF) << 5 | slot for r >= 1 (r <= sqrt(32 * 10240^2) <
+// 57927 keeps the difference below 2^27), slot for r = 0.  Keys order by
+// distance, then by slot.
+__device__ __forceinline__ uint32_t xkey(float r, uint32_t slot)
+{
+    return (__builtin_elementwise_sub_sat(__float_as_uint(r), 0x3F7FFFFFu) << 5) | slot;
+}
+
+// The distance of a search key, exact (0 for keys below 32).
+__device__ __forceinline__ float xkey_distance(uint32_t key)
+{
+    const uint32_t b = (key >> 5) + 0x3F7FFFFFu;
+    return key < 32u ? 0.0f : __uint_as_float(b);
+}
+
+// min of two binary64 values that are never NaN (one instruction; the
+// library's min also canonicalises its operands).
+__device__ __forceinline__ double min_f64(double a, double b)
+{
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
 }
 
 __device__ __forceinline__ int32_t pack2(int32_t lo, int32_t hi)

@@ -43,16 +43,9 @@ long long peak_cut(double theta)
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-// Eq8 on integer code sums D (distance x 4096): D / 4096 < tau  <=>
-// D < ceil(4096 tau).  Code sums stay below 2^18, so the saturated value
-// keeps every pixel.
-uint32_t tau_code(double tau)
-{
-    const double t = std::ceil(tau * 4096.0);
-    if (!(t > 0.0)) return 0u;
-    if (t >= 4294967295.0) return 0xffffffffu;
-    return (uint32_t)t;
-}
+// Eq8 on distance sums D in units of 1/4096: D / 4096 < tau  <=>  D < 4096 tau
+// (exact scaling; +inf keeps every pixel, tau <= 0 none).
+double tau4096(double tau) { return tau * 4096.0; }
 
 cpe_status decode_frame(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg, int32_t H, int32_t W,
                         float fg_threshold, double peak_threshold, double tau, cpe_centroid *centroids,
@@ -69,20 +62,10 @@ cpe_status decode_frame(cpe_decoder *h, hipStream_t stream, const void *emb, con
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess) return CPE_ERR_HIP;
     if (dev != h->device) return CPE_ERR_INVALID_ARG;
-    const FrameArgs fa{stream,    emb,           fg,     fg_threshold, peak_cut(peak_threshold),
-                       tau_code(tau), centroids, num_centroids, labels, score_map};
+    const FrameArgs fa{stream,       emb,       fg,            fg_threshold, peak_cut(peak_threshold),
+                       tau4096(tau), centroids, num_centroids, labels,       score_map};
     if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, fa) : launch_f32_hi(h, fa);
     return h->F <= 8 ? launch_f16_lo(h, fa) : launch_f16_hi(h, fa);
-}
-
-// IEEE binary16 bit pattern of an integer with |v| <= 1024 (exact).
-uint16_t half_of_small_int(int v)
-{
-    if (v == 0) return 0;
-    const uint16_t sign = v < 0 ? 0x8000u : 0u;
-    const int a = v < 0 ? -v : v;
-    const int e = 31 - __builtin_clz((unsigned)a);
-    return (uint16_t)(sign | ((e + 15) << 10) | ((a << (10 - e)) & 0x3ff));
 }
 
 // Distance at the centre of an m-bit bucket of fl32(S+1) (0 for S = 0).
@@ -184,24 +167,17 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     real_palette(bins_w, W, freq_x, h->palf_x);
     real_palette(bins_h, H, freq_y, h->palf_y);
 
-    // bucket tables: weight 2^15 e^-d (8-bit buckets), code 4096 d (9-bit
-    // buckets), d taken at the bucket centre of fl32(S+1)
+    // weight buckets: 2^15 e^-d, d taken at the centre of the 8-bit bucket
+    // of fl32(S+1)
     h->wt.resize(kWKeys);
-    h->ct.resize(kCKeys);
     for (int k = 0; k < kWKeys; k++) h->wt[k] = (uint16_t)std::rint(32768.0 * std::exp(-centre_distance(k, kWMant)));
-    for (int k = 0; k < kCKeys; k++) h->ct[k] = (uint16_t)std::rint(4096.0 * centre_distance(k, kCMant));
     // LDS order of the matrix-core kernels: bucket (e, t) at ((e + 31) & 31) << m | t,
     // so that (float bits >> (23 - m)) & (2^(m+5) - 1) indexes it directly
     std::vector<uint32_t> wt_pk(kWKeys);
-    std::vector<uint16_t> ct_pm(kCKeys);
     for (int k = 0; k < kWKeys; k++) {
         const int e = k >> kWMant, t = k & ((1 << kWMant) - 1);
         const int q = h->wt[k];
         wt_pk[(((e + 31) & 31) << kWMant) | t] = (uint32_t)f16_bits(q & 255) | ((uint32_t)f16_bits(q >> 8) << 16);
-    }
-    for (int k = 0; k < kCKeys; k++) {
-        const int e = k >> kCMant, t = k & ((1 << kCMant) - 1);
-        ct_pm[(((e + 31) & 31) << kCMant) | t] = h->ct[k];
     }
 
     auto pack = [&](int n, const std::vector<int16_t> &pal, std::vector<int32_t> &pk, std::vector<uint32_t> &n2) {
@@ -222,39 +198,50 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     pack(bins_w, h->pal_x, pkx, n2x);
     pack(bins_h, h->pal_y, pky, n2y);
 
-    // matrix-core operands: -2P = 128 hi + lo with lo in [-64, 63], zero-padded
-    // to 32 bins x 32 channels; |P|^2 + 1 per bin (1 for padded bins)
-    auto limbs = [&](int n, const std::vector<int16_t> &pal, const std::vector<uint32_t> &n2, std::vector<int8_t> &q,
-                     std::vector<uint32_t> &np1) {
-        q.assign(2 * 32 * 32, 0);
-        np1.assign(32, 1u);
-        if (n > kMfmaBins || twoF > 32) return;
-        for (int a = 0; a < n; a++) {
-            for (int c = 0; c < twoF; c++) {
-                const int m2 = -2 * (int)pal[(size_t)a * twoF + c];
+    // matrix-core operands: -2P = 128 hi + lo with lo in [-64, 63] (|hi| <= 64),
+    // as int8 MFMA operands [axis][kind][64 lanes][16 bytes]: lane l holds bin
+    // l & 31 and the K slots 16 g .. 16 g + 15 (g = l >> 5), whose channels are
+    // those the pixel operand of the same half holds (AxisOp in k_mfma.hpp):
+    // for 2F > 16 byte b is channel 8 g + b (b < 8) or 16 + 8 g + b - 8, kind 0
+    // = hi, kind 1 = lo; for 2F <= 16 bytes b and 8 + b both belong to channel
+    // 8 g + b, kinds (hi, 0), (lo, hi), (0, lo).  Padded bins and channels are
+    // 0, and |P|^2 + 1 per bin (1 for padded bins).
+    std::vector<int8_t> pop((size_t)2 * kPopKinds * 64 * 16, 0);
+    std::vector<uint32_t> np1x(32, 1u), np1y(32, 1u);
+    if (bins_w <= kMfmaBins && bins_h <= kMfmaBins) {
+        for (int ax = 0; ax < 2; ax++) {
+            const int n = ax ? bins_h : bins_w;
+            const std::vector<int16_t> &pal = ax ? h->pal_y : h->pal_x;
+            auto limb = [&](int bin, int c, int which) -> int {     // which 0: hi, 1: lo
+                if (bin >= n || c >= twoF) return 0;
+                const int m2 = -2 * (int)pal[(size_t)bin * twoF + c];
                 const int lo = ((m2 + 64) & 127) - 64;
-                const int hi = (m2 - lo) / 128;
-                q[a * 32 + c] = (int8_t)hi;
-                q[1024 + a * 32 + c] = (int8_t)lo;
-            }
-            np1[a] = n2[a] + 1u;
-        }
-    };
-    std::vector<int8_t> qx, qy;
-    std::vector<uint32_t> np1x, np1y;
-    limbs(bins_w, h->pal_x, n2x, qx, np1x);
-    limbs(bins_h, h->pal_y, n2y, qy, np1y);
-    // the same limbs as the per-lane fp16 MFMA operands (two K-steps of 16 channels)
-    std::vector<uint16_t> pop((size_t)2 * 2 * 2 * 64 * 8);
-    for (int ax = 0; ax < 2; ax++)
-        for (int limb = 0; limb < 2; limb++)
-            for (int j = 0; j < 2; j++)
-                for (int l = 0; l < 64; l++)
-                    for (int e = 0; e < 8; e++) {
-                        const std::vector<int8_t> &q = ax ? qy : qx;
-                        const int v = q[limb * 1024 + (l & 31) * 32 + 16 * j + 8 * (l >> 5) + e];
-                        pop[((((size_t)ax * 2 + limb) * 2 + j) * 64 + l) * 8 + e] = half_of_small_int(v);
+                return which ? lo : (m2 - lo) / 128;
+            };
+            for (int l = 0; l < 64; l++) {
+                const int bin = l & 31, g = l >> 5;
+                for (int b = 0; b < 16; b++) {
+                    int v[kPopKinds];
+                    if (twoF > 16) {
+                        const int c = b < 8 ? 8 * g + b : 16 + 8 * g + (b - 8);
+                        v[0] = limb(bin, c, 0);
+                        v[1] = limb(bin, c, 1);
+                        v[2] = 0;
+                    } else {
+                        const int c = 8 * g + (b & 7);
+                        v[0] = b < 8 ? limb(bin, c, 0) : 0;
+                        v[1] = b < 8 ? limb(bin, c, 1) : limb(bin, c, 0);
+                        v[2] = b < 8 ? 0 : limb(bin, c, 1);
                     }
+                    for (int k = 0; k < kPopKinds; k++)
+                        pop[(((size_t)ax * kPopKinds + k) * 64 + l) * 16 + b] = (int8_t)v[k];
+                }
+            }
+            std::vector<uint32_t> &np1 = ax ? np1y : np1x;
+            const std::vector<uint32_t> &n2 = ax ? n2y : n2x;
+            for (int bin = 0; bin < n; bin++) np1[bin] = n2[bin] + 1u;
+        }
+    }
 
     // one allocation: constants, replicated histograms, last histogram, peak list, counters
     size_t off = 0;
@@ -265,12 +252,11 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     };
     const size_t o_px = carve(pkx.size() * 4), o_py = carve(pky.size() * 4);
     const size_t o_nx = carve(n2x.size() * 4), o_ny = carve(n2y.size() * 4);
-    const size_t o_wt = carve(kWKeys * 2), o_ct = carve(kCKeys * 2);
+    const size_t o_wt = carve(kWKeys * 2);
     const size_t o_cx = carve(cx.size() * 4), o_cy = carve(cy.size() * 4);
-    const size_t o_qx = carve(qx.size()), o_qy = carve(qy.size());
     const size_t o_npx = carve(np1x.size() * 4), o_npy = carve(np1y.size() * 4);
-    const size_t o_pop = carve(pop.size() * 2);
-    const size_t o_wpk = carve(wt_pk.size() * 4), o_cpm = carve(ct_pm.size() * 2);
+    const size_t o_pop = carve(pop.size());
+    const size_t o_wpk = carve(wt_pk.size() * 4);
     const size_t o_hrep = carve((size_t)2 * kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
@@ -288,12 +274,11 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     };
     bool ok = up(o_px, pkx.data(), pkx.size() * 4) && up(o_py, pky.data(), pky.size() * 4) &&
               up(o_nx, n2x.data(), n2x.size() * 4) && up(o_ny, n2y.data(), n2y.size() * 4) &&
-              up(o_wt, h->wt.data(), kWKeys * 2) && up(o_ct, h->ct.data(), kCKeys * 2) &&
+              up(o_wt, h->wt.data(), kWKeys * 2) &&
               up(o_cx, cx.data(), cx.size() * 4) && up(o_cy, cy.data(), cy.size() * 4) &&
-              up(o_qx, qx.data(), qx.size()) && up(o_qy, qy.data(), qy.size()) &&
               up(o_npx, np1x.data(), np1x.size() * 4) && up(o_npy, np1y.data(), np1y.size() * 4) &&
-              up(o_pop, pop.data(), pop.size() * 2) &&
-              up(o_wpk, wt_pk.data(), wt_pk.size() * 4) && up(o_cpm, ct_pm.data(), ct_pm.size() * 2) &&
+              up(o_pop, pop.data(), pop.size()) &&
+              up(o_wpk, wt_pk.data(), wt_pk.size() * 4) &&
               hipMemset(d + o_hrep, 0, (size_t)2 * kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
               hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, (size_t)kMaxSlices * 4) == hipSuccess &&
@@ -308,16 +293,12 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->tb.n2_x = reinterpret_cast<const uint32_t *>(d + o_nx);
     h->tb.n2_y = reinterpret_cast<const uint32_t *>(d + o_ny);
     h->tb.wt = reinterpret_cast<const uint16_t *>(d + o_wt);
-    h->tb.ct = reinterpret_cast<const uint16_t *>(d + o_ct);
     h->tb.cx = reinterpret_cast<const float *>(d + o_cx);
     h->tb.cy = reinterpret_cast<const float *>(d + o_cy);
-    h->tb.qx = reinterpret_cast<const int8_t *>(d + o_qx);
-    h->tb.qy = reinterpret_cast<const int8_t *>(d + o_qy);
     h->tb.np1_x = reinterpret_cast<const uint32_t *>(d + o_npx);
     h->tb.np1_y = reinterpret_cast<const uint32_t *>(d + o_npy);
     h->tb.pop = reinterpret_cast<const uint32_t *>(d + o_pop);
     h->tb.wt_pk = reinterpret_cast<const uint32_t *>(d + o_wpk);
-    h->tb.ct_pm = reinterpret_cast<const uint16_t *>(d + o_cpm);
     h->hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
     h->hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
     h->peaks = reinterpret_cast<int32_t *>(d + o_peaks);
@@ -370,14 +351,12 @@ cpe_status cpe_decode_destroy(cpe_decoder *h)
     return e == hipSuccess ? CPE_OK : CPE_ERR_HIP;
 }
 
-cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *weights,
-                                 uint16_t *codes)
+cpe_status cpe_decode_get_tables(const cpe_decoder *h, int16_t *pal_x, int16_t *pal_y, uint16_t *weights)
 {
     if (!h) return CPE_ERR_INVALID_ARG;
     if (pal_x) std::memcpy(pal_x, h->pal_x.data(), h->pal_x.size() * sizeof(int16_t));
     if (pal_y) std::memcpy(pal_y, h->pal_y.data(), h->pal_y.size() * sizeof(int16_t));
     if (weights) std::memcpy(weights, h->wt.data(), h->wt.size() * sizeof(uint16_t));
-    if (codes) std::memcpy(codes, h->ct.data(), h->ct.size() * sizeof(uint16_t));
     return CPE_OK;
 }
 

@@ -14,7 +14,7 @@ struct cpe_decoder {
     cpe_dtype dtype;
     int device;
     std::vector<int16_t> pal_x, pal_y;   // host copies, [bins][2F]
-    std::vector<uint16_t> wt, ct;        // host copies of the bucket tables (bucket order)
+    std::vector<uint16_t> wt;            // host copy of the weight buckets (bucket order)
     unsigned char *dev;                  // single device allocation
     size_t dev_bytes;
     cpe::Tables tb;
@@ -43,7 +43,7 @@ struct FrameArgs {
     const void *emb, *fg;
     float fg_thr;
     long long cut;               // floor(peak_threshold * 2^30), saturated
-    uint32_t tau_code;           // a pixel is labelled iff its code sum < tau_code (Eq8)
+    double tau4096;              // a pixel is labelled iff its distance sum < 4096 tau (Eq8)
     cpe_centroid *cents;
     int32_t *num, *labels;
     float *score;

@@ -1,13 +1,15 @@
 // k_generic.hpp -- decoder kernels for any bin grid up to 128 x 128.
 //
 // One thread per foreground pixel computes the per-axis squared distances to
-// every palette entry with packed 16-bit dot products (Eq4/Eq10), turns them
-// into bucket weights and codes, and
-//   k_vote_generic    accumulates the soft votes (Eq6/Eq11) into a
-//                     register-tiled 64-bit histogram, flushed with global
-//                     atomics into one of the replicated histograms;
-//   k_assign_generic  assigns the pixel to the candidate with the smallest
-//                     code sum (Eq7), writes its label and score and counts it.
+// every palette entry with packed 16-bit dot products (Eq4/Eq10), and
+//   k_vote_generic    turns them into bucket weights and accumulates the soft
+//                     votes (Eq6/Eq11) into a register-tiled 64-bit
+//                     histogram, flushed with global atomics into one of the
+//                     replicated histograms;
+//   k_assign_generic  turns them into distances sqrt_cr(fl32(S)), assigns the
+//                     pixel to the candidate with the smallest exact distance
+//                     sum (Eq7, lowest index on ties), writes its label and
+//                     score and counts it.
 // Grids up to 32 x 32 bins use the matrix-core kernels of k_mfma.hpp instead.
 #pragma once
 
@@ -164,7 +166,7 @@ __global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb,
 template <typename T, int F>
 __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ emb, int32_t dstride, int32_t yoff,
                                                 const T *__restrict__ fg, int32_t npix,
-                                                float fg_thr, uint32_t tau_code, Tables tb, int32_t Bw, int32_t Bh,
+                                                float fg_thr, double tau4096, Tables tb, int32_t Bw, int32_t Bh,
                                                 const int32_t *__restrict__ peaks, const int32_t *__restrict__ kinfo,
                                                 cpe_centroid *__restrict__ cents, int32_t *__restrict__ labels,
                                                 float *__restrict__ score_map)
@@ -179,8 +181,7 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
     int32_t *s_list = reinterpret_cast<int32_t *>(s_ny + Bh);   // [TP]
     int32_t *s_n = s_list + TP;                                  // [4]
     int32_t *s_cnt = s_n + 4;                                    // [kCountCap]
-    int32_t *s_r = s_cnt + kCountCap;                            // [Bw + Bh][TP] codes
-    uint16_t *s_ct = reinterpret_cast<uint16_t *>(s_r + (Bw + Bh) * TP);   // [kCKeys]
+    float *s_r = reinterpret_cast<float *>(s_cnt + kCountCap);   // [Bw + Bh][TP] distances
 
     const int Kc = kinfo[0];
     const int ncnt = Kc < kCountCap ? Kc : kCountCap;
@@ -189,7 +190,6 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
     for (int i = tid; i < Bw; i += TP) s_nx[i] = tb.n2_x[i];
     for (int i = tid; i < Bh; i += TP) s_ny[i] = tb.n2_y[i];
     for (int i = tid; i < ncnt; i += TP) s_cnt[i] = 0;
-    for (int i = tid; i < kCKeys; i += TP) s_ct[i] = tb.ct[i];
 
     using L = PixelLayout<T, F>;
     for (int64_t tile = blockIdx.x; tile * TP < npix; tile += gridDim.x) {
@@ -217,23 +217,25 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
             for (int a = 0; a < Bw; a++)
-                s_r[a * TP + tid] = s_ct[dist_key<kCMant>(axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)))];
+                s_r[a * TP + tid] = sqrt_cr((float)axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)));
             for (int b = 0; b < Bh; b++)
-                s_r[(Bw + b) * TP + tid] = s_ct[dist_key<kCMant>(axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)))];
+                s_r[(Bw + b) * TP + tid] = sqrt_cr((float)axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)));
+            // Eq7: smallest exact sum (binary64 holds the sum of two binary32
+            // values exactly), lowest index on ties
             int best = 0;
             const int32_t pk0 = peaks[0];
-            int32_t bd = s_r[(pk0 & 0xffff) * TP + tid] + s_r[(Bw + (pk0 >> 16)) * TP + tid];
+            double bd = (double)s_r[(pk0 & 0xffff) * TP + tid] + (double)s_r[(Bw + (pk0 >> 16)) * TP + tid];
             for (int k = 1; k < Kc; k++) {
                 const int32_t pk = peaks[k];
-                const int32_t d = s_r[(pk & 0xffff) * TP + tid] + s_r[(Bw + (pk >> 16)) * TP + tid];
+                const double d = (double)s_r[(pk & 0xffff) * TP + tid] + (double)s_r[(Bw + (pk >> 16)) * TP + tid];
                 if (d < bd) {
                     bd = d;
                     best = k;
                 }
             }
-            if ((uint32_t)bd < tau_code) {     // Eq8 (tau_code = ceil(4096 tau))
+            if (bd < tau4096) {     // Eq8
                 labels[pp] = best + 1;
-                if (score_map) score_map[pp] = expf(-((float)bd * 0x1p-12f));
+                if (score_map) score_map[pp] = expf(-(float)(bd * 0x1p-12));
                 if (best < kCountCap)
                     atomicAdd(s_cnt + best, 1);
                 else

@@ -41,6 +41,49 @@
 // minimised over the peaks, which selects the smallest code sum and, on
 // ties, the lowest (row, column) -- slots keep the bins' order -- i.e. the
 // lowest centroid index.
+// k_mfma.hpp -- matrix-core decoder kernels for bin grids up to 32 x 32.
+//
+// Both passes stream the compact list of participating pixels written by
+// k_compact (or every pixel, when the frame has no foreground channel): the
+// list is cut into tiles of 32 consecutive entries, every workgroup gets a
+// contiguous run of tiles of the same length to within one, and its waves
+// take the run's tiles one at a time from a counter in LDS (so that they
+// finish together however the SIMDs favour older waves), always loading the
+// embedding rows of the next tile (and the list entries of the one after)
+// before computing the current one.  Every tile but the last is full.
+//
+// Per-axis distances (Eq4/Eq10).  The input X = rint(4096 v) (|X| <= 6144)
+// is split into int8 limbs X = 128 Xh + Xl (|Xh| <= 48, |Xl| <= 64) and the
+// palette into -2P = 128 hi + lo (|hi| <= 64, |lo| <= 64), so that
+//   S = |X|^2 + |P|^2 + 2^14 Xh.hi + 2^7 (Xh.lo + Xl.hi) + Xl.lo
+// with three dense [pixels x channels] x [channels x bins] contractions on
+// v_mfma_i32_32x32x32_i8 (exact int32 accumulation; the middle one takes two
+// instructions, or all three share one pixel operand when 2F <= 16, see
+// AxisOp); S < 2^32 follows modulo 2^32 from two shift-and-add instructions.
+// |X|^2 is three int8 dot products of the limbs.
+//
+// Pass 1, k_vote_mfma (recovery + soft voting, Eq5/Eq6/Eq11).  With pixels
+// as the MFMA rows, the distance result leaves in each lane one bin and 16
+// pixels -- exactly the operand layout of the vote contraction
+// H = Qx^T Qy over pixels, so the weights feed the second MFMA without any
+// data exchange between lanes.  A weight q <= 2^15 is split into fp16 limbs
+// q = 256 hi + lo; the four limb products accumulate in fp32 exactly as long
+// as at most 256 pixels are summed, after which they are added into a 64-bit
+// histogram in LDS.
+//
+// Pass 2, k_assign_mfma (assignment, Eq7, and label write-out).  Only the
+// candidate columns and rows are needed: they are numbered in ascending
+// order (slots), the MFMA rows are the slots' palette entries, each lane
+// holds one pixel and 16 slots, and distances are computed for the groups of
+// 8 slots that hold candidates: r = sqrtf(fl32(S)) correctly rounded, stored
+// in LDS as an x search key (distance bits and column slot, ordered by
+// distance then slot) or as the y distance itself.  The candidate search
+// walks batches of 4 columns of one row: the smallest x key of the batch
+// gives the row's best column, its distance plus the row's y distance is
+// summed exactly in binary64, and the row and column slots fill the low bits
+// of that sum (always zero there), so one binary64 minimum selects the
+// smallest distance sum and, on ties, the lowest (row, column) -- slots keep
+// the bins' order -- i.e. the lowest centroid index.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -49,51 +92,89 @@
 
 namespace cpe {
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kWpb2 = 12;            // waves per workgroup of the assignment kernel (3 per SIMD)
-constexpr int kPopBytes = 2 * 2 * 2 * 64 * 16;   // palette operands of both axes, limbs and K-steps
+constexpr int kPopBytes = 2 * kPopKinds * 64 * 16;   // palette operands of both axes
 
+// The int8 operand of one axis of one pixel, for the lane of half g = lane >> 5
+// of the MFMA, which holds the 16 K slots 16 g .. 16 g + 15.  The lane's
+// channels are c_b = 8 g + b and, for 2F > 16, 16 + 8 g + b (b = 0..7;
+// channels past 2F are zero).
+//   2F > 16: a[0] = Xh of the 16 channels, a[1] = Xl; with the palette
+//            operand kinds 0 = hi and 1 = lo (same channel order):
+//            Xh.hi, Xh.lo + Xl.hi, Xl.lo in four MFMAs;
+//   2F <= 16: a[0] = Xh of the 8 channels, then their Xl; with the kinds
+//            0 = (hi, 0), 1 = (lo, hi), 2 = (0, lo) the three products take
+//            one MFMA each.
 template <int F>
-struct AxisShape {
-    static constexpr int C = 2 * F;             // channels per axis
-    static constexpr int KS = (C + 15) / 16;    // MFMA K-steps of 16 channels
+struct AxisOp {
+    static constexpr bool kPacked = 2 * F <= 16;
+    static constexpr int N = kPacked ? 1 : 2;
+    i32x4 a[N];
 };
 
-// The fp32 value 1.5 * 2^23 (bit pattern 0x4B400000) onto which the limb
-// accumulators are summed.
-constexpr float kMagic = 12582912.0f;
-constexpr uint32_t kMagicBits = 0x4B400000u;
-
-// Round a pair of fp16 inputs to the 1/256 grid, clamped to [-1.5, 1.5]:
-// Xr = rint(256 v) as fp16, and accumulate Xr^2 (exact in fp32).  The
-// rounding is one fused multiply-add onto 1536: for |256 v| <= 512 the sum
-// lies in [1024, 2048], where fp16 spacing is 1, so it is rounded to the
-// nearest integer, ties to even (1536 is even); larger magnitudes (and
-// overflow to +-inf) leave that range and are clamped to 1536 +- 384 like
-// any value beyond 1.5.  A NaN clamps to 1536 - 384 (max returns the
-// non-NaN operand), i.e. to -1.5.
-__device__ __forceinline__ f16x2 fix_pair_f16(f16x2 v, float &n2)
+__device__ __forceinline__ i32x16 mfma8(i32x4 a, i32x4 b, i32x16 c)
 {
-    const f16x2 k256 = {(_Float16)256.0f, (_Float16)256.0f}, k1536 = {(_Float16)1536.0f, (_Float16)1536.0f};
-    const f16x2 lo = {(_Float16)1152.0f, (_Float16)1152.0f}, hi = {(_Float16)1920.0f, (_Float16)1920.0f};
-    f16x2 r = __builtin_elementwise_fma(v, k256, k1536);
-    r = __builtin_elementwise_max(r, lo);
-    r = __builtin_elementwise_min(r, hi);
-    r = r - k1536;
-    n2 = __builtin_amdgcn_fdot2(r, r, n2, false);
-    return r;
+    return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
 }
 
-// fp32 input: Xr = rint(256 clamp(v, -1.5, 1.5)) (a NaN clamps to -1.5, as
-// fmaxf returns the non-NaN operand), exact in fp16.
-__device__ __forceinline__ _Float16 fix_f32(float v)
+__device__ __forceinline__ f32x16 mfma16(f16x8 a, f16x8 b, f32x16 c)
 {
-    return (_Float16)rintf(fminf(fmaxf(v * 256.0f, -384.0f), 384.0f));
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// Row of the 32 x 32 MFMA result held by register r of a lane in group g.
+__device__ __forceinline__ constexpr int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+// int8 limbs of two channels: Xh = rint(32 c) and Xl = rint(128 (32 c - Xh)),
+// c = clamp(v, -1.5, 1.5), so that 128 Xh + Xl = rint(4096 c) (128 Xh is
+// even, so the ties agree).  In fp16: 32 c + 1536 lies in [1488, 1584], where
+// the spacing is 1, so the fused multiply-add rounds it to 1536 + Xh; 32 c -
+// Xh is exact (|.| <= 1/2) and 128 times it plus 1536 rounds to 1536 + Xl.
+// The low byte of each result's bit pattern 0x6600 + k is k as an int8.  A
+// NaN clamps to -1.5 (max returns the non-NaN operand).
+struct LimbPair {
+    uint32_t h, l;     // two fp16 bit patterns each
+};
+__device__ __forceinline__ LimbPair limbs_f16(f16x2 v)
+{
+    const f16x2 lo = {(_Float16)-1.5f, (_Float16)-1.5f}, hi = {(_Float16)1.5f, (_Float16)1.5f};
+    const f16x2 k32 = {(_Float16)32.0f, (_Float16)32.0f}, k128 = {(_Float16)128.0f, (_Float16)128.0f};
+    const f16x2 m = {(_Float16)1536.0f, (_Float16)1536.0f};
+    f16x2 c = __builtin_elementwise_max(v, lo);
+    c = __builtin_elementwise_min(c, hi);
+    const f16x2 h = __builtin_elementwise_fma(c, k32, m);
+    const f16x2 hv = h - m;
+    const f16x2 d = __builtin_elementwise_fma(c, k32, -hv);
+    const f16x2 l = __builtin_elementwise_fma(d, k128, m);
+    return {__builtin_bit_cast(uint32_t, h), __builtin_bit_cast(uint32_t, l)};
+}
+
+// The same in fp32 (exact: |32 c| < 2^22 around 1.5 * 2^23, whose spacing is
+// 1); the low byte of the bit pattern 0x4B400000 + k is k as an int8.
+__device__ __forceinline__ void limbs_f32(float v, uint32_t &h, uint32_t &l)
+{
+    constexpr float kM = 12582912.0f;
+    const float c = fminf(fmaxf(v, -1.5f), 1.5f);
+    const float hf = __builtin_fmaf(c, 32.0f, kM);
+    const float hv = hf - kM;
+    const float d = __builtin_fmaf(c, 32.0f, -hv);
+    const float lf = __builtin_fmaf(d, 128.0f, kM);
+    h = __float_as_uint(hf);
+    l = __float_as_uint(lf);
+}
+
+// Low bytes of the two halves of w0 (bytes 0, 1 of the result) and of w1
+// (bytes 2, 3).
+__device__ __forceinline__ uint32_t low_bytes(uint32_t w1, uint32_t w0)
+{
+    return __builtin_amdgcn_perm(w1, w0, 0x06040200u);
 }
 
 // Raw input words of one lane's operand slices: for each axis and K-step j
@@ -102,7 +183,7 @@ __device__ __forceinline__ _Float16 fix_f32(float v)
 template <typename T, int F>
 struct RawSlices {
     static constexpr int C = 2 * F;
-    static constexpr int KS = AxisShape<F>::KS;
+    static constexpr int KS = (C + 15) / 16;
     static constexpr bool kH = sizeof(T) == 2;
     // 16-byte aligned vector slices: whole K-steps, or a single 8-channel
     // slice per axis (F = 4) that the lanes of half 0 load
@@ -146,115 +227,100 @@ struct RawSlices {
             }
     }
 
-    // Rounded operands of one axis and its partial |Xr|^2.
-    __device__ __forceinline__ void convert(int ax, f16x8 (&X)[KS], float &n2) const
+    // int8 operand of one axis and this lane's part of |X|^2 over its
+    // channels (added to n2).
+    __device__ __forceinline__ void convert(int ax, AxisOp<F> &op, int &n2) const
     {
+        uint32_t hb[KS][2], lb[KS][2];      // packed limb bytes, 4 channels per word
 #pragma unroll
         for (int j = 0; j < KS; j++) {
             if constexpr (kH && kVec) {
-                u32x4 res;
+                LimbPair p[4];
 #pragma unroll
-                for (int q = 0; q < 4; q++) {
-                    const uint32_t word = w[ax][j][q];
-                    f16x2 v;
-                    __builtin_memcpy(&v, &word, 4);
-                    const f16x2 r = fix_pair_f16(v, n2);
-                    uint32_t o;
-                    __builtin_memcpy(&o, &r, 4);
-                    res[q] = o;
+                for (int q = 0; q < 4; q++) p[q] = limbs_f16(__builtin_bit_cast(f16x2, w[ax][j][q]));
+#pragma unroll
+                for (int q = 0; q < 2; q++) {
+                    hb[j][q] = low_bytes(p[2 * q + 1].h, p[2 * q].h);
+                    lb[j][q] = low_bytes(p[2 * q + 1].l, p[2 * q].l);
                 }
-                X[j] = __builtin_bit_cast(f16x8, res);
             } else {
+                uint32_t h[8], l[8];
 #pragma unroll
-                for (int q = 0; q < 4; q++) {
-                    const f16x2 r = {fix_f32(__uint_as_float(w[ax][j][2 * q])),
-                                     fix_f32(__uint_as_float(w[ax][j][2 * q + 1]))};
-                    X[j][2 * q] = r[0];
-                    X[j][2 * q + 1] = r[1];
-                    n2 = __builtin_amdgcn_fdot2(r, r, n2, false);
+                for (int s = 0; s < 8; s++) limbs_f32(__uint_as_float(w[ax][j][s]), h[s], l[s]);
+#pragma unroll
+                for (int q = 0; q < 2; q++) {
+                    hb[j][q] = low_bytes(__builtin_amdgcn_perm(h[4 * q + 3], h[4 * q + 2], 0x05040100u),
+                                         __builtin_amdgcn_perm(h[4 * q + 1], h[4 * q], 0x05040100u));
+                    lb[j][q] = low_bytes(__builtin_amdgcn_perm(l[4 * q + 3], l[4 * q + 2], 0x05040100u),
+                                         __builtin_amdgcn_perm(l[4 * q + 1], l[4 * q], 0x05040100u));
                 }
             }
         }
-    }
-};
-
-// Palette operand of lane `lane` (bin lane & 31, channels 16 j + 8 (lane >> 5)
-// + 0..7) for axis ax (0 = x, 1 = y), limb (0 = hi, 1 = lo) and K-step j.
-__device__ __forceinline__ f16x8 palette_operand(const uint32_t *__restrict__ pop, int ax, int limb, int j, int lane)
-{
-    const u32x4 w = *reinterpret_cast<const u32x4 *>(pop + ((((ax * 2 + limb) * 2 + j) * 64 + lane) * 4));
-    return __builtin_bit_cast(f16x8, w);
-}
-
-// Row of the 32 x 32 MFMA result held by register r of a lane in group g.
-__device__ __forceinline__ constexpr int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
-
-__device__ __forceinline__ f32x16 mfma16(f16x8 a, f16x8 b, f32x16 c)
-{
-    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
-}
-
-// Xr.hi and Xr.lo of one axis, accumulated onto the starting values ah, al
-// (kMagic plus the pixel's part, see below).
-// PIX_ROWS: pixels are the MFMA rows (pass 1) or its columns (pass 2).
-template <int KS, bool PIX_ROWS>
-__device__ __forceinline__ void axis_dot(const f16x8 (&X)[KS], const f16x8 (&ph)[KS], const f16x8 (&pl)[KS],
-                                         f32x16 &ah, f32x16 &al)
-{
+        int hh = 0, hl = 0, ll = 0;
 #pragma unroll
-    for (int j = 0; j < KS; j++) {
-        if constexpr (PIX_ROWS) {
-            ah = mfma16(X[j], ph[j], ah);
-            al = mfma16(X[j], pl[j], al);
+        for (int j = 0; j < KS; j++)
+#pragma unroll
+            for (int q = 0; q < 2; q++) {
+                hh = __builtin_amdgcn_sdot4((int)hb[j][q], (int)hb[j][q], hh, false);
+                hl = __builtin_amdgcn_sdot4((int)hb[j][q], (int)lb[j][q], hl, false);
+                ll = __builtin_amdgcn_sdot4((int)lb[j][q], (int)lb[j][q], ll, false);
+            }
+        n2 += (hh << 14) + (hl << 8) + ll;
+        if constexpr (AxisOp<F>::kPacked) {
+            op.a[0] = i32x4{(int)hb[0][0], (int)hb[0][1], (int)lb[0][0], (int)lb[0][1]};
         } else {
-            ah = mfma16(ph[j], X[j], ah);
-            al = mfma16(pl[j], X[j], al);
+            op.a[0] = i32x4{(int)hb[0][0], (int)hb[0][1], (int)hb[1][0], (int)hb[1][1]};
+            op.a[1] = i32x4{(int)lb[0][0], (int)lb[0][1], (int)lb[1][0], (int)lb[1][1]};
         }
     }
-}
-
-// S + 1 = 2048 A + 16 L + 256 |Xr|^2 + |P|^2 + 1 with A = Xr.hi and L =
-// Xr.lo.  The pixel's part 256 |Xr|^2 = 2048 (|Xr|^2 >> 3) + 16 (16 (|Xr|^2
-// & 7)) starts the two accumulators: ah = kMagic + (|Xr|^2 >> 3) + A and
-// al = kMagic + 16 (|Xr|^2 & 7) + L, both integers within 2^22 of kMagic,
-// so exact in fp32 and bits(ah) = 0x4B400000 + their offset.  Then
-// S + 1 = 2048 bits(ah) + 16 bits(al) + c (mod 2^32) with the bin's
-// constant c = |P|^2 + 1 - 2064 * 0x4B400000, and S + 1 < 2^32.
-struct PixelInit {
-    uint32_t a, l;    // bit patterns of the starting values of ah and al
 };
-__device__ __forceinline__ PixelInit pixel_init(float n2)
-{
-    const uint32_t u = (uint32_t)n2;    // |Xr|^2 <= 32 * 384^2, exact in fp32
-    return {kMagicBits + (u >> 3), kMagicBits + ((u & 7u) << 4)};
-}
-__device__ __forceinline__ uint32_t bin_const(uint32_t np1) { return np1 - 2064u * kMagicBits; }
 
-// Bits of fl32(S + 1) from the two accumulators and the remaining constant
-// (the bin's constant, plus 256 |Xr|^2 when both accumulators start at
-// kMagic), as
-// two shift-and-add instructions: the empty asm makes the first sum opaque,
-// which keeps the compiler from forming two shifts and a three-way add.
-// (The instructions themselves stay compiler-generated: the accumulators
-// are MFMA results, and only the compiler inserts the wait states a read of
-// them needs.)
-__device__ __forceinline__ uint32_t s1_bits(float ah, float al, uint32_t c)
+// Palette operand of kind k for axis ax of lane `lane` (bin lane & 31, K
+// slots 16 (lane >> 5) .. + 15).
+__device__ __forceinline__ i32x4 palette_operand(const uint32_t *__restrict__ pop, int ax, int k, int lane)
 {
-    uint32_t t = (__float_as_uint(al) << 4) + c;
-    asm("" : "+v"(t));
-    return __float_as_uint((float)((__float_as_uint(ah) << 11) + t));
+    return *reinterpret_cast<const i32x4 *>(pop + (((ax * kPopKinds + k) * 64 + lane) * 4));
 }
 
-// Starting values of one accumulator for the 16 pixels (rows acc_row(r, g))
-// of a lane in group g, from a per-wave LDS array indexed by pixel.
-__device__ __forceinline__ f32x16 row_init(const uint32_t *a, int g)
+// The three limb products of one axis: hh = Xh.hi, mid = Xh.lo + Xl.hi and
+// ll = ll0 + Xl.lo (ll0: the starting values).  PIX_ROWS: pixels are the
+// MFMA rows (pass 1) or its columns (pass 2).
+template <int F, bool PIX_ROWS>
+__device__ __forceinline__ void axis_products(const AxisOp<F> &X, const i32x4 (&P)[kPopKinds], i32x16 ll0,
+                                              i32x16 &hh, i32x16 &mid, i32x16 &ll)
 {
-    f32x16 v;
+    const i32x16 z = {};
+    auto mm = [](i32x4 px, i32x4 pal, i32x16 c) { return PIX_ROWS ? mfma8(px, pal, c) : mfma8(pal, px, c); };
+    if constexpr (AxisOp<F>::kPacked) {
+        hh = mm(X.a[0], P[0], z);
+        mid = mm(X.a[0], P[1], z);
+        ll = mm(X.a[0], P[2], ll0);
+    } else {
+        hh = mm(X.a[0], P[0], z);
+        mid = mm(X.a[0], P[1], z);
+        mid = mm(X.a[1], P[0], mid);
+        ll = mm(X.a[1], P[1], ll0);
+    }
+}
+
+// 2^14 hh + 2^7 mid + ll + c (mod 2^32) as two shift-and-add instructions
+// and one add.
+__device__ __forceinline__ uint32_t assemble(int hh, int mid, int ll, uint32_t c)
+{
+    const uint32_t t = ((uint32_t)hh << 7) + (uint32_t)mid;
+    return (t << 7) + (uint32_t)ll + c;
+}
+
+// Starting values of one accumulator for the 16 rows acc_row(r, g) of a lane
+// in group g, from an LDS array indexed by row.
+__device__ __forceinline__ i32x16 row_init(const uint32_t *a, int g)
+{
+    i32x16 v;
 #pragma unroll
     for (int r4 = 0; r4 < 4; r4++) {
         const u32x4 w = *reinterpret_cast<const u32x4 *>(a + 8 * r4 + 4 * g);
 #pragma unroll
-        for (int i = 0; i < 4; i++) v[4 * r4 + i] = __uint_as_float(w[i]);
+        for (int i = 0; i < 4; i++) v[4 * r4 + i] = (int)w[i];
     }
     return v;
 }
@@ -286,11 +352,10 @@ __device__ __forceinline__ int take_tile(int *next, int lane, int first, int wav
 constexpr int kHStride = kMfmaBins + 1;
 
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
-// the palette operands, and per wave the accumulator starting values of one
-// tile's pixels.
+// the palette operands, and per wave |X|^2 of one tile's pixels per axis.
 constexpr size_t kVoteLds(int wpb)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 128 * 4 + (kMaxSlices + 1) * 4 +
+    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
            16;
 }
 
@@ -317,15 +382,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     int32_t Bh, unsigned long long *__restrict__ hrep,
     cpe_centroid *__restrict__ cents, int32_t cap)
 {
-    constexpr int KS = AxisShape<F>::KS;
     constexpr int kWpb = kVoteWpb<T, F>;
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32][kHStride], b * kHStride + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kHStride);      // palette operands
-    uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][4][32]
-    int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 128);                       // [kMaxSlices + 1]
+    uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][2][32]
+    int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 64);                        // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -359,10 +423,9 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
     int t0, tend;
     block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
-    const uint32_t cbx = bin_const(np1x), cby = bin_const(np1y);
 
-    // this wave's starting values: [0] x ah, [1] x al, [2] y ah, [3] y al, by pixel
-    uint32_t *ini = s_ini + wv * 128;
+    // this wave's |X|^2 per axis: [0] x, [1] y, by pixel
+    uint32_t *ini = s_ini + wv * 64;
     f32x16 acc2 = {}, acc1 = {}, acc0 = {};
     int ntile = 0;
 
@@ -381,52 +444,47 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // Packed weight limbs of the 16 (pixel, bin) results of one axis; cb is
-    // the bin's constant (bin_const).
-    auto weights = [&](const f32x16 &ah, const f32x16 &al, uint32_t cb, uint32_t (&e)[16]) {
+    // Packed weight limbs of the 16 (pixel, bin) results of one axis: the
+    // accumulators start at the pixels' |X|^2, and cb = |P|^2 + 1 of this
+    // lane's bin completes S + 1, whose binary32 bits give the bucket.
+    auto weights = [&](const i32x16 &hh, const i32x16 &mid, const i32x16 &ll, uint32_t cb, uint32_t (&e)[16]) {
 #pragma unroll
-        for (int r = 0; r < 16; r++) e[r] = s_wt[(s1_bits(ah[r], al[r], cb) >> 15) & (kWKeys - 1)];
+        for (int r = 0; r < 16; r++) {
+            const uint32_t s1 = assemble(hh[r], mid[r], ll[r], cb);
+            e[r] = s_wt[(__float_as_uint((float)s1) >> 15) & (kWKeys - 1)];
+        }
     };
 
     // One tile of up to 32 pixels (queue slot m = lane & 31) from prefetched
     // input; `next` reuses the input registers once they are converted.
     auto tile = [&](RawSlices<T, F> &raw, int nvalid, auto next) {
-        float n2x = 0.0f, n2y = 0.0f;
-        f16x8 X[KS], Y[KS];
+        int n2x = 0, n2y = 0;
+        AxisOp<F> X, Y;
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
         next();
         n2x += __shfl_xor(n2x, 32);
         n2y += __shfl_xor(n2y, 32);
         if (g == 0) {
-            const PixelInit ix = pixel_init(n2x), iy = pixel_init(n2y);
-            ini[ln] = ix.a;
-            ini[32 + ln] = ix.l;
-            ini[64 + ln] = iy.a;
-            ini[96 + ln] = iy.l;
+            ini[ln] = (uint32_t)n2x;
+            ini[32 + ln] = (uint32_t)n2y;
         }
         uint32_t ex[16], ey[16];
         {
-            f16x8 ph[KS], pl[KS];
+            i32x4 P[kPopKinds];
 #pragma unroll
-            for (int j = 0; j < KS; j++) {
-                ph[j] = palette_operand(s_pop, 0, 0, j, lane);
-                pl[j] = palette_operand(s_pop, 0, 1, j, lane);
-            }
-            f32x16 ah = row_init(ini, g), al = row_init(ini + 32, g);
-            axis_dot<KS, true>(X, ph, pl, ah, al);
-            weights(ah, al, cbx, ex);
+            for (int k = 0; k < kPopKinds; k++) P[k] = palette_operand(s_pop, 0, k, lane);
+            i32x16 hh, mid, ll;
+            axis_products<F, true>(X, P, row_init(ini, g), hh, mid, ll);
+            weights(hh, mid, ll, np1x, ex);
         }
         {
-            f16x8 ph[KS], pl[KS];
+            i32x4 P[kPopKinds];
 #pragma unroll
-            for (int j = 0; j < KS; j++) {
-                ph[j] = palette_operand(s_pop, 1, 0, j, lane);
-                pl[j] = palette_operand(s_pop, 1, 1, j, lane);
-            }
-            f32x16 ah = row_init(ini + 64, g), al = row_init(ini + 96, g);
-            axis_dot<KS, true>(Y, ph, pl, ah, al);
-            weights(ah, al, cby, ey);
+            for (int k = 0; k < kPopKinds; k++) P[k] = palette_operand(s_pop, 1, k, lane);
+            i32x16 hh, mid, ll;
+            axis_products<F, true>(Y, P, row_init(ini + 32, g), hh, mid, ll);
+            weights(hh, mid, ll, np1y, ey);
         }
         if (nvalid < 32) {        // pixels past the end of the list vote nothing
             // (kept a real branch: only the last tile of a round is partial)
@@ -503,17 +561,17 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // ---------------------------------------------------------------------------
 // Pass 2: assignment + label write-out
 // ---------------------------------------------------------------------------
-// LDS bytes of k_assign_mfma: code table, palette operands, bin constants,
+// LDS bytes of k_assign_mfma: palette operands, |P|^2 by bin and by slot,
 // candidate batches, bin -> centroid table, counts, per wave x keys and y
-// keys [32 bins][kKeyStride] (u32), then the peak-extraction state.
-constexpr size_t kAssignLdsCore = (size_t)kCKeys * 2 + kPopBytes + 4 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
+// distances [32 slots][kKeyStride] (u32), then the peak-extraction state.
+constexpr size_t kAssignLdsCore = (size_t)kPopBytes + 4 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
                                   kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
                                   (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
                                   (kMaxSlices + 1) * 4 + 16;
-// then, 16-byte aligned, per wave the 32 search results of a tile, and the
-// summed vote histogram (32 x 32 slots)
+// then, 16-byte aligned, per wave the 32 search results of a tile (binary64
+// keys), and the summed vote histogram (32 x 32 slots)
 constexpr size_t kBestOff = (kAssignLdsCore + 15) & ~(size_t)15;
-constexpr size_t kSumOff = kBestOff + (size_t)kWpb2 * 32 * 4;
+constexpr size_t kSumOff = kBestOff + (size_t)kWpb2 * 32 * 8;
 constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
@@ -522,36 +580,30 @@ constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 // summed histogram `hlast`, and the grid clears `hzero`, the histograms the
 // next frame's vote launch accumulates into.
 //
-// Then, per tile of 32 pixels, the distance codes of both axes for the
-// candidate slots (palette entries of the slots' bins as the MFMA rows, so
-// that each lane holds one pixel and 16 slots) go to LDS as search keys:
-// x key (c_x << 16) | column slot and y key (c_y << 16) | 128 row slot, laid
-// out [slot][kKeyStride] so that lane m reads pixel m's key of any slot at a
-// fixed stride.  The low halves are written once; per tile only the codes
-// are stored, as 16-bit writes.  The candidate search walks the batches of 4
-// columns of one row (see the search below).  The sum of an x key and a y
-// key is ((c_x + c_y) << 16) | (128 row slot + column slot), taken with
-// unsigned saturation: codes are below 2^16 but a sum of two may not be.
-// The minimum is exact unless every candidate saturates (all code sums of
-// the pixel at least 2^16); such a pixel is searched again in 64 bits.
+// Then, per tile of 32 pixels, the distances of both axes for the candidate
+// slots (palette entries of the slots' bins as the MFMA rows, so that each
+// lane holds one pixel and 16 slots) go to LDS, laid out [slot][kKeyStride]
+// so that lane m finds pixel m's value of any slot at a fixed stride: x keys
+// (xkey: distance bits and column slot) and y distances (binary32 bits).
+// The candidate search walks the batches of 4 columns of one row (see the
+// search below).  A pixel is labelled iff its distance sum D (in units of
+// 1/4096) is below tau4096 = 4096 tau (Eq8; +inf: every pixel).
 template <typename T, int F>
 __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb2 / 4))) void k_assign_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
-    const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, uint32_t tau_code, Tables tb,
+    const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, double tau4096, Tables tb,
     const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hzero,
     unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
     cpe_centroid *__restrict__ cents, int32_t *__restrict__ num, int32_t *__restrict__ labels,
     float *__restrict__ score_map)
 {
-    constexpr int KS = AxisShape<F>::KS;
     constexpr int kThreads = kWpb2 * 64;
     static_assert(kThreads >= kPeakThreads, "the peak prologue takes two histogram slots per thread");
     static_assert(kAssignLds <= 160 * 1024, "LDS of one compute unit");
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kAssignLds];
-    uint16_t *s_ct = reinterpret_cast<uint16_t *>(smem);                            // [kCKeys]
-    uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_ct + kCKeys);                  // palette operands
-    uint32_t *s_cb = s_pop + kPopBytes / 4;                                          // [2][32] bin_const by bin
+    uint32_t *s_pop = reinterpret_cast<uint32_t *>(smem);                            // palette operands
+    uint32_t *s_cb = s_pop + kPopBytes / 4;                                          // [2][32] |P|^2 by bin
     uint32_t *s_cbs = s_cb + 2 * kMfmaBins;                                           // [2][32] by slot
     u32x4 *s_bo = reinterpret_cast<u32x4 *>(s_cbs + 2 * kMfmaBins);                // [kMaxBatchLds]
     uint32_t *s_bh = reinterpret_cast<uint32_t *>(s_bo + kMaxBatchLds);             // [kMaxBatchLds]
@@ -561,8 +613,8 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * kKeyStride);
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
-    uint32_t *s_best = reinterpret_cast<uint32_t *>(smem + kBestOff);                 // [kWpb2][32]
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem + kSumOff);  // [32 * 32] summed votes
+    unsigned long long *s_best = reinterpret_cast<unsigned long long *>(smem + kBestOff);   // [kWpb2][32]
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem + kSumOff);       // [32 * 32] summed votes
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -570,41 +622,18 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
 
     PeakLoad pld;                                   // issued before the table staging
     peaks_lds_load(hcur, Bw, Bh, pld);
-    // This wave's search keys, [bin][kKeyStride] per axis: x key of bin a,
-    // pixel m at kx[a * kKeyStride + m], y key of bin b at ky[...]; their
-    // low halves (a for x keys, 128 b for y keys) are written here, while
-    // the loads are in flight, and the codes fill the high halves per tile.
+    // This wave's search arrays, [slot][kKeyStride] per axis: x key of column
+    // slot j, pixel m at kx[j * kKeyStride + m], y distance of row slot j at
+    // ky[...].
     uint32_t *kx = s_keys + wv * 2 * kMfmaBins * kKeyStride;
     uint32_t *ky = kx + kMfmaBins * kKeyStride;
-    {
-        constexpr int kVecPerRow = kKeyStride / 4;
-#pragma unroll
-        for (int i = lane; i < 2 * kMfmaBins * kVecPerRow; i += 64) {
-            const int row = i / kVecPerRow;          // a power-of-two division: a shift
-            const uint32_t v = row < kMfmaBins ? (uint32_t)row : 128u * (uint32_t)(row - kMfmaBins);
-            const u32x4 v4 = {v, v, v, v};
-            reinterpret_cast<u32x4 *>(kx)[i] = v4;
-        }
-    }
     SliceLoad sl;
     if (list) slice_load(counts, nslices, sl);
-    {
-        constexpr int kN = kCKeys / 8, kPer = (kN + kThreads - 1) / kThreads;
-        u32x4 w[kPer];
-#pragma unroll
-        for (int k = 0; k < kPer; k++) {
-            const int i = k * kThreads + tid;
-            w[k] = reinterpret_cast<const u32x4 *>(tb.ct_pm)[i < kN ? i : 0];
-        }
-#pragma unroll
-        for (int k = 0; k < kPer; k++) {
-            const int i = k * kThreads + tid;
-            if (i < kN) reinterpret_cast<u32x4 *>(s_ct)[i] = w[k];
-        }
-        for (int i = tid; i < kPopBytes / 16; i += kThreads)
-            reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
-        if (tid < 2 * kMfmaBins)
-            s_cb[tid] = bin_const(tid < kMfmaBins ? tb.np1_x[tid] : tb.np1_y[tid - kMfmaBins]);
+    for (int i = tid; i < kPopBytes / 16; i += kThreads)
+        reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
+    if (tid < 2 * kMfmaBins) {
+        const int bin = tid & (kMfmaBins - 1);
+        s_cb[tid] = tid < kMfmaBins ? (bin < Bw ? tb.n2_x[bin] : 0u) : (bin < Bh ? tb.n2_y[bin] : 0u);
     }
     for (int i = tid; i < kMfmaBins * kMfmaBins; i += kThreads) s_cnt[i] = 0;
     if (tid == 0) *s_next = 0;
@@ -656,55 +685,44 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     }
     const int nbat = min(pl.nbat, kMaxBatchLds);    // a multiple of kBatchPad
 
-
     // The MFMA rows are the candidate slots: the palette operands of slot j's
-    // bin, gathered once and kept in registers for the whole run; codes are
-    // computed only for the groups of 8 slots that hold candidates.
+    // bin, gathered once and kept in registers for the whole run; distances
+    // are computed only for the groups of 8 slots that hold candidates.
     const int nslot[2] = {__builtin_amdgcn_readfirstlane(pl.ncol), __builtin_amdgcn_readfirstlane(pl.nrow)};
-    f16x8 pop_h[2][KS], pop_l[2][KS];
+    i32x4 pop[2][kPopKinds];
 #pragma unroll
     for (int ax = 0; ax < 2; ax++) {
         const int bin = ax ? pl.rowbin[ln] : pl.colbin[ln];
 #pragma unroll
-        for (int j = 0; j < KS; j++) {
-            pop_h[ax][j] = palette_operand(s_pop, ax, 0, j, g * 32 + bin);
-            pop_l[ax][j] = palette_operand(s_pop, ax, 1, j, g * 32 + bin);
-        }
+        for (int k = 0; k < kPopKinds; k++) pop[ax][k] = palette_operand(s_pop, ax, k, g * 32 + bin);
     }
 
-    // Codes of one tile into the keys' high halves (pixel m = lane & 31; this
-    // lane's 16 bins acc_row(r, g) of each axis); `next` reuses the input
-    // registers once they are converted.
+    // Distances of one tile (pixel m = lane & 31; this lane's 16 slots
+    // acc_row(r, g) of each axis); `next` reuses the input registers once
+    // they are converted.  The accumulators of the Xl.lo products start at
+    // the slots' |P|^2; the pixel's |X|^2 completes S.
     auto codes = [&](RawSlices<T, F> &raw, auto next) {
-        float n2x = 0.0f, n2y = 0.0f;
-        f16x8 X[KS], Y[KS];
+        int n2x = 0, n2y = 0;
+        AxisOp<F> X, Y;
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
         next();
-        // the pixel's part of the constant: 256 |Xr|^2, the accumulators
-        // starting at kMagic (one starting value shared by all four)
-        const uint32_t npx = (uint32_t)(n2x + __shfl_xor(n2x, 32)) << 8;
-        const uint32_t npy = (uint32_t)(n2y + __shfl_xor(n2y, 32)) << 8;
+        const uint32_t npx = (uint32_t)(n2x + __shfl_xor(n2x, 32));
+        const uint32_t npy = (uint32_t)(n2y + __shfl_xor(n2y, 32));
 #pragma unroll
         for (int ax = 0; ax < 2; ax++) {
-            f32x16 ah, al;
-#pragma unroll
-            for (int r = 0; r < 16; r++) {
-                ah[r] = kMagic;
-                al[r] = kMagic;
-            }
-            axis_dot<KS, false>(ax ? Y : X, pop_h[ax], pop_l[ax], ah, al);
+            i32x16 hh, mid, ll;
+            axis_products<F, false>(ax ? Y : X, pop[ax], row_init(s_cbs + ax * kMfmaBins, g), hh, mid, ll);
             const uint32_t np = ax ? npy : npx;
-            // high half of key (slot acc_row(r, g), pixel ln)
-            uint16_t *dst = reinterpret_cast<uint16_t *>((ax ? ky : kx) + 4 * g * kKeyStride + ln) + 1;
+            uint32_t *dst = (ax ? ky : kx) + 4 * g * kKeyStride + ln;
 #pragma unroll
             for (int r4 = 0; r4 < 4; r4++) {
                 if (8 * r4 >= nslot[ax]) break;      // wave-uniform: no candidate in slots 8 r4 ..
-                const u32x4 cb = *reinterpret_cast<const u32x4 *>(s_cbs + ax * kMfmaBins + 8 * r4 + 4 * g);
 #pragma unroll
                 for (int i = 0; i < 4; i++) {
                     const int r = 4 * r4 + i;
-                    dst[2 * kKeyStride * (8 * r4 + i)] = s_ct[(s1_bits(ah[r], al[r], np + cb[i]) >> 14) & (kCKeys - 1)];
+                    const float d = sqrt_cr((float)assemble(hh[r], mid[r], ll[r], np));
+                    dst[kKeyStride * (8 * r4 + i)] = ax ? __float_as_uint(d) : xkey(d, (uint32_t)acc_row(r, g));
                 }
             }
         }
@@ -713,63 +731,58 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     // Candidate search.  Lane l serves the four pixels 4 q .. 4 q + 3
     // (q = l & 7) for the batches j, j + 8, ... (j = l >> 3): one 16-byte
     // read fetches a column's keys of its four pixels, so each address
-    // computation and each read serve four pixels.  The eight lanes of a
-    // pixel quad then combine their minima, and lane m takes pixel m's
+    // computation and each read serve four pixels.  Per batch and pixel the
+    // smallest of the 4 x keys is the row's best column among them; its
+    // distance plus the row's y distance, summed exactly in binary64, has
+    // at least 12 zero bits at the bottom of its mantissa (both distances are
+    // 0 or binary32 values of at least 1, so the sum is a multiple of 2^-23
+    // below 2^17), which take 32 row slot + column slot.  The eight lanes of
+    // a pixel quad then combine their minima, and lane m takes pixel m's
     // result through LDS; lanes of half 0 write the labels of valid pixels.
-    uint32_t *best_w = s_best + wv * 32;
+    unsigned long long *best_w = s_best + wv * 32;
     auto search = [&](int pix, int nvalid) {
         __builtin_amdgcn_wave_barrier();
         const int q = lane & 7, j0 = lane >> 3;
         const unsigned char *kxq = reinterpret_cast<const unsigned char *>(kx + 4 * q);
         const unsigned char *kyq = reinterpret_cast<const unsigned char *>(ky + 4 * q);
-        uint32_t b4[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+        double b4[4] = {__builtin_inf(), __builtin_inf(), __builtin_inf(), __builtin_inf()};
 #pragma unroll 2
         for (int bi = j0; bi < nbat; bi += 8) {     // nbat is a multiple of 8: the same count for every lane
             const u32x4 o = s_bo[bi];
-            const uint32_t hb = s_bh[bi];
+            const uint32_t hb = s_bh[bi], rowbits = hb >> 2;    // hb = 128 row slot
             const u32x4 v0 = *reinterpret_cast<const u32x4 *>(kxq + o.x);
             const u32x4 v1 = *reinterpret_cast<const u32x4 *>(kxq + o.y);
             const u32x4 v2 = *reinterpret_cast<const u32x4 *>(kxq + o.z);
             const u32x4 v3 = *reinterpret_cast<const u32x4 *>(kxq + o.w);
-            const u32x4 yk = *reinterpret_cast<const u32x4 *>(kyq + hb);
+            const u32x4 yd = *reinterpret_cast<const u32x4 *>(kyq + hb);
 #pragma unroll
-            for (int e = 0; e < 4; e++)
-                b4[e] = min(b4[e], __builtin_elementwise_add_sat((uint32_t)min(min(v0[e], v1[e]), min(v2[e], v3[e])),
-                                                                 yk[e]));
+            for (int e = 0; e < 4; e++) {
+                const uint32_t m = min(min(v0[e], v1[e]), min(v2[e], v3[e]));
+                const double sum = (double)xkey_distance(m) + (double)__uint_as_float(yd[e]);
+                const unsigned long long key = (unsigned long long)__double_as_longlong(sum) | ((m & 31u) | rowbits);
+                b4[e] = min_f64(b4[e], __longlong_as_double((long long)key));
+            }
         }
 #pragma unroll
         for (int e = 0; e < 4; e++) {
-            b4[e] = min(b4[e], (uint32_t)__shfl_xor((int)b4[e], 8));
-            b4[e] = min(b4[e], (uint32_t)__shfl_xor((int)b4[e], 16));
-            b4[e] = min(b4[e], (uint32_t)__shfl_xor((int)b4[e], 32));
+            b4[e] = min_f64(b4[e], __shfl_xor(b4[e], 8));
+            b4[e] = min_f64(b4[e], __shfl_xor(b4[e], 16));
+            b4[e] = min_f64(b4[e], __shfl_xor(b4[e], 32));
         }
         if (lane < 8) {
-            const u32x4 w4 = {b4[0], b4[1], b4[2], b4[3]};
-            *reinterpret_cast<u32x4 *>(best_w + 4 * q) = w4;
+#pragma unroll
+            for (int e = 0; e < 4; e++) best_w[4 * q + e] = (unsigned long long)__double_as_longlong(b4[e]);
         }
         __builtin_amdgcn_wave_barrier();
-        const uint32_t best = best_w[ln];
-        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
-        const unsigned char *kyl = reinterpret_cast<const unsigned char *>(ky + ln);
-        uint32_t sum = best >> 16, idx = best & 0xffffu;   // code sum and 128 (row slot) + column slot
-        if (best == 0xffffffffu) {   // every sum saturated: all batches again, in 64 bits
-            unsigned long long b64 = ~0ull;
-            for (int bi = 0; bi < nbat; bi++) {
-                const u32x4 o = s_bo[bi];
-                const unsigned long long yk = *reinterpret_cast<const uint32_t *>(kyl + s_bh[bi]);
-#pragma unroll
-                for (int c = 0; c < 4; c++)
-                    b64 = min(b64, (unsigned long long)*reinterpret_cast<const uint32_t *>(kxl + o[c]) + yk);
-            }
-            sum = (uint32_t)(b64 >> 16);
-            idx = (uint32_t)b64 & 0xffffu;
-        }
+        const unsigned long long best = best_w[ln];
         if (g == 0 && ln < nvalid) {
-            if (sum < tau_code) {      // Eq8 (tau_code = ceil(4096 tau))
-                const int a = pl.colbin[idx & 31u], b = pl.rowbin[(idx >> 7) & 31u];
+            const uint32_t idx = (uint32_t)best & 1023u;        // 32 row slot + column slot
+            const double D = __longlong_as_double((long long)(best & ~1023ull));
+            if (D < tau4096) {      // Eq8
+                const int a = pl.colbin[idx & 31u], b = pl.rowbin[idx >> 5];
                 const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
                 labels[pix] = k + 1;
-                if (score_map) score_map[pix] = expf(-((float)sum * 0x1p-12f));
+                if (score_map) score_map[pix] = expf(-(float)(D * 0x1p-12));
                 atomicAdd(s_cnt + k, 1);
             } else {
                 labels[pix] = 0;

@@ -88,7 +88,7 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
         launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
-               (const int32_t *)h->counts, nslices, slice_px, npix, fa.tau_code, h->tb,
+               (const int32_t *)h->counts, nslices, slice_px, npix, fa.tau4096, h->tb,
                (const unsigned long long *)hcur, hnext, h->hlast, Bw, Bh, cut, h->cap, cents, num, labels, score);
     } else {
         const size_t fixed = tables + 16 + kWKeys * 2;
@@ -100,12 +100,12 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
         const PeakOut po{cents, num, h->peaks, h->kinfo};
         launch(1, k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, h->hrep, h->hlast,
                Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
-        const size_t fixed2 = tables + 16 + kCountCap * 4 + kCKeys * 2;
+        const size_t fixed2 = tables + 16 + kCountCap * 4;
         const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
         const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
-        launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, dstride, yoff, g, npix, fg_thr, fa.tau_code, h->tb, Bw, Bh,
+        launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, dstride, yoff, g, npix, fg_thr, fa.tau4096, h->tb, Bw, Bh,
                (const int32_t *)h->peaks, (const int32_t *)h->kinfo, cents, labels, score);
     }
     return hipGetLastError() == hipSuccess ? CPE_OK : CPE_ERR_HIP;

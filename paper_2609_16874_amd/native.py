@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libcpe_decode.so")
 
 CPE_OK, CPE_ERR_INVALID_ARG, CPE_ERR_UNSUPPORTED, CPE_ERR_OUT_OF_MEMORY, CPE_ERR_HIP = range(5)
 CPE_F32, CPE_F16 = 0, 1
-W_KEYS, C_KEYS = 8192, 16384
+W_KEYS = 8192
 
 CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y", "<f4"),
                            ("score", "<f8"), ("npix", "<i4"), ("reserved", "<i4")])
@@ -27,7 +27,7 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 # Every entry point declared in include/cpe_decode.h.
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
-           "cpe_decode_set_stage_events", "cpe_decode_naive")
+           "cpe_decode_set_stage_events", "cpe_decode_naive", "cpe_check_sqrt")
 STAGE_EVENTS = 6
 MFMA_BINS = 32
 
@@ -74,7 +74,7 @@ def library():
         lib.cpe_status_string.restype = ctypes.c_char_p
         lib.cpe_status_string.argtypes = [i32]
         lib.cpe_decode_get_tables.restype = i32
-        lib.cpe_decode_get_tables.argtypes = [P, P, P, P, P]
+        lib.cpe_decode_get_tables.argtypes = [P, P, P, P]
         lib.cpe_decode_get_histogram.restype = i32
         lib.cpe_decode_get_histogram.argtypes = [P, P, P]
         lib.cpe_decode_workspace_bytes.restype = ctypes.c_size_t
@@ -83,6 +83,8 @@ def library():
         lib.cpe_decode_set_stage_events.argtypes = [P, P, i32]
         lib.cpe_decode_naive.restype = i32
         lib.cpe_decode_naive.argtypes = [P, P, P, P, i32, i32, ctypes.c_float, ctypes.c_double, P, P, P, P]
+        lib.cpe_check_sqrt.restype = i32
+        lib.cpe_check_sqrt.argtypes = [P, P]
         _lib = lib
     return _lib
 
@@ -165,12 +167,10 @@ class Decoder:
         pal_x = np.empty((self.bins_w, 2 * self.F), np.int16)
         pal_y = np.empty((self.bins_h, 2 * self.F), np.int16)
         wt = np.empty(W_KEYS, np.uint16)
-        ct = np.empty(C_KEYS, np.uint16)
-        st = library().cpe_decode_get_tables(self._h, pal_x.ctypes.data, pal_y.ctypes.data, wt.ctypes.data,
-                                             ct.ctypes.data)
+        st = library().cpe_decode_get_tables(self._h, pal_x.ctypes.data, pal_y.ctypes.data, wt.ctypes.data)
         if st != CPE_OK:
             raise CpeError(st, "cpe_decode_get_tables")
-        return pal_x, pal_y, wt, ct
+        return pal_x, pal_y, wt
 
     def set_stage_events(self, events) -> int:
         """``events``: a ctypes array of CPE_STAGE_EVENTS hipEvent_t handles, or
@@ -224,6 +224,18 @@ class Decoder:
         if out["score_map"] is not None:
             res["score_map"] = out["score_map"].cpu().numpy()
         return res
+
+
+def check_sqrt(stream=None) -> int:
+    """cpe_check_sqrt: the number of binary32 inputs on which the library's
+    square root differs from the correctly rounded one (synchronises)."""
+    import torch
+    out = torch.empty(1, dtype=torch.int64, device="cuda")
+    st = library().cpe_check_sqrt(_stream_ptr(stream), _ptr(out))
+    if st != CPE_OK:
+        raise CpeError(st, "cpe_check_sqrt")
+    torch.cuda.synchronize()
+    return int(out.item())
 
 
 def torch_dtype(dtype: str):

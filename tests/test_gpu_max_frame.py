@@ -78,7 +78,7 @@ def test_largest_frame_counts_every_pixel_once():
     print(f"largest frame: {H} x {W} f16 D=4, {N} pixels", flush=True)
     dec = native().Decoder(H, W, 1, "f16", fx, fy, BINS, BINS, 16)
     try:
-        pal_x, pal_y, _, _ = dec.tables()
+        pal_x, pal_y, _ = dec.tables()
         assert np.array_equal(pal_x, small["pal_x"]) and np.array_equal(pal_y, small["pal_y"])
         emb = torch.from_numpy(pixel_value()).cuda().expand(N, 4).contiguous()
         fg = torch.ones(N, dtype=torch.float16, device="cuda")

@@ -2,9 +2,10 @@
 ABI, against the CPU oracle.
 
 * cpe_decode_ex with the Eq8 mask threshold tau: thresholds taken from the
-  oracle's own distance distribution (code sums read back from its tau = inf
-  score map), both on an attained code sum (the strict test decides pixels
-  sitting exactly on it) and half a code unit above; tau = 0 and tau = inf.
+  oracle's own distance distribution (the winning distance sums of its tau =
+  inf labels, recomputed exactly from its palettes), both on an attained sum
+  (the strict test decides pixels sitting exactly on it) and half a unit of
+  1/4096 above; tau = 0 and tau = inf.
 * cpe_decode_ex without a foreground channel: every pixel votes and is
   labelled (the participating set of Section 3.1), on the matrix-core and the
   generic kernels.
@@ -30,10 +31,24 @@ pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "configs.json")
 
 
-def code_sums(ref):
-    """Winning code sums D of the labelled pixels, from expf(-D / 4096)."""
-    lab = ref["labels"]
-    return np.rint(-4096.0 * np.log(ref["score_map"][lab > 0].astype(np.float64))).astype(np.int64)
+def code_sums(ref, emb, F):
+    """Winning distance sums D (units of 1/4096) of the labelled pixels of an
+    oracle decode: the input on the 1/4096 grid, S exact against the
+    oracle's palettes, r = the float32 square root of S rounded to float32,
+    r_x + r_y summed exactly in float64."""
+    lab = ref["labels"].reshape(-1)
+    sel = lab > 0
+    Dch = emb.shape[-1]
+    v = np.clip(emb.reshape(-1, Dch)[sel].astype(np.float32), -1.5, 1.5)
+    X = np.rint(np.float32(4096.0) * v).astype(np.int64)
+    k = lab[sel] - 1
+    a, b = ref["centroids"]["bin_x"][k], ref["centroids"]["bin_y"][k]
+
+    def dist(Xa, P):
+        S = ((Xa - P.astype(np.int64)) ** 2).sum(-1)
+        return np.sqrt(S.astype(np.float32)).astype(np.float64)
+
+    return dist(X[:, :2 * F], ref["pal_x"][a]) + dist(X[:, Dch // 2:Dch // 2 + 2 * F], ref["pal_y"][b])
 
 
 def run_ex(dec, emb, fg, fg_thr, theta, tau):
@@ -64,7 +79,8 @@ def test_mask_threshold_parity(cfg, bins):
     fx, fy = spec.freqs()
     cap = th["capacity"]
     base = oracle.decode(f.emb, f.fg, fx, fy, b, b, cap, spec.fg_threshold, th["peak_threshold"])
-    D = np.sort(code_sums(base))
+    D = np.sort(code_sums(base, f.emb, spec.n_freq))
+    np.testing.assert_allclose(np.exp(-D / 4096.0), np.sort(base["score_map"][base["labels"] > 0])[::-1], rtol=1e-6)
     taus = [0.0, D[len(D) // 3] / 4096.0, (D[len(D) // 2] + 0.5) / 4096.0, D[(3 * len(D)) // 4] / 4096.0, math.inf]
     dec = native().Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, b, b, cap)
     for tau in taus:
@@ -110,7 +126,7 @@ def test_ragged_frames_with_options(case):
     ref0 = oracle.decode(emb, fg, fx, fy, bw, bh, cap, 0.5, 0.0)
     theta = 0.05 * ref0["hist"].max() * 2.0 ** -30
     base = oracle.decode(emb, fg, fx, fy, bw, bh, cap, 0.5, theta)
-    D = np.sort(code_sums(base))
+    D = np.sort(code_sums(base, emb, F))
     dec = native().Decoder(H, W, F, "f32" if dt == np.float32 else "f16", fx, fy, bw, bh, cap)
     for use_fg, tau in ((True, D[len(D) // 2] / 4096.0), (False, math.inf), (False, D[len(D) // 4] / 4096.0)):
         g = fg if use_fg else None
@@ -222,11 +238,11 @@ def test_option_and_mask_argument_errors():
     dec.close()
 
 
-def test_far_pixels_with_saturating_code_sums():
-    """Foreground pixels whose every x + y code sum is at least 2^16 (the
-    32-bit search keys saturate and the kernel searches them again in 64
-    bits): labels, counts and scores equal the oracle's, with no mask
-    threshold and with tau on either side of some of their sums."""
+def test_far_pixels():
+    """Foreground pixels far from every candidate (squared distances far
+    above 2^24, where fl32(S) rounds; distances near the largest the input
+    range allows): labels, counts and scores equal the oracle's, with no mask
+    threshold and with tau on either side of some of their distance sums."""
     from tests import farframe
     emb, fg, fx, fy, theta, far = farframe.make()
     dec = native().Decoder(farframe.H, farframe.W, farframe.F, "f32", fx, fy, farframe.BINS, farframe.BINS,
@@ -234,9 +250,6 @@ def test_far_pixels_with_saturating_code_sums():
     for tau in (math.inf, 20.0, 100.0):
         print(f"far pixels tau {tau}", flush=True)
         ref = oracle.decode(emb, fg, fx, fy, farframe.BINS, farframe.BINS, farframe.CAP, 0.5, theta, tau=tau)
-        if tau == math.inf:
-            sums = farframe.candidate_code_sums(ref, emb, farframe.F)
-            assert sums[far].min() >= 2 ** 16
         got = run_ex(dec, emb, fg, 0.5, theta, tau)
         assert_parity(got, ref, farframe.CAP)
         if tau == 20.0:     # some far pixels below tau, some above

@@ -75,3 +75,40 @@ def test_full_count_equals_the_standard_decode():
         assert_parity(gpu_decode(dec, f.emb, f.fg, spec.fg_threshold, theta), ref, dec.capacity)
     finally:
         dec.close()
+
+
+def test_workload4_batch_resolved_back_to_back():
+    """The resolved-harmonics decode of all 16 frames of the batch workload,
+    back to back on one handle and one stream, each frame's histogram copied
+    out right after its decode; every frame against the oracle."""
+    spec = synth.CONFIGS[4]
+    fx, fy = spec.freqs()
+    th = resolved_thresholds()["4"]
+    n = th["n_freq"]
+    fx, fy = fx[:n], fy[:n]
+    nat = native()
+    dec = nat.Decoder(spec.H, spec.W, n, spec.dtype, fx, fy, spec.bins, spec.bins, D=spec.D)
+    try:
+        frames = [synth.make_frame(4, i) for i in range(spec.n_frames)]
+        embs = [torch.from_numpy(fr.emb).cuda() for fr in frames]
+        fgs = [torch.from_numpy(fr.fg).cuda() for fr in frames]
+        outs = [dec.new_outputs(score=True) for _ in frames]
+        hists = [torch.empty((spec.bins, spec.bins), dtype=torch.int64, device="cuda") for _ in frames]
+        for i in range(len(frames)):
+            o = outs[i]
+            assert dec.decode(embs[i], fgs[i], spec.fg_threshold, th["peak_threshold"], o["centroids"],
+                              o["num_centroids"], o["labels"], o["score_map"]) == 0
+            assert dec.histogram(hists[i]) == 0
+        torch.cuda.synchronize()
+        for i, fr in enumerate(frames):
+            print(f"resolved batch frame {i}", flush=True)
+            ref = oracle.decode(fr.emb, fr.fg, fx, fy, spec.bins, spec.bins, dec.capacity, spec.fg_threshold,
+                                th["peak_threshold"])
+            K = int(outs[i]["num_centroids"].item())
+            got = {"K": K,
+                   "centroids": outs[i]["centroids"].cpu().numpy().view(nat.CENTROID_DTYPE)[:min(K, dec.capacity)],
+                   "labels": outs[i]["labels"].cpu().numpy(), "score_map": outs[i]["score_map"].cpu().numpy(),
+                   "hist": hists[i].cpu().numpy().view(np.uint64)}
+            assert_parity(got, ref, dec.capacity)
+    finally:
+        dec.close()
