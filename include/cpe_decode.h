@@ -47,9 +47,14 @@
  * to the host: it only enqueues work on `stream`.
  *
  * Errors.  Argument errors are detected on the host before any work is
- * enqueued and return CPE_ERR_INVALID_ARG; a failed launch returns
- * CPE_ERR_HIP.  Data-dependent outcomes (no centroid, more centroids than
- * the capacity) are reported through the device outputs, never as errors.
+ * enqueued and return CPE_ERR_INVALID_ARG.  A decode clears the calling
+ * thread's last HIP error, then checks it after each of its launches: a
+ * failed launch returns CPE_ERR_HIP at once (the frame's outputs are then
+ * undefined).  No state carries over between frames -- every frame starts by
+ * clearing its vote histograms -- so the next decode on the same handle is
+ * unaffected by a failed one.  Data-dependent outcomes (no centroid, more
+ * centroids than the capacity) are reported through the device outputs,
+ * never as errors.
  *
  * Threading.  A handle may be used by one stream at a time (its scratch is
  * per handle); separate handles are independent.
@@ -221,6 +226,14 @@ cpe_status cpe_decode_get_histogram(cpe_decoder *h, hipStream_t stream, uint64_t
  * the assignment's distances are exactly those of Eq4 as defined above.
  */
 cpe_status cpe_check_sqrt(hipStream_t stream, unsigned long long *mismatches);
+
+/*
+ * Testing: make the next decode on this handle stop before its launch
+ * `launch` (0, 1 or 2, numbered as for cpe_decode_set_stage_events; -1
+ * cancels) and return CPE_ERR_HIP as if that launch had failed; the earlier
+ * launches of that frame are enqueued.  One-shot.
+ */
+cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch);
 
 /* Bytes of device memory the handle holds (constants + scratch). */
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h);

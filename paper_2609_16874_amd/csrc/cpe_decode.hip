@@ -64,8 +64,8 @@ cpe_status decode_frame(cpe_decoder *h, hipStream_t stream, const void *emb, con
     if (dev != h->device) return CPE_ERR_INVALID_ARG;
     const FrameArgs fa{stream,       emb,       fg,            fg_threshold, peak_cut(peak_threshold),
                        tau4096(tau), centroids, num_centroids, labels,       score_map};
-    if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, fa) : launch_f32_hi(h, fa);
-    return h->F <= 8 ? launch_f16_lo(h, fa) : launch_f16_hi(h, fa);
+    if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, h->sc, fa) : launch_f32_hi(h, h->sc, fa);
+    return h->F <= 8 ? launch_f16_lo(h, h->sc, fa) : launch_f16_hi(h, h->sc, fa);
 }
 
 // Distance at the centre of an m-bit bucket of fl32(S+1) (0 for S = 0).
@@ -257,7 +257,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_npx = carve(np1x.size() * 4), o_npy = carve(np1y.size() * 4);
     const size_t o_pop = carve(pop.size());
     const size_t o_wpk = carve(wt_pk.size() * 4);
-    const size_t o_hrep = carve((size_t)2 * kReplicas * nb * 8);
+    const size_t o_hrep = carve((size_t)kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
     const size_t o_kinfo = carve(16);
@@ -279,7 +279,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               up(o_npx, np1x.data(), np1x.size() * 4) && up(o_npy, np1y.data(), np1y.size() * 4) &&
               up(o_pop, pop.data(), pop.size()) &&
               up(o_wpk, wt_pk.data(), wt_pk.size() * 4) &&
-              hipMemset(d + o_hrep, 0, (size_t)2 * kReplicas * nb * 8) == hipSuccess &&
+              hipMemset(d + o_hrep, 0, (size_t)kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
               hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, (size_t)kMaxSlices * 4) == hipSuccess &&
               hipDeviceSynchronize() == hipSuccess;
@@ -299,13 +299,13 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->tb.np1_y = reinterpret_cast<const uint32_t *>(d + o_npy);
     h->tb.pop = reinterpret_cast<const uint32_t *>(d + o_pop);
     h->tb.wt_pk = reinterpret_cast<const uint32_t *>(d + o_wpk);
-    h->hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
-    h->hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
-    h->peaks = reinterpret_cast<int32_t *>(d + o_peaks);
-    h->kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
-    h->counts = reinterpret_cast<int32_t *>(d + o_count);
-    h->list = reinterpret_cast<int32_t *>(d + o_list);
-    h->parity = 0;
+    h->sc.hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
+    h->sc.hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
+    h->sc.peaks = reinterpret_cast<int32_t *>(d + o_peaks);
+    h->sc.kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
+    h->sc.counts = reinterpret_cast<int32_t *>(d + o_count);
+    h->sc.list = reinterpret_cast<int32_t *>(d + o_list);
+    h->fail_at = -1;
     *out = h;
     return CPE_OK;
 }
@@ -364,7 +364,14 @@ cpe_status cpe_decode_get_histogram(cpe_decoder *h, hipStream_t stream, uint64_t
 {
     if (!h || !hist || !aligned(hist, 8)) return CPE_ERR_INVALID_ARG;
     const size_t bytes = (size_t)h->bins_w * h->bins_h * 8;
-    return hipMemcpyAsync(hist, h->hlast, bytes, hipMemcpyDeviceToDevice, stream) == hipSuccess ? CPE_OK : CPE_ERR_HIP;
+    return hipMemcpyAsync(hist, h->sc.hlast, bytes, hipMemcpyDeviceToDevice, stream) == hipSuccess ? CPE_OK : CPE_ERR_HIP;
+}
+
+cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch)
+{
+    if (!h || launch < -1 || launch > 2) return CPE_ERR_INVALID_ARG;
+    h->fail_at = launch;
+    return CPE_OK;
 }
 
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h) { return h ? h->dev_bytes : 0; }

@@ -9,6 +9,23 @@
 
 #include "cpe_common.hpp"
 
+namespace cpe {
+
+// Per-frame scratch of the launch sequence: everything a decode writes and
+// reads besides the caller's inputs and outputs and the handle's constants.
+// Nothing in it carries over from one frame to the next: the first launch of
+// every frame clears the vote histograms.
+struct Scratch {
+    unsigned long long *hrep;    // [kReplicas][nb] vote histograms
+    unsigned long long *hlast;   // [nb] summed histogram of the frame
+    int32_t *peaks;              // [cap] a | b << 16 (generic path)
+    int32_t *kinfo;              // [0] = min(K, cap), [1] = K (generic path)
+    int32_t *counts;             // [kMaxSlices] entries per slice of the participating-pixel list
+    int32_t *list;               // participating pixels, in slices: H*W + one slice
+};
+
+}  // namespace cpe
+
 struct cpe_decoder {
     int32_t H, W, D, F, bins_w, bins_h, cap;
     cpe_dtype dtype;
@@ -18,14 +35,8 @@ struct cpe_decoder {
     unsigned char *dev;                  // single device allocation
     size_t dev_bytes;
     cpe::Tables tb;
-    unsigned long long *hrep;            // [2][kReplicas][nb]: vote histograms by frame parity
-                                         //   (the generic path uses the first set only)
-    unsigned long long *hlast;           // [nb] summed histogram of the latest frame
-    int32_t *peaks;                      // [cap] a | b << 16 (generic path)
-    int32_t *kinfo;                      // [0] = min(K, cap), [1] = K (generic path)
-    int32_t *list;                       // participating pixels of the current frame, in slices
-    int32_t *counts;                     // [kMaxSlices] entries per slice
-    int parity;                          // histogram set of the next frame (matrix-core path)
+    cpe::Scratch sc;                     // per-frame scratch, in the device allocation
+    int fail_at;                         // test hook: the next decode stops before this launch (-1: none)
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;
     // per-tuple ablation (cpe_decode_naive): real palettes gamma(bin centre)
@@ -49,12 +60,13 @@ struct FrameArgs {
     float *score;
 };
 
-// Enqueue the kernels of one frame for element type T and F harmonics; each
-// is defined in one of the launch_*.hip translation units.
-cpe_status launch_f32_lo(cpe_decoder *h, const FrameArgs &a);   // F = 1..8
-cpe_status launch_f32_hi(cpe_decoder *h, const FrameArgs &a);   // F = 9..16
-cpe_status launch_f16_lo(cpe_decoder *h, const FrameArgs &a);
-cpe_status launch_f16_hi(cpe_decoder *h, const FrameArgs &a);
+// Enqueue the kernels of one frame for element type T and F harmonics, with
+// the per-frame scratch sc; each is defined in one of the launch_*.hip
+// translation units.
+cpe_status launch_f32_lo(cpe_decoder *h, const Scratch &sc, const FrameArgs &a);   // F = 1..8
+cpe_status launch_f32_hi(cpe_decoder *h, const Scratch &sc, const FrameArgs &a);   // F = 9..16
+cpe_status launch_f16_lo(cpe_decoder *h, const Scratch &sc, const FrameArgs &a);
+cpe_status launch_f16_hi(cpe_decoder *h, const Scratch &sc, const FrameArgs &a);
 
 // Enqueue the binary masks of centroids first .. first+count-1 (masks.hip).
 cpe_status launch_masks(hipStream_t stream, const int32_t *labels, int64_t npix, int32_t first, int32_t count,

@@ -9,9 +9,10 @@
 // atomics: the consumers concatenate the slices through the prefix sum of
 // the counts (slice_prefix / ListCursor).  The non-participating pixels get
 // their final outputs here: label 0 and, if a score map is requested,
-// score 0.  The vote and assignment launches then stream equal shares of
-// the list in full tiles, so their work does not depend on where in the
-// frame the foreground lies.
+// score 0.  The launch also clears the frame's vote histograms, which the
+// vote launch then accumulates into.  The vote and assignment launches then
+// stream equal shares of the list in full tiles, so their work does not
+// depend on where in the frame the foreground lies.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -44,8 +45,11 @@ __host__ __device__ inline int slice_count(int64_t npix)
 template <typename T, bool VEC>
 __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict__ fg, int32_t npix, float fg_thr,
                                                              int32_t *__restrict__ list, int32_t *__restrict__ counts,
-                                                             int32_t *__restrict__ labels, float *__restrict__ score)
+                                                             int32_t *__restrict__ labels, float *__restrict__ score,
+                                                             unsigned long long *__restrict__ hclear, int32_t nclear)
 {
+    for (int i = blockIdx.x * kCompactThreads + threadIdx.x; i < nclear; i += gridDim.x * kCompactThreads)
+        hclear[i] = 0ull;
     __shared__ int s_wave[kCompactThreads / 64];
     __shared__ int32_t s_out[kCompactSpan];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -128,6 +132,16 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict
     }
     if (tid == 0) counts[blockIdx.x] = base;
 }
+
+namespace {   // one private copy per translation unit that launches it
+
+// Zero n words (the vote histograms of a frame without a compaction launch).
+__global__ __launch_bounds__(256) void k_clear_u64(unsigned long long *__restrict__ p, int32_t n)
+{
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0ull;
+}
+
+}  // namespace
 
 // Exclusive prefix sums s_pref[0 .. nslices] of the slice counts (LDS),
 // s_pref[nslices] = |S|, by the first wave: slice_load issues the loads

@@ -372,7 +372,7 @@ template <typename T, int F>
 constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 //
 // Every workgroup adds its histogram into one of the kReplicas vote
-// histograms `hrep` (zeroed beforehand); the assignment launch that follows
+// histograms `hrep` (zeroed by the frame's first launch); the assignment launch that follows
 // sums them and extracts the peaks.  Workgroup 0 also resets the pixel
 // counts of the centroid records, which the assignment launch accumulates.
 template <typename T, int F>
@@ -577,8 +577,7 @@ constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
 // writes the centroid records (all fields but the pixel count), K and the
-// summed histogram `hlast`, and the grid clears `hzero`, the histograms the
-// next frame's vote launch accumulates into.
+// summed histogram `hlast`.
 //
 // Then, per tile of 32 pixels, the distances of both axes for the candidate
 // slots (palette entries of the slots' bins as the MFMA rows, so that each
@@ -592,8 +591,7 @@ template <typename T, int F>
 __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb2 / 4))) void k_assign_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
     const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, double tau4096, Tables tb,
-    const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hzero,
-    unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
+    const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
     cpe_centroid *__restrict__ cents, int32_t *__restrict__ num, int32_t *__restrict__ labels,
     float *__restrict__ score_map)
 {
@@ -671,7 +669,6 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         for (int i = tid; i < nb; i += kThreads) hlast[i] = s_h[(i / Bw) * 32 + i % Bw];
         if (tid == 0) *num = pl.K;
     }
-    for (int i = blockIdx.x * kThreads + tid; i < kReplicas * nb; i += gridDim.x * kThreads) hzero[i] = 0ull;
 
     if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
         ListCursor c0;

@@ -11,8 +11,7 @@
 //                 table and the candidate batches of the assignment search.
 //   peak_extract  any grid: the stand-alone kernel k_peaks between the
 //                 generic vote and assignment kernels; it writes the records,
-//                 K, the compact list and the summed histogram to memory and
-//                 clears the replicated histograms for the next frame.
+//                 K, the compact list and the summed histogram to memory.
 //
 // Candidate batches.  The first min(K, cap) candidates are grouped by row b
 // into batches of 4 columns (a row's last batch repeats its last column,
@@ -321,7 +320,7 @@ struct PeakOut {
 // scratch of Bw * Bh u64; s_pk: LDS scratch of max_peaks(Bw, Bh) ints.
 // Until the last barrier every result goes to LDS only, so that no barrier
 // waits for global stores; the outputs are written at the end.
-__device__ __forceinline__ void peak_extract(unsigned long long *__restrict__ hrep,
+__device__ __forceinline__ void peak_extract(const unsigned long long *__restrict__ hrep,
                                              unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
                                              long long cut, int32_t cap, const float *__restrict__ cx,
                                              const float *__restrict__ cy, const PeakOut &po,
@@ -355,11 +354,7 @@ __device__ __forceinline__ void peak_extract(unsigned long long *__restrict__ hr
         po.cents[k] = rec;
         po.peaks[k] = a | (b << 16);
     }
-    for (int i = tid; i < nb; i += blockDim.x) {
-        hlast[i] = s_h[i];
-#pragma unroll
-        for (int r = 0; r < kReplicas; r++) hrep[(size_t)r * nb + i] = 0ull;
-    }
+    for (int i = tid; i < nb; i += blockDim.x) hlast[i] = s_h[i];
     if (tid == 0) {
         *po.num = K;
         po.kinfo[0] = Kc;
@@ -369,7 +364,7 @@ __device__ __forceinline__ void peak_extract(unsigned long long *__restrict__ hr
 
 namespace {   // one private copy per translation unit that launches it
 
-__global__ __launch_bounds__(1024) void k_peaks(unsigned long long *__restrict__ hrep,
+__global__ __launch_bounds__(1024) void k_peaks(const unsigned long long *__restrict__ hrep,
                                                 unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh,
                                                 long long cut, int32_t cap, const float *__restrict__ cx,
                                                 const float *__restrict__ cy, PeakOut po)

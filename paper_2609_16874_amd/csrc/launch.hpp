@@ -26,7 +26,7 @@ inline int pick_tile(size_t fixed, size_t per_px, size_t budget)
 }
 
 template <typename T, int F>
-cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
+cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
 {
     hipStream_t stream = fa.stream;
     const float fg_thr = fa.fg_thr;
@@ -40,90 +40,105 @@ cpe_status launch_all(cpe_decoder *h, const FrameArgs &fa)
     const T *e = static_cast<const T *>(emb);
     const int32_t dstride = h->D, yoff = h->D / 2;     // channels per pixel; first channel of the y block
     const T *g = static_cast<const T *>(fg);
+    // the test hook: the decode stops before launch fail_at, as if it had failed
+    const int fail_at = h->fail_at;
+    h->fail_at = -1;
+    // A launch error is reported by the launch itself: the thread's last
+    // error (possibly left by the caller's earlier HIP calls) is cleared
+    // first and read after every launch.
+    (void)hipGetLastError();
     // Launch i of the frame; with stage events on, the dispatch itself
-    // records events 2i and 2i + 1 at the kernel's start and end.
+    // records events 2i and 2i + 1 at the kernel's start and end.  Returns
+    // false if the launch failed (or the test hook stops the frame here).
     auto launch = [&](int i, auto kernel, dim3 grid, dim3 block, size_t lds, auto... args) {
+        if (i == fail_at) return false;
         if (h->stage_on)
             hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, stream, h->stage_ev[2 * i],
                                   h->stage_ev[2 * i + 1], 0u, args...);
         else
             hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
-    };
-    auto skip = [&](int i) {           // a launch this frame does not need: its events coincide
-        if (h->stage_on) {
-            (void)hipEventRecord(h->stage_ev[2 * i], stream);
-            (void)hipEventRecord(h->stage_ev[2 * i + 1], stream);
-        }
+        return hipGetLastError() == hipSuccess;
     };
     const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;
     const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
+    const int nclear = kReplicas * nb;
+    const int clear_grid = (nclear + 255) / 256 < 64 ? (nclear + 255) / 256 : 64;
 
     if (mfma) {
         // the participating pixels as a compact list (every pixel when the
-        // frame has no foreground channel), recovery + voting into this
-        // frame's histograms, then the assignment launch, which extracts the
-        // peaks in its prologue and clears the other parity's histograms and
-        // list counter for the next frame
-        const int par = h->parity;
-        h->parity ^= 1;
-        unsigned long long *hcur = h->hrep + (size_t)par * kReplicas * nb;
-        unsigned long long *hnext = h->hrep + (size_t)(par ^ 1) * kReplicas * nb;
-        int32_t *list = g ? h->list : nullptr;
+        // frame has no foreground channel) and the vote histograms cleared,
+        // recovery + voting into them, then the assignment launch, which
+        // extracts the peaks in its prologue
+        int32_t *list = g ? sc.list : nullptr;
         const int nslices = slice_count(npix), slice_px = slice_pixels(npix);
+        bool ok;
         if (!g)
-            skip(0);
+            ok = launch(0, k_clear_u64, dim3(clear_grid), dim3(256), 0, sc.hrep, nclear);
         else if (((uintptr_t)g & 15u) == 0)
-            launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, h->counts,
-                   labels, score);
+            ok = launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list,
+                        sc.counts, labels, score, sc.hrep, nclear);
         else
-            launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, h->counts,
-                   labels, score);
+            ok = launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list,
+                        sc.counts, labels, score, sc.hrep, nclear);
+        if (!ok) return CPE_ERR_HIP;
         // grids: at most one workgroup per compute unit, no more waves than tiles
         constexpr int wpb = kVoteWpb<T, F>;
         const int64_t tiles = ((int64_t)npix + 31) / 32;
         const int64_t wgs = (tiles + wpb - 1) / wpb;
         const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
-               (const int32_t *)h->counts, nslices, slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap);
+        if (!launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
+                    (const int32_t *)sc.counts, nslices, slice_px, npix, h->tb, Bw, Bh, sc.hrep, cents, h->cap))
+            return CPE_ERR_HIP;
         const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
-               (const int32_t *)h->counts, nslices, slice_px, npix, fa.tau4096, h->tb,
-               (const unsigned long long *)hcur, hnext, h->hlast, Bw, Bh, cut, h->cap, cents, num, labels, score);
+        if (!launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
+                    (const int32_t *)sc.counts, nslices, slice_px, npix, fa.tau4096, h->tb,
+                    (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score))
+            return CPE_ERR_HIP;
     } else {
+        // the vote histograms cleared (before launch 0's start event), then
+        // recovery + voting, peak extraction, assignment
+        if (fail_at == 0) return CPE_ERR_HIP;
+        hipLaunchKernelGGL(k_clear_u64, dim3(clear_grid), dim3(256), 0, stream, sc.hrep, nclear);
+        if (hipGetLastError() != hipSuccess) return CPE_ERR_HIP;
         const size_t fixed = tables + 16 + kWKeys * 2;
         const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
         const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 2;
         const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
         const int grid = (int)(tiles < 1024 ? tiles : 1024);
-        launch(0, k_vote_generic<T, F>, dim3(grid), dim3(tp), lds, e, dstride, yoff, g, npix, fg_thr, h->tb, Bw, Bh, h->hrep);
-        const PeakOut po{cents, num, h->peaks, h->kinfo};
-        launch(1, k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4, h->hrep, h->hlast,
-               Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
+        if (!launch(0, k_vote_generic<T, F>, dim3(grid), dim3(tp), lds, e, dstride, yoff, g, npix, fg_thr, h->tb, Bw,
+                    Bh, sc.hrep))
+            return CPE_ERR_HIP;
+        const PeakOut po{cents, num, sc.peaks, sc.kinfo};
+        if (!launch(1, k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4,
+                    (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po))
+            return CPE_ERR_HIP;
         const size_t fixed2 = tables + 16 + kCountCap * 4;
         const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
         const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
-        launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, dstride, yoff, g, npix, fg_thr, fa.tau4096, h->tb, Bw, Bh,
-               (const int32_t *)h->peaks, (const int32_t *)h->kinfo, cents, labels, score);
+        if (!launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, dstride, yoff, g, npix, fg_thr,
+                    fa.tau4096, h->tb, Bw, Bh, (const int32_t *)sc.peaks, (const int32_t *)sc.kinfo, cents, labels,
+                    score))
+            return CPE_ERR_HIP;
     }
-    return hipGetLastError() == hipSuccess ? CPE_OK : CPE_ERR_HIP;
+    return CPE_OK;
 }
 
 
 #define CPE_LAUNCH_RANGE(NAME, T, F0)                                       \
-    cpe_status NAME(cpe_decoder *h, const FrameArgs &a)                     \
+    cpe_status NAME(cpe_decoder *h, const Scratch &sc, const FrameArgs &a)  \
     {                                                                       \
         switch (h->F - (F0)) {                                              \
-        case 0: return launch_all<T, (F0) + 0>(h, a);                       \
-        case 1: return launch_all<T, (F0) + 1>(h, a);                       \
-        case 2: return launch_all<T, (F0) + 2>(h, a);                       \
-        case 3: return launch_all<T, (F0) + 3>(h, a);                       \
-        case 4: return launch_all<T, (F0) + 4>(h, a);                       \
-        case 5: return launch_all<T, (F0) + 5>(h, a);                       \
-        case 6: return launch_all<T, (F0) + 6>(h, a);                       \
-        case 7: return launch_all<T, (F0) + 7>(h, a);                       \
+        case 0: return launch_all<T, (F0) + 0>(h, sc, a);                   \
+        case 1: return launch_all<T, (F0) + 1>(h, sc, a);                   \
+        case 2: return launch_all<T, (F0) + 2>(h, sc, a);                   \
+        case 3: return launch_all<T, (F0) + 3>(h, sc, a);                   \
+        case 4: return launch_all<T, (F0) + 4>(h, sc, a);                   \
+        case 5: return launch_all<T, (F0) + 5>(h, sc, a);                   \
+        case 6: return launch_all<T, (F0) + 6>(h, sc, a);                   \
+        case 7: return launch_all<T, (F0) + 7>(h, sc, a);                   \
         default: return CPE_ERR_UNSUPPORTED;                                \
         }                                                                   \
     }

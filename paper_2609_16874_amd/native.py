@@ -27,7 +27,8 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 # Every entry point declared in include/cpe_decode.h.
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
-           "cpe_decode_set_stage_events", "cpe_decode_naive", "cpe_check_sqrt")
+           "cpe_decode_set_stage_events", "cpe_decode_naive", "cpe_check_sqrt",
+           "cpe_decode_test_fail_launch")
 STAGE_EVENTS = 6
 MFMA_BINS = 32
 
@@ -83,6 +84,8 @@ def library():
         lib.cpe_decode_set_stage_events.argtypes = [P, P, i32]
         lib.cpe_decode_naive.restype = i32
         lib.cpe_decode_naive.argtypes = [P, P, P, P, i32, i32, ctypes.c_float, ctypes.c_double, P, P, P, P]
+        lib.cpe_decode_test_fail_launch.restype = i32
+        lib.cpe_decode_test_fail_launch.argtypes = [P, i32]
         lib.cpe_check_sqrt.restype = i32
         lib.cpe_check_sqrt.argtypes = [P, P]
         _lib = lib
@@ -159,6 +162,11 @@ class Decoder:
         return library().cpe_decode_naive(self._h, _stream_ptr(stream), _ptr(emb), _ptr(fg), self.H, self.W,
                                           float(fg_threshold), float(peak_threshold), _ptr(centroids),
                                           _ptr(num_centroids), _ptr(labels), _ptr(hist))
+
+    def test_fail_launch(self, launch: int) -> int:
+        """cpe_decode_test_fail_launch: the next decode stops before launch
+        ``launch`` and reports CPE_ERR_HIP."""
+        return library().cpe_decode_test_fail_launch(self._h, int(launch))
 
     def histogram(self, out, stream=None) -> int:
         return library().cpe_decode_get_histogram(self._h, _stream_ptr(stream), _ptr(out))

@@ -256,3 +256,35 @@ def test_far_pixels():
             lab = got["labels"].reshape(-1)[far]
             assert 0 < int((lab > 0).sum()) < len(far)
     dec.close()
+
+
+@pytest.mark.parametrize("bins,fail", [(32, 0), (32, 1), (32, 2), (48, 0), (48, 1), (48, 2)])
+def test_decode_after_a_failed_one_matches_the_oracle(bins, fail):
+    """A decode that stops before one of its launches (the test hook reports
+    it as a failed launch, CPE_ERR_HIP, after enqueueing the launches before
+    it) leaves nothing behind: the next decode on the same handle, of another
+    frame, equals the oracle bit for bit.  Matrix-core and generic kernels."""
+    nat = native()
+    spec = synth.CONFIGS[1]
+    fx, fy = spec.freqs()
+    frames = [synth.make_frame(1, i) for i in range(3)]
+    theta = thresholds()["1"]["peak_threshold"] * (bins / 32.0) ** -2
+    cap = ((bins + 1) // 2) ** 2
+    dec = nat.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, bins, bins, cap)
+    print(f"bins {bins}, failure before launch {fail}", flush=True)
+    first = gpu_decode(dec, frames[0].emb, frames[0].fg, spec.fg_threshold, theta)
+    assert first["K"] > 0
+    e = torch.from_numpy(frames[1].emb).cuda()
+    g = torch.from_numpy(frames[1].fg).cuda()
+    out = dec.new_outputs(score=True)
+    assert dec.test_fail_launch(fail) == 0
+    st = dec.decode(e, g, spec.fg_threshold, theta, out["centroids"], out["num_centroids"], out["labels"],
+                    out["score_map"])
+    assert st == nat.CPE_ERR_HIP
+    torch.cuda.synchronize()
+    got = gpu_decode(dec, frames[2].emb, frames[2].fg, spec.fg_threshold, theta)
+    ref = oracle.decode(frames[2].emb, frames[2].fg, fx, fy, bins, bins, cap, spec.fg_threshold, theta)
+    assert ref["K"] > 0
+    assert_parity(got, ref, cap)
+    assert dec.test_fail_launch(3) == nat.CPE_ERR_INVALID_ARG
+    dec.close()
