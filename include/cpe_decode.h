@@ -177,6 +177,31 @@ cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, co
                          float *score_map);
 
 /*
+ * cpe_decode_ex for callers that cannot allocate device memory around a
+ * decode (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same frame, arguments, outputs and errors as
+ * cpe_decode_ex, and the handle's constants, but the per-frame scratch (vote
+ * histograms, participating-pixel list, slice counts, peak list) is a static
+ * device array of the library, about 9.1 MB, held by each device the
+ * library runs on until the process ends, instead of the handle's.  The
+ * call itself allocates nothing.
+ *   Limit: frames of at most 2,097,152 pixels (H*W <= 2^21, e.g. 1024 x
+ *   2048); a handle for a larger frame gets CPE_ERR_UNSUPPORTED.  The
+ *   array's device address is looked up by cpe_decode_create on its device;
+ *   if that lookup failed the call returns CPE_ERR_HIP.
+ *   Every call on a device shares that device's array: calls that overlap in
+ *   time on one device (other streams, other threads, other handles) race
+ *   and give undefined results; calls ordered on one stream are safe, since
+ *   each frame clears what it accumulates into.
+ *   cpe_decode_get_histogram does not see these frames (it returns the
+ *   handle's latest cpe_decode / cpe_decode_ex frame).
+ */
+cpe_status cpe_decode_noalloc(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg,
+                              int32_t H, int32_t W, const cpe_decode_options *opt,
+                              cpe_centroid *centroids, int32_t *num_centroids, int32_t *labels,
+                              float *score_map);
+
+/*
  * Binary instance masks M^_m of Eq8 from a label map written by cpe_decode or
  * cpe_decode_ex on this handle, asynchronously on `stream`:
  *   masks[m][p] = 1 if labels[p] == first + m + 1, else 0,

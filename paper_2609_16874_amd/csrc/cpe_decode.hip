@@ -21,6 +21,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -47,9 +48,9 @@ bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // (exact scaling; +inf keeps every pixel, tau <= 0 none).
 double tau4096(double tau) { return tau * 4096.0; }
 
-cpe_status decode_frame(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg, int32_t H, int32_t W,
-                        float fg_threshold, double peak_threshold, double tau, cpe_centroid *centroids,
-                        int32_t *num_centroids, int32_t *labels, float *score_map)
+cpe_status decode_frame(cpe_decoder *h, const Scratch *sc, hipStream_t stream, const void *emb, const void *fg,
+                        int32_t H, int32_t W, float fg_threshold, double peak_threshold, double tau,
+                        cpe_centroid *centroids, int32_t *num_centroids, int32_t *labels, float *score_map)
 {
     if (!h || !emb || !centroids || !num_centroids || !labels) return CPE_ERR_INVALID_ARG;
     if (H != h->H || W != h->W) return CPE_ERR_INVALID_ARG;
@@ -64,8 +65,9 @@ cpe_status decode_frame(cpe_decoder *h, hipStream_t stream, const void *emb, con
     if (dev != h->device) return CPE_ERR_INVALID_ARG;
     const FrameArgs fa{stream,       emb,       fg,            fg_threshold, peak_cut(peak_threshold),
                        tau4096(tau), centroids, num_centroids, labels,       score_map};
-    if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, h->sc, fa) : launch_f32_hi(h, h->sc, fa);
-    return h->F <= 8 ? launch_f16_lo(h, h->sc, fa) : launch_f16_hi(h, h->sc, fa);
+    const Scratch &s = sc ? *sc : h->sc;
+    if (h->dtype == CPE_F32) return h->F <= 8 ? launch_f32_lo(h, s, fa) : launch_f32_hi(h, s, fa);
+    return h->F <= 8 ? launch_f16_lo(h, s, fa) : launch_f16_hi(h, s, fa);
 }
 
 // Distance at the centre of an m-bit bucket of fl32(S+1) (0 for S = 0).
@@ -82,6 +84,62 @@ uint16_t f16_bits(int v)   // exact for the small integers used here (|v| <= 204
     uint16_t b;
     std::memcpy(&b, &hv, 2);
     return b;
+}
+
+// ---------------------------------------------------------------------------
+// Per-frame scratch of cpe_decode_noalloc: a static device array, one copy
+// per device, for frames of up to kStaticMaxPixels pixels and any bin grid.
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address is looked up once per device (hipGetSymbolAddress, with the
+// device current, from cpe_decode_create) and only that address is used.
+// ---------------------------------------------------------------------------
+constexpr int64_t kStaticMaxPixels = 1LL << 21;     // 2,097,152 pixels, e.g. 1024 x 2048
+constexpr int kStaticMaxBins = kMaxBins * kMaxBins;
+constexpr size_t kStaticHrep = 0;                                               // [kReplicas][bins]
+constexpr size_t kStaticHlast = kStaticHrep + (size_t)kReplicas * kStaticMaxBins * 8;
+constexpr size_t kStaticPeaks = kStaticHlast + (size_t)kStaticMaxBins * 8;
+constexpr size_t kStaticKinfo = kStaticPeaks + (size_t)kStaticMaxBins * 4;
+constexpr size_t kStaticCounts = kStaticKinfo + 256;
+constexpr size_t kStaticList = kStaticCounts + (size_t)kMaxSlices * 4;
+constexpr size_t kStaticBytes = kStaticList + ((size_t)kStaticMaxPixels + kCompactSpan) * 4;
+static_assert(kStaticMaxPixels <= (int64_t)kMaxSlices * kCompactSpan, "one compaction step per slice: one slice "
+              "of kCompactSpan pixels bounds the list's tail");
+
+__device__ __align__(256) unsigned char scratch[kStaticBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+unsigned char *g_scratch[kMaxDevices];     // device address of `scratch` per device (null: not looked up)
+
+// Look up the device address of `scratch` on the current device `dev`, once.
+bool init_static_scratch(int dev)
+{
+    if (dev < 0 || dev >= kMaxDevices) return false;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch[dev]) return true;
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return false;
+    g_scratch[dev] = static_cast<unsigned char *>(ptr);
+    return true;
+}
+
+unsigned char *static_scratch(int dev)
+{
+    if (dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    return g_scratch[dev];
+}
+
+Scratch static_layout(unsigned char *base)
+{
+    Scratch sc;
+    sc.hrep = reinterpret_cast<unsigned long long *>(base + kStaticHrep);
+    sc.hlast = reinterpret_cast<unsigned long long *>(base + kStaticHlast);
+    sc.peaks = reinterpret_cast<int32_t *>(base + kStaticPeaks);
+    sc.kinfo = reinterpret_cast<int32_t *>(base + kStaticKinfo);
+    sc.counts = reinterpret_cast<int32_t *>(base + kStaticCounts);
+    sc.list = reinterpret_cast<int32_t *>(base + kStaticList);
+    return sc;
 }
 
 }  // namespace
@@ -134,6 +192,9 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
         delete h;
         return CPE_ERR_HIP;
     }
+    // the device address of cpe_decode_noalloc's scratch on this device (a
+    // failed lookup only makes that entry point report CPE_ERR_HIP)
+    (void)init_static_scratch(h->device);
     const int F = n_freq, twoF = 2 * n_freq, nb = bins_w * bins_h;
 
     // Eq9 palettes: gamma at the bin centres (a+1) * extent / (n+1), x4096.
@@ -315,8 +376,8 @@ cpe_status cpe_decode(cpe_decoder *h, hipStream_t stream, const void *emb, const
                       int32_t *labels, float *score_map)
 {
     if (!fg) return CPE_ERR_INVALID_ARG;
-    return decode_frame(h, stream, emb, fg, H, W, fg_threshold, peak_threshold, INFINITY, centroids, num_centroids,
-                        labels, score_map);
+    return decode_frame(h, nullptr, stream, emb, fg, H, W, fg_threshold, peak_threshold, INFINITY, centroids,
+                        num_centroids, labels, score_map);
 }
 
 cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg, int32_t H, int32_t W,
@@ -326,8 +387,22 @@ cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, co
     if (!opt || opt->reserved != 0) return CPE_ERR_INVALID_ARG;
     // without a foreground channel the threshold is never read
     const float fg_thr = fg ? opt->fg_threshold : 0.0f;
-    return decode_frame(h, stream, emb, fg, H, W, fg_thr, opt->peak_threshold, opt->tau, centroids, num_centroids,
-                        labels, score_map);
+    return decode_frame(h, nullptr, stream, emb, fg, H, W, fg_thr, opt->peak_threshold, opt->tau, centroids,
+                        num_centroids, labels, score_map);
+}
+
+cpe_status cpe_decode_noalloc(cpe_decoder *h, hipStream_t stream, const void *emb, const void *fg, int32_t H,
+                              int32_t W, const cpe_decode_options *opt, cpe_centroid *centroids,
+                              int32_t *num_centroids, int32_t *labels, float *score_map)
+{
+    if (!h || !opt || opt->reserved != 0) return CPE_ERR_INVALID_ARG;
+    if ((int64_t)h->H * h->W > kStaticMaxPixels) return CPE_ERR_UNSUPPORTED;
+    unsigned char *base = static_scratch(h->device);
+    if (!base) return CPE_ERR_HIP;
+    const Scratch sc = static_layout(base);
+    const float fg_thr = fg ? opt->fg_threshold : 0.0f;
+    return decode_frame(h, &sc, stream, emb, fg, H, W, fg_thr, opt->peak_threshold, opt->tau, centroids,
+                        num_centroids, labels, score_map);
 }
 
 cpe_status cpe_decode_masks(cpe_decoder *h, hipStream_t stream, const int32_t *labels, int32_t H, int32_t W,

@@ -28,7 +28,7 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
            "cpe_decode_set_stage_events", "cpe_decode_naive", "cpe_check_sqrt",
-           "cpe_decode_test_fail_launch")
+           "cpe_decode_test_fail_launch", "cpe_decode_noalloc")
 STAGE_EVENTS = 6
 MFMA_BINS = 32
 
@@ -84,6 +84,8 @@ def library():
         lib.cpe_decode_set_stage_events.argtypes = [P, P, i32]
         lib.cpe_decode_naive.restype = i32
         lib.cpe_decode_naive.argtypes = [P, P, P, P, i32, i32, ctypes.c_float, ctypes.c_double, P, P, P, P]
+        lib.cpe_decode_noalloc.restype = i32
+        lib.cpe_decode_noalloc.argtypes = [P, P, P, P, i32, i32, ctypes.POINTER(DecodeOptions), P, P, P, P]
         lib.cpe_decode_test_fail_launch.restype = i32
         lib.cpe_decode_test_fail_launch.argtypes = [P, i32]
         lib.cpe_check_sqrt.restype = i32
@@ -147,6 +149,15 @@ class Decoder:
         return library().cpe_decode_ex(self._h, _stream_ptr(stream), _ptr(emb), _ptr(fg), self.H, self.W,
                                        ctypes.byref(opt), _ptr(centroids), _ptr(num_centroids), _ptr(labels),
                                        _ptr(score_map))
+
+    def decode_noalloc(self, emb, fg, fg_threshold: float, peak_threshold: float, tau: float, centroids,
+                       num_centroids, labels, score_map=None, stream=None, reserved: int = 0) -> int:
+        """cpe_decode_noalloc: cpe_decode_ex with the library's static per-device
+        scratch instead of the handle's."""
+        opt = DecodeOptions(float(fg_threshold), int(reserved), float(peak_threshold), float(tau))
+        return library().cpe_decode_noalloc(self._h, _stream_ptr(stream), _ptr(emb), _ptr(fg), self.H, self.W,
+                                            ctypes.byref(opt), _ptr(centroids), _ptr(num_centroids), _ptr(labels),
+                                            _ptr(score_map))
 
     def masks(self, labels, first: int, count: int, masks, stream=None, H: Optional[int] = None,
               W: Optional[int] = None) -> int:

@@ -1,0 +1,88 @@
+"""GPU test of cpe_decode_noalloc (the entry point that allocates nothing):
+its outputs equal those of cpe_decode_ex on the same handle and frame, on two
+calls in a row that share the static scratch, the second with a smaller
+frame (and a no-foreground, Eq8-threshold decode of a third), and frames
+beyond its limit are refused."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2609_16874_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def native():
+    from paper_2609_16874_amd import native as nat
+    return nat
+
+
+def _run(dec, fn, emb, fg, fg_thr, theta, tau):
+    nat = native()
+    out = dec.new_outputs(score=True)
+    out["labels"].fill_(-7)
+    out["score_map"].fill_(-1.0)
+    st = fn(emb, fg, fg_thr, theta, tau, out["centroids"], out["num_centroids"], out["labels"], out["score_map"])
+    assert st == nat.CPE_OK, st
+    torch.cuda.synchronize()
+    K = int(out["num_centroids"].item())
+    return {"K": K, "centroids": out["centroids"].cpu().numpy().view(nat.CENTROID_DTYPE)[:min(K, dec.capacity)],
+            "labels": out["labels"].cpu().numpy(), "score_map": out["score_map"].cpu().numpy()}
+
+
+def _same(a, b):
+    assert a["K"] == b["K"]
+    assert np.array_equal(a["centroids"], b["centroids"])
+    assert np.array_equal(a["labels"], b["labels"])
+    np.testing.assert_allclose(a["score_map"], b["score_map"], rtol=1e-5, atol=0)
+
+
+def test_noalloc_equals_decode_ex_on_two_calls_in_a_row():
+    nat = native()
+    cases = []
+    # call 1: the 640x640 workload with 16 harmonics (fp16); call 2: a smaller
+    # ragged fp32 frame with 8 harmonics and another bin grid; call 3: the
+    # 256x256 workload without a foreground channel and with an Eq8 threshold
+    f2 = synth.make_frame(2)
+    s2 = f2.spec
+    cases.append((s2, f2.emb, f2.fg, 32, 1.0, math.inf))
+    rng = np.random.default_rng(5)
+    H, W, F = 77, 53, 8
+    fx = np.array([2 * math.pi * 2 ** k / W for k in range(F)])
+    fy = np.array([2 * math.pi * 2 ** k / H for k in range(F)])
+    inst = rng.integers(0, 5, size=(H, W))
+    cx, cy = rng.uniform(0, W, 5), rng.uniform(0, H, 5)
+    emb = (synth.encode_positions(cx[inst], cy[inst], fx, fy) + 0.1 * rng.standard_normal((H, W, 4 * F)))
+    small = dict(H=H, W=W, n_freq=F, dtype="f32", fx=fx, fy=fy)
+    cases.append((small, emb.astype(np.float32), ((inst > 0) + 0.05 * rng.standard_normal((H, W))).astype(np.float32),
+                  20, 0.3, math.inf))
+    f1 = synth.make_frame(1)
+    cases.append((f1.spec, f1.emb, None, 32, 30.0, 5.4))
+    for i, (spec, emb_np, fg_np, bins, theta, tau) in enumerate(cases):
+        if isinstance(spec, dict):
+            dec = nat.Decoder(spec["H"], spec["W"], spec["n_freq"], spec["dtype"], spec["fx"], spec["fy"], bins, bins)
+        else:
+            fxs, fys = spec.freqs()
+            dec = nat.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fxs, fys, bins, bins)
+        print(f"no-alloc call {i + 1}: {dec.H}x{dec.W} F={dec.F} {dec.dtype} bins {bins}", flush=True)
+        emb = torch.from_numpy(np.ascontiguousarray(emb_np)).cuda()
+        fg = None if fg_np is None else torch.from_numpy(np.ascontiguousarray(fg_np)).cuda()
+        got = _run(dec, dec.decode_noalloc, emb, fg, 0.5, theta, tau)
+        ref = _run(dec, dec.decode_ex, emb, fg, 0.5, theta, tau)
+        assert ref["K"] > 0
+        _same(got, ref)
+        dec.close()
+
+
+def test_noalloc_refuses_frames_beyond_its_limit():
+    nat = native()
+    fx = np.array([2 * math.pi / 2048])
+    dec = nat.Decoder(1025, 2048, 1, "f16", fx, fx, 8, 8)      # 2,099,200 pixels > 2^21
+    out = dec.new_outputs()
+    emb = torch.zeros((1025, 2048, 4), dtype=torch.float16, device="cuda")
+    fg = torch.zeros((1025, 2048), dtype=torch.float16, device="cuda")
+    st = dec.decode_noalloc(emb, fg, 0.5, 0.0, math.inf, out["centroids"], out["num_centroids"], out["labels"])
+    assert st == nat.CPE_ERR_UNSUPPORTED
+    dec.close()
