@@ -69,22 +69,6 @@ __device__ __forceinline__ float sqrt_cr(float x)
     return r;
 }
 
-// Search key of an x distance r = sqrt_cr(fl32(S)) and its column slot:
-// (bits(r) - 0x3F7FFFFF) << 5 | slot for r >= 1 (r <= sqrt(32 * 10240^2) <
-// 57927 keeps the difference below 2^27), slot for r = 0.  Keys order by
-// distance, then by slot.
-__device__ __forceinline__ uint32_t xkey(float r, uint32_t slot)
-{
-    return (__builtin_elementwise_sub_sat(__float_as_uint(r), 0x3F7FFFFFu) << 5) | slot;
-}
-
-// The distance of a search key, exact (0 for keys below 32).
-__device__ __forceinline__ float xkey_distance(uint32_t key)
-{
-    const uint32_t b = (key >> 5) + 0x3F7FFFFFu;
-    return key < 32u ? 0.0f : __uint_as_float(b);
-}
-
 // min of two binary64 values that are never NaN (one instruction; the
 // library's min also canonicalises its operands).
 __device__ __forceinline__ double min_f64(double a, double b)

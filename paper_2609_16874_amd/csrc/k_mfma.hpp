@@ -76,14 +76,14 @@
 // order (slots), the MFMA rows are the slots' palette entries, each lane
 // holds one pixel and 16 slots, and distances are computed for the groups of
 // 8 slots that hold candidates: r = sqrtf(fl32(S)) correctly rounded, stored
-// in LDS as an x search key (distance bits and column slot, ordered by
-// distance then slot) or as the y distance itself.  The candidate search
-// walks batches of 4 columns of one row: the smallest x key of the batch
-// gives the row's best column, its distance plus the row's y distance is
-// summed exactly in binary64, and the row and column slots fill the low bits
-// of that sum (always zero there), so one binary64 minimum selects the
-// smallest distance sum and, on ties, the lowest (row, column) -- slots keep
-// the bins' order -- i.e. the lowest centroid index.
+// in LDS as binary32 bits (which order like the distances, r >= 0).  The
+// candidate search walks batches of 4 columns of one row, in (row, column)
+// order: the smallest x distance of the batch plus the row's y distance is
+// summed exactly in binary64, the batch index fills the low bits of that sum
+// (always zero there), and one binary64 minimum selects the smallest distance
+// sum and, on ties, the first batch; within it the first column attaining
+// the batch's x minimum wins.  Slots keep the bins' order, so this is the
+// lowest centroid index among the smallest sums.
 #pragma once
 
 #include "cpe_common.hpp"
@@ -581,9 +581,9 @@ constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 //
 // Then, per tile of 32 pixels, the distances of both axes for the candidate
 // slots (palette entries of the slots' bins as the MFMA rows, so that each
-// lane holds one pixel and 16 slots) go to LDS, laid out [slot][kKeyStride]
-// so that lane m finds pixel m's value of any slot at a fixed stride: x keys
-// (xkey: distance bits and column slot) and y distances (binary32 bits).
+// lane holds one pixel and 16 slots) go to LDS as binary32 bits, laid out
+// [slot][kKeyStride] so that lane m finds pixel m's value of any slot at a
+// fixed stride.
 // The candidate search walks the batches of 4 columns of one row (see the
 // search below).  A pixel is labelled iff its distance sum D (in units of
 // 1/4096) is below tau4096 = 4096 tau (Eq8; +inf: every pixel).
@@ -719,7 +719,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
                 for (int i = 0; i < 4; i++) {
                     const int r = 4 * r4 + i;
                     const float d = sqrt_cr((float)assemble(hh[r], mid[r], ll[r], np));
-                    dst[kKeyStride * (8 * r4 + i)] = ax ? __float_as_uint(d) : xkey(d, (uint32_t)acc_row(r, g));
+                    dst[kKeyStride * (8 * r4 + i)] = __float_as_uint(d);
                 }
             }
         }
@@ -727,15 +727,16 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
 
     // Candidate search.  Lane l serves the four pixels 4 q .. 4 q + 3
     // (q = l & 7) for the batches j, j + 8, ... (j = l >> 3): one 16-byte
-    // read fetches a column's keys of its four pixels, so each address
+    // read fetches a column's distances of its four pixels, so each address
     // computation and each read serve four pixels.  Per batch and pixel the
-    // smallest of the 4 x keys is the row's best column among them; its
-    // distance plus the row's y distance, summed exactly in binary64, has
-    // at least 12 zero bits at the bottom of its mantissa (both distances are
-    // 0 or binary32 values of at least 1, so the sum is a multiple of 2^-23
-    // below 2^17), which take 32 row slot + column slot.  The eight lanes of
-    // a pixel quad then combine their minima, and lane m takes pixel m's
-    // result through LDS; lanes of half 0 write the labels of valid pixels.
+    // smallest of the 4 x distances plus the row's y distance, summed exactly
+    // in binary64, has at least 12 zero bits at the bottom of its mantissa
+    // (both distances are 0 or binary32 values of at least 1, so the sum is a
+    // multiple of 2^-23 below 2^17), which take the batch index (< 128).  The
+    // eight lanes of a pixel quad then combine their minima, and lane m takes
+    // pixel m's result through LDS, finds the first column of the winning
+    // batch with the batch's smallest x distance, and (lanes of half 0, valid
+    // pixels) writes its label.
     unsigned long long *best_w = s_best + wv * 32;
     auto search = [&](int pix, int nvalid) {
         __builtin_amdgcn_wave_barrier();
@@ -746,7 +747,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
 #pragma unroll 2
         for (int bi = j0; bi < nbat; bi += 8) {     // nbat is a multiple of 8: the same count for every lane
             const u32x4 o = s_bo[bi];
-            const uint32_t hb = s_bh[bi], rowbits = hb >> 2;    // hb = 128 row slot
+            const uint32_t hb = s_bh[bi];
             const u32x4 v0 = *reinterpret_cast<const u32x4 *>(kxq + o.x);
             const u32x4 v1 = *reinterpret_cast<const u32x4 *>(kxq + o.y);
             const u32x4 v2 = *reinterpret_cast<const u32x4 *>(kxq + o.z);
@@ -755,8 +756,9 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
 #pragma unroll
             for (int e = 0; e < 4; e++) {
                 const uint32_t m = min(min(v0[e], v1[e]), min(v2[e], v3[e]));
-                const double sum = (double)xkey_distance(m) + (double)__uint_as_float(yd[e]);
-                const unsigned long long key = (unsigned long long)__double_as_longlong(sum) | ((m & 31u) | rowbits);
+                const double sum = (double)__uint_as_float(m) + (double)__uint_as_float(yd[e]);
+                const unsigned long long sb = (unsigned long long)__double_as_longlong(sum);
+                const unsigned long long key = (sb & ~0xffffffffull) | ((uint32_t)sb | (uint32_t)bi);
                 b4[e] = min_f64(b4[e], __longlong_as_double((long long)key));
             }
         }
@@ -772,11 +774,20 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         }
         __builtin_amdgcn_wave_barrier();
         const unsigned long long best = best_w[ln];
+        const int bi = (int)((uint32_t)best & 127u);
+        const double D = __longlong_as_double((long long)(best & ~127ull));
+        const u32x4 o = s_bo[bi];
+        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
+        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
+        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
+        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
+        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+        const uint32_t wm = min(min(w0, w1), min(w2, w3));
+        const uint32_t col = (w0 == wm ? o.x : w1 == wm ? o.y : w2 == wm ? o.z : o.w) >> 7;   // column slot
+        const uint32_t row = s_bh[bi] >> 7;                                                      // row slot
         if (g == 0 && ln < nvalid) {
-            const uint32_t idx = (uint32_t)best & 1023u;        // 32 row slot + column slot
-            const double D = __longlong_as_double((long long)(best & ~1023ull));
             if (D < tau4096) {      // Eq8
-                const int a = pl.colbin[idx & 31u], b = pl.rowbin[idx >> 5];
+                const int a = pl.colbin[col], b = pl.rowbin[row];
                 const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
                 labels[pix] = k + 1;
                 if (score_map) score_map[pix] = expf(-(float)(D * 0x1p-12));
