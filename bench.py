@@ -117,8 +117,8 @@ def frame_bytes(spec, frame):
         "literal": npx * spec.D * es + 4 * npx,
         "compact": npx * es + 4 * nfg + 4 * (npx - nfg),
         "recover_vote": 4 * nfg + nfg * spec.D * es,
-        "peaks": 0,
         "assign_label": 4 * nfg + nfg * spec.D * es + 4 * nfg,
+        "peaks_assign_label": npx * spec.D * es + npx * es + 4 * npx,
         "n_fg": nfg,
     }
 
@@ -265,7 +265,7 @@ def bench_config(cfg, steps, warmup, n_frames=None, bins=None, th=None, loaded=N
 
 def cpu_baseline(cfg, frames, budget_s=12.0):
     """The oracle on the step's frames in order, cycling through them until
-    about budget_s seconds of CPU work are done."""
+    about budget_s seconds of CPU work are done (at least one decode)."""
     import oracle
     th = thresholds()[str(cfg)]
     spec = frames[0].spec
@@ -352,7 +352,7 @@ def sweep(steps, warmup):
         s, fr, ms, st, by, ws = bench_config(5, steps, warmup, bins=b, th=th, loaded=loaded)
         out["bins_sweep"].append({"workload": s.name, "bins": b, "ms_per_frame": round(ms, 5),
                                   "frames_per_s": round(1000.0 / ms, 1), "workspace_bytes": ws,
-                                  "path": "matrix-core" if b <= 32 else "generic",
+                                  "path": "matrix-core" if b <= 32 else "matrix-core vote, generic assignment",
                                   "stages_ms": {k: round(v, 5) for k, v in st.items()},
                                   "paper_ms_orin_nano_fp32": PAPER_TABLE1_MS[b]})
     del loaded
@@ -476,6 +476,8 @@ def main():
                                   "ms_per_frame_stats": bench_config.latency,
                                   "stages_ms": {k: round(v, 5) for k, v in st.items()},
                                   "quality_vs_instances": b["quality"]}
+            if cfg == 3 and not args.no_cpu:      # one oracle decode of the frame, one core
+                extra["cfg3"]["cpu_baseline"] = cpu_baseline(3, loaded[1], budget_s=0.1)
             # the same frame decoded with only the harmonics the 32x32 grid resolves
             fx, fy = s.freqs()
             n = harmonics.resolved_pair(fx, fy, s.W, s.H, s.bins, s.bins)

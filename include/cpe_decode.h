@@ -268,11 +268,12 @@ size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
  * launches its i-th kernel (i = 0, 1, 2) so that the dispatch itself records
  * events[2i] when the kernel starts and events[2i+1] when it ends, on the
  * decode's stream; hipEventElapsedTime(events[2i], events[2i+1]) is then that
- * kernel's duration.  Grids up to 32 x 32 bins: 0 = compaction of the
- * participating pixels, 1 = recovery + voting, 2 = peak extraction +
- * assignment (without a foreground channel launch 0 is skipped and its two
- * events are recorded back to back).  Larger grids: 0 = recovery + voting,
- * 1 = peak extraction, 2 = assignment.  `n_events` must be CPE_STAGE_EVENTS;
+ * kernel's duration: 0 = compaction of the participating pixels and
+ * clearing of the vote histograms (only the clearing without a foreground
+ * channel), 1 = recovery + voting, 2 = peak extraction + assignment (one
+ * kernel for grids up to 32 x 32 bins; above, events 4 and 5 bracket the
+ * peak kernel and the assignment kernel that follows it).  `n_events` must
+ * be CPE_STAGE_EVENTS;
  * the caller owns the events and must keep them alive while set.  NULL
  * switches the recording off.
  */

@@ -19,6 +19,7 @@ constexpr int kMaxBins = 128;
 constexpr int kCountCap = 1024;       // centroids whose pixel counts are privatised in LDS
 constexpr int kMfmaBins = 32;         // bin grids up to 32 x 32 take the matrix-core path
 constexpr int kPopKinds = 3;          // int8 palette operand kinds per axis (AxisOp in k_mfma.hpp)
+constexpr int kMaxBinBlocks = (kMaxBins + kMfmaBins - 1) / kMfmaBins;   // blocks of 32 bins per axis
 
 typedef short v2s __attribute__((ext_vector_type(2)));
 
@@ -32,10 +33,11 @@ struct Tables {
     const float *cx;          // [Bw] bin centres (pixels)
     const float *cy;          // [Bh]
     // matrix-core path (bins <= 32)
-    const uint32_t *np1_x;    // [32] |P_w[bin]|^2 + 1 (1 for padded bins)
-    const uint32_t *np1_y;    // [32]
-    const uint32_t *pop;      // [axis][kind][64 lanes][4 words]: the int8 palette operand of lane l
-                              //   (bin l & 31, K slots 16 (l >> 5) .. + 15); see k_mfma.hpp
+    const uint32_t *np1_x;    // [kMaxBinBlocks * 32] |P_w[bin]|^2 + 1 (1 for padded bins)
+    const uint32_t *np1_y;    // [kMaxBinBlocks * 32]
+    const uint32_t *pop;      // [axis][block][kind][64 lanes][4 words]: the int8 palette operand of
+                              //   lane l (bin 32 block + (l & 31), K slots 16 (l >> 5) .. + 15);
+                              //   see k_mfma.hpp
     const uint32_t *wt_pk;    // [kWKeys] weight as two fp16 limbs (q & 255) | (q >> 8) << 16,
                               //          at LDS position ((e + 31) & 31) * 256 + t
 };

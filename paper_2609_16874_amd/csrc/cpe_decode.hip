@@ -7,14 +7,14 @@
 //
 // Launches per frame on the caller's stream (launch.hpp), no allocation, no
 // host synchronisation, no host copy:
+//   compact participating-pixel list, vote histograms cleared (k_compact);
 //   vote    per-pixel recovery + soft voting into replicated 64-bit histograms
-//           (k_vote_mfma for grids up to 32 x 32, k_vote_generic otherwise);
-//   peaks   local-maxima search and compaction (k_peaks, larger grids only);
+//           (k_vote_mfma, one pass per block of 32 x 32 bins);
+//   peaks   local-maxima search and compaction (k_peaks, grids above 32 x 32);
 //   assign  nearest-candidate assignment, label and score write-out, pixel
-//           counts (k_assign_mfma / k_assign_generic).
-// For grids up to 32 x 32 every assignment workgroup extracts the peaks in
-// its prologue, so a frame is two launches.  cpe_decode_masks expands a
-// label map into binary masks (masks.hip).
+//           counts (k_assign_mfma, whose workgroups extract the peaks in
+//           their prologue, for grids up to 32 x 32; k_assign_generic above).
+// cpe_decode_masks expands a label map into binary masks (masks.hip).
 
 #include <hip/hip_runtime.h>
 
@@ -260,27 +260,28 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     pack(bins_h, h->pal_y, pky, n2y);
 
     // matrix-core operands: -2P = 128 hi + lo with lo in [-64, 63] (|hi| <= 64),
-    // as int8 MFMA operands [axis][kind][64 lanes][16 bytes]: lane l holds bin
-    // l & 31 and the K slots 16 g .. 16 g + 15 (g = l >> 5), whose channels are
-    // those the pixel operand of the same half holds (AxisOp in k_mfma.hpp):
-    // for 2F > 16 byte b is channel 8 g + b (b < 8) or 16 + 8 g + b - 8, kind 0
-    // = hi, kind 1 = lo; for 2F <= 16 bytes b and 8 + b both belong to channel
-    // 8 g + b, kinds (hi, 0), (lo, hi), (0, lo).  Padded bins and channels are
-    // 0, and |P|^2 + 1 per bin (1 for padded bins).
-    std::vector<int8_t> pop((size_t)2 * kPopKinds * 64 * 16, 0);
-    std::vector<uint32_t> np1x(32, 1u), np1y(32, 1u);
-    if (bins_w <= kMfmaBins && bins_h <= kMfmaBins) {
-        for (int ax = 0; ax < 2; ax++) {
-            const int n = ax ? bins_h : bins_w;
-            const std::vector<int16_t> &pal = ax ? h->pal_y : h->pal_x;
-            auto limb = [&](int bin, int c, int which) -> int {     // which 0: hi, 1: lo
-                if (bin >= n || c >= twoF) return 0;
-                const int m2 = -2 * (int)pal[(size_t)bin * twoF + c];
-                const int lo = ((m2 + 64) & 127) - 64;
-                return which ? lo : (m2 - lo) / 128;
-            };
+    // as int8 MFMA operands [axis][block of 32 bins][kind][64 lanes][16 bytes]:
+    // lane l holds bin 32 block + (l & 31) and the K slots 16 g .. 16 g + 15
+    // (g = l >> 5), whose channels are those the pixel operand of the same half
+    // holds (AxisOp in k_mfma.hpp): for 2F > 16 byte b is channel 8 g + b
+    // (b < 8) or 16 + 8 g + b - 8, kind 0 = hi, kind 1 = lo; for 2F <= 16 bytes b
+    // and 8 + b both belong to channel 8 g + b, kinds (hi, 0), (lo, hi),
+    // (0, lo).  Padded bins and channels are 0, and |P|^2 + 1 per bin (1 for
+    // padded bins).
+    std::vector<int8_t> pop((size_t)2 * kMaxBinBlocks * kPopKinds * 64 * 16, 0);
+    std::vector<uint32_t> np1x(kMaxBinBlocks * 32, 1u), np1y(kMaxBinBlocks * 32, 1u);
+    for (int ax = 0; ax < 2; ax++) {
+        const int n = ax ? bins_h : bins_w;
+        const std::vector<int16_t> &pal = ax ? h->pal_y : h->pal_x;
+        auto limb = [&](int bin, int c, int which) -> int {     // which 0: hi, 1: lo
+            if (bin >= n || c >= twoF) return 0;
+            const int m2 = -2 * (int)pal[(size_t)bin * twoF + c];
+            const int lo = ((m2 + 64) & 127) - 64;
+            return which ? lo : (m2 - lo) / 128;
+        };
+        for (int blk = 0; blk < kMaxBinBlocks; blk++)
             for (int l = 0; l < 64; l++) {
-                const int bin = l & 31, g = l >> 5;
+                const int bin = 32 * blk + (l & 31), g = l >> 5;
                 for (int b = 0; b < 16; b++) {
                     int v[kPopKinds];
                     if (twoF > 16) {
@@ -295,13 +296,12 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
                         v[2] = b < 8 ? 0 : limb(bin, c, 1);
                     }
                     for (int k = 0; k < kPopKinds; k++)
-                        pop[(((size_t)ax * kPopKinds + k) * 64 + l) * 16 + b] = (int8_t)v[k];
+                        pop[((((size_t)ax * kMaxBinBlocks + blk) * kPopKinds + k) * 64 + l) * 16 + b] = (int8_t)v[k];
                 }
             }
-            std::vector<uint32_t> &np1 = ax ? np1y : np1x;
-            const std::vector<uint32_t> &n2 = ax ? n2y : n2x;
-            for (int bin = 0; bin < n; bin++) np1[bin] = n2[bin] + 1u;
-        }
+        std::vector<uint32_t> &np1 = ax ? np1y : np1x;
+        const std::vector<uint32_t> &n2 = ax ? n2y : n2x;
+        for (int bin = 0; bin < n; bin++) np1[bin] = n2[bin] + 1u;
     }
 
     // one allocation: constants, replicated histograms, last histogram, peak list, counters

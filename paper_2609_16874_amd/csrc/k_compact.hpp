@@ -136,7 +136,7 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact(const T *__restrict
 namespace {   // one private copy per translation unit that launches it
 
 // Zero n words (the vote histograms of a frame without a compaction launch).
-__global__ __launch_bounds__(256) void k_clear_u64(unsigned long long *__restrict__ p, int32_t n)
+__global__ __launch_bounds__(256) __attribute__((unused)) void k_clear_u64(unsigned long long *__restrict__ p, int32_t n)
 {
     for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0ull;
 }

@@ -1,19 +1,19 @@
-// k_generic.hpp -- decoder kernels for any bin grid up to 128 x 128.
+// k_generic.hpp -- the assignment kernel for bin grids above 32 x 32 (up to
+// 128 x 128).
 //
 // One thread per foreground pixel computes the per-axis squared distances to
-// every palette entry with packed 16-bit dot products (Eq4/Eq10), and
-//   k_vote_generic    turns them into bucket weights and accumulates the soft
-//                     votes (Eq6/Eq11) into a register-tiled 64-bit
-//                     histogram, flushed with global atomics into one of the
-//                     replicated histograms;
-//   k_assign_generic  turns them into distances sqrt_cr(fl32(S)), assigns the
-//                     pixel to the candidate with the smallest exact distance
-//                     sum (Eq7, lowest index on ties), writes its label and
-//                     score and counts it.
-// Grids up to 32 x 32 bins use the matrix-core kernels of k_mfma.hpp instead.
+// every palette entry with packed 16-bit dot products (Eq4/Eq10), turns them
+// into distances sqrt_cr(fl32(S)), assigns the pixel to the candidate with
+// the smallest exact distance sum (Eq7, lowest index on ties), writes its
+// label and score and counts it.  The candidates come from the stand-alone
+// peak kernel (k_peaks.hpp); the votes of every grid are cast by the
+// matrix-core kernel of k_mfma.hpp, and grids up to 32 x 32 also take its
+// matrix-core assignment.
 #pragma once
 
 #include "cpe_common.hpp"
+#include "k_compact.hpp"
+#include "k_peaks.hpp"
 
 namespace cpe {
 
@@ -56,117 +56,27 @@ struct PixelLayout {
 };
 
 // ---------------------------------------------------------------------------
-// S1 + S2: recovery and soft voting
-// ---------------------------------------------------------------------------
-template <typename T, int F>
-__global__ __launch_bounds__(256) void k_vote_generic(const T *__restrict__ emb, int32_t dstride, int32_t yoff,
-                                              const T *__restrict__ fg, int32_t npix,
-                                              float fg_thr, Tables tb, int32_t Bw, int32_t Bh,
-                                              unsigned long long *__restrict__ hrep)
-{
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int TP = blockDim.x;
-    const int tid = threadIdx.x;
-    int32_t *s_px = reinterpret_cast<int32_t *>(smem);
-    int32_t *s_py = s_px + Bw * F;
-    uint32_t *s_nx = reinterpret_cast<uint32_t *>(s_py + Bh * F);
-    uint32_t *s_ny = s_nx + Bw;
-    int32_t *s_list = reinterpret_cast<int32_t *>(s_ny + Bh);   // [TP]
-    int32_t *s_n = s_list + TP;                                  // [4]
-    uint16_t *s_wt = reinterpret_cast<uint16_t *>(s_n + 4);      // [kWKeys]
-    uint16_t *s_qx = s_wt + kWKeys;                              // [Bw][TP]
-    uint16_t *s_qy = s_qx + Bw * TP;                             // [Bh][TP]
-
-    for (int i = tid; i < Bw * F; i += TP) s_px[i] = tb.pal_x[i];
-    for (int i = tid; i < Bh * F; i += TP) s_py[i] = tb.pal_y[i];
-    for (int i = tid; i < Bw; i += TP) s_nx[i] = tb.n2_x[i];
-    for (int i = tid; i < Bh; i += TP) s_ny[i] = tb.n2_y[i];
-    for (int i = tid; i < kWKeys; i += TP) s_wt[i] = tb.wt[i];
-
-    using L = PixelLayout<T, F>;
-    const int nb = Bw * Bh;
-    const int per_chunk = 4 * TP;
-    const int nchunks = (nb + per_chunk - 1) / per_chunk;
-    unsigned long long *hdst = hrep + (size_t)(blockIdx.x % kReplicas) * nb;
-
-    unsigned long long acc[4] = {0ull, 0ull, 0ull, 0ull};
-    int ba[4], bb[4];
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-        int bin = j * TP + tid;
-        ba[j] = bin % Bw;
-        bb[j] = (bin / Bw) < Bh ? bin / Bw : 0;
-    }
-
-    for (int64_t tile = blockIdx.x; tile * TP < npix; tile += gridDim.x) {
-        if (tid == 0) *s_n = 0;
-        __syncthreads();
-        const int64_t p = tile * TP + tid;
-        if (p < npix && fg_value<T>(fg, p) > fg_thr) {
-            int slot = atomicAdd(s_n, 1);
-            s_list[slot] = (int32_t)p;
-        }
-        __syncthreads();
-        const int n = *s_n;
-        if (tid < n) {
-            const T *row = emb + (size_t)s_list[tid] * dstride;
-            int32_t xk[F], yk[F];
-            load_block<T, F, L::kAlignX>(row, xk);
-            load_block<T, F, L::kAlignY>(row + yoff, yk);
-            const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
-            const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
-            for (int a = 0; a < Bw; a++)
-                s_qx[a * TP + tid] = s_wt[dist_key<kWMant>(axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)))];
-            for (int b = 0; b < Bh; b++)
-                s_qy[b * TP + tid] = s_wt[dist_key<kWMant>(axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)))];
-        }
-        __syncthreads();
-        if (nchunks == 1) {
-            for (int i = 0; i < n; i++) {
-#pragma unroll
-                for (int j = 0; j < 4; j++)
-                    acc[j] += (unsigned long long)((uint32_t)s_qx[ba[j] * TP + i] * (uint32_t)s_qy[bb[j] * TP + i]);
-            }
-        } else {
-            for (int c = 0; c < nchunks; c++) {
-                unsigned long long part[4] = {0ull, 0ull, 0ull, 0ull};
-                int ca[4], cb[4];
-#pragma unroll
-                for (int j = 0; j < 4; j++) {
-                    int bin = c * per_chunk + j * TP + tid;
-                    ca[j] = bin % Bw;
-                    cb[j] = (bin / Bw) < Bh ? bin / Bw : 0;
-                }
-                for (int i = 0; i < n; i++) {
-#pragma unroll
-                    for (int j = 0; j < 4; j++)
-                        part[j] += (unsigned long long)((uint32_t)s_qx[ca[j] * TP + i] * (uint32_t)s_qy[cb[j] * TP + i]);
-                }
-#pragma unroll
-                for (int j = 0; j < 4; j++) {
-                    int bin = c * per_chunk + j * TP + tid;
-                    if (bin < nb && part[j]) atomicAdd(hdst + bin, part[j]);
-                }
-            }
-        }
-        __syncthreads();
-    }
-    if (nchunks == 1) {
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-            int bin = j * TP + tid;
-            if (bin < nb && acc[j]) atomicAdd(hdst + bin, acc[j]);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
 // S4 + S5: assignment, label write-out, counts
 // ---------------------------------------------------------------------------
+// LDS bytes of k_assign_generic before its per-pixel distances: palettes,
+// norms, counts, candidate slots and the slice prefix.
+__host__ __device__ constexpr size_t generic_assign_fixed(int Bw, int Bh, int F, int kmax)
+{
+    return ((size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4 + (size_t)kCountCap * 4 + (size_t)kmax * 4 +
+            2 * (size_t)kMaxBins * 2 + 2 * (size_t)kMaxBins / 8 + (size_t)(kMaxSlices + 1) * 4 + 64 + 15) &
+           ~(size_t)15;
+}
+
+// One thread per participating pixel (entries of the compact list written by
+// k_compact, or every pixel without a foreground channel).  The candidate
+// columns and rows are numbered in ascending order (slots); each thread
+// computes its pixel's distances to the slots' palette entries only, then
+// scans the candidates in index order.
 template <typename T, int F>
 __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ emb, int32_t dstride, int32_t yoff,
-                                                const T *__restrict__ fg, int32_t npix,
-                                                float fg_thr, double tau4096, Tables tb, int32_t Bw, int32_t Bh,
+                                                const int32_t *__restrict__ list, const int32_t *__restrict__ counts,
+                                                int32_t nslices, int32_t slice_px, int32_t npix,
+                                                double tau4096, Tables tb, int32_t Bw, int32_t Bh,
                                                 const int32_t *__restrict__ peaks, const int32_t *__restrict__ kinfo,
                                                 cpe_centroid *__restrict__ cents, int32_t *__restrict__ labels,
                                                 float *__restrict__ score_map)
@@ -174,60 +84,89 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
     extern __shared__ __align__(16) unsigned char smem[];
     const int TP = blockDim.x;
     const int tid = threadIdx.x;
+    const int kmax = max_peaks(Bw, Bh);
     int32_t *s_px = reinterpret_cast<int32_t *>(smem);
     int32_t *s_py = s_px + Bw * F;
     uint32_t *s_nx = reinterpret_cast<uint32_t *>(s_py + Bh * F);
     uint32_t *s_ny = s_nx + Bw;
-    int32_t *s_list = reinterpret_cast<int32_t *>(s_ny + Bh);   // [TP]
-    int32_t *s_n = s_list + TP;                                  // [4]
-    int32_t *s_cnt = s_n + 4;                                    // [kCountCap]
-    float *s_r = reinterpret_cast<float *>(s_cnt + kCountCap);   // [Bw + Bh][TP] distances
+    int32_t *s_cnt = reinterpret_cast<int32_t *>(s_ny + Bh);     // [kCountCap]
+    int32_t *s_pk = s_cnt + kCountCap;                           // [kmax] column slot | row slot << 16
+    uint16_t *s_slot = reinterpret_cast<uint16_t *>(s_pk + kmax); // [2][kMaxBins] bin -> slot
+    uint32_t *s_mask = reinterpret_cast<uint32_t *>(s_slot + 2 * kMaxBins);   // [2][kMaxBins / 32]
+    int *s_pref = reinterpret_cast<int *>(s_mask + 2 * kMaxBins / 32);      // [kMaxSlices + 1]
+    int *s_ns = s_pref + kMaxSlices + 1;                                     // [2] candidate columns, rows
+    float *s_r = reinterpret_cast<float *>(smem + generic_assign_fixed(Bw, Bh, F, kmax));  // [slots][TP]
 
     const int Kc = kinfo[0];
     const int ncnt = Kc < kCountCap ? Kc : kCountCap;
+    SliceLoad sl;
+    if (list) slice_load(counts, nslices, sl);
     for (int i = tid; i < Bw * F; i += TP) s_px[i] = tb.pal_x[i];
     for (int i = tid; i < Bh * F; i += TP) s_py[i] = tb.pal_y[i];
     for (int i = tid; i < Bw; i += TP) s_nx[i] = tb.n2_x[i];
     for (int i = tid; i < Bh; i += TP) s_ny[i] = tb.n2_y[i];
     for (int i = tid; i < ncnt; i += TP) s_cnt[i] = 0;
+    for (int i = tid; i < 2 * kMaxBins / 32; i += TP) s_mask[i] = 0u;
+    if (list) slice_scan(sl, nslices, s_pref);
+    __syncthreads();
+    // candidate columns and rows as bit masks, then their slots in ascending order
+    for (int k = tid; k < Kc; k += TP) {
+        const int32_t pk = peaks[k], a = pk & 0xffff, b = pk >> 16;
+        atomicOr(&s_mask[a >> 5], 1u << (a & 31));
+        atomicOr(&s_mask[kMaxBins / 32 + (b >> 5)], 1u << (b & 31));
+    }
+    __syncthreads();
+    for (int i = tid; i < 2 * kMaxBins; i += TP) {
+        const int ax = i / kMaxBins, bin = i % kMaxBins;
+        const uint32_t *m = s_mask + ax * (kMaxBins / 32);
+        int below = __popc(m[bin >> 5] & ((1u << (bin & 31)) - 1u));
+        for (int w = 0; w < (bin >> 5); w++) below += __popc(m[w]);
+        s_slot[i] = (uint16_t)below;
+        if (bin == kMaxBins - 1) s_ns[ax] = below + (int)((m[bin >> 5] >> 31) & 1u);
+    }
+    __syncthreads();
+    for (int k = tid; k < Kc; k += TP) {
+        const int32_t pk = peaks[k];
+        s_pk[k] = (int32_t)s_slot[pk & 0xffff] | ((int32_t)s_slot[kMaxBins + (pk >> 16)] << 16);
+    }
+    __syncthreads();
+    const int ncol = s_ns[0], nrow = s_ns[1];
 
     using L = PixelLayout<T, F>;
-    for (int64_t tile = blockIdx.x; tile * TP < npix; tile += gridDim.x) {
-        if (tid == 0) *s_n = 0;
-        __syncthreads();
-        const int64_t p = tile * TP + tid;
-        if (p < npix) {
-            const bool part = Kc > 0 && fg_value<T>(fg, p) > fg_thr;
-            if (part) {
-                int slot = atomicAdd(s_n, 1);
-                s_list[slot] = (int32_t)p;
-            } else {
-                labels[p] = 0;
-                if (score_map) score_map[p] = 0.0f;
+    const int n = list ? s_pref[nslices] : npix;
+    const int stride = gridDim.x * TP;
+    const int first = blockIdx.x * TP + (tid & ~63);             // the wave's first entry
+    ListCursor cur;
+    cur.start(list, s_pref, nslices, slice_px, first < n ? first : 0);
+    for (int i = blockIdx.x * TP + tid; i - tid + (tid & ~63) < n; i += stride) {
+        if (i < n) {
+            const int32_t pp = cur.pixel(i);
+            if (Kc == 0) {
+                labels[pp] = 0;
+                if (score_map) score_map[pp] = 0.0f;
+                continue;
             }
-        }
-        __syncthreads();
-        const int n = *s_n;
-        if (tid < n) {
-            const int32_t pp = s_list[tid];
             const T *row = emb + (size_t)pp * dstride;
             int32_t xk[F], yk[F];
             load_block<T, F, L::kAlignX>(row, xk);
             load_block<T, F, L::kAlignY>(row + yoff, yk);
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
-            for (int a = 0; a < Bw; a++)
-                s_r[a * TP + tid] = sqrt_cr((float)axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)));
-            for (int b = 0; b < Bh; b++)
-                s_r[(Bw + b) * TP + tid] = sqrt_cr((float)axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)));
+            // distances of the candidate columns and rows (the slots' bins)
+            for (int a = 0, s = 0; a < Bw; a++)
+                if ((s_mask[a >> 5] >> (a & 31)) & 1u)
+                    s_r[(s++) * TP + tid] = sqrt_cr((float)axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)));
+            for (int b = 0, s = ncol; b < Bh; b++)
+                if ((s_mask[kMaxBins / 32 + (b >> 5)] >> (b & 31)) & 1u)
+                    s_r[(s++) * TP + tid] = sqrt_cr((float)axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)));
             // Eq7: smallest exact sum (binary64 holds the sum of two binary32
             // values exactly), lowest index on ties
             int best = 0;
-            const int32_t pk0 = peaks[0];
-            double bd = (double)s_r[(pk0 & 0xffff) * TP + tid] + (double)s_r[(Bw + (pk0 >> 16)) * TP + tid];
+            const int32_t pk0 = s_pk[0];
+            double bd = (double)s_r[(pk0 & 0xffff) * TP + tid] + (double)s_r[(ncol + (pk0 >> 16)) * TP + tid];
             for (int k = 1; k < Kc; k++) {
-                const int32_t pk = peaks[k];
-                const double d = (double)s_r[(pk & 0xffff) * TP + tid] + (double)s_r[(Bw + (pk >> 16)) * TP + tid];
+                const int32_t pk = s_pk[k];
+                const double d = (double)s_r[(pk & 0xffff) * TP + tid] + (double)s_r[(ncol + (pk >> 16)) * TP + tid];
                 if (d < bd) {
                     bd = d;
                     best = k;
@@ -245,8 +184,8 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
                 if (score_map) score_map[pp] = 0.0f;
             }
         }
-        __syncthreads();
     }
+    (void)nrow;
     __syncthreads();
     for (int i = tid; i < ncnt; i += TP)
         if (s_cnt[i]) atomicAdd(&cents[i].npix, s_cnt[i]);

@@ -282,6 +282,17 @@ __device__ __forceinline__ i32x4 palette_operand(const uint32_t *__restrict__ po
     return *reinterpret_cast<const i32x4 *>(pop + (((ax * kPopKinds + k) * 64 + lane) * 4));
 }
 
+// Word group i (16 bytes) of the LDS palette operands [axis][kind][64][16] for
+// the x bins of block bx and the y bins of block by, from the table
+// [axis][kMaxBinBlocks][kind][64][16].
+__device__ __forceinline__ u32x4 pop_block(const uint32_t *__restrict__ pop, int i, int bx, int by)
+{
+    constexpr int kAxis = kPopKinds * 64;                 // 16-byte groups per axis and block
+    const int ax = i / kAxis, r = i % kAxis;
+    const int blk = ax ? by : bx;
+    return reinterpret_cast<const u32x4 *>(pop)[(ax * kMaxBinBlocks + blk) * kAxis + r];
+}
+
 // The three limb products of one axis: hh = Xh.hi, mid = Xh.lo + Xl.hi and
 // ll = ll0 + Xl.lo (ll0: the starting values).  PIX_ROWS: pixels are the
 // MFMA rows (pass 1) or its columns (pass 2).
@@ -383,6 +394,8 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     cpe_centroid *__restrict__ cents, int32_t cap)
 {
     constexpr int kWpb = kVoteWpb<T, F>;
+    // blocks of 32 x 32 bins: one pass over the workgroup's tiles per block
+    const int nbx = (Bw + kMfmaBins - 1) / kMfmaBins, nby = (Bh + kMfmaBins - 1) / kMfmaBins;
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
@@ -396,9 +409,10 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     const int g = lane >> 5, ln = lane & 31;
     SliceLoad sl;
     if (list) slice_load(counts, nslices, sl);
-    // the bin constants of this lane's bin (loaded with the tables, not after
-    // the barrier, where they would cost a memory round trip of their own)
-    const uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
+    // the bin constants of this lane's bin in the first block (loaded with
+    // the tables, not after the barrier, where they would cost a memory round
+    // trip of their own)
+    uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
     {
         constexpr int kThreads = kWpb * 64, kN = kWKeys / 4, kPer = (kN + kThreads - 1) / kThreads;
         u32x4 w[kPer];
@@ -413,8 +427,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             if (i < kN) reinterpret_cast<u32x4 *>(s_wt)[i] = w[k];
         }
         for (int i = tid; i < kMfmaBins * kHStride; i += kThreads) s_h[i] = 0ull;
-        for (int i = tid; i < kPopBytes / 16; i += kThreads)
-            reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
+        for (int i = tid; i < kPopBytes / 16; i += kThreads) reinterpret_cast<u32x4 *>(s_pop)[i] = pop_block(tb.pop, i, 0, 0);
         if (tid == 0) *s_next = 0;
         if (list) slice_scan(sl, nslices, s_pref);
     }
@@ -518,41 +531,57 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    int t = t0 + wv;
-    ListCursor cur_list;
-    cur_list.start(list, s_pref, nslices, slice_px, t < tend ? 32 * t : 0);
-    // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
-    auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
-    // the next tile's rows are loaded as soon as the current ones are converted
-    RawSlices<T, F> raw;
-    int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it
-    if (t < tend) {
-        raw.load(emb + (size_t)pixel(t) * dstride, yoff, g);
-        tn = take_tile(s_next, lane, t0, kWpb);
-        if (tn < tend) idx = pixel(tn);
-    }
-    while (t < tend) {
-        int tnn = tend;
-        tile(raw, min(32, n - 32 * t), [&]() {
-            if (tn < tend) {
-                raw.load(emb + (size_t)idx * dstride, yoff, g);
-                tnn = take_tile(s_next, lane, t0, kWpb);
-                if (tnn < tend) idx = pixel(tnn);
-            }
-        });
-        t = tn;
-        tn = tnn;
-    }
-    fold();
+    for (int blk = 0; blk < nbx * nby; blk++) {
+        const int bx = blk % nbx, by = blk / nbx;
+        if (blk > 0) {
+            // the next block: its palette operands and bin constants, a clear
+            // histogram and tile counter (the previous pass has flushed)
+            np1x = tb.np1_x[kMfmaBins * bx + ln];
+            np1y = tb.np1_y[kMfmaBins * by + ln];
+            for (int i = tid; i < kMfmaBins * kHStride; i += blockDim.x) s_h[i] = 0ull;
+            for (int i = tid; i < kPopBytes / 16; i += blockDim.x)
+                reinterpret_cast<u32x4 *>(s_pop)[i] = pop_block(tb.pop, i, bx, by);
+            if (tid == 0) *s_next = 0;
+            __syncthreads();
+        }
+        int t = t0 + wv;
+        ListCursor cur_list;
+        cur_list.start(list, s_pref, nslices, slice_px, t < tend ? 32 * t : 0);
+        // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
+        auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
+        // the next tile's rows are loaded as soon as the current ones are converted
+        RawSlices<T, F> raw;
+        int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it
+        if (t < tend) {
+            raw.load(emb + (size_t)pixel(t) * dstride, yoff, g);
+            tn = take_tile(s_next, lane, t0, kWpb);
+            if (tn < tend) idx = pixel(tn);
+        }
+        while (t < tend) {
+            int tnn = tend;
+            tile(raw, min(32, n - 32 * t), [&]() {
+                if (tn < tend) {
+                    raw.load(emb + (size_t)idx * dstride, yoff, g);
+                    tnn = take_tile(s_next, lane, t0, kWpb);
+                    if (tnn < tend) idx = pixel(tnn);
+                }
+            });
+            t = tn;
+            tn = tnn;
+        }
+        fold();
+        ntile = 0;
 
-    // one global atomic per bin of the grid
-    __syncthreads();
-    const int nb = Bw * Bh;
-    unsigned long long *dst = hrep + (size_t)(blockIdx.x % kReplicas) * nb;
-    for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
-        const int b = i / kMfmaBins, a = i % kMfmaBins;
-        const unsigned long long v = s_h[b * kHStride + a];
-        if (a < Bw && b < Bh && v) atomicAdd(dst + b * Bw + a, v);
+        // one global atomic per bin of the block
+        __syncthreads();
+        const int nb = Bw * Bh;
+        unsigned long long *dst = hrep + (size_t)(blockIdx.x % kReplicas) * nb;
+        for (int i = tid; i < kMfmaBins * kMfmaBins; i += blockDim.x) {
+            const int b = kMfmaBins * by + i / kMfmaBins, a = kMfmaBins * bx + i % kMfmaBins;
+            const unsigned long long v = s_h[(i / kMfmaBins) * kHStride + i % kMfmaBins];
+            if (a < Bw && b < Bh && v) atomicAdd(dst + b * Bw + a, v);
+        }
+        __syncthreads();
     }
     if (blockIdx.x == 0)
         for (int k = tid; k < cap; k += blockDim.x) cents[k].npix = 0;
@@ -627,8 +656,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     uint32_t *ky = kx + kMfmaBins * kKeyStride;
     SliceLoad sl;
     if (list) slice_load(counts, nslices, sl);
-    for (int i = tid; i < kPopBytes / 16; i += kThreads)
-        reinterpret_cast<u32x4 *>(s_pop)[i] = reinterpret_cast<const u32x4 *>(tb.pop)[i];
+    for (int i = tid; i < kPopBytes / 16; i += kThreads) reinterpret_cast<u32x4 *>(s_pop)[i] = pop_block(tb.pop, i, 0, 0);
     if (tid < 2 * kMfmaBins) {
         const int bin = tid & (kMfmaBins - 1);
         s_cb[tid] = tid < kMfmaBins ? (bin < Bw ? tb.n2_x[bin] : 0u) : (bin < Bh ? tb.n2_y[bin] : 0u);

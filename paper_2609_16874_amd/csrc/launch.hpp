@@ -59,36 +59,35 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
             hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
         return hipGetLastError() == hipSuccess;
     };
-    const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;
-    const size_t tables = (size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4;
+    const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;     // the matrix-core assignment (and its peak prologue)
     const int nclear = kReplicas * nb;
     const int clear_grid = (nclear + 255) / 256 < 64 ? (nclear + 255) / 256 : 64;
 
+    // launch 0: the participating pixels as a compact list (every pixel when
+    // the frame has no foreground channel) and the vote histograms cleared
+    int32_t *list = g ? sc.list : nullptr;
+    const int nslices = slice_count(npix), slice_px = slice_pixels(npix);
+    bool ok;
+    if (!g)
+        ok = launch(0, k_clear_u64, dim3(clear_grid), dim3(256), 0, sc.hrep, nclear);
+    else if (((uintptr_t)g & 15u) == 0)
+        ok = launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, sc.counts,
+                    labels, score, sc.hrep, nclear);
+    else
+        ok = launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, sc.counts,
+                    labels, score, sc.hrep, nclear);
+    if (!ok) return CPE_ERR_HIP;
+    // launch 1: recovery + voting, one pass per block of 32 x 32 bins; grid:
+    // at most one workgroup per compute unit, no more waves than tiles
+    constexpr int wpb = kVoteWpb<T, F>;
+    const int64_t tiles = ((int64_t)npix + 31) / 32;
+    const int64_t wgs = (tiles + wpb - 1) / wpb;
+    const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
+    if (!launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
+                (const int32_t *)sc.counts, nslices, slice_px, npix, h->tb, Bw, Bh, sc.hrep, cents, h->cap))
+        return CPE_ERR_HIP;
     if (mfma) {
-        // the participating pixels as a compact list (every pixel when the
-        // frame has no foreground channel) and the vote histograms cleared,
-        // recovery + voting into them, then the assignment launch, which
-        // extracts the peaks in its prologue
-        int32_t *list = g ? sc.list : nullptr;
-        const int nslices = slice_count(npix), slice_px = slice_pixels(npix);
-        bool ok;
-        if (!g)
-            ok = launch(0, k_clear_u64, dim3(clear_grid), dim3(256), 0, sc.hrep, nclear);
-        else if (((uintptr_t)g & 15u) == 0)
-            ok = launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list,
-                        sc.counts, labels, score, sc.hrep, nclear);
-        else
-            ok = launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list,
-                        sc.counts, labels, score, sc.hrep, nclear);
-        if (!ok) return CPE_ERR_HIP;
-        // grids: at most one workgroup per compute unit, no more waves than tiles
-        constexpr int wpb = kVoteWpb<T, F>;
-        const int64_t tiles = ((int64_t)npix + 31) / 32;
-        const int64_t wgs = (tiles + wpb - 1) / wpb;
-        const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-        if (!launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
-                    (const int32_t *)sc.counts, nslices, slice_px, npix, h->tb, Bw, Bh, sc.hrep, cents, h->cap))
-            return CPE_ERR_HIP;
+        // launch 2: peak extraction in every workgroup's prologue, assignment
         const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
         if (!launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
@@ -96,32 +95,37 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
                     (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score))
             return CPE_ERR_HIP;
     } else {
-        // the vote histograms cleared (before launch 0's start event), then
-        // recovery + voting, peak extraction, assignment
-        if (fail_at == 0) return CPE_ERR_HIP;
-        hipLaunchKernelGGL(k_clear_u64, dim3(clear_grid), dim3(256), 0, stream, sc.hrep, nclear);
-        if (hipGetLastError() != hipSuccess) return CPE_ERR_HIP;
-        const size_t fixed = tables + 16 + kWKeys * 2;
-        const int tp = pick_tile(fixed, (size_t)(Bw + Bh) * 2 + 4, 96 * 1024);
-        const size_t lds = fixed + (size_t)tp * 4 + (size_t)(Bw + Bh) * tp * 2;
-        const int64_t tiles = ((int64_t)npix + tp - 1) / tp;
-        const int grid = (int)(tiles < 1024 ? tiles : 1024);
-        if (!launch(0, k_vote_generic<T, F>, dim3(grid), dim3(tp), lds, e, dstride, yoff, g, npix, fg_thr, h->tb, Bw,
-                    Bh, sc.hrep))
-            return CPE_ERR_HIP;
+        // launch 2 (larger grids): the stand-alone peak kernel, then the
+        // generic assignment; the stage events bracket both (start of the
+        // first, end of the second)
+        if (fail_at == 2) return CPE_ERR_HIP;
         const PeakOut po{cents, num, sc.peaks, sc.kinfo};
-        if (!launch(1, k_peaks, dim3(1), dim3(1024), (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4,
-                    (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po))
-            return CPE_ERR_HIP;
-        const size_t fixed2 = tables + 16 + kCountCap * 4;
-        const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4 + 4, 120 * 1024);
-        const size_t lds2 = fixed2 + (size_t)tp2 * 4 + (size_t)(Bw + Bh) * tp2 * 4;
+        const size_t plds = (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4;
+        if (h->stage_on)
+            hipExtLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (uint32_t)plds, stream, h->stage_ev[4], nullptr, 0u,
+                                  (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx,
+                                  h->tb.cy, po);
+        else
+            hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), plds, stream, (const unsigned long long *)sc.hrep,
+                               sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
+        if (hipGetLastError() != hipSuccess) return CPE_ERR_HIP;
+        const size_t fixed2 = generic_assign_fixed(Bw, Bh, F, max_peaks(Bw, Bh));
+        const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4, 120 * 1024);
+        const size_t lds2 = fixed2 + (size_t)(Bw + Bh) * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
-        if (!launch(2, k_assign_generic<T, F>, dim3(grid2), dim3(tp2), lds2, e, dstride, yoff, g, npix, fg_thr,
-                    fa.tau4096, h->tb, Bw, Bh, (const int32_t *)sc.peaks, (const int32_t *)sc.kinfo, cents, labels,
-                    score))
-            return CPE_ERR_HIP;
+        auto assign_kernel = k_assign_generic<T, F>;
+        if (h->stage_on)
+            hipExtLaunchKernelGGL(assign_kernel, dim3(grid2), dim3(tp2), (uint32_t)lds2, stream, nullptr,
+                                  h->stage_ev[5], 0u, e, dstride, yoff, (const int32_t *)list,
+                                  (const int32_t *)sc.counts, nslices, slice_px, npix, fa.tau4096, h->tb, Bw, Bh,
+                                  (const int32_t *)sc.peaks, (const int32_t *)sc.kinfo, cents, labels, score);
+        else
+            hipLaunchKernelGGL(assign_kernel, dim3(grid2), dim3(tp2), lds2, stream, e, dstride, yoff,
+                               (const int32_t *)list, (const int32_t *)sc.counts, nslices, slice_px, npix,
+                               fa.tau4096, h->tb, Bw, Bh, (const int32_t *)sc.peaks, (const int32_t *)sc.kinfo, cents,
+                               labels, score);
+        if (hipGetLastError() != hipSuccess) return CPE_ERR_HIP;
     }
     return CPE_OK;
 }

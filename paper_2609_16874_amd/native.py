@@ -34,10 +34,10 @@ MFMA_BINS = 32
 
 
 def stage_names(bins_w: int, bins_h: int):
-    """Names of the three launches of a frame, as timed by the stage events."""
+    """Names of the three stages of a frame, as timed by the stage events."""
     if bins_w <= MFMA_BINS and bins_h <= MFMA_BINS:
         return ("compact", "recover_vote", "assign_label")
-    return ("recover_vote", "peaks", "assign_label")
+    return ("compact", "recover_vote", "peaks_assign_label")
 
 _lib = None
 
