@@ -99,7 +99,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kWpb2 = 12;            // waves per workgroup of the assignment kernel (3 per SIMD)
 constexpr int kPopBytes = 2 * kPopKinds * 64 * 16;   // palette operands of both axes
 
 // The int8 operand of one axis of one pixel, for the lane of half g = lane >> 5
@@ -386,7 +385,10 @@ constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 // histograms `hrep` (zeroed by the frame's first launch); the assignment launch that follows
 // sums them and extracts the peaks.  Workgroup 0 also resets the pixel
 // counts of the centroid records, which the assignment launch accumulates.
-template <typename T, int F>
+// MULTI: grids above 32 x 32 bins (one pass per block of 32 x 32 bins);
+// otherwise the single block is compiled without the pass loop, whose
+// registers would otherwise spill.
+template <typename T, int F, bool MULTI>
 __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
     const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, Tables tb, int32_t Bw,
@@ -395,7 +397,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 {
     constexpr int kWpb = kVoteWpb<T, F>;
     // blocks of 32 x 32 bins: one pass over the workgroup's tiles per block
-    const int nbx = (Bw + kMfmaBins - 1) / kMfmaBins, nby = (Bh + kMfmaBins - 1) / kMfmaBins;
+    const int nbx = MULTI ? (Bw + kMfmaBins - 1) / kMfmaBins : 1, nby = MULTI ? (Bh + kMfmaBins - 1) / kMfmaBins : 1;
     // All LDS is static, so that table addresses are compile-time constants.
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
@@ -533,7 +535,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 
     for (int blk = 0; blk < nbx * nby; blk++) {
         const int bx = blk % nbx, by = blk / nbx;
-        if (blk > 0) {
+        if (MULTI && blk > 0) {
             // the next block: its palette operands and bin constants, a clear
             // histogram and tile counter (the previous pass has flushed)
             np1x = tb.np1_x[kMfmaBins * bx + ln];
@@ -590,18 +592,30 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
 // ---------------------------------------------------------------------------
 // Pass 2: assignment + label write-out
 // ---------------------------------------------------------------------------
+// Waves per SIMD of the assignment kernel: four where the register
+// allocation fits 128 registers without spilling (vector input slices and up
+// to 9 harmonics, or fp16 with 16), three otherwise; one workgroup per
+// compute unit.
+template <typename T, int F>
+constexpr int kAssignWaves = (F <= 9 || (sizeof(T) == 2 && F == 16)) ? 4 : 3;
+template <typename T, int F>
+constexpr int kAssignWpb = 4 * kAssignWaves<T, F>;
+
 // LDS bytes of k_assign_mfma: palette operands, |P|^2 by bin and by slot,
-// candidate batches, bin -> centroid table, counts, per wave x keys and y
-// distances [32 slots][kKeyStride] (u32), then the peak-extraction state.
-constexpr size_t kAssignLdsCore = (size_t)kPopBytes + 4 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 +
-                                  kMfmaBins * kMfmaBins * 2 + kMfmaBins * kMfmaBins * 4 +
-                                  (size_t)kWpb2 * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
-                                  (kMaxSlices + 1) * 4 + 16;
+// candidate batches, bin -> centroid table, counts, per wave x and y
+// distances [32 slots][kKeyStride] (u32), then the peak-extraction state;
 // then, 16-byte aligned, per wave the 32 search results of a tile (binary64
-// keys), and the summed vote histogram (32 x 32 slots)
-constexpr size_t kBestOff = (kAssignLdsCore + 15) & ~(size_t)15;
-constexpr size_t kSumOff = kBestOff + (size_t)kWpb2 * 32 * 8;
-constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
+// keys).  The summed vote histogram (32 x 32 slots, 8 KB) of the prologue
+// shares its bytes with the first waves' distance arrays, which are written
+// only after it is no longer read.
+constexpr size_t kAssignLdsCore(int wpb)
+{
+    return (size_t)kPopBytes + 4 * kMfmaBins * 4 + (size_t)kMaxBatchLds * 20 + kMfmaBins * kMfmaBins * 2 +
+           kMfmaBins * kMfmaBins * 4 + (size_t)wpb * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
+           (kMaxSlices + 1) * 4 + 16;
+}
+constexpr size_t kBestOff(int wpb) { return (kAssignLdsCore(wpb) + 15) & ~(size_t)15; }
+constexpr size_t kAssignLds(int wpb) { return kBestOff(wpb) + (size_t)wpb * 32 * 8; }
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -617,18 +631,20 @@ constexpr size_t kAssignLds = kSumOff + (size_t)kMfmaBins * kMfmaBins * 8;
 // search below).  A pixel is labelled iff its distance sum D (in units of
 // 1/4096) is below tau4096 = 4096 tau (Eq8; +inf: every pixel).
 template <typename T, int F>
-__global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb2 / 4))) void k_assign_mfma(
+__global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kAssignWaves<T, F>))) void k_assign_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
     const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, double tau4096, Tables tb,
     const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
     cpe_centroid *__restrict__ cents, int32_t *__restrict__ num, int32_t *__restrict__ labels,
     float *__restrict__ score_map)
 {
+    constexpr int kWpb2 = kAssignWpb<T, F>;
     constexpr int kThreads = kWpb2 * 64;
     static_assert(kThreads >= kPeakThreads, "the peak prologue takes two histogram slots per thread");
-    static_assert(kAssignLds <= 160 * 1024, "LDS of one compute unit");
+    static_assert(kAssignLds(kWpb2) <= 160 * 1024, "LDS of one compute unit");
+    static_assert(kMfmaBins * kMfmaBins * 8 <= 2 * kMfmaBins * kKeyStride * 4, "the summed histogram fits in wave 0's arrays");
     // All LDS is static, so that table addresses are compile-time constants.
-    __shared__ __align__(16) unsigned char smem[kAssignLds];
+    __shared__ __align__(16) unsigned char smem[kAssignLds(kWpb2)];
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(smem);                            // palette operands
     uint32_t *s_cb = s_pop + kPopBytes / 4;                                          // [2][32] |P|^2 by bin
     uint32_t *s_cbs = s_cb + 2 * kMfmaBins;                                           // [2][32] by slot
@@ -640,8 +656,8 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
     PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * kKeyStride);
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
-    unsigned long long *s_best = reinterpret_cast<unsigned long long *>(smem + kBestOff);   // [kWpb2][32]
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem + kSumOff);       // [32 * 32] summed votes
+    unsigned long long *s_best = reinterpret_cast<unsigned long long *>(smem + kBestOff(kWpb2));   // [kWpb2][32]
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_keys);              // [32 * 32] summed votes
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -697,6 +713,7 @@ __global__ __launch_bounds__(kWpb2 * 64) __attribute__((amdgpu_waves_per_eu(kWpb
         for (int i = tid; i < nb; i += kThreads) hlast[i] = s_h[(i / Bw) * 32 + i % Bw];
         if (tid == 0) *num = pl.K;
     }
+    __syncthreads();        // s_h is read; its bytes become distance arrays
 
     if (Kc == 0) {              // no centroid: every participating pixel is unlabelled
         ListCursor c0;

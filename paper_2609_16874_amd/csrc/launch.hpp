@@ -83,14 +83,16 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
     const int64_t tiles = ((int64_t)npix + 31) / 32;
     const int64_t wgs = (tiles + wpb - 1) / wpb;
     const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-    if (!launch(1, k_vote_mfma<T, F>, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
+    auto vote_kernel = mfma ? k_vote_mfma<T, F, false> : k_vote_mfma<T, F, true>;
+    if (!launch(1, vote_kernel, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
                 (const int32_t *)sc.counts, nslices, slice_px, npix, h->tb, Bw, Bh, sc.hrep, cents, h->cap))
         return CPE_ERR_HIP;
     if (mfma) {
         // launch 2: peak extraction in every workgroup's prologue, assignment
-        const int64_t wgs2 = (tiles + kWpb2 - 1) / kWpb2;
+        constexpr int wpb2 = kAssignWpb<T, F>;
+        const int64_t wgs2 = (tiles + wpb2 - 1) / wpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        if (!launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(kWpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
+        if (!launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(wpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
                     (const int32_t *)sc.counts, nslices, slice_px, npix, fa.tau4096, h->tb,
                     (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score))
             return CPE_ERR_HIP;
