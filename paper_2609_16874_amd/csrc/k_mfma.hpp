@@ -1,47 +1,5 @@
-// k_mfma.hpp -- matrix-core decoder kernels for bin grids up to 32 x 32.
-//
-// Both passes stream the compact list of participating pixels written by
-// k_compact (or every pixel, when the frame has no foreground channel): the
-// list is cut into tiles of 32 consecutive entries, every workgroup gets a
-// contiguous run of tiles of the same length to within one, and its waves
-// take the run's tiles one at a time from a counter in LDS (so that they
-// finish together however the SIMDs favour older waves), always loading the
-// embedding rows of the next tile (and the list entries of the one after)
-// before computing the current one.  Every tile but the last is full.
-//
-// Per-axis distances (Eq4/Eq10).  With the input on its 1/256 grid,
-// X = 16 Xr (Xr = rint(256 clamp(v, -1.5, 1.5)), |Xr| <= 384, exact in fp16)
-// and the palette limbs -2P = 128 hi + lo (|hi|, |lo| <= 64, exact in fp16),
-// S + 1 = 256 |Xr|^2 + (|P|^2 + 1) + 16 (128 Xr.hi + Xr.lo).  The two dot
-// products are dense [pixels x channels] x [channels x bins] contractions:
-// v_mfma_f32_32x32x16_f16 accumulating onto 1.5 * 2^23, where every partial
-// sum (at most 32 * 384 * 64 < 2^22 in magnitude) stays in the binade of unit
-// spacing, so the accumulator's bit pattern minus 0x4B400000 is the exact
-// integer: S + 1 follows from the two bit patterns with two shift-adds and
-// one add, modulo 2^32 (S + 1 < 2^32).  |Xr|^2 <= 32 * 384^2 < 2^24 is an
-// exact fp32 dot product of the fp16 operands.
-//
-// Pass 1, k_vote_mfma (recovery + soft voting, Eq5/Eq6/Eq11).  With pixels
-// as the MFMA rows, the distance result leaves in each lane one bin and 16
-// pixels -- exactly the operand layout of the vote contraction
-// H = Qx^T Qy over pixels, so the weights feed the second MFMA without any
-// data exchange between lanes.  A weight q <= 2^15 is split into fp16 limbs
-// q = 256 hi + lo; the four limb products accumulate in fp32 exactly as long
-// as at most 256 pixels are summed, after which they are added into a 64-bit
-// histogram in LDS.
-//
-// Pass 2, k_assign_mfma (assignment, Eq7, and label write-out).  Only the
-// candidate columns and rows are needed: they are numbered in ascending
-// order (slots), the MFMA rows are the slots' palette entries, each lane
-// holds one pixel and 16 slots, and codes are computed for the groups of 8
-// slots that hold candidates.  The codes go to LDS as the high halves of
-// search keys whose low halves hold the slot index, laid out so that one lane
-// serves one pixel, and the candidate search walks the batches of 4 columns
-// of one row: the key (c_x + c_y) * 2^16 + (128 row slot + column slot) is
-// minimised over the peaks, which selects the smallest code sum and, on
-// ties, the lowest (row, column) -- slots keep the bins' order -- i.e. the
-// lowest centroid index.
-// k_mfma.hpp -- matrix-core decoder kernels for bin grids up to 32 x 32.
+// k_mfma.hpp -- matrix-core decoder kernels: the vote for every bin grid (in
+// passes over blocks of 32 x 32 bins), the assignment for grids up to 32 x 32.
 //
 // Both passes stream the compact list of participating pixels written by
 // k_compact (or every pixel, when the frame has no foreground channel): the
@@ -743,7 +701,7 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     // acc_row(r, g) of each axis); `next` reuses the input registers once
     // they are converted.  The accumulators of the Xl.lo products start at
     // the slots' |P|^2; the pixel's |X|^2 completes S.
-    auto codes = [&](RawSlices<T, F> &raw, auto next) {
+    auto distances = [&](RawSlices<T, F> &raw, auto next) {
         int n2x = 0, n2y = 0;
         AxisOp<F> X, Y;
         raw.convert(0, X, n2x);
@@ -853,7 +811,7 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     }
     while (t < tend) {
         int tnn = tend, ipnn = 0;
-        codes(raw, [&]() {
+        distances(raw, [&]() {
             if (tn < tend) {
                 raw.load(emb + (size_t)ipn * dstride, yoff, g);
                 tnn = take_tile(s_next, lane, t0, kWpb2);

@@ -243,7 +243,7 @@ __device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, in
     }
     __syncthreads();
     // Slots: the candidate columns and rows, each numbered in ascending
-    // order; the assignment computes codes for slots only, and its key
+    // order; the assignment computes distances for slots only, and its
     // arrays, batches and bin constants are indexed by slot.  Lane j of the
     // first wave numbers column j and row j and scatters them (and their
     // bin constants, s_cb [2][32] by bin -> s_cbs [2][32] by slot).
