@@ -65,6 +65,11 @@ def measured_traffic(workload_tag, stage):
         return None
 
 
+def progress(msg):
+    """A progress line on stderr (stdout carries only the JSON result)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+
 def thresholds():
     with open(GOLDEN) as fh:
         return json.load(fh)["configs"]
@@ -433,8 +438,10 @@ def main():
                           "workspace_bytes": ws}), flush=True)
         return
 
+    progress("16x640x640 workload")
     spec, frames, ms_step, stages, bytes_, ws = bench_config(4, args.steps, args.warmup)
     latency = bench_config.latency
+    progress(f"16x640x640: {ms_step / len(frames):.5f} ms per frame")
     copy_gbs = copy_bandwidth()
     nfr = len(frames)
     fps = nfr * 1000.0 / ms_step
@@ -478,6 +485,7 @@ def main():
             resolved = json.load(fh)["resolved"]
         extra = {}
         for cfg in (2, 3):
+            progress(f"secondary workload {cfg}")
             loaded = load_workload(cfg)
             s, fr, ms, st, b, _ = bench_config(cfg, max(1, args.steps // 2), max(1, args.warmup // 2),
                                                loaded=loaded, quality=True, min_warm_ms=150.0)
@@ -503,9 +511,11 @@ def main():
             del fr, loaded
         # Table 3's naive-vs-optimised contrast on this GPU: the paper's own
         # shape (704x704, L = 4) and a 640x640 D = 64 frame
+        progress("naive ablation")
         extra["naive_ablation"] = [naive_ablation(5), naive_ablation(2)]
         result["extra"] = extra
     if not args.no_cpu:
+        progress("CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(4, frames)
     print(json.dumps(result), flush=True)
 
