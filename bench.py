@@ -366,7 +366,8 @@ def sweep(steps, warmup):
     loaded = load_workload(5)
     for b in synth.SWEEP_BINS:
         th = sw[str(b)]
-        s, fr, ms, st, by, ws = bench_config(5, steps, warmup, bins=b, th=th, loaded=loaded)
+        progress(f"sweep: {b}x{b} bins")
+        s, fr, ms, st, by, ws = bench_config(5, steps, warmup, bins=b, th=th, loaded=loaded, min_warm_ms=150.0)
         out["bins_sweep"].append({"workload": s.name, "bins": b, "ms_per_frame": round(ms, 5),
                                   "frames_per_s": round(1000.0 / ms, 1), "workspace_bytes": ws,
                                   "path": "matrix-core" if b <= 32 else "matrix-core vote, generic assignment",
@@ -374,7 +375,8 @@ def sweep(steps, warmup):
                                   "paper_ms_orin_nano_fp32": PAPER_TABLE1_MS[b]})
     del loaded
     for cfg in sorted(synth.CONFIGS):
-        s, fr, ms, st, by, ws = bench_config(cfg, steps, warmup)
+        progress(f"resolution series: workload {cfg}")
+        s, fr, ms, st, by, ws = bench_config(cfg, steps, warmup, min_warm_ms=150.0)
         nfr = len(fr)
         out["resolution"].append({"workload": s.name, "pixels": s.H * s.W, "D": s.D, "dtype": s.dtype,
                                   "ms_per_frame": round(ms / nfr, 5), "frames_per_s": round(nfr * 1000.0 / ms, 1),
