@@ -747,7 +747,6 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
         const unsigned char *kxq = reinterpret_cast<const unsigned char *>(kx + 4 * q);
         const unsigned char *kyq = reinterpret_cast<const unsigned char *>(ky + 4 * q);
         double b4[4] = {__builtin_inf(), __builtin_inf(), __builtin_inf(), __builtin_inf()};
-#pragma unroll 2
         for (int bi = j0; bi < nbat; bi += 8) {     // nbat is a multiple of 8: the same count for every lane
             const u32x4 o = s_bo[bi];
             const uint32_t hb = s_bh[bi];
