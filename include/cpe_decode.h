@@ -50,9 +50,10 @@
  * enqueued and return CPE_ERR_INVALID_ARG.  A decode clears the calling
  * thread's last HIP error, then checks it after each of its launches: a
  * failed launch returns CPE_ERR_HIP at once (the frame's outputs are then
- * undefined).  No state carries over between frames -- every frame starts by
- * clearing its vote histograms -- so the next decode on the same handle is
- * unaffected by a failed one.  Data-dependent outcomes (no centroid, more
+ * undefined).  No state carries over between frames -- a frame accumulates
+ * its votes into one of two histogram sets, left clear by the frame before
+ * it, and its first launch clears the other set for the next frame -- so the
+ * next decode on the same handle is unaffected by a failed one.  Data-dependent outcomes (no centroid, more
  * centroids than the capacity) are reported through the device outputs,
  * never as errors.
  *
@@ -182,7 +183,7 @@ cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, co
  * forbid hipMalloc): the same frame, arguments, outputs and errors as
  * cpe_decode_ex, and the handle's constants, but the per-frame scratch (vote
  * histograms, participating-pixel list, slice counts, peak list) is a static
- * device array of the library, about 9.1 MB, held by each device the
+ * device array of the library, about 10.7 MB, held by each device the
  * library runs on until the process ends, instead of the handle's.  The
  * call itself allocates nothing.
  *   Limit: frames of at most 2,097,152 pixels (H*W <= 2^21, e.g. 1024 x
@@ -192,7 +193,8 @@ cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, co
  *   Every call on a device shares that device's array: calls that overlap in
  *   time on one device (other streams, other threads, other handles) race
  *   and give undefined results; calls ordered on one stream are safe, since
- *   each frame clears what it accumulates into.
+ *   each frame finds the histograms it accumulates into clear and clears
+ *   those of the next call, whatever its handle.
  *   cpe_decode_get_histogram does not see these frames (it returns the
  *   handle's latest cpe_decode / cpe_decode_ex frame).
  */
@@ -256,7 +258,8 @@ cpe_status cpe_check_sqrt(hipStream_t stream, unsigned long long *mismatches);
  * Testing: make the next decode on this handle stop before its launch
  * `launch` (0, 1 or 2, numbered as for cpe_decode_set_stage_events; -1
  * cancels) and return CPE_ERR_HIP as if that launch had failed; the earlier
- * launches of that frame are enqueued.  One-shot.
+ * launches of that frame are enqueued (none before launch 1 in a two-launch
+ * frame).  One-shot.
  */
 cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch);
 
@@ -269,11 +272,14 @@ size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
  * events[2i] when the kernel starts and events[2i+1] when it ends, on the
  * decode's stream; hipEventElapsedTime(events[2i], events[2i+1]) is then that
  * kernel's duration: 0 = compaction of the participating pixels and
- * clearing of the vote histograms (only the clearing without a foreground
- * channel), 1 = recovery + voting, 2 = peak extraction + assignment (one
- * kernel for grids up to 32 x 32 bins; above, events 4 and 5 bracket the
- * peak kernel and the assignment kernel that follows it).  `n_events` must
- * be CPE_STAGE_EVENTS;
+ * clearing of the next frame's vote histograms (only the clearing without a
+ * foreground channel), 1 = recovery + voting, 2 = peak extraction +
+ * assignment (one kernel for grids up to 32 x 32 bins; above, events 4 and 5
+ * bracket the peak kernel and the assignment kernel that follows it).
+ * Frames of up to 2^21 pixels on grids up to 32 x 32 bins take two
+ * launches: kernel 1 also compacts and clears, and events 0 and 1 are
+ * recorded back to back, with no kernel between them.  `n_events` must be
+ * CPE_STAGE_EVENTS;
  * the caller owns the events and must keep them alive while set.  NULL
  * switches the recording off.
  */

@@ -20,6 +20,11 @@ constexpr int kCountCap = 1024;       // centroids whose pixel counts are privat
 constexpr int kMfmaBins = 32;         // bin grids up to 32 x 32 take the matrix-core path
 constexpr int kPopKinds = 3;          // int8 palette operand kinds per axis (AxisOp in k_mfma.hpp)
 constexpr int kMaxBinBlocks = (kMaxBins + kMfmaBins - 1) / kMfmaBins;   // blocks of 32 bins per axis
+constexpr int kMaxSlices = 256;       // workgroups of the compaction (slices of the pixel list)
+constexpr int64_t kFusedMaxPixels = 1LL << 21;   // frames the vote launch compacts itself (two launches)
+constexpr int kFusedMaxSeg = 8192;               // listed pixels per workgroup of that launch (LDS)
+constexpr int kFusedSteps = kFusedMaxSeg / 64;   // its 64-pixel steps per workgroup
+static_assert(kFusedSteps <= 128, "two steps per lane in the folded compaction's prefix sum");
 
 typedef short v2s __attribute__((ext_vector_type(2)));
 

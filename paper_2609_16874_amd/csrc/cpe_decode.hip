@@ -44,6 +44,14 @@ long long peak_cut(double theta)
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// List entries a frame of npix pixels may need: the compaction launch's
+// slices (npix and at most one slice more), or the folded compaction's
+// segments (npix and at most one 1024-pixel slice per workgroup more).
+constexpr int64_t list_entries(int64_t npix)
+{
+    return npix + slice_pixels(npix) + (int64_t)kMaxSlices * 1024;
+}
+
 // Eq8 on distance sums D in units of 1/4096: D / 4096 < tau  <=>  D < 4096 tau
 // (exact scaling; +inf keeps every pixel, tau <= 0 none).
 double tau4096(double tau) { return tau * 4096.0; }
@@ -95,23 +103,28 @@ uint16_t f16_bits(int v)   // exact for the small integers used here (|v| <= 204
 // ---------------------------------------------------------------------------
 constexpr int64_t kStaticMaxPixels = 1LL << 21;     // 2,097,152 pixels, e.g. 1024 x 2048
 constexpr int kStaticMaxBins = kMaxBins * kMaxBins;
-constexpr size_t kStaticHrep = 0;                                               // [kReplicas][bins]
-constexpr size_t kStaticHlast = kStaticHrep + (size_t)kReplicas * kStaticMaxBins * 8;
+constexpr size_t kStaticSet = (size_t)kReplicas * kStaticMaxBins;                // words per histogram set
+constexpr size_t kStaticHrep = 0;                                               // [2][kReplicas][bins]
+constexpr size_t kStaticHlast = kStaticHrep + 2 * kStaticSet * 8;
 constexpr size_t kStaticPeaks = kStaticHlast + (size_t)kStaticMaxBins * 8;
 constexpr size_t kStaticKinfo = kStaticPeaks + (size_t)kStaticMaxBins * 4;
 constexpr size_t kStaticCounts = kStaticKinfo + 256;
 constexpr size_t kStaticList = kStaticCounts + (size_t)kMaxSlices * 4;
-constexpr size_t kStaticBytes = kStaticList + ((size_t)kStaticMaxPixels + kCompactSpan) * 4;
+constexpr size_t kStaticBytes = kStaticList + (size_t)list_entries(kStaticMaxPixels) * 4;
 static_assert(kStaticMaxPixels <= (int64_t)kMaxSlices * kCompactSpan, "one compaction step per slice: one slice "
               "of kCompactSpan pixels bounds the list's tail");
+static_assert(kStaticMaxPixels <= kFusedMaxPixels, "the folded compaction serves every frame of the static scratch");
 
 __device__ __align__(256) unsigned char scratch[kStaticBytes];
 
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mutex;
 unsigned char *g_scratch[kMaxDevices];     // device address of `scratch` per device (null: not looked up)
+int g_parity[kMaxDevices];                 // histogram set of the next frame in `scratch`, per device
+size_t g_dirty[kMaxDevices][2];            // words of each set that may be nonzero, per device
 
-// Look up the device address of `scratch` on the current device `dev`, once.
+// Look up the device address of `scratch` on the current device `dev` and
+// clear its histogram sets, once.
 bool init_static_scratch(int dev)
 {
     if (dev < 0 || dev >= kMaxDevices) return false;
@@ -119,7 +132,12 @@ bool init_static_scratch(int dev)
     if (g_scratch[dev]) return true;
     void *ptr = nullptr;
     if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return false;
-    g_scratch[dev] = static_cast<unsigned char *>(ptr);
+    unsigned char *base = static_cast<unsigned char *>(ptr);
+    if (hipMemset(base + kStaticHrep, 0, 2 * kStaticSet * 8) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+        return false;
+    g_parity[dev] = 0;
+    g_dirty[dev][0] = g_dirty[dev][1] = 0;
+    g_scratch[dev] = base;
     return true;
 }
 
@@ -130,10 +148,15 @@ unsigned char *static_scratch(int dev)
     return g_scratch[dev];
 }
 
-Scratch static_layout(unsigned char *base)
+// Its sets have the largest grid's stride, so that handles of any grid
+// sharing the array find the set they start on clear.
+Scratch static_layout(unsigned char *base, int dev)
 {
     Scratch sc;
     sc.hrep = reinterpret_cast<unsigned long long *>(base + kStaticHrep);
+    sc.set_stride = kStaticSet;
+    sc.parity = &g_parity[dev];
+    sc.dirty = g_dirty[dev];
     sc.hlast = reinterpret_cast<unsigned long long *>(base + kStaticHlast);
     sc.peaks = reinterpret_cast<int32_t *>(base + kStaticPeaks);
     sc.kinfo = reinterpret_cast<int32_t *>(base + kStaticKinfo);
@@ -318,12 +341,12 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_npx = carve(np1x.size() * 4), o_npy = carve(np1y.size() * 4);
     const size_t o_pop = carve(pop.size());
     const size_t o_wpk = carve(wt_pk.size() * 4);
-    const size_t o_hrep = carve((size_t)kReplicas * nb * 8);
+    const size_t o_hrep = carve(2 * (size_t)kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
     const size_t o_kinfo = carve(16);
     const size_t o_count = carve((size_t)kMaxSlices * 4);
-    const size_t o_list = carve(((size_t)H * W + (size_t)slice_pixels((int64_t)H * W)) * 4);
+    const size_t o_list = carve((size_t)list_entries((int64_t)H * W) * 4);
     h->dev_bytes = off;
     if (hipMalloc(&h->dev, off) != hipSuccess) {
         delete h;
@@ -340,7 +363,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               up(o_npx, np1x.data(), np1x.size() * 4) && up(o_npy, np1y.data(), np1y.size() * 4) &&
               up(o_pop, pop.data(), pop.size()) &&
               up(o_wpk, wt_pk.data(), wt_pk.size() * 4) &&
-              hipMemset(d + o_hrep, 0, (size_t)kReplicas * nb * 8) == hipSuccess &&
+              hipMemset(d + o_hrep, 0, 2 * (size_t)kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
               hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, (size_t)kMaxSlices * 4) == hipSuccess &&
               hipDeviceSynchronize() == hipSuccess;
@@ -361,6 +384,11 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->tb.pop = reinterpret_cast<const uint32_t *>(d + o_pop);
     h->tb.wt_pk = reinterpret_cast<const uint32_t *>(d + o_wpk);
     h->sc.hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
+    h->sc.set_stride = (size_t)kReplicas * nb;
+    h->parity = 0;
+    h->sc.parity = &h->parity;
+    h->dirty[0] = h->dirty[1] = 0;
+    h->sc.dirty = h->dirty;
     h->sc.hlast = reinterpret_cast<unsigned long long *>(d + o_hlast);
     h->sc.peaks = reinterpret_cast<int32_t *>(d + o_peaks);
     h->sc.kinfo = reinterpret_cast<int32_t *>(d + o_kinfo);
@@ -399,7 +427,7 @@ cpe_status cpe_decode_noalloc(cpe_decoder *h, hipStream_t stream, const void *em
     if ((int64_t)h->H * h->W > kStaticMaxPixels) return CPE_ERR_UNSUPPORTED;
     unsigned char *base = static_scratch(h->device);
     if (!base) return CPE_ERR_HIP;
-    const Scratch sc = static_layout(base);
+    const Scratch sc = static_layout(base, h->device);
     const float fg_thr = fg ? opt->fg_threshold : 0.0f;
     return decode_frame(h, &sc, stream, emb, fg, H, W, fg_thr, opt->peak_threshold, opt->tau, centroids,
                         num_centroids, labels, score_map);

@@ -13,16 +13,46 @@ namespace cpe {
 
 // Per-frame scratch of the launch sequence: everything a decode writes and
 // reads besides the caller's inputs and outputs and the handle's constants.
-// Nothing in it carries over from one frame to the next: the first launch of
-// every frame clears the vote histograms.
+// The vote histograms come in two sets of set_stride words each.  A frame
+// accumulates into set *parity, which is clear when the frame starts, and
+// its first launch that runs clears the first dirty[1 - *parity] words of
+// the other set (the ones an earlier frame may have written); *parity flips
+// once that launch is enqueued.  So every frame starts on a clear set, also
+// after a decode that failed part-way.
 struct Scratch {
-    unsigned long long *hrep;    // [kReplicas][nb] vote histograms
+    unsigned long long *hrep;    // [2][set_stride]: per set [kReplicas][nb] vote histograms
+    size_t set_stride;           // words per set (>= kReplicas * nb)
+    int *parity;                 // host: the set of the next frame (0 or 1)
+    size_t *dirty;               // host: [2] leading words of each set that may be nonzero
     unsigned long long *hlast;   // [nb] summed histogram of the frame
     int32_t *peaks;              // [cap] a | b << 16 (generic path)
     int32_t *kinfo;              // [0] = min(K, cap), [1] = K (generic path)
     int32_t *counts;             // [kMaxSlices] entries per slice of the participating-pixel list
-    int32_t *list;               // participating pixels, in slices: H*W + one slice
+    int32_t *list;               // participating pixels, in slices (list_entries() in cpe_decode.hip)
 };
+
+// The folded compaction's plan for a frame of npix pixels (FusedArgs in
+// k_mfma.hpp): slices of `slice` pixels dealt to `grid` workgroups, each
+// listing at most seg_cap pixels; ok = false when the frame is too large.
+struct FusedPlan {
+    bool ok;
+    int slice, grid, seg_cap;
+};
+inline FusedPlan fused_plan(int64_t npix)
+{
+    FusedPlan fp{false, 64, 1, 64};
+    if (npix < 1 || npix > kFusedMaxPixels) return fp;
+    // 64-pixel slices (one wave step); 1024 when a workgroup owns 4096
+    // pixels or more (at 1024 x 2048: eight slices each, whose foreground
+    // counts vary less between workgroups than 128 slices of 64 pixels)
+    const int64_t per_wg = (npix + kMaxSlices - 1) / kMaxSlices;
+    const int slice = per_wg >= 4096 ? 1024 : 64;
+    const int64_t nsl = (npix + slice - 1) / slice;
+    const int64_t grid = nsl < kMaxSlices ? nsl : kMaxSlices;
+    const int64_t seg = (nsl + grid - 1) / grid * slice;
+    if (seg > kFusedMaxSeg) return fp;
+    return FusedPlan{true, slice, (int)grid, (int)seg};
+}
 
 }  // namespace cpe
 
@@ -36,6 +66,8 @@ struct cpe_decoder {
     size_t dev_bytes;
     cpe::Tables tb;
     cpe::Scratch sc;                     // per-frame scratch, in the device allocation
+    int parity;                          // histogram set of the next frame (sc.parity points here)
+    size_t dirty[2];                     // words of each set that may be nonzero (sc.dirty points here)
     int fail_at;                         // test hook: the next decode stops before this launch (-1: none)
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;

@@ -22,19 +22,18 @@ namespace cpe {
 constexpr int kCompactThreads = 1024;
 constexpr int kCompactPer = 8;                                   // pixels per lane
 constexpr int kCompactSpan = kCompactThreads * kCompactPer;      // pixels per workgroup and step
-constexpr int kMaxSlices = 256;                                  // workgroups of the compaction
 // Largest frame: every slice end (at most one slice, 2^23 pixels, past the
 // frame) and every tile offset then stays below 2^31, so pixel and list
 // positions are int32 throughout.
 constexpr int64_t kMaxPixels = (1LL << 31) - (1LL << 23);
 
 // Pixels per slice for a frame of npix pixels, and the number of slices.
-__host__ __device__ inline int slice_pixels(int64_t npix)
+__host__ __device__ constexpr int slice_pixels(int64_t npix)
 {
     const int64_t steps = (npix + (int64_t)kMaxSlices * kCompactSpan - 1) / ((int64_t)kMaxSlices * kCompactSpan);
     return (int)(steps * kCompactSpan);
 }
-__host__ __device__ inline int slice_count(int64_t npix)
+__host__ __device__ constexpr int slice_count(int64_t npix)
 {
     const int64_t r = slice_pixels(npix);
     return (int)((npix + r - 1) / r);

@@ -320,12 +320,61 @@ __device__ __forceinline__ int take_tile(int *next, int lane, int first, int wav
 constexpr int kHStride = kMfmaBins + 1;
 
 // LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
-// the palette operands, and per wave |X|^2 of one tile's pixels per axis.
-constexpr size_t kVoteLds(int wpb)
+// the palette operands, per wave |X|^2 of one tile's pixels per axis, the
+// slice prefix sums and counters; with the compaction folded in (FUSED),
+// the workgroup's own participating pixels.
+constexpr size_t kVoteLds(int wpb, bool fused)
 {
     return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
-           16;
+           16 + (fused ? (size_t)kFusedMaxSeg * 4 : 0);
 }
+
+// Eight foreground values from pixel p0 on (p0 a multiple of 8): one (fp16)
+// or two (fp32) 16-byte loads when the plane is 16-byte aligned and the
+// eight lie below lim, else one load per pixel below lim (0 beyond).
+template <typename T>
+__device__ __forceinline__ void load8(const T *fg, int p0, int lim, bool vec, float v[8])
+{
+    if (vec && p0 + 8 <= lim) {
+        if constexpr (sizeof(T) == 2) {
+            const uint4 w = *reinterpret_cast<const uint4 *>(fg + p0);
+            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                v[2 * i] = half_bits_to_float(ww[i] & 0xffffu);
+                v[2 * i + 1] = half_bits_to_float(ww[i] >> 16);
+            }
+        } else {
+            const float4 a = *reinterpret_cast<const float4 *>(fg + p0);
+            const float4 b = *reinterpret_cast<const float4 *>(fg + p0 + 4);
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; i++) v[i] = fg && p0 + i < lim ? load_scalar<T>(fg + p0 + i) : 0.0f;
+    }
+}
+
+// The compaction folded into the vote launch (frames of up to kFusedMaxPixels
+// pixels, grids up to 32 x 32): the frame is cut into slices of `slice`
+// pixels (a multiple of 64), dealt to the workgroups in turn (slice s to
+// workgroup s mod G); each workgroup lists its participating pixels in LDS,
+// in any order, votes on them, and writes them to its segment of the list
+// (list[b * seg_cap ..], seg_cap >= its slices' pixels) and their number to
+// counts[b], which the assignment launch reads as its slices.  The other
+// pixels get their final outputs here.  The launch also clears `hnext`, the
+// histograms of the next frame.
+struct FusedArgs {
+    const void *fg;              // foreground plane (element type of the embedding), or null: every pixel
+    float fg_thr;
+    int32_t slice, seg_cap;
+    int32_t *list, *counts;
+    int32_t *labels;
+    float *score;
+    unsigned long long *hnext;
+    int32_t nnext;
+};
 
 // Waves per SIMD the register allocation must allow: three for fp16 inputs
 // with up to 8 or exactly 16 harmonics (one workgroup of 12 waves per compute
@@ -346,29 +395,32 @@ constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 // MULTI: grids above 32 x 32 bins (one pass per block of 32 x 32 bins);
 // otherwise the single block is compiled without the pass loop, whose
 // registers would otherwise spill.
-template <typename T, int F, bool MULTI>
+template <typename T, int F, bool MULTI, bool FUSED>
 __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
     const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, Tables tb, int32_t Bw,
     int32_t Bh, unsigned long long *__restrict__ hrep,
-    cpe_centroid *__restrict__ cents, int32_t cap)
+    cpe_centroid *__restrict__ cents, int32_t cap, FusedArgs fz)
 {
+    static_assert(!(MULTI && FUSED), "the folded compaction serves single-block grids");
     constexpr int kWpb = kVoteWpb<T, F>;
     // blocks of 32 x 32 bins: one pass over the workgroup's tiles per block
     const int nbx = MULTI ? (Bw + kMfmaBins - 1) / kMfmaBins : 1, nby = MULTI ? (Bh + kMfmaBins - 1) / kMfmaBins : 1;
     // All LDS is static, so that table addresses are compile-time constants.
-    __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb)];
+    __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb, FUSED)];
     uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32][kHStride], b * kHStride + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kHStride);      // palette operands
     uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][2][32]
     int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 64);                        // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
+    int *s_cnt = s_next + 1;                                                          // FUSED: pixels listed
+    int *s_list = s_pref + kMaxSlices + 5;                                            // FUSED: [kFusedMaxSeg]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
     SliceLoad sl;
-    if (list) slice_load(counts, nslices, sl);
+    if (!FUSED && list) slice_load(counts, nslices, sl);
     // the bin constants of this lane's bin in the first block (loaded with
     // the tables, not after the barrier, where they would cost a memory round
     // trip of their own)
@@ -381,6 +433,120 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             const int i = k * kThreads + tid;
             w[k] = reinterpret_cast<const u32x4 *>(tb.wt_pk)[i < kN ? i : 0];
         }
+        if constexpr (FUSED) {
+            // While the table loads are in flight: this workgroup's slices
+            // b, b + G, ... in steps of 64 lanes x V consecutive pixels
+            // (V = 8 when the slices hold whole steps of 512 pixels, else 1),
+            // the loads of U steps in flight together; an LDS counter hands
+            // out the listed pixels' positions, U steps at a time.
+            if (tid == 0) *s_cnt = 0;
+            __syncthreads();
+            const int G = gridDim.x, b = blockIdx.x;
+            const int nsl = (npix + fz.slice - 1) / fz.slice;
+            const int mine = b < nsl ? (nsl - 1 - b) / G + 1 : 0;
+            const T *fgp = static_cast<const T *>(fz.fg);
+            int32_t *seg = fz.list + (size_t)b * fz.seg_cap;
+            auto take = [&](int tot) {
+                int base = 0;
+                if (lane == 0 && tot) base = atomicAdd(s_cnt, tot);
+                return __builtin_amdgcn_readfirstlane(base);
+            };
+            if (fz.slice % 512 == 0) {
+                const int per = fz.slice >> 9, steps = mine * per;
+                const bool vec = fgp && ((uintptr_t)fgp & 15u) == 0;
+                constexpr int U = 2;
+                for (int j0 = wv; j0 < steps; j0 += U * kWpb) {
+                    float v[U][8];
+                    int p0[U];
+                    uint32_t m[U], valid[U];
+                    int c[U], incl[U], tot = 0;
+#pragma unroll
+                    for (int u = 0; u < U; u++) {
+                        const int j = j0 + u * kWpb;
+                        p0[u] = (b + G * (j / per)) * fz.slice + (j % per) * 512 + lane * 8;
+                        load8<T>(fgp, p0[u], j < steps ? npix : 0, vec, v[u]);
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; u++) {
+                        const bool live = j0 + u * kWpb < steps;      // uniform
+                        m[u] = valid[u] = 0;
+#pragma unroll
+                        for (int i = 0; i < 8; i++) {
+                            const bool in = live && p0[u] + i < npix;
+                            valid[u] |= (in ? 1u : 0u) << i;
+                            m[u] |= (in && (!fgp || v[u][i] > fz.fg_thr) ? 1u : 0u) << i;   // a NaN never exceeds it
+                        }
+                        c[u] = __popc(m[u]);
+                        incl[u] = wave_incl_sum(c[u]);
+                        tot += __builtin_amdgcn_readlane(incl[u], 63);
+                    }
+                    int base = take(tot);
+#pragma unroll
+                    for (int u = 0; u < U; u++) {
+                        int off = base + incl[u] - c[u];                // < the slices' pixels <= seg_cap
+#pragma unroll
+                        for (int i = 0; i < 8; i++)
+                            if ((m[u] >> i) & 1u) {
+                                s_list[off] = p0[u] + i;
+                                seg[off] = p0[u] + i;
+                                off++;
+                            }
+                        base += __builtin_amdgcn_readlane(incl[u], 63);
+                        const uint32_t bg = valid[u] & ~m[u];
+                        if (bg == 0xffu) {
+                            const int4 z = {0, 0, 0, 0};
+                            reinterpret_cast<int4 *>(fz.labels + p0[u])[0] = z;     // labels: 16-byte aligned
+                            reinterpret_cast<int4 *>(fz.labels + p0[u])[1] = z;
+                        } else if (bg) {
+#pragma unroll
+                            for (int i = 0; i < 8; i++)
+                                if ((bg >> i) & 1u) fz.labels[p0[u] + i] = 0;
+                        }
+                        if (fz.score && bg) {
+#pragma unroll
+                            for (int i = 0; i < 8; i++)
+                                if ((bg >> i) & 1u) fz.score[p0[u] + i] = 0.0f;
+                        }
+                    }
+                }
+            } else {
+                const int per = fz.slice >> 6, steps = mine * per;
+                constexpr int U = 4;
+                for (int j0 = wv; j0 < steps; j0 += U * kWpb) {
+                    float v[U];
+                    int p[U];
+                    unsigned long long m[U];
+                    int tot = 0;
+#pragma unroll
+                    for (int u = 0; u < U; u++) {
+                        const int j = j0 + u * kWpb;
+                        p[u] = (b + G * (j / per)) * fz.slice + (j % per) * 64 + lane;
+                        v[u] = fgp && j < steps && p[u] < npix ? load_scalar<T>(fgp + p[u]) : 0.0f;
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; u++) {
+                        const bool in = j0 + u * kWpb < steps && p[u] < npix;
+                        m[u] = __ballot(in && (!fgp || v[u] > fz.fg_thr));   // a NaN never exceeds it
+                        tot += (int)__popcll(m[u]);
+                        if (in && !((m[u] >> lane) & 1ull)) {
+                            fz.labels[p[u]] = 0;
+                            if (fz.score) fz.score[p[u]] = 0.0f;
+                        }
+                    }
+                    int base = take(tot);
+#pragma unroll
+                    for (int u = 0; u < U; u++) {
+                        if ((m[u] >> lane) & 1ull) {
+                            const int pos = base + lane_prefix(m[u]);     // < the slices' pixels <= seg_cap
+                            s_list[pos] = p[u];
+                            seg[pos] = p[u];
+                        }
+                        base += (int)__popcll(m[u]);
+                    }
+                }
+            }
+            for (int i = b * kThreads + tid; i < fz.nnext; i += G * kThreads) fz.hnext[i] = 0ull;
+        }
 #pragma unroll
         for (int k = 0; k < kPer; k++) {
             const int i = k * kThreads + tid;
@@ -389,13 +555,19 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         for (int i = tid; i < kMfmaBins * kHStride; i += kThreads) s_h[i] = 0ull;
         for (int i = tid; i < kPopBytes / 16; i += kThreads) reinterpret_cast<u32x4 *>(s_pop)[i] = pop_block(tb.pop, i, 0, 0);
         if (tid == 0) *s_next = 0;
-        if (list) slice_scan(sl, nslices, s_pref);
+        if (!FUSED && list) slice_scan(sl, nslices, s_pref);
     }
     __syncthreads();
-    // the workgroup's run of tiles
-    const int n = list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
+    // the workgroup's run of tiles: a share of the list, or (FUSED) its own pixels
+    const int n = FUSED ? *s_cnt : list ? s_pref[nslices] : npix, ntiles = (n + 31) >> 5;
     int t0, tend;
-    block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
+    if constexpr (FUSED) {
+        t0 = 0;
+        tend = ntiles;
+        if (tid == 0) fz.counts[blockIdx.x] = n;
+    } else {
+        block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
+    }
 
     // this wave's |X|^2 per axis: [0] x, [1] y, by pixel
     uint32_t *ini = s_ini + wv * 64;
@@ -506,9 +678,15 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
         int t = t0 + wv;
         ListCursor cur_list;
-        cur_list.start(list, s_pref, nslices, slice_px, t < tend ? 32 * t : 0);
+        if (!FUSED) cur_list.start(list, s_pref, nslices, slice_px, t < tend ? 32 * t : 0);
         // lane m of tile tt: entry 32 tt + m, or the tile's first entry past the end
-        auto pixel = [&](int tt) { return cur_list.pixel(32 * tt + ln < n ? 32 * tt + ln : 32 * tt); };
+        auto pixel = [&](int tt) {
+            const int e = 32 * tt + ln < n ? 32 * tt + ln : 32 * tt;
+            if constexpr (FUSED)
+                return s_list[e];
+            else
+                return cur_list.pixel(e);
+        };
         // the next tile's rows are loaded as soon as the current ones are converted
         RawSlices<T, F> raw;
         int tn = tend, idx = 0;                            // next tile, and this lane's pixel in it

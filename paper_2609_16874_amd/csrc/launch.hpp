@@ -60,33 +60,75 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
         return hipGetLastError() == hipSuccess;
     };
     const bool mfma = Bw <= kMfmaBins && Bh <= kMfmaBins;     // the matrix-core assignment (and its peak prologue)
-    const int nclear = kReplicas * nb;
-    const int clear_grid = (nclear + 255) / 256 < 64 ? (nclear + 255) / 256 : 64;
-
-    // launch 0: the participating pixels as a compact list (every pixel when
-    // the frame has no foreground channel) and the vote histograms cleared
-    int32_t *list = g ? sc.list : nullptr;
-    const int nslices = slice_count(npix), slice_px = slice_pixels(npix);
-    bool ok;
-    if (!g)
-        ok = launch(0, k_clear_u64, dim3(clear_grid), dim3(256), 0, sc.hrep, nclear);
-    else if (((uintptr_t)g & 15u) == 0)
-        ok = launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, sc.counts,
-                    labels, score, sc.hrep, nclear);
-    else
-        ok = launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list, sc.counts,
-                    labels, score, sc.hrep, nclear);
-    if (!ok) return CPE_ERR_HIP;
-    // launch 1: recovery + voting, one pass per block of 32 x 32 bins; grid:
-    // at most one workgroup per compute unit, no more waves than tiles
+    // the frame's histogram set (clear) and the next frame's, whose first
+    // nclear words an earlier frame may have written
+    const int par = *sc.parity & 1;
+    unsigned long long *hcur = sc.hrep + (size_t)par * sc.set_stride;
+    unsigned long long *hnext = sc.hrep + (size_t)(1 - par) * sc.set_stride;
+    const size_t nclear = sc.dirty[1 - par];
+    const size_t nused = (size_t)kReplicas * nb;
+    // once the clearing launch is enqueued: the other set is the next frame's
+    auto flip = [&]() {
+        sc.dirty[1 - par] = 0;
+        *sc.parity = 1 - par;
+    };
     constexpr int wpb = kVoteWpb<T, F>;
     const int64_t tiles = ((int64_t)npix + 31) / 32;
-    const int64_t wgs = (tiles + wpb - 1) / wpb;
-    const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
-    auto vote_kernel = mfma ? k_vote_mfma<T, F, false> : k_vote_mfma<T, F, true>;
-    if (!launch(1, vote_kernel, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
-                (const int32_t *)sc.counts, nslices, slice_px, npix, h->tb, Bw, Bh, sc.hrep, cents, h->cap))
-        return CPE_ERR_HIP;
+    int32_t *list = sc.list;
+    int nslices, slice_px;
+    const FusedPlan fp = fused_plan(npix);
+    if (mfma && fp.ok) {
+        // Two launches.  Launch 0 would be the compaction, which the vote
+        // launch does itself here: its events record back to back.
+        if (fail_at == 0) return CPE_ERR_HIP;
+        if (h->stage_on) {
+            if (hipEventRecord(h->stage_ev[0], stream) != hipSuccess ||
+                hipEventRecord(h->stage_ev[1], stream) != hipSuccess)
+                return CPE_ERR_HIP;
+        }
+        // launch 1: compaction of each workgroup's slices, recovery +
+        // voting on them, the next frame's histograms cleared
+        const FusedArgs fz{fg, fg_thr, fp.slice, fp.seg_cap, list, sc.counts, labels, score,
+                           hnext, (int32_t)nclear};
+        if (sc.dirty[par] < nused) sc.dirty[par] = nused;
+        if (!launch(1, k_vote_mfma<T, F, false, true>, dim3(fp.grid), dim3(wpb * 64), 0, e, dstride, yoff,
+                    (const int32_t *)nullptr, (const int32_t *)nullptr, 0, 0, npix, h->tb, Bw, Bh, hcur, cents,
+                    h->cap, fz))
+            return CPE_ERR_HIP;
+        flip();
+        nslices = fp.grid;             // the assignment reads the workgroups' segments as its slices
+        slice_px = fp.seg_cap;
+    } else {
+        // launch 0: the participating pixels as a compact list (every pixel
+        // when the frame has no foreground channel), the next frame's
+        // histograms cleared
+        const int64_t cg = ((int64_t)nclear + 255) / 256;
+        const int clear_grid = cg < 1 ? 1 : cg > 64 ? 64 : (int)cg;
+        nslices = slice_count(npix);
+        slice_px = slice_pixels(npix);
+        if (!g) list = nullptr;
+        bool ok;
+        if (!g)
+            ok = launch(0, k_clear_u64, dim3(clear_grid), dim3(256), 0, hnext, (int32_t)nclear);
+        else if (((uintptr_t)g & 15u) == 0)
+            ok = launch(0, k_compact<T, true>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list,
+                        sc.counts, labels, score, hnext, (int32_t)nclear);
+        else
+            ok = launch(0, k_compact<T, false>, dim3(nslices), dim3(kCompactThreads), 0, g, npix, fg_thr, list,
+                        sc.counts, labels, score, hnext, (int32_t)nclear);
+        if (!ok) return CPE_ERR_HIP;
+        flip();
+        // launch 1: recovery + voting, one pass per block of 32 x 32 bins;
+        // grid: at most one workgroup per compute unit, no more waves than tiles
+        const int64_t wgs = (tiles + wpb - 1) / wpb;
+        const int grid = (int)(wgs < kVoteGrid ? wgs : kVoteGrid);
+        auto vote_kernel = mfma ? k_vote_mfma<T, F, false, false> : k_vote_mfma<T, F, true, false>;
+        if (sc.dirty[par] < nused) sc.dirty[par] = nused;
+        if (!launch(1, vote_kernel, dim3(grid), dim3(wpb * 64), 0, e, dstride, yoff, (const int32_t *)list,
+                    (const int32_t *)sc.counts, nslices, slice_px, npix, h->tb, Bw, Bh, hcur, cents, h->cap,
+                    FusedArgs{}))
+            return CPE_ERR_HIP;
+    }
     if (mfma) {
         // launch 2: peak extraction in every workgroup's prologue, assignment
         constexpr int wpb2 = kAssignWpb<T, F>;
@@ -94,7 +136,7 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
         if (!launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(wpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
                     (const int32_t *)sc.counts, nslices, slice_px, npix, fa.tau4096, h->tb,
-                    (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score))
+                    (const unsigned long long *)hcur, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score))
             return CPE_ERR_HIP;
     } else {
         // launch 2 (larger grids): the stand-alone peak kernel, then the
@@ -105,10 +147,10 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
         const size_t plds = (size_t)nb * 8 + (size_t)max_peaks(Bw, Bh) * 4;
         if (h->stage_on)
             hipExtLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), (uint32_t)plds, stream, h->stage_ev[4], nullptr, 0u,
-                                  (const unsigned long long *)sc.hrep, sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx,
+                                  (const unsigned long long *)hcur, sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx,
                                   h->tb.cy, po);
         else
-            hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), plds, stream, (const unsigned long long *)sc.hrep,
+            hipLaunchKernelGGL(k_peaks, dim3(1), dim3(1024), plds, stream, (const unsigned long long *)hcur,
                                sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
         if (hipGetLastError() != hipSuccess) return CPE_ERR_HIP;
         const size_t fixed2 = generic_assign_fixed(Bw, Bh, F, max_peaks(Bw, Bh));

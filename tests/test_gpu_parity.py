@@ -206,6 +206,48 @@ def test_shapes_and_bins(case):
     assert_parity(got, ref, cap)
 
 
+def _misaligned(t):
+    """A device copy of t whose data starts one element past a 16-byte boundary."""
+    buf = torch.empty(t.numel() + 16, dtype=t.dtype, device="cuda")
+    v = buf[1:1 + t.numel()].view(t.shape)
+    v.copy_(t)
+    assert v.data_ptr() % 16 != 0 and v.data_ptr() % t.element_size() == 0
+    return v
+
+
+# Frames whose vote launch lists the participating pixels itself: 64-pixel
+# slices (640 x 640), 1024-pixel slices read eight pixels per lane (frames
+# above 2^20 pixels), ragged last slices, fp16 and fp32 foreground planes,
+# 16-byte aligned or aligned to their element only.
+FG_CASES = [(640, 640, 4, np.float16, True), (1023, 1027, 4, np.float32, True), (1024, 1024, 4, np.float32, False),
+            (1025, 1029, 3, np.float16, False), (1025, 1029, 3, np.float16, True)]
+
+
+@pytest.mark.parametrize("case", FG_CASES, ids=[f"{c[0]}x{c[1]}_{np.dtype(c[3]).name}_{'shifted' if c[4] else 'aligned'}"
+                                                for c in FG_CASES])
+def test_foreground_plane_layouts(case):
+    H, W, F, dt, shifted = case
+    rng = np.random.default_rng(H * 7 + W)
+    emb, fg, fx, fy = _random_frame(rng, H, W, F, dt)
+    ref0 = oracle.decode(emb, fg, fx, fy, 32, 32, 256, 0.5, 0.0)
+    theta = 0.05 * ref0["hist"].max() * 2.0 ** -30
+    ref = oracle.decode(emb, fg, fx, fy, 32, 32, 256, 0.5, theta)
+    assert ref["K"] > 0
+    dec = native().Decoder(H, W, F, "f32" if dt == np.float32 else "f16", fx, fy, 32, 32, 256)
+    print(f"{H}x{W} {np.dtype(dt).name} foreground {'shifted' if shifted else 'aligned'}", flush=True)
+    e = torch.from_numpy(emb).cuda()
+    g = torch.from_numpy(fg).cuda()
+    if shifted:
+        g = _misaligned(g)
+    got = dec.run(e, g, 0.5, theta, score=True)
+    hist = torch.empty((32, 32), dtype=torch.int64, device="cuda")
+    assert dec.histogram(hist) == 0
+    torch.cuda.synchronize()
+    got["hist"] = hist.cpu().numpy().view(np.uint64)
+    assert_parity(got, ref, 256)
+    dec.close()
+
+
 def test_no_centroid_and_empty_foreground():
     rng = np.random.default_rng(1)
     emb, fg, fx, fy = _random_frame(rng, 48, 40, 4, np.float32)

@@ -1,8 +1,9 @@
 """GPU test of cpe_decode_noalloc (the entry point that allocates nothing):
 its outputs equal those of cpe_decode_ex on the same handle and frame, on two
 calls in a row that share the static scratch, the second with a smaller
-frame (and a no-foreground, Eq8-threshold decode of a third), and frames
-beyond its limit are refused."""
+frame (then a no-foreground, Eq8-threshold decode, and decodes that switch
+between bin grids of 32 x 32 and 48 x 48), and frames beyond its limit are
+refused."""
 import math
 
 import numpy as np
@@ -60,6 +61,13 @@ def test_noalloc_equals_decode_ex_on_two_calls_in_a_row():
                   20, 0.3, math.inf))
     f1 = synth.make_frame(1)
     cases.append((f1.spec, f1.emb, None, 32, 30.0, 5.4))
+    # then the 256x256 workload on a 48 x 48 grid (the generic kernels, more
+    # histogram words than any grid above), and the 640x640 one again: each
+    # call starts on histograms the calls before it left clear
+    theta48 = 2.5 * (48 / 32.0) ** -2
+    cases.append((f1.spec, f1.emb, f1.fg, 48, theta48, math.inf))
+    cases.append((s2, f2.emb, f2.fg, 32, 1.0, math.inf))
+    cases.append((f1.spec, f1.emb, f1.fg, 48, theta48, math.inf))
     for i, (spec, emb_np, fg_np, bins, theta, tau) in enumerate(cases):
         if isinstance(spec, dict):
             dec = nat.Decoder(spec["H"], spec["W"], spec["n_freq"], spec["dtype"], spec["fx"], spec["fy"], bins, bins)
