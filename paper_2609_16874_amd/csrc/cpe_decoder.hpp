@@ -32,8 +32,9 @@ struct Scratch {
 };
 
 // The folded compaction's plan for a frame of npix pixels (FusedArgs in
-// k_mfma.hpp): slices of `slice` pixels dealt to `grid` workgroups, each
-// listing at most seg_cap pixels; ok = false when the frame is too large.
+// k_mfma.hpp): `grid` workgroups, each voting on slices of `slice` pixels
+// dealt to it in turn and listing a range of seg_cap pixels (a multiple of
+// 8) for the assignment; ok = false when the frame is too large.
 struct FusedPlan {
     bool ok;
     int slice, grid, seg_cap;
@@ -49,8 +50,8 @@ inline FusedPlan fused_plan(int64_t npix)
     const int slice = per_wg >= 4096 ? 1024 : 64;
     const int64_t nsl = (npix + slice - 1) / slice;
     const int64_t grid = nsl < kMaxSlices ? nsl : kMaxSlices;
-    const int64_t seg = (nsl + grid - 1) / grid * slice;
-    if (seg > kFusedMaxSeg) return fp;
+    if ((nsl + grid - 1) / grid * slice > kFusedMaxSeg) return fp;     // the vote's list in LDS
+    const int64_t seg = ((npix + grid - 1) / grid + 7) / 8 * 8;
     return FusedPlan{true, slice, (int)grid, (int)seg};
 }
 

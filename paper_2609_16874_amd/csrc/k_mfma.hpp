@@ -357,13 +357,15 @@ __device__ __forceinline__ void load8(const T *fg, int p0, int lim, bool vec, fl
 }
 
 // The compaction folded into the vote launch (frames of up to kFusedMaxPixels
-// pixels, grids up to 32 x 32): the frame is cut into slices of `slice`
-// pixels (a multiple of 64), dealt to the workgroups in turn (slice s to
-// workgroup s mod G); each workgroup lists its participating pixels in LDS,
-// in any order, votes on them, and writes them to its segment of the list
-// (list[b * seg_cap ..], seg_cap >= its slices' pixels) and their number to
-// counts[b], which the assignment launch reads as its slices.  The other
-// pixels get their final outputs here.  The launch also clears `hnext`, the
+// pixels, grids up to 32 x 32).  Workgroup b lists the participating pixels
+// twice: those of its range b * seg_cap .. (b + 1) * seg_cap - 1 of the
+// frame (seg_cap a multiple of 8) into list[b * seg_cap ..], their number
+// into counts[b] -- the assignment launch reads these segments as its slices,
+// in the frame's order -- and those of the slices of `slice` pixels (a
+// multiple of 64) dealt to it in turn (slice s to workgroup s mod G), in
+// LDS, in any order: the pixels it votes on, spread over the frame so that
+// the workgroups' shares of votes stay even.  The pixels outside the list
+// get their final outputs here.  The launch also clears `hnext`, the
 // histograms of the next frame.
 struct FusedArgs {
     const void *fg;              // foreground plane (element type of the embedding), or null: every pixel
@@ -414,7 +416,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][2][32]
     int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 64);                        // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
-    int *s_cnt = s_next + 1;                                                          // FUSED: pixels listed
+    int *s_cnt = s_next + 1;                                                          // FUSED: [2] pixels listed (LDS, global)
     int *s_list = s_pref + kMaxSlices + 5;                                            // FUSED: [kFusedMaxSeg]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -434,64 +436,76 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             w[k] = reinterpret_cast<const u32x4 *>(tb.wt_pk)[i < kN ? i : 0];
         }
         if constexpr (FUSED) {
-            // While the table loads are in flight: this workgroup's slices
-            // b, b + G, ... in steps of 64 lanes x V consecutive pixels
-            // (V = 8 when the slices hold whole steps of 512 pixels, else 1),
-            // the loads of U steps in flight together; an LDS counter hands
-            // out the listed pixels' positions, U steps at a time.
-            if (tid == 0) *s_cnt = 0;
+            // While the table loads are in flight, two lists of the
+            // participating pixels: (a) the assignment's, of this workgroup's
+            // range lo .. hi-1 of the frame, in global memory, with the other
+            // pixels' final outputs; (b) the vote's own, of its slices b,
+            // b + G, ..., in LDS.  Both in steps of 64 lanes x 8 consecutive
+            // pixels (b: slice r of the workgroup, chunk of 8 o, from lane
+            // chunk 64 k + lane = r * slice / 8 + o), the loads of U steps in
+            // flight together; LDS counters hand out the positions.
+            if (tid == 0) s_cnt[0] = s_cnt[1] = 0;
             __syncthreads();
             const int G = gridDim.x, b = blockIdx.x;
+            const T *fgp = static_cast<const T *>(fz.fg);
+            const bool vec = fgp && ((uintptr_t)fgp & 15u) == 0;
+            const int lo = b * fz.seg_cap, hi = lo + fz.seg_cap < npix ? lo + fz.seg_cap : npix;
+            const int steps_a = hi > lo ? (hi - lo + 511) >> 9 : 0;
             const int nsl = (npix + fz.slice - 1) / fz.slice;
             const int mine = b < nsl ? (nsl - 1 - b) / G + 1 : 0;
-            const T *fgp = static_cast<const T *>(fz.fg);
-            int32_t *seg = fz.list + (size_t)b * fz.seg_cap;
-            auto take = [&](int tot) {
-                int base = 0;
-                if (lane == 0 && tot) base = atomicAdd(s_cnt, tot);
-                return __builtin_amdgcn_readfirstlane(base);
-            };
-            if (fz.slice % 512 == 0) {
-                const int per = fz.slice >> 9, steps = mine * per;
-                const bool vec = fgp && ((uintptr_t)fgp & 15u) == 0;
-                constexpr int U = 2;
-                for (int j0 = wv; j0 < steps; j0 += U * kWpb) {
-                    float v[U][8];
-                    int p0[U];
-                    uint32_t m[U], valid[U];
-                    int c[U], incl[U], tot = 0;
+            const int csh = __builtin_ctz(fz.slice) - 3;                // log2 of the 8-pixel chunks per slice
+            const int steps = steps_a + ((mine << csh) + 63) / 64;
+            int32_t *seg = fz.list + (size_t)lo;
+            constexpr int U = 3;
+            for (int j0 = wv; j0 < steps; j0 += U * kWpb) {
+                float v[U][8];
+                int p0[U], lim[U];
 #pragma unroll
-                    for (int u = 0; u < U; u++) {
-                        const int j = j0 + u * kWpb;
-                        p0[u] = (b + G * (j / per)) * fz.slice + (j % per) * 512 + lane * 8;
-                        load8<T>(fgp, p0[u], j < steps ? npix : 0, vec, v[u]);
+                for (int u = 0; u < U; u++) {
+                    const int j = j0 + u * kWpb;
+                    if (j < steps_a) {
+                        p0[u] = lo + j * 512 + lane * 8;
+                        lim[u] = hi;
+                    } else {
+                        const int c = (j - steps_a) * 64 + lane, r = c >> csh;
+                        p0[u] = (b + G * r) * fz.slice + ((c & ((1 << csh) - 1)) << 3);
+                        lim[u] = j < steps && r < mine ? npix : 0;
                     }
+                    load8<T>(fgp, p0[u], lim[u], vec, v[u]);
+                }
+                uint32_t m[U], valid[U];
+                int c[U], incl[U], tot_a = 0, tot_b = 0;
 #pragma unroll
-                    for (int u = 0; u < U; u++) {
-                        const bool live = j0 + u * kWpb < steps;      // uniform
-                        m[u] = valid[u] = 0;
+                for (int u = 0; u < U; u++) {
+                    m[u] = valid[u] = 0;
 #pragma unroll
-                        for (int i = 0; i < 8; i++) {
-                            const bool in = live && p0[u] + i < npix;
-                            valid[u] |= (in ? 1u : 0u) << i;
-                            m[u] |= (in && (!fgp || v[u][i] > fz.fg_thr) ? 1u : 0u) << i;   // a NaN never exceeds it
-                        }
-                        c[u] = __popc(m[u]);
-                        incl[u] = wave_incl_sum(c[u]);
-                        tot += __builtin_amdgcn_readlane(incl[u], 63);
+                    for (int i = 0; i < 8; i++) {
+                        const bool in = p0[u] + i < lim[u];
+                        valid[u] |= (in ? 1u : 0u) << i;
+                        m[u] |= (in && (!fgp || v[u][i] > fz.fg_thr) ? 1u : 0u) << i;   // a NaN never exceeds it
                     }
-                    int base = take(tot);
+                    c[u] = __popc(m[u]);
+                    incl[u] = wave_incl_sum(c[u]);
+                    const int t = __builtin_amdgcn_readlane(incl[u], 63);
+                    if (j0 + u * kWpb < steps_a)
+                        tot_a += t;
+                    else
+                        tot_b += t;
+                }
+                int base_a = 0, base_b = 0;
+                if (lane == 0 && tot_a) base_a = atomicAdd(&s_cnt[1], tot_a);
+                if (lane == 0 && tot_b) base_b = atomicAdd(&s_cnt[0], tot_b);
+                base_a = __builtin_amdgcn_readfirstlane(base_a);
+                base_b = __builtin_amdgcn_readfirstlane(base_b);
 #pragma unroll
-                    for (int u = 0; u < U; u++) {
-                        int off = base + incl[u] - c[u];                // < the slices' pixels <= seg_cap
+                for (int u = 0; u < U; u++) {
+                    const int t = __builtin_amdgcn_readlane(incl[u], 63);
+                    if (j0 + u * kWpb < steps_a) {
+                        int off = base_a + incl[u] - c[u];              // < hi - lo <= seg_cap
 #pragma unroll
                         for (int i = 0; i < 8; i++)
-                            if ((m[u] >> i) & 1u) {
-                                s_list[off] = p0[u] + i;
-                                seg[off] = p0[u] + i;
-                                off++;
-                            }
-                        base += __builtin_amdgcn_readlane(incl[u], 63);
+                            if ((m[u] >> i) & 1u) seg[off++] = p0[u] + i;
+                        base_a += t;
                         const uint32_t bg = valid[u] & ~m[u];
                         if (bg == 0xffu) {
                             const int4 z = {0, 0, 0, 0};
@@ -507,41 +521,12 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
                             for (int i = 0; i < 8; i++)
                                 if ((bg >> i) & 1u) fz.score[p0[u] + i] = 0.0f;
                         }
-                    }
-                }
-            } else {
-                const int per = fz.slice >> 6, steps = mine * per;
-                constexpr int U = 4;
-                for (int j0 = wv; j0 < steps; j0 += U * kWpb) {
-                    float v[U];
-                    int p[U];
-                    unsigned long long m[U];
-                    int tot = 0;
+                    } else {
+                        int off = base_b + incl[u] - c[u];              // < the slices' pixels <= kFusedMaxSeg
 #pragma unroll
-                    for (int u = 0; u < U; u++) {
-                        const int j = j0 + u * kWpb;
-                        p[u] = (b + G * (j / per)) * fz.slice + (j % per) * 64 + lane;
-                        v[u] = fgp && j < steps && p[u] < npix ? load_scalar<T>(fgp + p[u]) : 0.0f;
-                    }
-#pragma unroll
-                    for (int u = 0; u < U; u++) {
-                        const bool in = j0 + u * kWpb < steps && p[u] < npix;
-                        m[u] = __ballot(in && (!fgp || v[u] > fz.fg_thr));   // a NaN never exceeds it
-                        tot += (int)__popcll(m[u]);
-                        if (in && !((m[u] >> lane) & 1ull)) {
-                            fz.labels[p[u]] = 0;
-                            if (fz.score) fz.score[p[u]] = 0.0f;
-                        }
-                    }
-                    int base = take(tot);
-#pragma unroll
-                    for (int u = 0; u < U; u++) {
-                        if ((m[u] >> lane) & 1ull) {
-                            const int pos = base + lane_prefix(m[u]);     // < the slices' pixels <= seg_cap
-                            s_list[pos] = p[u];
-                            seg[pos] = p[u];
-                        }
-                        base += (int)__popcll(m[u]);
+                        for (int i = 0; i < 8; i++)
+                            if ((m[u] >> i) & 1u) s_list[off++] = p0[u] + i;
+                        base_b += t;
                     }
                 }
             }
@@ -564,7 +549,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     if constexpr (FUSED) {
         t0 = 0;
         tend = ntiles;
-        if (tid == 0) fz.counts[blockIdx.x] = n;
+        if (tid == 0) fz.counts[blockIdx.x] = s_cnt[1];
     } else {
         block_run(ntiles, blockIdx.x, gridDim.x, t0, tend);
     }
