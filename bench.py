@@ -33,7 +33,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E peak, GB/s
 GOLDEN = os.path.join(ROOT, "tests", "golden", "configs.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
-STAGE_KERNEL = {"compact": "k_compact", "recover_vote": "k_vote_mfma", "assign_label": "k_assign_mfma"}
+STAGE_KERNEL = {"compact": "k_compact", "recover_vote": "k_vote_mfma", "compact_vote": "k_vote_mfma",
+                "assign_label": "k_assign_mfma"}
 
 
 def source_sha256():
@@ -122,6 +123,7 @@ def frame_bytes(spec, frame):
         "literal": npx * spec.D * es + 4 * npx,
         "compact": npx * es + 4 * nfg + 4 * (npx - nfg),
         "recover_vote": 4 * nfg + nfg * spec.D * es,
+        "compact_vote": npx * es + 4 * nfg + 4 * (npx - nfg) + nfg * spec.D * es,
         "assign_label": 4 * nfg + nfg * spec.D * es + 4 * nfg,
         "peaks_assign_label": npx * spec.D * es + npx * es + 4 * npx,
         "n_fg": nfg,
@@ -211,10 +213,11 @@ def copy_bandwidth(mib=256, reps=10):
 
 
 def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
-    """Average duration of each of the frame's three kernels over reps x
-    frames, from the start and end events their dispatches record."""
+    """Average duration of each of the frame's kernels over reps x frames,
+    from the start and end events their dispatches record."""
     from paper_2609_16874_amd import native
-    names = native.stage_names(dec.bins_w, dec.bins_h)
+    layout = native.stage_layout(dec)
+    names = [n for n, _ in layout]
     ev = HipEvents(native.STAGE_EVENTS)
     assert dec.set_stage_events(ev.ev) == 0
     acc = np.zeros(len(names))
@@ -223,7 +226,7 @@ def stage_times(dec, embs, fgs, outs, fg_thr, theta, reps):
         for i in range(len(embs)):
             o = outs[i]
             assert dec.decode(embs[i], fgs[i], fg_thr, theta, o["centroids"], o["num_centroids"], o["labels"]) == 0
-            acc += [ev.elapsed_ms(2 * k, 2 * k + 1) for k in range(len(names))]
+            acc += [ev.elapsed_ms(2 * i, 2 * i + 1) for _, i in layout]
             n += 1
     dec.set_stage_events(None)
     ev.close()

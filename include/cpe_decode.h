@@ -267,6 +267,14 @@ cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch);
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
 
 /*
+ * Kernels each frame of this handle launches: 2 when the vote launch also
+ * lists the participating pixels (frames of up to 2^21 pixels on grids up to
+ * 32 x 32 bins), else 3 (numbered as for cpe_decode_set_stage_events); 0 for
+ * NULL.
+ */
+int32_t cpe_decode_launch_count(const cpe_decoder *h);
+
+/*
  * Profiling: when `events` is non-NULL, every later cpe_decode on this handle
  * launches its i-th kernel (i = 0, 1, 2) so that the dispatch itself records
  * events[2i] when the kernel starts and events[2i+1] when it ends, on the

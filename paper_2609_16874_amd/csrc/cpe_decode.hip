@@ -479,6 +479,13 @@ cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch)
 
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h) { return h ? h->dev_bytes : 0; }
 
+int32_t cpe_decode_launch_count(const cpe_decoder *h)
+{
+    if (!h) return 0;
+    const bool mfma = h->bins_w <= kMfmaBins && h->bins_h <= kMfmaBins;
+    return mfma && fused_plan((int64_t)h->H * h->W).ok ? 2 : 3;
+}
+
 cpe_status cpe_decode_set_stage_events(cpe_decoder *h, hipEvent_t *events, int32_t n_events)
 {
     if (!h) return CPE_ERR_INVALID_ARG;

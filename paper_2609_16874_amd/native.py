@@ -28,16 +28,19 @@ CENTROID_DTYPE = np.dtype([("bin_x", "<i4"), ("bin_y", "<i4"), ("x", "<f4"), ("y
 EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks", "cpe_decode_destroy",
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
            "cpe_decode_set_stage_events", "cpe_decode_naive", "cpe_check_sqrt",
-           "cpe_decode_test_fail_launch", "cpe_decode_noalloc")
+           "cpe_decode_test_fail_launch", "cpe_decode_noalloc", "cpe_decode_launch_count")
 STAGE_EVENTS = 6
 MFMA_BINS = 32
 
 
-def stage_names(bins_w: int, bins_h: int):
-    """Names of the three stages of a frame, as timed by the stage events."""
-    if bins_w <= MFMA_BINS and bins_h <= MFMA_BINS:
-        return ("compact", "recover_vote", "assign_label")
-    return ("compact", "recover_vote", "peaks_assign_label")
+def stage_layout(dec):
+    """The stages of one frame of decoder dec as (name, launch index i):
+    stage events 2i and 2i+1 bracket it."""
+    if dec.launch_count() == 2:
+        return (("compact_vote", 1), ("assign_label", 2))
+    if dec.bins_w <= MFMA_BINS and dec.bins_h <= MFMA_BINS:
+        return (("compact", 0), ("recover_vote", 1), ("assign_label", 2))
+    return (("compact", 0), ("recover_vote", 1), ("peaks_assign_label", 2))
 
 _lib = None
 
@@ -80,6 +83,8 @@ def library():
         lib.cpe_decode_get_histogram.argtypes = [P, P, P]
         lib.cpe_decode_workspace_bytes.restype = ctypes.c_size_t
         lib.cpe_decode_workspace_bytes.argtypes = [P]
+        lib.cpe_decode_launch_count.restype = i32
+        lib.cpe_decode_launch_count.argtypes = [P]
         lib.cpe_decode_set_stage_events.restype = i32
         lib.cpe_decode_set_stage_events.argtypes = [P, P, i32]
         lib.cpe_decode_naive.restype = i32
@@ -200,6 +205,9 @@ class Decoder:
 
     def workspace_bytes(self) -> int:
         return int(library().cpe_decode_workspace_bytes(self._h))
+
+    def launch_count(self) -> int:
+        return int(library().cpe_decode_launch_count(self._h))
 
     def close(self):
         if getattr(self, "_h", None):

@@ -41,6 +41,7 @@ def test_status_strings_and_null_handles():
     assert lib.cpe_decode_get_tables(None, None, None, None, None) == native.CPE_ERR_INVALID_ARG
     assert lib.cpe_decode_get_histogram(None, None, None) == native.CPE_ERR_INVALID_ARG
     assert lib.cpe_decode_workspace_bytes(None) == 0
+    assert lib.cpe_decode_launch_count(None) == 0
     opt = native.DecodeOptions(0.5, 0, 0.0, float("inf"))
     assert lib.cpe_decode_ex(None, None, None, None, 4, 4, ctypes.byref(opt), None, None, None, None) == \
         native.CPE_ERR_INVALID_ARG
