@@ -215,10 +215,12 @@ def _misaligned(t):
     return v
 
 
-# Frames whose vote launch lists the participating pixels itself: 64-pixel
-# slices (640 x 640), 1024-pixel slices read eight pixels per lane (frames
-# above 2^20 pixels), ragged last slices, fp16 and fp32 foreground planes,
-# 16-byte aligned or aligned to their element only.
+# Frames whose vote launch lists the participating pixels itself, eight
+# consecutive pixels per lane: 64-pixel slices (640 x 640) and 1024-pixel
+# slices (frames above 2^20 pixels) for the vote, contiguous ranges for the
+# assignment, ragged last slices and ranges, fp16 and fp32 foreground planes,
+# 16-byte aligned (vector loads) or aligned to their element only (one load
+# per pixel).
 FG_CASES = [(640, 640, 4, np.float16, True), (1023, 1027, 4, np.float32, True), (1024, 1024, 4, np.float32, False),
             (1025, 1029, 3, np.float16, False), (1025, 1029, 3, np.float16, True)]
 
