@@ -288,3 +288,41 @@ def test_decode_after_a_failed_one_matches_the_oracle(bins, fail):
     assert_parity(got, ref, cap)
     assert dec.test_fail_launch(3) == nat.CPE_ERR_INVALID_ARG
     dec.close()
+
+
+def test_launch_count_and_stage_events():
+    """Frames of up to 2^21 pixels on grids up to 32 x 32 take two launches
+    (the vote launch compacts): stage events 0 and 1 are recorded back to
+    back, 2-3 and 4-5 bracket the two kernels; larger grids and frames take
+    three.  The decode with events on still equals the oracle."""
+    import bench
+    nat = native()
+    spec = synth.CONFIGS[1]
+    fx, fy = spec.freqs()
+    th = thresholds()["1"]
+    f = synth.make_frame(1)
+    for bins, launches in ((32, 2), (48, 3)):
+        theta = th["peak_threshold"] * (bins / 32.0) ** -2
+        cap = ((bins + 1) // 2) ** 2
+        dec = nat.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, bins, bins, cap)
+        assert dec.launch_count() == launches
+        assert [i for _, i in nat.stage_layout(dec)] == ([1, 2] if launches == 2 else [0, 1, 2])
+        ev = bench.HipEvents(nat.STAGE_EVENTS)
+        assert dec.set_stage_events(ev.ev) == 0
+        got = gpu_decode(dec, f.emb, f.fg, spec.fg_threshold, theta)
+        ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(3)]
+        assert dec.set_stage_events(None) == 0
+        ev.close()
+        print(f"bins {bins}: {launches} launches, stage ms {ms}", flush=True)
+        assert ms[1] > 0 and ms[2] > 0
+        if launches == 2:
+            assert ms[0] < ms[1]          # no kernel between events 0 and 1
+        else:
+            assert ms[0] > 0
+        ref = oracle.decode(f.emb, f.fg, fx, fy, bins, bins, cap, spec.fg_threshold, theta)
+        assert_parity(got, ref, cap)
+        dec.close()
+    fx1 = np.array([2 * math.pi / 2048])
+    big = nat.Decoder(1025, 2048, 1, "f16", fx1, fx1, 32, 32)      # 2,099,200 pixels > 2^21
+    assert big.launch_count() == 3
+    big.close()
