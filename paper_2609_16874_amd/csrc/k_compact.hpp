@@ -1,6 +1,8 @@
 // k_compact.hpp -- the participating set S of Eq6 as a compact pixel list.
 //
-// One launch per frame before the vote.  Workgroup s of the grid owns the
+// One launch before the vote in frames of three launches (frames above
+// kFusedMaxPixels pixels, grids above 32 x 32 bins; the vote launch lists
+// the pixels itself otherwise).  Workgroup s of the grid owns the
 // pixel range [s R, (s + 1) R) (R a multiple of 8192) and writes the indices
 // of its participating pixels, in raster order, to its slice list[s R ..]
 // and their number to counts[s]; every lane tests 8 consecutive foreground
@@ -9,8 +11,8 @@
 // atomics: the consumers concatenate the slices through the prefix sum of
 // the counts (slice_prefix / ListCursor).  The non-participating pixels get
 // their final outputs here: label 0 and, if a score map is requested,
-// score 0.  The launch also clears the frame's vote histograms, which the
-// vote launch then accumulates into.  The vote and assignment launches then
+// score 0.  The launch also clears the next frame's vote histograms (this
+// frame's were cleared before it).  The vote and assignment launches then
 // stream equal shares of the list in full tiles, so their work does not
 // depend on where in the frame the foreground lies.
 #pragma once

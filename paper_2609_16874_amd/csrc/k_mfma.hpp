@@ -391,12 +391,14 @@ template <typename T, int F>
 constexpr int kVoteWpb = 4 * kVoteWaves<T, F>;
 //
 // Every workgroup adds its histogram into one of the kReplicas vote
-// histograms `hrep` (zeroed by the frame's first launch); the assignment launch that follows
-// sums them and extracts the peaks.  Workgroup 0 also resets the pixel
-// counts of the centroid records, which the assignment launch accumulates.
+// histograms `hrep` (clear when the frame starts: an earlier launch cleared
+// them); the assignment launch that follows sums them and extracts the
+// peaks.  Workgroup 0 also resets the pixel counts of the centroid records,
+// which the assignment launch accumulates.
 // MULTI: grids above 32 x 32 bins (one pass per block of 32 x 32 bins);
 // otherwise the single block is compiled without the pass loop, whose
-// registers would otherwise spill.
+// registers would otherwise spill.  FUSED: the launch lists the
+// participating pixels itself (FusedArgs); list and counts are then unused.
 template <typename T, int F, bool MULTI, bool FUSED>
 __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kVoteWaves<T, F>))) void k_vote_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
