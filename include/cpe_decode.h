@@ -183,7 +183,7 @@ cpe_status cpe_decode_ex(cpe_decoder *h, hipStream_t stream, const void *emb, co
  * forbid hipMalloc): the same frame, arguments, outputs and errors as
  * cpe_decode_ex, and the handle's constants, but the per-frame scratch (vote
  * histograms, participating-pixel list, slice counts, peak list) is a static
- * device array of the library, about 10.7 MB, held by each device the
+ * device array of the library, about 9.7 MB, held by each device the
  * library runs on until the process ends, instead of the handle's.  The
  * call itself allocates nothing.
  *   Limit: frames of at most 2,097,152 pixels (H*W <= 2^21, e.g. 1024 x

@@ -45,11 +45,14 @@ long long peak_cut(double theta)
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // List entries a frame of npix pixels may need: the compaction launch's
-// slices (npix and at most one slice more), or the folded compaction's
-// segments (npix and at most one 1024-pixel slice per workgroup more).
+// slices hold npix entries with at most one slice (slice_pixels) of slack;
+// the folded compaction's segments (one per workgroup, each a range of a
+// multiple of 8 pixels) at most 8 entries per workgroup, which that slice
+// covers.
+static_assert(kCompactSpan >= 8 * kMaxSlices, "one compaction slice covers the folded segments' slack");
 constexpr int64_t list_entries(int64_t npix)
 {
-    return npix + slice_pixels(npix) + (int64_t)kMaxSlices * 1024;
+    return npix + slice_pixels(npix);
 }
 
 // Eq8 on distance sums D in units of 1/4096: D / 4096 < tau  <=>  D < 4096 tau
