@@ -59,11 +59,13 @@ struct PixelLayout {
 // S4 + S5: assignment, label write-out, counts
 // ---------------------------------------------------------------------------
 // LDS bytes of k_assign_generic before its per-pixel distances: palettes,
-// norms, counts, candidate slots and the slice prefix.
+// norms, counts, candidate slots, the slots' bins, the candidate rows'
+// first candidates and the slice prefix.
 __host__ __device__ constexpr size_t generic_assign_fixed(int Bw, int Bh, int F, int kmax)
 {
     return ((size_t)(Bw + Bh) * F * 4 + (size_t)(Bw + Bh) * 4 + (size_t)kCountCap * 4 + (size_t)kmax * 4 +
-            2 * (size_t)kMaxBins * 2 + 2 * (size_t)kMaxBins / 8 + (size_t)(kMaxSlices + 1) * 4 + 64 + 15) &
+            2 * (size_t)kMaxBins * 2 + 2 * (size_t)kMaxBins / 8 + 2 * (size_t)kMaxBins * 2 +
+            (size_t)(kMaxBins + 1) * 4 + (size_t)(kMaxSlices + 1) * 4 + 64 + 15) &
            ~(size_t)15;
 }
 
@@ -71,7 +73,12 @@ __host__ __device__ constexpr size_t generic_assign_fixed(int Bw, int Bh, int F,
 // k_compact, or every pixel without a foreground channel).  The candidate
 // columns and rows are numbered in ascending order (slots); each thread
 // computes its pixel's distances to the slots' palette entries only, then
-// scans the candidates in index order.
+// scans the candidate rows in order: the candidates are in bin order, so
+// each row's candidates are a contiguous run of indices, and within a row
+// the smallest sum r_y + r_x belongs to the smallest r_x (the binary64 sum
+// of two binary32 values is exact, hence strictly increasing in r_x).  The
+// first row with the smallest sum, and in it the first candidate with that
+// row's smallest r_x, is the lowest index attaining the minimum (Eq7).
 template <typename T, int F>
 __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ emb, int32_t dstride, int32_t yoff,
                                                 const int32_t *__restrict__ list, const int32_t *__restrict__ counts,
@@ -93,9 +100,11 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
     int32_t *s_pk = s_cnt + kCountCap;                           // [kmax] column slot | row slot << 16
     uint16_t *s_slot = reinterpret_cast<uint16_t *>(s_pk + kmax); // [2][kMaxBins] bin -> slot
     uint32_t *s_mask = reinterpret_cast<uint32_t *>(s_slot + 2 * kMaxBins);   // [2][kMaxBins / 32]
-    int *s_pref = reinterpret_cast<int *>(s_mask + 2 * kMaxBins / 32);      // [kMaxSlices + 1]
+    uint16_t *s_sbin = reinterpret_cast<uint16_t *>(s_mask + 2 * kMaxBins / 32);  // [2][kMaxBins] slot -> bin
+    int *s_rfirst = reinterpret_cast<int *>(s_sbin + 2 * kMaxBins);          // [kMaxBins + 1] first candidate of a row slot
+    int *s_pref = s_rfirst + kMaxBins + 1;                                   // [kMaxSlices + 1]
     int *s_ns = s_pref + kMaxSlices + 1;                                     // [2] candidate columns, rows
-    float *s_r = reinterpret_cast<float *>(smem + generic_assign_fixed(Bw, Bh, F, kmax));  // [slots][TP]
+    float *s_r = reinterpret_cast<float *>(smem + generic_assign_fixed(Bw, Bh, F, kmax));  // [column slots][TP]
 
     const int Kc = kinfo[0];
     const int ncnt = Kc < kCountCap ? Kc : kCountCap;
@@ -122,13 +131,18 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
         int below = __popc(m[bin >> 5] & ((1u << (bin & 31)) - 1u));
         for (int w = 0; w < (bin >> 5); w++) below += __popc(m[w]);
         s_slot[i] = (uint16_t)below;
+        if ((m[bin >> 5] >> (bin & 31)) & 1u) s_sbin[ax * kMaxBins + below] = (uint16_t)bin;
         if (bin == kMaxBins - 1) s_ns[ax] = below + (int)((m[bin >> 5] >> 31) & 1u);
     }
     __syncthreads();
     for (int k = tid; k < Kc; k += TP) {
         const int32_t pk = peaks[k];
-        s_pk[k] = (int32_t)s_slot[pk & 0xffff] | ((int32_t)s_slot[kMaxBins + (pk >> 16)] << 16);
+        const int rs = s_slot[kMaxBins + (pk >> 16)];
+        s_pk[k] = (int32_t)s_slot[pk & 0xffff] | (rs << 16);
+        // candidates are in bin order: a row slot's candidates are a run of indices
+        if (k == 0 || (peaks[k - 1] >> 16) != (pk >> 16)) s_rfirst[rs] = k;
     }
+    if (tid == 0) s_rfirst[s_ns[1]] = Kc;
     __syncthreads();
     const int ncol = s_ns[0], nrow = s_ns[1];
 
@@ -152,26 +166,36 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
             load_block<T, F, L::kAlignY>(row + yoff, yk);
             const uint32_t nX = (uint32_t)dot_pk<F>(xk, xk);
             const uint32_t nY = (uint32_t)dot_pk<F>(yk, yk);
-            // distances of the candidate columns and rows (the slots' bins)
-            for (int a = 0, s = 0; a < Bw; a++)
-                if ((s_mask[a >> 5] >> (a & 31)) & 1u)
-                    s_r[(s++) * TP + tid] = sqrt_cr((float)axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)));
-            for (int b = 0, s = ncol; b < Bh; b++)
-                if ((s_mask[kMaxBins / 32 + (b >> 5)] >> (b & 31)) & 1u)
-                    s_r[(s++) * TP + tid] = sqrt_cr((float)axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)));
-            // Eq7: smallest exact sum (binary64 holds the sum of two binary32
-            // values exactly), lowest index on ties
-            int best = 0;
-            const int32_t pk0 = s_pk[0];
-            double bd = (double)s_r[(pk0 & 0xffff) * TP + tid] + (double)s_r[(ncol + (pk0 >> 16)) * TP + tid];
-            for (int k = 1; k < Kc; k++) {
-                const int32_t pk = s_pk[k];
-                const double d = (double)s_r[(pk & 0xffff) * TP + tid] + (double)s_r[(ncol + (pk >> 16)) * TP + tid];
+            // distances of the candidate columns (the column slots' bins)
+            for (int s = 0; s < ncol; s++) {
+                const int a = s_sbin[s];
+                s_r[s * TP + tid] = sqrt_cr((float)axis_s(nX, s_nx[a], dot_pk<F>(xk, s_px + a * F)));
+            }
+            // Eq7 by rows: the smallest column distance of each row's run (the
+            // binary32 bits of distances >= 0 order like their values), plus the
+            // row's distance (computed here, once per row), summed exactly in
+            // binary64; strict < keeps the first row
+            const uint32_t *s_rb = reinterpret_cast<const uint32_t *>(s_r);
+            double bd = __builtin_inf();
+            int brow = 0;
+            uint32_t bm = 0u;
+            for (int r = 0, k = 0; r < nrow; r++) {
+                const int kend = s_rfirst[r + 1];
+                uint32_t m = 0xffffffffu;
+                for (; k < kend; k++) m = min(m, s_rb[(s_pk[k] & 0xffff) * TP + tid]);
+                const int b = s_sbin[kMaxBins + r];
+                const float ry = sqrt_cr((float)axis_s(nY, s_ny[b], dot_pk<F>(yk, s_py + b * F)));
+                const double d = (double)__uint_as_float(m) + (double)ry;
                 if (d < bd) {
                     bd = d;
-                    best = k;
+                    brow = r;
+                    bm = m;
                 }
             }
+            // the first candidate of that row with its smallest column distance
+            int best = s_rfirst[brow];
+            const int blast = s_rfirst[brow + 1] - 1;
+            while (best < blast && s_rb[(s_pk[best] & 0xffff) * TP + tid] != bm) best++;
             if (bd < tau4096) {     // Eq8
                 labels[pp] = best + 1;
                 if (score_map) score_map[pp] = expf(-(float)(bd * 0x1p-12));
@@ -185,7 +209,6 @@ __global__ __launch_bounds__(256) void k_assign_generic(const T *__restrict__ em
             }
         }
     }
-    (void)nrow;
     __syncthreads();
     for (int i = tid; i < ncnt; i += TP)
         if (s_cnt[i]) atomicAdd(&cents[i].npix, s_cnt[i]);

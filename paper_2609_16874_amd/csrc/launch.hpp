@@ -154,8 +154,8 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
                                sc.hlast, Bw, Bh, cut, h->cap, h->tb.cx, h->tb.cy, po);
         if (hipGetLastError() != hipSuccess) return CPE_ERR_HIP;
         const size_t fixed2 = generic_assign_fixed(Bw, Bh, F, max_peaks(Bw, Bh));
-        const int tp2 = pick_tile(fixed2, (size_t)(Bw + Bh) * 4, 120 * 1024);
-        const size_t lds2 = fixed2 + (size_t)(Bw + Bh) * tp2 * 4;
+        const int tp2 = pick_tile(fixed2, (size_t)Bw * 4, 120 * 1024);     // per pixel: its column distances
+        const size_t lds2 = fixed2 + (size_t)Bw * tp2 * 4;
         const int64_t tiles2 = ((int64_t)npix + tp2 - 1) / tp2;
         const int grid2 = (int)(tiles2 < 2048 ? tiles2 : 2048);
         auto assign_kernel = k_assign_generic<T, F>;
