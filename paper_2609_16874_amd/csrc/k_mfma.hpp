@@ -312,7 +312,7 @@ __device__ __forceinline__ int take_tile(int *next, int lane, int first, int wav
 }
 
 // ---------------------------------------------------------------------------
-// Pass 1: recovery + soft voting (+ the peak extraction in the last workgroup)
+// Pass 1: recovery + soft voting
 // ---------------------------------------------------------------------------
 // Row stride (in 64-bit words) of the vote kernel's LDS histogram: one word
 // of padding per row puts the 32 rows that one fold instruction touches
