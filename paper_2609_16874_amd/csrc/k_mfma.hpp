@@ -1,12 +1,15 @@
 // k_mfma.hpp -- matrix-core decoder kernels: the vote for every bin grid (in
 // passes over blocks of 32 x 32 bins), the assignment for grids up to 32 x 32.
 //
-// Both passes stream the compact list of participating pixels written by
-// k_compact (or every pixel, when the frame has no foreground channel): the
-// list is cut into tiles of 32 consecutive entries, every workgroup gets a
-// contiguous run of tiles of the same length to within one, and its waves
-// take the run's tiles one at a time from a counter in LDS (so that they
-// finish together however the SIMDs favour older waves), always loading the
+// Both passes stream a compact list of participating pixels (or every
+// pixel, when the frame has no foreground channel), cut into tiles of 32
+// consecutive entries.  The assignment, and the vote of three-launch
+// frames, read the list in global memory (written by k_compact, or by the
+// vote launch in two-launch frames): every workgroup gets a contiguous run
+// of tiles of the same length to within one.  In two-launch frames the vote
+// lists its own share of the pixels in LDS (FusedArgs).  The waves take
+// their tiles one at a time from a counter in LDS (so that they finish
+// together however the SIMDs favour older waves), always loading the
 // embedding rows of the next tile (and the list entries of the one after)
 // before computing the current one.  Every tile but the last is full.
 //
