@@ -311,3 +311,22 @@ def test_argument_errors_on_device():
     assert dec.decode(e, g, 0.5, 0.0, None, *args[1:]) == nat.CPE_ERR_INVALID_ARG
     torch.cuda.synchronize()
     dec.close()
+
+
+@pytest.mark.parametrize("H,W", [(1024, 2048), (1, 2097153)])
+def test_frames_at_the_two_launch_limit(H, W):
+    """The largest frame whose vote launch lists the pixels itself (2^21
+    pixels, two launches) and one pixel more (the compaction launch first,
+    three launches): both equal the oracle."""
+    nat = native()
+    rng = np.random.default_rng(H + W)
+    emb, fg, fx, fy = _random_frame(rng, H, W, 1, np.float16)
+    ref0 = oracle.decode(emb, fg, fx, fy, 8, 8, 16, 0.5, 0.0)
+    theta = 0.05 * ref0["hist"].max() * 2.0 ** -30
+    dec = nat.Decoder(H, W, 1, "f16", fx, fy, 8, 8, 16)
+    assert dec.launch_count() == (2 if H * W <= 2 ** 21 else 3)
+    print(f"{H}x{W}: {dec.launch_count()} launches", flush=True)
+    got, ref = run_pair(emb, fg, fx, fy, 8, 8, 16, 0.5, theta, dec=dec)
+    assert ref["K"] > 0
+    assert_parity(got, ref, 16)
+    dec.close()
