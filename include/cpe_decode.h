@@ -263,6 +263,15 @@ cpe_status cpe_check_sqrt(hipStream_t stream, unsigned long long *mismatches);
  */
 cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch);
 
+/*
+ * Testing: with on != 0, every later label-only decode on this handle (no
+ * score map, tau = +inf, grids up to 32 x 32 bins) treats every tile as a
+ * near tie of its fast assignment search and recomputes it with correctly
+ * rounded distances and the exact search, the path such tiles take (the
+ * labels must not change); 0 restores the default.
+ */
+cpe_status cpe_decode_test_exact_search(cpe_decoder *h, int32_t on);
+
 /* Bytes of device memory the handle holds (constants + scratch). */
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h);
 

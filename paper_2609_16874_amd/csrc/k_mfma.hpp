@@ -47,6 +47,8 @@
 // lowest centroid index among the smallest sums.
 #pragma once
 
+#include <type_traits>
+
 #include "cpe_common.hpp"
 #include "k_compact.hpp"
 #include "k_peaks.hpp"
@@ -57,6 +59,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 
@@ -322,15 +325,24 @@ __device__ __forceinline__ int take_tile(int *next, int lane, int first, int wav
 // (lanes = y bins, fixed x bin) into distinct banks.
 constexpr int kHStride = kMfmaBins + 1;
 
-// LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
-// the palette operands, per wave |X|^2 of one tile's pixels per axis, the
-// slice prefix sums and counters; with the compaction folded in (FUSED),
-// the workgroup's own participating pixels.
+// LDS of k_vote_mfma: the 64-bit histogram, the palette operands, per wave
+// |X|^2 of one tile's pixels per axis, the slice prefix sums and counters;
+// at byte kVoteTab the weight byte tables ([2][kWKeys]: low bytes, high
+// bytes); then, with the compaction folded in (FUSED), the workgroup's own
+// participating pixels.  The kernel's only LDS object starts at LDS address
+// 0, so that table entry k of a bucket key K = k + kWKeyBase (the shifted
+// bits of fl32(S+1)) sits at LDS address K: the key itself is the address,
+// with the byte offset of the high table in the instruction's offset field.
+constexpr size_t kVoteHead(int wpb)
+{
+    return kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 + 16;
+}
+constexpr size_t kVoteTab = kWKeyBase;
 constexpr size_t kVoteLds(int wpb, bool fused)
 {
-    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
-           16 + (fused ? (size_t)kFusedMaxSeg * 4 : 0);
+    return kVoteTab + 2 * (size_t)kWKeys + (fused ? (size_t)kFusedMaxSeg * 4 : 0);
 }
+static_assert(kVoteHead(12) <= kVoteTab, "the vote kernel's other LDS data lies below its weight tables");
 
 // Eight foreground values from pixel p0 on (p0 a multiple of 8): one (fp16)
 // or two (fp32) 16-byte loads when the plane is 16-byte aligned and the
@@ -414,15 +426,16 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     // blocks of 32 x 32 bins: one pass over the workgroup's tiles per block
     const int nbx = MULTI ? (Bw + kMfmaBins - 1) / kMfmaBins : 1, nby = MULTI ? (Bh + kMfmaBins - 1) / kMfmaBins : 1;
     // All LDS is static, so that table addresses are compile-time constants.
+    static_assert(kVoteHead(kWpb) <= kVoteTab, "LDS layout");
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb, FUSED)];
-    uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32][kHStride], b * kHStride + a
+    unsigned char *s_wt = smem + kVoteTab;                                            // [2][kWKeys] weight bytes
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem);          // [32][kHStride], b * kHStride + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kHStride);      // palette operands
     uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][2][32]
     int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 64);                        // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
     int *s_cnt = s_next + 1;                                                          // FUSED: [2] pixels listed (LDS, global)
-    int *s_list = s_pref + kMaxSlices + 5;                                            // FUSED: [kFusedMaxSeg]
+    int *s_list = reinterpret_cast<int *>(s_wt + 2 * kWKeys);                        // FUSED: [kFusedMaxSeg]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -433,12 +446,12 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     // trip of their own)
     uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
     {
-        constexpr int kThreads = kWpb * 64, kN = kWKeys / 4, kPer = (kN + kThreads - 1) / kThreads;
+        constexpr int kThreads = kWpb * 64, kN = 2 * kWKeys / 16, kPer = (kN + kThreads - 1) / kThreads;
         u32x4 w[kPer];
 #pragma unroll
         for (int k = 0; k < kPer; k++) {
             const int i = k * kThreads + tid;
-            w[k] = reinterpret_cast<const u32x4 *>(tb.wt_pk)[i < kN ? i : 0];
+            w[k] = reinterpret_cast<const u32x4 *>(tb.wt8)[i < kN ? i : 0];
         }
         if constexpr (FUSED) {
             // While the table loads are in flight, two lists of the
@@ -543,13 +556,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     int ntile = 0;
 
     // Add the limb sums into the workgroup's histogram (this wave owns every
-    // (a, b) exactly once, so its own atomics never collide).
+    // (a, b) exactly once, so its own atomics never collide).  The limbs are
+    // fp16 subnormals (k 2^-24), so the sums are integers times 2^-48.
     auto fold = [&]() {
 #pragma unroll
         for (int r = 0; r < 16; r++) {
-            const unsigned long long v = ((unsigned long long)(uint32_t)acc2[r] << 16) +
-                                         ((unsigned long long)(uint32_t)acc1[r] << 8) +
-                                         (unsigned long long)(uint32_t)acc0[r];
+            const unsigned long long v = ((unsigned long long)(uint32_t)(acc2[r] * 0x1p48f) << 16) +
+                                         ((unsigned long long)(uint32_t)(acc1[r] * 0x1p48f) << 8) +
+                                         (unsigned long long)(uint32_t)(acc0[r] * 0x1p48f);
             atomicAdd(&s_h[ln * kHStride + acc_row(r, g)], v);
             acc2[r] = 0.0f;
             acc1[r] = 0.0f;
@@ -557,14 +571,24 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // Packed weight limbs of the 16 (pixel, bin) results of one axis: the
-    // accumulators start at the pixels' |X|^2, and cb = |P|^2 + 1 of this
-    // lane's bin completes S + 1, whose binary32 bits give the bucket.
-    auto weights = [&](const i32x16 &hh, const i32x16 &mid, const i32x16 &ll, uint32_t cb, uint32_t (&e)[16]) {
+    // Weight limbs of the 16 (pixel, bin) results of one axis, as the fp16
+    // operand halves of the vote contraction: the accumulators start at the
+    // pixels' |X|^2, and cb = |P|^2 + 1 of this lane's bin completes S + 1,
+    // whose binary32 bits shifted right by 15 are the bucket key K, which is
+    // also the LDS address of its low byte (the high byte is 2^13 above), so
+    // the key needs no masking.  Each byte, zero-extended into one 16-bit
+    // half of an operand register, is the fp16 subnormal k 2^-24: results
+    // 2i and 2i + 1 in the halves of lo[i] and hi[i].
+    static_assert(kVoteTab == kWKeyBase, "weight bytes at their key's LDS address");
+    auto weights = [&](const i32x16 &hh, const i32x16 &mid, const i32x16 &ll, uint32_t cb, uint32_t (&lo)[8],
+                       uint32_t (&hi)[8]) {
+        const unsigned char *tab = s_wt - kWKeyBase;
 #pragma unroll
-        for (int r = 0; r < 16; r++) {
-            const uint32_t s1 = assemble(hh[r], mid[r], ll[r], cb);
-            e[r] = s_wt[(__float_as_uint((float)s1) >> 15) & (kWKeys - 1)];
+        for (int i = 0; i < 8; i++) {
+            const uint32_t k0 = __float_as_uint((float)assemble(hh[2 * i], mid[2 * i], ll[2 * i], cb)) >> 15;
+            const uint32_t k1 = __float_as_uint((float)assemble(hh[2 * i + 1], mid[2 * i + 1], ll[2 * i + 1], cb)) >> 15;
+            lo[i] = (uint32_t)tab[k0] | ((uint32_t)tab[k1] << 16);
+            hi[i] = (uint32_t)tab[kWKeys + k0] | ((uint32_t)tab[kWKeys + k1] << 16);
         }
     };
 
@@ -582,14 +606,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             ini[ln] = (uint32_t)n2x;
             ini[32 + ln] = (uint32_t)n2y;
         }
-        uint32_t ex[16], ey[16];
+        uint32_t xlo[8], xhi[8], ylo[8], yhi[8];
         {
             i32x4 P[kPopKinds];
 #pragma unroll
             for (int k = 0; k < kPopKinds; k++) P[k] = palette_operand(s_pop, 0, k, lane);
             i32x16 hh, mid, ll;
             axis_products<F, true>(X, P, row_init(ini, g), hh, mid, ll);
-            weights(hh, mid, ll, np1x, ex);
+            weights(hh, mid, ll, np1x, xlo, xhi);
         }
         {
             i32x4 P[kPopKinds];
@@ -597,14 +621,18 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             for (int k = 0; k < kPopKinds; k++) P[k] = palette_operand(s_pop, 1, k, lane);
             i32x16 hh, mid, ll;
             axis_products<F, true>(Y, P, row_init(ini + 32, g), hh, mid, ll);
-            weights(hh, mid, ll, np1y, ey);
+            weights(hh, mid, ll, np1y, ylo, yhi);
         }
         if (nvalid < 32) {        // pixels past the end of the list vote nothing
             // (kept a real branch: only the last tile of a round is partial)
             __asm__ volatile("" ::: "memory");
 #pragma unroll
-            for (int r = 0; r < 16; r++)
-                if (acc_row(r, g) >= nvalid) ex[r] = 0u;
+            for (int i = 0; i < 8; i++) {
+                const uint32_t m = (acc_row(2 * i, g) < nvalid ? 0xffffu : 0u) |
+                                   (acc_row(2 * i + 1, g) < nvalid ? 0xffff0000u : 0u);
+                xlo[i] &= m;
+                xhi[i] &= m;
+            }
         }
         // vote: K = the 16 pixels of this lane, in two MFMAs of 8
 #pragma unroll
@@ -612,11 +640,10 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             u32x4 xl, xh, yl, yh;
 #pragma unroll
             for (int s = 0; s < 4; s++) {
-                const int r = 8 * t + 2 * s;
-                xl[s] = __builtin_amdgcn_perm(ex[r + 1], ex[r], 0x05040100u);
-                xh[s] = __builtin_amdgcn_perm(ex[r + 1], ex[r], 0x07060302u);
-                yl[s] = __builtin_amdgcn_perm(ey[r + 1], ey[r], 0x05040100u);
-                yh[s] = __builtin_amdgcn_perm(ey[r + 1], ey[r], 0x07060302u);
+                xl[s] = xlo[4 * t + s];
+                xh[s] = xhi[4 * t + s];
+                yl[s] = ylo[4 * t + s];
+                yh[s] = yhi[4 * t + s];
             }
             const f16x8 XL = __builtin_bit_cast(f16x8, xl), XH = __builtin_bit_cast(f16x8, xh);
             const f16x8 YL = __builtin_bit_cast(f16x8, yl), YH = __builtin_bit_cast(f16x8, yh);
@@ -734,13 +761,13 @@ constexpr size_t kAssignLds(int wpb) { return kBestOff(wpb) + (size_t)wpb * 32 *
 // The candidate search walks the batches of 4 columns of one row (see the
 // search below).  A pixel is labelled iff its distance sum D (in units of
 // 1/4096) is below tau4096 = 4096 tau (Eq8; +inf: every pixel).
-template <typename T, int F>
+template <typename T, int F, bool FAST>
 __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_waves_per_eu(kAssignWaves<T, F>))) void k_assign_mfma(
     const T *__restrict__ emb, int32_t dstride, int32_t yoff, const int32_t *__restrict__ list,
     const int32_t *__restrict__ counts, int32_t nslices, int32_t slice_px, int32_t npix, double tau4096, Tables tb,
     const unsigned long long *__restrict__ hcur, unsigned long long *__restrict__ hlast, int32_t Bw, int32_t Bh, long long cut, int32_t cap,
     cpe_centroid *__restrict__ cents, int32_t *__restrict__ num, int32_t *__restrict__ labels,
-    float *__restrict__ score_map)
+    float *__restrict__ score_map, int32_t force_exact)
 {
     constexpr int kWpb2 = kAssignWpb<T, F>;
     constexpr int kThreads = kWpb2 * 64;
@@ -835,19 +862,15 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     // bin, gathered once and kept in registers for the whole run; distances
     // are computed only for the groups of 8 slots that hold candidates.
     const int nslot[2] = {__builtin_amdgcn_readfirstlane(pl.ncol), __builtin_amdgcn_readfirstlane(pl.nrow)};
-    i32x4 pop[2][kPopKinds];
-#pragma unroll
-    for (int ax = 0; ax < 2; ax++) {
-        const int bin = ax ? pl.rowbin[ln] : pl.colbin[ln];
-#pragma unroll
-        for (int k = 0; k < kPopKinds; k++) pop[ax][k] = palette_operand(s_pop, ax, k, g * 32 + bin);
-    }
+    const int slotbin[2] = {g * 32 + pl.colbin[ln], g * 32 + pl.rowbin[ln]};
 
     // Distances of one tile (pixel m = lane & 31; this lane's 16 slots
     // acc_row(r, g) of each axis); `next` reuses the input registers once
     // they are converted.  The accumulators of the Xl.lo products start at
-    // the slots' |P|^2; the pixel's |X|^2 completes S.
-    auto distances = [&](RawSlices<T, F> &raw, auto next) {
+    // the slots' |P|^2; the pixel's |X|^2 completes S.  EXACT: the correctly
+    // rounded square root of fl32(S); otherwise the hardware square root,
+    // within one binary32 step of it (the fast search below).
+    auto distances = [&](auto exact, RawSlices<T, F> &raw, auto next) {
         int n2x = 0, n2y = 0;
         AxisOp<F> X, Y;
         raw.convert(0, X, n2x);
@@ -858,7 +881,10 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
 #pragma unroll
         for (int ax = 0; ax < 2; ax++) {
             i32x16 hh, mid, ll;
-            axis_products<F, false>(ax ? Y : X, pop[ax], row_init(s_cbs + ax * kMfmaBins, g), hh, mid, ll);
+            i32x4 pop[kPopKinds];
+#pragma unroll
+            for (int k = 0; k < kPopKinds; k++) pop[k] = palette_operand(s_pop, ax, k, slotbin[ax]);
+            axis_products<F, false>(ax ? Y : X, pop, row_init(s_cbs + ax * kMfmaBins, g), hh, mid, ll);
             const uint32_t np = ax ? npy : npx;
             uint32_t *dst = (ax ? ky : kx) + 4 * g * kKeyStride + ln;
 #pragma unroll
@@ -867,7 +893,8 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
 #pragma unroll
                 for (int i = 0; i < 4; i++) {
                     const int r = 4 * r4 + i;
-                    const float d = sqrt_cr((float)assemble(hh[r], mid[r], ll[r], np));
+                    const float x = (float)assemble(hh[r], mid[r], ll[r], np);
+                    const float d = decltype(exact)::value ? sqrt_cr(x) : __builtin_amdgcn_sqrtf(x);
                     dst[kKeyStride * (8 * r4 + i)] = __float_as_uint(d);
                 }
             }
@@ -948,6 +975,140 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
         __builtin_amdgcn_wave_barrier();
     };
 
+    // Fast search (labels only: no score map, tau = +inf).  The distances
+    // are the hardware square roots r~ of fl32(S), each within one binary32
+    // step of the correctly rounded r (cpe_check_sqrt verifies the step
+    // correction of sqrt_cr, which only tries r~ and its two neighbours, on
+    // every input).  Lane l serves the pixels 2p, 2p + 1 (p = l & 15) over the
+    // batches j, j + 4, ... (j = l >> 4) of the unpadded list, so that no
+    // batch is seen twice, and keeps per pixel the smallest binary32 sum
+    // fl(min x~ + y~) of a batch, its batch, and the second smallest.  A
+    // step at v is at most 2^-23 v, so a batch's true minimum D lies within
+    // 2^-21 of its approximate sum; if the second smallest sum exceeds the
+    // smallest by at least 32 steps (> 2^-19 relative), every other batch's
+    // D exceeds the winning batch's.  Within the winning batch (one row,
+    // exact distances of one y), a column whose r~ is at least 3 steps above
+    // the batch's smallest r~ is strictly farther.  When both hold the
+    // winner is the unique minimiser of the exact sums, i.e. the candidate
+    // the exact search selects.  Otherwise (near ties, within a few units
+    // in the last place) the wave recomputes the tile exactly; false is
+    // returned and nothing is written.
+    const int nbr = min(pl.nbat_real, kMaxBatchLds);
+    auto search_fast = [&](int pix, int nvalid) -> bool {
+        __builtin_amdgcn_wave_barrier();
+        int lo = lane;
+        __asm__ volatile("" : "+v"(lo));        // recomputed per tile, not held across the loop
+        const int p = lo & 15, j0 = lo >> 4;
+        const unsigned char *kxp = reinterpret_cast<const unsigned char *>(kx + 2 * p);
+        const unsigned char *kyp = reinterpret_cast<const unsigned char *>(ky + 2 * p);
+        float b[2] = {__builtin_inff(), __builtin_inff()}, s2[2] = {__builtin_inff(), __builtin_inff()};
+        int bx[2] = {0, 0};
+        for (int bi = j0; bi < nbr; bi += 4) {
+            const u32x4 o = s_bo[bi];
+            const uint32_t hb = s_bh[bi];
+            const u32x2 v0 = *reinterpret_cast<const u32x2 *>(kxp + o.x);
+            const u32x2 v1 = *reinterpret_cast<const u32x2 *>(kxp + o.y);
+            const u32x2 v2 = *reinterpret_cast<const u32x2 *>(kxp + o.z);
+            const u32x2 v3 = *reinterpret_cast<const u32x2 *>(kxp + o.w);
+            const u32x2 yd = *reinterpret_cast<const u32x2 *>(kyp + hb);
+#pragma unroll
+            for (int e = 0; e < 2; e++) {
+                const uint32_t m = min(min(v0[e], v1[e]), min(v2[e], v3[e]));
+                const float sm = __uint_as_float(m) + __uint_as_float(yd[e]);
+                s2[e] = __builtin_amdgcn_fmed3f(b[e], s2[e], sm);
+                bx[e] = sm < b[e] ? bi : bx[e];
+                b[e] = sm < b[e] ? sm : b[e];
+            }
+        }
+        // combine the four lanes of a pixel pair (equal smallest sums leave
+        // a second smallest equal to the smallest)
+        // (as bit patterns, which order like the non-negative sums)
+        uint32_t ub[2], us[2];
+#pragma unroll
+        for (int e = 0; e < 2; e++) {
+            ub[e] = __float_as_uint(b[e]);
+            us[e] = __float_as_uint(s2[e]);
+        }
+#pragma unroll
+        for (int d = 16; d <= 32; d <<= 1)
+#pragma unroll
+            for (int e = 0; e < 2; e++) {
+                const uint32_t ob = __shfl_xor(ub[e], d), os = __shfl_xor(us[e], d);
+                const int ox = __shfl_xor(bx[e], d);
+                us[e] = min(min(us[e], os), max(ub[e], ob));
+                bx[e] = ob < ub[e] ? ox : bx[e];
+                ub[e] = min(ub[e], ob);
+            }
+        // lane m (either half) takes pixel m's result from lane
+        // (m >> 1) + 16 (m & 1), which offers its pixel 2p + (j & 1)
+        const int src = (ln >> 1) + 16 * (ln & 1);
+        const bool hi = (j0 & 1) != 0;
+        const uint32_t bb = __shfl(hi ? ub[1] : ub[0], src), ss = __shfl(hi ? us[1] : us[0], src);
+        const int bi = __shfl(hi ? bx[1] : bx[0], src);
+        const u32x4 o = s_bo[bi];
+        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
+        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
+        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
+        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
+        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+        const uint32_t wm = min(min(w0, w1), min(w2, w3));
+        const uint32_t oc = w0 == wm ? o.x : w1 == wm ? o.y : w2 == wm ? o.z : o.w;   // first column at the minimum
+        const bool near = (o.x != oc && w0 - wm < 3u) || (o.y != oc && w1 - wm < 3u) ||
+                          (o.z != oc && w2 - wm < 3u) || (o.w != oc && w3 - wm < 3u);
+        const bool amb = near || ss - bb < 32u;
+        const bool valid = g == 0 && ln < nvalid;
+        if (force_exact || __ballot(amb && valid)) return false;
+        if (valid) {
+            const int a = pl.colbin[oc >> 7], bb_ = pl.rowbin[s_bh[bi] >> 7];
+            const int k = s_rank[bb_ * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
+            labels[pix] = k + 1;
+            atomicAdd(s_cnt + k, 1);
+        }
+        __builtin_amdgcn_wave_barrier();
+        return true;
+    };
+
+    // Exact search of the tiles the fast search leaves undecided: lane m
+    // (either half: half g takes the batches g, g + 2, ...) scans every batch
+    // for pixel m with the keys of the exact search above (binary64 sum of
+    // the batch's smallest x distance and the row's y distance, batch index
+    // in the low bits), then takes the first column of the winning batch at
+    // the batch's minimum: the same candidate as the exact search.
+    auto search_pix = [&](int pix, int nvalid) {
+        __builtin_amdgcn_wave_barrier();
+        const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
+        const unsigned char *kyl = reinterpret_cast<const unsigned char *>(ky + ln);
+        double best = __builtin_inf();
+        for (int bi = g; bi < nbr; bi += 2) {
+            const u32x4 o = s_bo[bi];
+            const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
+            const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
+            const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
+            const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+            const uint32_t yv = *reinterpret_cast<const uint32_t *>(kyl + s_bh[bi]);
+            const uint32_t m = min(min(w0, w1), min(w2, w3));
+            const double sum = (double)__uint_as_float(m) + (double)__uint_as_float(yv);
+            const unsigned long long sb = (unsigned long long)__double_as_longlong(sum);
+            best = min_f64(best, __longlong_as_double((long long)((sb & ~0xffffffffull) | ((uint32_t)sb | (uint32_t)bi))));
+        }
+        best = min_f64(best, __shfl_xor(best, 32));
+        const int bi = (int)((uint32_t)__double_as_longlong(best) & 127u);
+        const u32x4 o = s_bo[bi];
+        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
+        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
+        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
+        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+        const uint32_t wm = min(min(w0, w1), min(w2, w3));
+        const uint32_t col = (w0 == wm ? o.x : w1 == wm ? o.y : w2 == wm ? o.z : o.w) >> 7;
+        if (g == 0 && ln < nvalid) {
+            const int a = pl.colbin[col], b = pl.rowbin[s_bh[bi] >> 7];
+            const int k = s_rank[b * kMfmaBins + a] & (kMfmaBins * kMfmaBins - 1);
+            labels[pix] = k + 1;
+            atomicAdd(s_cnt + k, 1);
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+
     // the next tile's rows are loaded as soon as the current ones are converted
     int tn = tend, ipn = 0;                             // next tile; this lane's pixel in it
     if (t < tend) {
@@ -956,14 +1117,26 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     }
     while (t < tend) {
         int tnn = tend, ipnn = 0;
-        distances(raw, [&]() {
+        auto next = [&]() {
             if (tn < tend) {
                 raw.load(emb + (size_t)ipn * dstride, yoff, g);
                 tnn = take_tile(s_next, lane, t0, kWpb2);
                 if (tnn < tend) ipnn = pixel(tnn);
             }
-        });
-        search(ip, min(32, n - 32 * t));
+        };
+        const int nvalid = min(32, n - 32 * t);
+        if constexpr (FAST) {
+            distances(std::false_type{}, raw, next);
+            if (!search_fast(ip, nvalid)) {
+                raw.load(emb + (size_t)ip * dstride, yoff, g);          // this tile's rows again
+                distances(std::true_type{}, raw, []() {});
+                if (tn < tend) raw.load(emb + (size_t)ipn * dstride, yoff, g);   // the next tile's rows again
+                search_pix(ip, nvalid);
+            }
+        } else {
+            distances(std::true_type{}, raw, next);
+            search(ip, nvalid);
+        }
         t = tn;
         tn = tnn;
         ip = ipn;

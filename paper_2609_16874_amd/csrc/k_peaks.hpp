@@ -127,7 +127,8 @@ struct PeakLds {
     int wave[2 * kPeakThreads / 64];  // per-wave counts of the two slot passes (slot-owning waves)
     uint32_t rowmask[kLdsPeakBins];   // bit a of row b: (a, b) is one of the first min(K, cap) candidates
     uint32_t colmask;                 // bit a: column a holds one of them
-    int K, Kc, nbat;
+    int K, Kc, nbat;                  // nbat: batches, padded to a multiple of kBatchPad
+    int nbat_real;                    // batches before the padding
     int ncol, nrow;                   // candidate columns and rows
     uint8_t colbin[kLdsPeakBins];     // column of column slot j (ascending; 0 past ncol)
     uint8_t rowbin[kLdsPeakBins];     // row of row slot j (ascending; 0 past nrow)
@@ -299,6 +300,7 @@ __device__ __forceinline__ void peaks_lds_find(int Bw, int Bh, long long cut, in
             pl.K = K;
             pl.Kc = Kc;
             pl.nbat = padded;
+            pl.nbat_real = total;
             pl.ncol = __popc(cm);
             pl.nrow = __popcll(rows);
         }

@@ -134,9 +134,13 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
         constexpr int wpb2 = kAssignWpb<T, F>;
         const int64_t wgs2 = (tiles + wpb2 - 1) / wpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        if (!launch(2, k_assign_mfma<T, F>, dim3(grid2), dim3(wpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
+        // labels only (no score map, no Eq8 threshold): the fast search
+        const bool fast = score == nullptr && !(fa.tau4096 < __builtin_inf());
+        auto assign_kernel = fast ? k_assign_mfma<T, F, true> : k_assign_mfma<T, F, false>;
+        if (!launch(2, assign_kernel, dim3(grid2), dim3(wpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
                     (const int32_t *)sc.counts, nslices, slice_px, npix, fa.tau4096, h->tb,
-                    (const unsigned long long *)hcur, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score))
+                    (const unsigned long long *)hcur, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score,
+                    (int32_t)h->force_exact))
             return CPE_ERR_HIP;
     } else {
         // launch 2 (larger grids): the stand-alone peak kernel, then the

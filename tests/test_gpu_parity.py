@@ -35,6 +35,9 @@ def native():
 
 
 def gpu_decode(dec, emb, fg, fg_thr, theta, score=True):
+    """One decode with the score map (the assignment's exact search) and,
+    with score, a second one without it (labels only: the fast search that
+    the benchmark runs), whose records and labels go to res["fast"]."""
     e = torch.from_numpy(np.ascontiguousarray(emb)).cuda()
     g = torch.from_numpy(np.ascontiguousarray(fg)).cuda()
     res = dec.run(e, g, fg_thr, theta, score=score)
@@ -42,10 +45,18 @@ def gpu_decode(dec, emb, fg, fg_thr, theta, score=True):
     assert dec.histogram(hist) == 0
     torch.cuda.synchronize()
     res["hist"] = hist.cpu().numpy().view(np.uint64)
+    if score:
+        fast = dec.run(e, g, fg_thr, theta, score=False)
+        assert dec.histogram(hist) == 0
+        torch.cuda.synchronize()
+        fast["hist"] = hist.cpu().numpy().view(np.uint64)
+        res["fast"] = fast
     return res
 
 
 def assert_parity(got, ref, capacity, check_score=True):
+    if "fast" in got:
+        assert_parity(got["fast"], ref, capacity, check_score=False)
     assert got["K"] == ref["K"], (got["K"], ref["K"])
     assert np.array_equal(got["hist"], ref["hist"]), "vote histogram differs"
     assert len(got["centroids"]) == min(ref["K"], capacity)
@@ -120,23 +131,51 @@ def test_workload4_batch_back_to_back():
     frames = [synth.make_frame(4, i) for i in range(spec.n_frames)]
     embs = [torch.from_numpy(fr.emb).cuda() for fr in frames]
     fgs = [torch.from_numpy(fr.fg).cuda() for fr in frames]
-    outs = [dec.new_outputs(score=True) for _ in frames]
-    hists = [torch.empty((spec.bins, spec.bins), dtype=torch.int64, device="cuda") for _ in frames]
-    for i in range(len(frames)):
-        o = outs[i]
-        assert dec.decode(embs[i], fgs[i], spec.fg_threshold, th["peak_threshold"], o["centroids"],
-                          o["num_centroids"], o["labels"], o["score_map"]) == 0
-        assert dec.histogram(hists[i]) == 0
+    # pass 0: labels only, as the benchmark decodes (the fast assignment
+    # search); pass 1: with the score map (the exact search)
+    runs = []
+    for score in (False, True):
+        outs = [dec.new_outputs(score=score) for _ in frames]
+        hists = [torch.empty((spec.bins, spec.bins), dtype=torch.int64, device="cuda") for _ in frames]
+        for i in range(len(frames)):
+            o = outs[i]
+            assert dec.decode(embs[i], fgs[i], spec.fg_threshold, th["peak_threshold"], o["centroids"],
+                              o["num_centroids"], o["labels"], o["score_map"]) == 0
+            assert dec.histogram(hists[i]) == 0
+        runs.append((outs, hists))
     torch.cuda.synchronize()
     for i, fr in enumerate(frames):
         print(f"config 4 frame {i}", flush=True)
         ref = oracle.decode(fr.emb, fr.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
                             th["peak_threshold"])
-        K = int(outs[i]["num_centroids"].item())
-        got = {"K": K, "centroids": outs[i]["centroids"].cpu().numpy().view(nat.CENTROID_DTYPE)[:min(K, dec.capacity)],
-               "labels": outs[i]["labels"].cpu().numpy(), "score_map": outs[i]["score_map"].cpu().numpy(),
-               "hist": hists[i].cpu().numpy().view(np.uint64)}
-        assert_parity(got, ref, th["capacity"])
+        for outs, hists in runs:
+            K = int(outs[i]["num_centroids"].item())
+            got = {"K": K, "centroids": outs[i]["centroids"].cpu().numpy().view(nat.CENTROID_DTYPE)[:min(K, dec.capacity)],
+                   "labels": outs[i]["labels"].cpu().numpy(), "hist": hists[i].cpu().numpy().view(np.uint64)}
+            if outs[i]["score_map"] is not None:
+                got["score_map"] = outs[i]["score_map"].cpu().numpy()
+            assert_parity(got, ref, th["capacity"])
+    dec.close()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_every_tile_through_the_exact_search(cfg):
+    """Label-only decodes with every tile sent down the path that near ties
+    of the fast assignment search take (recomputed with correctly rounded
+    distances, exact search): equal to the oracle; then back to the default."""
+    nat = native()
+    spec = synth.CONFIGS[cfg]
+    th = thresholds()[str(cfg)]
+    f = synth.make_frame(cfg)
+    fx, fy = spec.freqs()
+    dec = nat.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, spec.bins, spec.bins, th["capacity"])
+    ref = oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
+                        th["peak_threshold"])
+    for forced in (True, False):
+        print(f"config {cfg}: exact search forced {forced}", flush=True)
+        assert dec.test_exact_search(forced) == 0
+        got = gpu_decode(dec, f.emb, f.fg, spec.fg_threshold, th["peak_threshold"], score=False)
+        assert_parity(got, ref, th["capacity"], check_score=False)
     dec.close()
 
 
