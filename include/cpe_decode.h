@@ -264,13 +264,16 @@ cpe_status cpe_check_sqrt(hipStream_t stream, unsigned long long *mismatches);
 cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch);
 
 /*
- * Testing: with on != 0, every later label-only decode on this handle (no
- * score map, tau = +inf, grids up to 32 x 32 bins) treats every tile as a
- * near tie of its fast assignment search and recomputes it with correctly
- * rounded distances and the exact search, the path such tiles take (the
- * labels must not change); 0 restores the default.
+ * Testing: the assignment search of later label-only decodes on this handle
+ * (no score map, tau = +inf, grids up to 32 x 32 bins).  mode 0 (default):
+ * the fast search (hardware square roots, near ties recomputed exactly) on
+ * frames of at least 2^20 pixels, the exact search on smaller ones; 1: the
+ * fast-search kernel at any size with every tile treated as a near tie,
+ * i.e. recomputed with correctly rounded distances and the exact search;
+ * 2: the fast search at any size.  The labels are the same in every mode.
+ * CPE_ERR_INVALID_ARG for another mode.
  */
-cpe_status cpe_decode_test_exact_search(cpe_decoder *h, int32_t on);
+cpe_status cpe_decode_test_search_mode(cpe_decoder *h, int32_t mode);
 
 /* Bytes of device memory the handle holds (constants + scratch). */
 size_t cpe_decode_workspace_bytes(const cpe_decoder *h);

@@ -43,11 +43,9 @@ struct Tables {
     const uint32_t *pop;      // [axis][block][kind][64 lanes][4 words]: the int8 palette operand of
                               //   lane l (bin 32 block + (l & 31), K slots 16 (l >> 5) .. + 15);
                               //   see k_mfma.hpp
-    const uint8_t *wt8;       // [2][kWKeys] the bytes of the weights, bucket order: q & 255, then q >> 8
+    const uint32_t *wt_pk;    // [kWKeys] weight as two fp16 limbs (q & 255) | (q >> 8) << 16,
+                              //          at LDS position ((e + 31) & 31) * 256 + t
 };
-
-// Bit pattern of fl32(S+1) >> (23 - kWMant) for S + 1 = 1: the first bucket.
-constexpr uint32_t kWKeyBase = 127u << kWMant;
 
 // Input to fixed point: rint(4096 clamp(v, -1.5, 1.5)), the input on the
 // palette's grid of 1/4096; a NaN clamps to -1.5 (fmaxf/fminf return the

@@ -89,6 +89,14 @@ double centre_distance(int key, int m)
     return std::sqrt(std::ldexp(1.0 + ((double)t + 0.5) / (double)(1 << m), e) - 1.0) / 4096.0;
 }
 
+uint16_t f16_bits(int v)   // exact for the small integers used here (|v| <= 2048)
+{
+    const _Float16 hv = (_Float16)(float)v;
+    uint16_t b;
+    std::memcpy(&b, &hv, 2);
+    return b;
+}
+
 // ---------------------------------------------------------------------------
 // Per-frame scratch of cpe_decode_noalloc: a static device array, one copy
 // per device, for frames of up to kStaticMaxPixels pixels and any bin grid.
@@ -250,12 +258,13 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     // of fl32(S+1)
     h->wt.resize(kWKeys);
     for (int k = 0; k < kWKeys; k++) h->wt[k] = (uint16_t)std::rint(32768.0 * std::exp(-centre_distance(k, kWMant)));
-    // the matrix-core vote's byte tables: low bytes of the weights, then high
-    // bytes, in bucket order (index = (float bits >> (23 - m)) - kWKeyBase)
-    std::vector<uint8_t> wt8(2 * kWKeys);
+    // LDS order of the matrix-core kernels: bucket (e, t) at ((e + 31) & 31) << m | t,
+    // so that (float bits >> (23 - m)) & (2^(m+5) - 1) indexes it directly
+    std::vector<uint32_t> wt_pk(kWKeys);
     for (int k = 0; k < kWKeys; k++) {
-        wt8[k] = (uint8_t)(h->wt[k] & 255);
-        wt8[kWKeys + k] = (uint8_t)(h->wt[k] >> 8);
+        const int e = k >> kWMant, t = k & ((1 << kWMant) - 1);
+        const int q = h->wt[k];
+        wt_pk[(((e + 31) & 31) << kWMant) | t] = (uint32_t)f16_bits(q & 255) | ((uint32_t)f16_bits(q >> 8) << 16);
     }
 
     auto pack = [&](int n, const std::vector<int16_t> &pal, std::vector<int32_t> &pk, std::vector<uint32_t> &n2) {
@@ -334,7 +343,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     const size_t o_cx = carve(cx.size() * 4), o_cy = carve(cy.size() * 4);
     const size_t o_npx = carve(np1x.size() * 4), o_npy = carve(np1y.size() * 4);
     const size_t o_pop = carve(pop.size());
-    const size_t o_wpk = carve(wt8.size());
+    const size_t o_wpk = carve(wt_pk.size() * 4);
     const size_t o_hrep = carve(2 * (size_t)kReplicas * nb * 8);
     const size_t o_hlast = carve((size_t)nb * 8);
     const size_t o_peaks = carve((size_t)centroid_capacity * 4);
@@ -356,7 +365,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
               up(o_cx, cx.data(), cx.size() * 4) && up(o_cy, cy.data(), cy.size() * 4) &&
               up(o_npx, np1x.data(), np1x.size() * 4) && up(o_npy, np1y.data(), np1y.size() * 4) &&
               up(o_pop, pop.data(), pop.size()) &&
-              up(o_wpk, wt8.data(), wt8.size()) &&
+              up(o_wpk, wt_pk.data(), wt_pk.size() * 4) &&
               hipMemset(d + o_hrep, 0, 2 * (size_t)kReplicas * nb * 8) == hipSuccess &&
               hipMemset(d + o_hlast, 0, (size_t)nb * 8) == hipSuccess &&
               hipMemset(d + o_kinfo, 0, 16) == hipSuccess && hipMemset(d + o_count, 0, (size_t)kMaxSlices * 4) == hipSuccess &&
@@ -376,7 +385,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->tb.np1_x = reinterpret_cast<const uint32_t *>(d + o_npx);
     h->tb.np1_y = reinterpret_cast<const uint32_t *>(d + o_npy);
     h->tb.pop = reinterpret_cast<const uint32_t *>(d + o_pop);
-    h->tb.wt8 = reinterpret_cast<const uint8_t *>(d + o_wpk);
+    h->tb.wt_pk = reinterpret_cast<const uint32_t *>(d + o_wpk);
     h->sc.hrep = reinterpret_cast<unsigned long long *>(d + o_hrep);
     h->sc.set_stride = (size_t)kReplicas * nb;
     h->parity = 0;
@@ -389,7 +398,7 @@ cpe_status cpe_decode_create(cpe_decoder **out, int32_t H, int32_t W, int32_t D,
     h->sc.counts = reinterpret_cast<int32_t *>(d + o_count);
     h->sc.list = reinterpret_cast<int32_t *>(d + o_list);
     h->fail_at = -1;
-    h->force_exact = false;
+    h->search_mode = 0;
     *out = h;
     return CPE_OK;
 }
@@ -472,10 +481,10 @@ cpe_status cpe_decode_test_fail_launch(cpe_decoder *h, int32_t launch)
     return CPE_OK;
 }
 
-cpe_status cpe_decode_test_exact_search(cpe_decoder *h, int32_t on)
+cpe_status cpe_decode_test_search_mode(cpe_decoder *h, int32_t mode)
 {
-    if (!h) return CPE_ERR_INVALID_ARG;
-    h->force_exact = on != 0;
+    if (!h || mode < 0 || mode > 2) return CPE_ERR_INVALID_ARG;
+    h->search_mode = mode;
     return CPE_OK;
 }
 

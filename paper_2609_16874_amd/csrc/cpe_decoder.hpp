@@ -70,7 +70,7 @@ struct cpe_decoder {
     int parity;                          // histogram set of the next frame (sc.parity points here)
     size_t dirty[2];                     // words of each set that may be nonzero (sc.dirty points here)
     int fail_at;                         // test hook: the next decode stops before this launch (-1: none)
-    bool force_exact;                    // test hook: every tile takes the exact assignment search
+    int search_mode;                     // test hook: 0 default, 1 every tile exact, 2 fast search at any size
     hipEvent_t stage_ev[CPE_STAGE_EVENTS];
     bool stage_on;
     // per-tuple ablation (cpe_decode_naive): real palettes gamma(bin centre)

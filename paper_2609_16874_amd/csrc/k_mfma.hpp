@@ -325,24 +325,15 @@ __device__ __forceinline__ int take_tile(int *next, int lane, int first, int wav
 // (lanes = y bins, fixed x bin) into distinct banks.
 constexpr int kHStride = kMfmaBins + 1;
 
-// LDS of k_vote_mfma: the 64-bit histogram, the palette operands, per wave
-// |X|^2 of one tile's pixels per axis, the slice prefix sums and counters;
-// at byte kVoteTab the weight byte tables ([2][kWKeys]: low bytes, high
-// bytes); then, with the compaction folded in (FUSED), the workgroup's own
-// participating pixels.  The kernel's only LDS object starts at LDS address
-// 0, so that table entry k of a bucket key K = k + kWKeyBase (the shifted
-// bits of fl32(S+1)) sits at LDS address K: the key itself is the address,
-// with the byte offset of the high table in the instruction's offset field.
-constexpr size_t kVoteHead(int wpb)
-{
-    return kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 + 16;
-}
-constexpr size_t kVoteTab = kWKeyBase;
+// LDS bytes of k_vote_mfma: the packed weight table, the 64-bit histogram,
+// the palette operands, per wave |X|^2 of one tile's pixels per axis, the
+// slice prefix sums and counters; with the compaction folded in (FUSED),
+// the workgroup's own participating pixels.
 constexpr size_t kVoteLds(int wpb, bool fused)
 {
-    return kVoteTab + 2 * (size_t)kWKeys + (fused ? (size_t)kFusedMaxSeg * 4 : 0);
+    return (size_t)kWKeys * 4 + kMfmaBins * kHStride * 8 + kPopBytes + (size_t)wpb * 64 * 4 + (kMaxSlices + 1) * 4 +
+           16 + (fused ? (size_t)kFusedMaxSeg * 4 : 0);
 }
-static_assert(kVoteHead(12) <= kVoteTab, "the vote kernel's other LDS data lies below its weight tables");
 
 // Eight foreground values from pixel p0 on (p0 a multiple of 8): one (fp16)
 // or two (fp32) 16-byte loads when the plane is 16-byte aligned and the
@@ -426,16 +417,15 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     // blocks of 32 x 32 bins: one pass over the workgroup's tiles per block
     const int nbx = MULTI ? (Bw + kMfmaBins - 1) / kMfmaBins : 1, nby = MULTI ? (Bh + kMfmaBins - 1) / kMfmaBins : 1;
     // All LDS is static, so that table addresses are compile-time constants.
-    static_assert(kVoteHead(kWpb) <= kVoteTab, "LDS layout");
     __shared__ __align__(16) unsigned char smem[kVoteLds(kWpb, FUSED)];
-    unsigned char *s_wt = smem + kVoteTab;                                            // [2][kWKeys] weight bytes
-    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(smem);          // [32][kHStride], b * kHStride + a
+    uint32_t *s_wt = reinterpret_cast<uint32_t *>(smem);                              // [kWKeys] fp16 limb pairs
+    unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_wt + kWKeys);  // [32][kHStride], b * kHStride + a
     uint32_t *s_pop = reinterpret_cast<uint32_t *>(s_h + kMfmaBins * kHStride);      // palette operands
     uint32_t *s_ini = s_pop + kPopBytes / 4;                                          // [kWpb][2][32]
     int *s_pref = reinterpret_cast<int *>(s_ini + kWpb * 64);                        // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
     int *s_cnt = s_next + 1;                                                          // FUSED: [2] pixels listed (LDS, global)
-    int *s_list = reinterpret_cast<int *>(s_wt + 2 * kWKeys);                        // FUSED: [kFusedMaxSeg]
+    int *s_list = s_pref + kMaxSlices + 5;                                            // FUSED: [kFusedMaxSeg]
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int g = lane >> 5, ln = lane & 31;
@@ -446,12 +436,12 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     // trip of their own)
     uint32_t np1x = tb.np1_x[ln], np1y = tb.np1_y[ln];
     {
-        constexpr int kThreads = kWpb * 64, kN = 2 * kWKeys / 16, kPer = (kN + kThreads - 1) / kThreads;
+        constexpr int kThreads = kWpb * 64, kN = kWKeys / 4, kPer = (kN + kThreads - 1) / kThreads;
         u32x4 w[kPer];
 #pragma unroll
         for (int k = 0; k < kPer; k++) {
             const int i = k * kThreads + tid;
-            w[k] = reinterpret_cast<const u32x4 *>(tb.wt8)[i < kN ? i : 0];
+            w[k] = reinterpret_cast<const u32x4 *>(tb.wt_pk)[i < kN ? i : 0];
         }
         if constexpr (FUSED) {
             // While the table loads are in flight, two lists of the
@@ -556,14 +546,13 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
     int ntile = 0;
 
     // Add the limb sums into the workgroup's histogram (this wave owns every
-    // (a, b) exactly once, so its own atomics never collide).  The limbs are
-    // fp16 subnormals (k 2^-24), so the sums are integers times 2^-48.
+    // (a, b) exactly once, so its own atomics never collide).
     auto fold = [&]() {
 #pragma unroll
         for (int r = 0; r < 16; r++) {
-            const unsigned long long v = ((unsigned long long)(uint32_t)(acc2[r] * 0x1p48f) << 16) +
-                                         ((unsigned long long)(uint32_t)(acc1[r] * 0x1p48f) << 8) +
-                                         (unsigned long long)(uint32_t)(acc0[r] * 0x1p48f);
+            const unsigned long long v = ((unsigned long long)(uint32_t)acc2[r] << 16) +
+                                         ((unsigned long long)(uint32_t)acc1[r] << 8) +
+                                         (unsigned long long)(uint32_t)acc0[r];
             atomicAdd(&s_h[ln * kHStride + acc_row(r, g)], v);
             acc2[r] = 0.0f;
             acc1[r] = 0.0f;
@@ -571,24 +560,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         }
     };
 
-    // Weight limbs of the 16 (pixel, bin) results of one axis, as the fp16
-    // operand halves of the vote contraction: the accumulators start at the
-    // pixels' |X|^2, and cb = |P|^2 + 1 of this lane's bin completes S + 1,
-    // whose binary32 bits shifted right by 15 are the bucket key K, which is
-    // also the LDS address of its low byte (the high byte is 2^13 above), so
-    // the key needs no masking.  Each byte, zero-extended into one 16-bit
-    // half of an operand register, is the fp16 subnormal k 2^-24: results
-    // 2i and 2i + 1 in the halves of lo[i] and hi[i].
-    static_assert(kVoteTab == kWKeyBase, "weight bytes at their key's LDS address");
-    auto weights = [&](const i32x16 &hh, const i32x16 &mid, const i32x16 &ll, uint32_t cb, uint32_t (&lo)[8],
-                       uint32_t (&hi)[8]) {
-        const unsigned char *tab = s_wt - kWKeyBase;
+    // Packed weight limbs of the 16 (pixel, bin) results of one axis: the
+    // accumulators start at the pixels' |X|^2, and cb = |P|^2 + 1 of this
+    // lane's bin completes S + 1, whose binary32 bits give the bucket.
+    auto weights = [&](const i32x16 &hh, const i32x16 &mid, const i32x16 &ll, uint32_t cb, uint32_t (&e)[16]) {
 #pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const uint32_t k0 = __float_as_uint((float)assemble(hh[2 * i], mid[2 * i], ll[2 * i], cb)) >> 15;
-            const uint32_t k1 = __float_as_uint((float)assemble(hh[2 * i + 1], mid[2 * i + 1], ll[2 * i + 1], cb)) >> 15;
-            lo[i] = (uint32_t)tab[k0] | ((uint32_t)tab[k1] << 16);
-            hi[i] = (uint32_t)tab[kWKeys + k0] | ((uint32_t)tab[kWKeys + k1] << 16);
+        for (int r = 0; r < 16; r++) {
+            const uint32_t s1 = assemble(hh[r], mid[r], ll[r], cb);
+            e[r] = s_wt[(__float_as_uint((float)s1) >> 15) & (kWKeys - 1)];
         }
     };
 
@@ -606,14 +585,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             ini[ln] = (uint32_t)n2x;
             ini[32 + ln] = (uint32_t)n2y;
         }
-        uint32_t xlo[8], xhi[8], ylo[8], yhi[8];
+        uint32_t ex[16], ey[16];
         {
             i32x4 P[kPopKinds];
 #pragma unroll
             for (int k = 0; k < kPopKinds; k++) P[k] = palette_operand(s_pop, 0, k, lane);
             i32x16 hh, mid, ll;
             axis_products<F, true>(X, P, row_init(ini, g), hh, mid, ll);
-            weights(hh, mid, ll, np1x, xlo, xhi);
+            weights(hh, mid, ll, np1x, ex);
         }
         {
             i32x4 P[kPopKinds];
@@ -621,18 +600,14 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             for (int k = 0; k < kPopKinds; k++) P[k] = palette_operand(s_pop, 1, k, lane);
             i32x16 hh, mid, ll;
             axis_products<F, true>(Y, P, row_init(ini + 32, g), hh, mid, ll);
-            weights(hh, mid, ll, np1y, ylo, yhi);
+            weights(hh, mid, ll, np1y, ey);
         }
         if (nvalid < 32) {        // pixels past the end of the list vote nothing
             // (kept a real branch: only the last tile of a round is partial)
             __asm__ volatile("" ::: "memory");
 #pragma unroll
-            for (int i = 0; i < 8; i++) {
-                const uint32_t m = (acc_row(2 * i, g) < nvalid ? 0xffffu : 0u) |
-                                   (acc_row(2 * i + 1, g) < nvalid ? 0xffff0000u : 0u);
-                xlo[i] &= m;
-                xhi[i] &= m;
-            }
+            for (int r = 0; r < 16; r++)
+                if (acc_row(r, g) >= nvalid) ex[r] = 0u;
         }
         // vote: K = the 16 pixels of this lane, in two MFMAs of 8
 #pragma unroll
@@ -640,10 +615,11 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             u32x4 xl, xh, yl, yh;
 #pragma unroll
             for (int s = 0; s < 4; s++) {
-                xl[s] = xlo[4 * t + s];
-                xh[s] = xhi[4 * t + s];
-                yl[s] = ylo[4 * t + s];
-                yh[s] = yhi[4 * t + s];
+                const int r = 8 * t + 2 * s;
+                xl[s] = __builtin_amdgcn_perm(ex[r + 1], ex[r], 0x05040100u);
+                xh[s] = __builtin_amdgcn_perm(ex[r + 1], ex[r], 0x07060302u);
+                yl[s] = __builtin_amdgcn_perm(ey[r + 1], ey[r], 0x05040100u);
+                yh[s] = __builtin_amdgcn_perm(ey[r + 1], ey[r], 0x07060302u);
             }
             const f16x8 XL = __builtin_bit_cast(f16x8, xl), XH = __builtin_bit_cast(f16x8, xh);
             const f16x8 YL = __builtin_bit_cast(f16x8, yl), YH = __builtin_bit_cast(f16x8, yh);

@@ -16,6 +16,9 @@ namespace cpe {
 // waves) and one assignment workgroup of 12 waves per compute unit.
 constexpr int64_t kVoteGrid = 256;
 constexpr int64_t kAssignGrid = 256;
+// Frames from this many pixels take the fast assignment search when only
+// labels are requested.
+constexpr int64_t kFastSearchPixels = 1 << 20;
 
 // Largest pixel tile (threads per block) whose LDS footprint fits the budget.
 inline int pick_tile(size_t fixed, size_t per_px, size_t budget)
@@ -134,13 +137,16 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
         constexpr int wpb2 = kAssignWpb<T, F>;
         const int64_t wgs2 = (tiles + wpb2 - 1) / wpb2;
         const int grid2 = (int)(wgs2 < kAssignGrid ? wgs2 : kAssignGrid);
-        // labels only (no score map, no Eq8 threshold): the fast search
-        const bool fast = score == nullptr && !(fa.tau4096 < __builtin_inf());
+        // labels only (no score map, no Eq8 threshold) on large frames: the
+        // fast search, which pays off when every wave has several tiles (it
+        // shortens each tile's work but lengthens its dependency chain)
+        const bool labels_only = score == nullptr && !(fa.tau4096 < __builtin_inf());
+        const bool fast = labels_only && (h->search_mode != 0 || (int64_t)npix >= kFastSearchPixels);
         auto assign_kernel = fast ? k_assign_mfma<T, F, true> : k_assign_mfma<T, F, false>;
         if (!launch(2, assign_kernel, dim3(grid2), dim3(wpb2 * 64), 0, e, dstride, yoff, (const int32_t *)list,
                     (const int32_t *)sc.counts, nslices, slice_px, npix, fa.tau4096, h->tb,
                     (const unsigned long long *)hcur, sc.hlast, Bw, Bh, cut, h->cap, cents, num, labels, score,
-                    (int32_t)h->force_exact))
+                    (int32_t)(h->search_mode == 1)))
             return CPE_ERR_HIP;
     } else {
         // launch 2 (larger grids): the stand-alone peak kernel, then the

@@ -29,7 +29,7 @@ EXPORTS = ("cpe_decode_create", "cpe_decode", "cpe_decode_ex", "cpe_decode_masks
            "cpe_status_string", "cpe_decode_get_tables", "cpe_decode_get_histogram", "cpe_decode_workspace_bytes",
            "cpe_decode_set_stage_events", "cpe_decode_naive", "cpe_check_sqrt",
            "cpe_decode_test_fail_launch", "cpe_decode_noalloc", "cpe_decode_launch_count",
-           "cpe_decode_test_exact_search")
+           "cpe_decode_test_search_mode")
 STAGE_EVENTS = 6
 MFMA_BINS = 32
 
@@ -94,8 +94,8 @@ def library():
         lib.cpe_decode_noalloc.argtypes = [P, P, P, P, i32, i32, ctypes.POINTER(DecodeOptions), P, P, P, P]
         lib.cpe_decode_test_fail_launch.restype = i32
         lib.cpe_decode_test_fail_launch.argtypes = [P, i32]
-        lib.cpe_decode_test_exact_search.restype = i32
-        lib.cpe_decode_test_exact_search.argtypes = [P, i32]
+        lib.cpe_decode_test_search_mode.restype = i32
+        lib.cpe_decode_test_search_mode.argtypes = [P, i32]
         lib.cpe_check_sqrt.restype = i32
         lib.cpe_check_sqrt.argtypes = [P, P]
         _lib = lib
@@ -187,10 +187,11 @@ class Decoder:
         ``launch`` and reports CPE_ERR_HIP."""
         return library().cpe_decode_test_fail_launch(self._h, int(launch))
 
-    def test_exact_search(self, on: bool) -> int:
-        """cpe_decode_test_exact_search: label-only decodes recompute every
-        tile with the exact assignment search (on) or only near ties (off)."""
-        return library().cpe_decode_test_exact_search(self._h, int(bool(on)))
+    def test_search_mode(self, mode: int) -> int:
+        """cpe_decode_test_search_mode: 0 default (fast search on frames of
+        2^20 pixels or more), 1 every tile recomputed exactly, 2 the fast
+        search at any size."""
+        return library().cpe_decode_test_search_mode(self._h, int(mode))
 
     def histogram(self, out, stream=None) -> int:
         return library().cpe_decode_get_histogram(self._h, _stream_ptr(stream), _ptr(out))

@@ -158,11 +158,12 @@ def test_workload4_batch_back_to_back():
     dec.close()
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_every_tile_through_the_exact_search(cfg):
-    """Label-only decodes with every tile sent down the path that near ties
-    of the fast assignment search take (recomputed with correctly rounded
-    distances, exact search): equal to the oracle; then back to the default."""
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_fast_and_exact_assignment_searches(cfg):
+    """Label-only decodes in every search mode: the fast search at any size,
+    every tile sent down the path that near ties of the fast search take
+    (recomputed with correctly rounded distances, exact search), and the
+    default: all equal to the oracle."""
     nat = native()
     spec = synth.CONFIGS[cfg]
     th = thresholds()[str(cfg)]
@@ -171,9 +172,9 @@ def test_every_tile_through_the_exact_search(cfg):
     dec = nat.Decoder(spec.H, spec.W, spec.n_freq, spec.dtype, fx, fy, spec.bins, spec.bins, th["capacity"])
     ref = oracle.decode(f.emb, f.fg, fx, fy, spec.bins, spec.bins, th["capacity"], spec.fg_threshold,
                         th["peak_threshold"])
-    for forced in (True, False):
-        print(f"config {cfg}: exact search forced {forced}", flush=True)
-        assert dec.test_exact_search(forced) == 0
+    for mode in (2, 1, 0):
+        print(f"config {cfg}: search mode {mode}", flush=True)
+        assert dec.test_search_mode(mode) == 0
         got = gpu_decode(dec, f.emb, f.fg, spec.fg_threshold, th["peak_threshold"], score=False)
         assert_parity(got, ref, th["capacity"], check_score=False)
     dec.close()
