@@ -238,6 +238,20 @@ struct RawSlices {
     }
 };
 
+
+// An empty asm that takes the converted operands and clobbers memory: the
+// next tile's row loads, which follow it, issue after the conversion and
+// reuse the input registers (otherwise the compiler hoists them above the
+// conversion and copies 16 registers per tile).
+template <int F>
+__device__ __forceinline__ void after_convert(AxisOp<F> &X, AxisOp<F> &Y, int &n2x, int &n2y)
+{
+    if constexpr (AxisOp<F>::kPacked)
+        __asm__ volatile("" : "+v"(X.a[0]), "+v"(Y.a[0]), "+v"(n2x), "+v"(n2y) : : "memory");
+    else
+        __asm__ volatile("" : "+v"(X.a[0]), "+v"(X.a[1]), "+v"(Y.a[0]), "+v"(Y.a[1]), "+v"(n2x), "+v"(n2y) : : "memory");
+}
+
 // Palette operand of kind k for axis ax of lane `lane` (bin lane & 31, K
 // slots 16 (lane >> 5) .. + 15).
 __device__ __forceinline__ i32x4 palette_operand(const uint32_t *__restrict__ pop, int ax, int k, int lane)
@@ -578,6 +592,7 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
         AxisOp<F> X, Y;
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
+        after_convert(X, Y, n2x, n2y);
         next();
         n2x += __shfl_xor(n2x, 32);
         n2y += __shfl_xor(n2y, 32);
@@ -838,7 +853,16 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     // bin, gathered once and kept in registers for the whole run; distances
     // are computed only for the groups of 8 slots that hold candidates.
     const int nslot[2] = {__builtin_amdgcn_readfirstlane(pl.ncol), __builtin_amdgcn_readfirstlane(pl.nrow)};
+    // (the fast kernel reads them from LDS per tile: its search needs the
+    // registers)
     const int slotbin[2] = {g * 32 + pl.colbin[ln], g * 32 + pl.rowbin[ln]};
+    i32x4 popr[2][kPopKinds];
+    if constexpr (!FAST) {
+#pragma unroll
+        for (int ax = 0; ax < 2; ax++)
+#pragma unroll
+            for (int k = 0; k < kPopKinds; k++) popr[ax][k] = palette_operand(s_pop, ax, k, slotbin[ax]);
+    }
 
     // Distances of one tile (pixel m = lane & 31; this lane's 16 slots
     // acc_row(r, g) of each axis); `next` reuses the input registers once
@@ -859,7 +883,7 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
             i32x16 hh, mid, ll;
             i32x4 pop[kPopKinds];
 #pragma unroll
-            for (int k = 0; k < kPopKinds; k++) pop[k] = palette_operand(s_pop, ax, k, slotbin[ax]);
+            for (int k = 0; k < kPopKinds; k++) pop[k] = FAST ? palette_operand(s_pop, ax, k, slotbin[ax]) : popr[ax][k];
             axis_products<F, false>(ax ? Y : X, pop, row_init(s_cbs + ax * kMfmaBins, g), hh, mid, ll);
             const uint32_t np = ax ? npy : npx;
             uint32_t *dst = (ax ? ky : kx) + 4 * g * kKeyStride + ln;
