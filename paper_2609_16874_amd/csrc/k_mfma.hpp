@@ -979,40 +979,54 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     // are the hardware square roots r~ of fl32(S), each within one binary32
     // step of the correctly rounded r (cpe_check_sqrt verifies the step
     // correction of sqrt_cr, which only tries r~ and its two neighbours, on
-    // every input).  Lane l serves the pixels 2p, 2p + 1 (p = l & 15) over the
-    // batches j, j + 4, ... (j = l >> 4) of the unpadded list, so that no
-    // batch is seen twice, and keeps per pixel the smallest binary32 sum
-    // fl(min x~ + y~) of a batch, its batch, and the second smallest.  A
-    // step at v is at most 2^-23 v, so a batch's true minimum D lies within
-    // 2^-21 of its approximate sum; if the second smallest sum exceeds the
-    // smallest by at least 32 steps (> 2^-19 relative), every other batch's
-    // D exceeds the winning batch's.  Within the winning batch (one row,
-    // exact distances of one y), a column whose r~ is at least 3 steps above
-    // the batch's smallest r~ is strictly farther.  When both hold the
-    // winner is the unique minimiser of the exact sums, i.e. the candidate
-    // the exact search selects.  Otherwise (near ties, within a few units
-    // in the last place) the wave recomputes the tile exactly; false is
-    // returned and nothing is written.
+    // every input).  Lane l serves the pixels 4q .. 4q + 3 (q = l & 7) over
+    // the batches j, j + 8, ... (j = l >> 3) of the unpadded list, so that no
+    // batch is seen twice (one 16-byte read fetches a column's distances of
+    // its four pixels; the next batch's offsets are read ahead), and keeps
+    // per pixel the smallest binary32 sum fl(min x~ + y~) of a batch, its
+    // batch, and the second smallest.  A step at v is at most 2^-23 v, so a
+    // batch's true minimum D lies within 2^-21 of its approximate sum; if
+    // the second smallest sum exceeds the smallest by at least 32 steps
+    // (> 2^-19 relative), every other batch's D exceeds the winning batch's.
+    // Within the winning batch (one row, exact distances of one y), a column
+    // whose r~ is at least 3 steps above the batch's smallest r~ is strictly
+    // farther.  When both hold the winner is the unique minimiser of the
+    // exact sums, i.e. the candidate the exact search selects.  Otherwise
+    // (near ties, within a few units in the last place) the wave recomputes
+    // the tile exactly; false is returned and nothing is written.
     const int nbr = min(pl.nbat_real, kMaxBatchLds);
     auto search_fast = [&](int pix, int nvalid) -> bool {
         __builtin_amdgcn_wave_barrier();
         int lo = lane;
         __asm__ volatile("" : "+v"(lo));        // recomputed per tile, not held across the loop
-        const int p = lo & 15, j0 = lo >> 4;
-        const unsigned char *kxp = reinterpret_cast<const unsigned char *>(kx + 2 * p);
-        const unsigned char *kyp = reinterpret_cast<const unsigned char *>(ky + 2 * p);
-        float b[2] = {__builtin_inff(), __builtin_inff()}, s2[2] = {__builtin_inff(), __builtin_inff()};
-        int bx[2] = {0, 0};
-        for (int bi = j0; bi < nbr; bi += 4) {
-            const u32x4 o = s_bo[bi];
-            const uint32_t hb = s_bh[bi];
-            const u32x2 v0 = *reinterpret_cast<const u32x2 *>(kxp + o.x);
-            const u32x2 v1 = *reinterpret_cast<const u32x2 *>(kxp + o.y);
-            const u32x2 v2 = *reinterpret_cast<const u32x2 *>(kxp + o.z);
-            const u32x2 v3 = *reinterpret_cast<const u32x2 *>(kxp + o.w);
-            const u32x2 yd = *reinterpret_cast<const u32x2 *>(kyp + hb);
+        const int q = lo & 7, j0 = lo >> 3;
+        const unsigned char *kxq = reinterpret_cast<const unsigned char *>(kx + 4 * q);
+        const unsigned char *kyq = reinterpret_cast<const unsigned char *>(ky + 4 * q);
+        float b[4], s2[4];
+        int bx[4];
 #pragma unroll
-            for (int e = 0; e < 2; e++) {
+        for (int e = 0; e < 4; e++) {
+            b[e] = s2[e] = __builtin_inff();
+            bx[e] = 0;
+        }
+        u32x4 o = {};
+        uint32_t hb = 0;
+        if (j0 < nbr) {
+            o = s_bo[j0];
+            hb = s_bh[j0];
+        }
+        for (int bi = j0; bi < nbr; bi += 8) {
+            const u32x4 v0 = *reinterpret_cast<const u32x4 *>(kxq + o.x);
+            const u32x4 v1 = *reinterpret_cast<const u32x4 *>(kxq + o.y);
+            const u32x4 v2 = *reinterpret_cast<const u32x4 *>(kxq + o.z);
+            const u32x4 v3 = *reinterpret_cast<const u32x4 *>(kxq + o.w);
+            const u32x4 yd = *reinterpret_cast<const u32x4 *>(kyq + hb);
+            if (bi + 8 < nbr) {             // the next batch's offsets, read ahead
+                o = s_bo[bi + 8];
+                hb = s_bh[bi + 8];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
                 const uint32_t m = min(min(v0[e], v1[e]), min(v2[e], v3[e]));
                 const float sm = __uint_as_float(m) + __uint_as_float(yd[e]);
                 s2[e] = __builtin_amdgcn_fmed3f(b[e], s2[e], sm);
@@ -1020,42 +1034,51 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
                 b[e] = sm < b[e] ? sm : b[e];
             }
         }
-        // combine the four lanes of a pixel pair (equal smallest sums leave
-        // a second smallest equal to the smallest)
-        // (as bit patterns, which order like the non-negative sums)
-        uint32_t ub[2], us[2];
+        // the eight lanes of a pixel quad combine through LDS (the y array
+        // is no longer read): pixel m's partial j (smallest, second, batch)
+        // at word 25 m + 3 j (an odd pixel stride spreads the banks); half g
+        // of the wave merges j = 4g .. 4g + 3 for pixel m = lane & 31, then
+        // the two halves exchange (as bit patterns, which order like the
+        // non-negative sums; equal smallest sums leave a second smallest
+        // equal to the smallest)
+        __builtin_amdgcn_wave_barrier();
+        uint32_t *part = ky;
 #pragma unroll
-        for (int e = 0; e < 2; e++) {
-            ub[e] = __float_as_uint(b[e]);
-            us[e] = __float_as_uint(s2[e]);
+        for (int e = 0; e < 4; e++) {
+            uint32_t *w = part + (4 * q + e) * 25 + 3 * j0;
+            w[0] = __float_as_uint(b[e]);
+            w[1] = __float_as_uint(s2[e]);
+            w[2] = (uint32_t)bx[e];
         }
+        __builtin_amdgcn_wave_barrier();
+        uint32_t ub = 0xffffffffu, us = 0xffffffffu, ux = 0;
 #pragma unroll
-        for (int d = 16; d <= 32; d <<= 1)
-#pragma unroll
-            for (int e = 0; e < 2; e++) {
-                const uint32_t ob = __shfl_xor(ub[e], d), os = __shfl_xor(us[e], d);
-                const int ox = __shfl_xor(bx[e], d);
-                us[e] = min(min(us[e], os), max(ub[e], ob));
-                bx[e] = ob < ub[e] ? ox : bx[e];
-                ub[e] = min(ub[e], ob);
-            }
-        // lane m (either half) takes pixel m's result from lane
-        // (m >> 1) + 16 (m & 1), which offers its pixel 2p + (j & 1)
-        const int src = (ln >> 1) + 16 * (ln & 1);
-        const bool hi = (j0 & 1) != 0;
-        const uint32_t bb = __shfl(hi ? ub[1] : ub[0], src), ss = __shfl(hi ? us[1] : us[0], src);
-        const int bi = __shfl(hi ? bx[1] : bx[0], src);
-        const u32x4 o = s_bo[bi];
+        for (int jj = 0; jj < 4; jj++) {
+            const uint32_t *rp = part + ln * 25 + 3 * (4 * g + jj);
+            const u32x4 r = {rp[0], rp[1], rp[2], 0u};
+            us = min(min(us, r.y), max(ub, r.x));
+            ux = r.x < ub ? r.z : ux;
+            ub = min(ub, r.x);
+        }
+        {
+            const uint32_t ob = __shfl_xor(ub, 32), os = __shfl_xor(us, 32), ox = __shfl_xor(ux, 32);
+            us = min(min(us, os), max(ub, ob));
+            ux = ob < ub ? ox : ux;
+            ub = min(ub, ob);
+        }
+        __builtin_amdgcn_wave_barrier();
+        const int bi = (int)ux;
+        const u32x4 ow = s_bo[bi];
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
-        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
-        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
-        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
-        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + ow.x);
+        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + ow.y);
+        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + ow.z);
+        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + ow.w);
         const uint32_t wm = min(min(w0, w1), min(w2, w3));
-        const uint32_t oc = w0 == wm ? o.x : w1 == wm ? o.y : w2 == wm ? o.z : o.w;   // first column at the minimum
-        const bool near = (o.x != oc && w0 - wm < 3u) || (o.y != oc && w1 - wm < 3u) ||
-                          (o.z != oc && w2 - wm < 3u) || (o.w != oc && w3 - wm < 3u);
-        const bool amb = near || ss - bb < 32u;
+        const uint32_t oc = w0 == wm ? ow.x : w1 == wm ? ow.y : w2 == wm ? ow.z : ow.w;   // first column at the minimum
+        const bool near = (ow.x != oc && w0 - wm < 3u) || (ow.y != oc && w1 - wm < 3u) ||
+                          (ow.z != oc && w2 - wm < 3u) || (ow.w != oc && w3 - wm < 3u);
+        const bool amb = near || us - ub < 32u;
         const bool valid = g == 0 && ln < nvalid;
         if (force_exact || __ballot(amb && valid)) return false;
         if (valid) {
