@@ -725,9 +725,9 @@ constexpr int kAssignWpb = 4 * kAssignWaves<T, F>;
 
 // LDS bytes of k_assign_mfma: palette operands, |P|^2 by bin and by slot,
 // candidate batches, bin -> centroid table, counts, per wave x and y
-// distances [32 slots][kKeyStride] (u32), then the peak-extraction state;
-// then, 16-byte aligned, per wave the 32 search results of a tile (binary64
-// keys).  The summed vote histogram (32 x 32 slots, 8 KB) of the prologue
+// distances [32 slots][kKeyStride] (u32), then the peak-extraction state
+// (the searches merge their lanes' partial results in a wave's y array once
+// it is no longer read).  The summed vote histogram (32 x 32 slots, 8 KB) of the prologue
 // shares its bytes with the first waves' distance arrays, which are written
 // only after it is no longer read.
 constexpr size_t kAssignLdsCore(int wpb)
@@ -736,8 +736,7 @@ constexpr size_t kAssignLdsCore(int wpb)
            kMfmaBins * kMfmaBins * 4 + (size_t)wpb * 2 * kMfmaBins * kKeyStride * 4 + sizeof(PeakLds) +
            (kMaxSlices + 1) * 4 + 16;
 }
-constexpr size_t kBestOff(int wpb) { return (kAssignLdsCore(wpb) + 15) & ~(size_t)15; }
-constexpr size_t kAssignLds(int wpb) { return kBestOff(wpb) + (size_t)wpb * 32 * 8; }
+constexpr size_t kAssignLds(int wpb) { return (kAssignLdsCore(wpb) + 15) & ~(size_t)15; }
 
 // Every workgroup first sums the vote histograms `hcur` of the vote launch
 // and extracts the peaks in LDS (identical in every workgroup); workgroup 0
@@ -778,7 +777,6 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     PeakLds &pl = *reinterpret_cast<PeakLds *>(s_keys + kWpb2 * 2 * kMfmaBins * kKeyStride);
     int *s_pref = reinterpret_cast<int *>(&pl + 1);                                  // [kMaxSlices + 1]
     int *s_next = s_pref + kMaxSlices + 1;                                            // next tile of the run
-    unsigned long long *s_best = reinterpret_cast<unsigned long long *>(smem + kBestOff(kWpb2));   // [kWpb2][32]
     unsigned long long *s_h = reinterpret_cast<unsigned long long *>(s_keys);              // [32 * 32] summed votes
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -909,25 +907,28 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     // in binary64, has at least 12 zero bits at the bottom of its mantissa
     // (both distances are 0 or binary32 values of at least 1, so the sum is a
     // multiple of 2^-23 below 2^17), which take the batch index (< 128).  The
-    // eight lanes of a pixel quad then combine their minima, and lane m takes
-    // pixel m's result through LDS, finds the first column of the winning
-    // batch with the batch's smallest x distance, and (lanes of half 0, valid
+    // eight lanes of a pixel quad then combine their minima through LDS; lane
+    // m takes pixel m's result, finds the first column of the winning batch
+    // with the batch's smallest x distance, and (lanes of half 0, valid
     // pixels) writes its label.
-    unsigned long long *best_w = s_best + wv * 32;
     auto search = [&](int pix, int nvalid) {
         __builtin_amdgcn_wave_barrier();
         const int q = lane & 7, j0 = lane >> 3;
         const unsigned char *kxq = reinterpret_cast<const unsigned char *>(kx + 4 * q);
         const unsigned char *kyq = reinterpret_cast<const unsigned char *>(ky + 4 * q);
         double b4[4] = {__builtin_inf(), __builtin_inf(), __builtin_inf(), __builtin_inf()};
+        u32x4 o = s_bo[j0];                         // j0 < 8 <= nbat
+        uint32_t hb = s_bh[j0];
         for (int bi = j0; bi < nbat; bi += 8) {     // nbat is a multiple of 8: the same count for every lane
-            const u32x4 o = s_bo[bi];
-            const uint32_t hb = s_bh[bi];
             const u32x4 v0 = *reinterpret_cast<const u32x4 *>(kxq + o.x);
             const u32x4 v1 = *reinterpret_cast<const u32x4 *>(kxq + o.y);
             const u32x4 v2 = *reinterpret_cast<const u32x4 *>(kxq + o.z);
             const u32x4 v3 = *reinterpret_cast<const u32x4 *>(kxq + o.w);
             const u32x4 yd = *reinterpret_cast<const u32x4 *>(kyq + hb);
+            if (bi + 8 < nbat) {                    // the next batch's offsets, read ahead
+                o = s_bo[bi + 8];
+                hb = s_bh[bi + 8];
+            }
 #pragma unroll
             for (int e = 0; e < 4; e++) {
                 const uint32_t m = min(min(v0[e], v1[e]), min(v2[e], v3[e]));
@@ -937,28 +938,31 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
                 b4[e] = min_f64(b4[e], __longlong_as_double((long long)key));
             }
         }
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-            b4[e] = min_f64(b4[e], __shfl_xor(b4[e], 8));
-            b4[e] = min_f64(b4[e], __shfl_xor(b4[e], 16));
-            b4[e] = min_f64(b4[e], __shfl_xor(b4[e], 32));
-        }
-        if (lane < 8) {
-#pragma unroll
-            for (int e = 0; e < 4; e++) best_w[4 * q + e] = (unsigned long long)__double_as_longlong(b4[e]);
-        }
+        // the eight lanes of a pixel quad combine through LDS (the y array
+        // is no longer read): pixel m's partial key j at double 9 m + j (an
+        // odd pixel stride spreads the banks); half g of the wave takes
+        // j = 4g .. 4g + 3 for pixel m = lane & 31, then the halves exchange
         __builtin_amdgcn_wave_barrier();
-        const unsigned long long best = best_w[ln];
+        double *part = reinterpret_cast<double *>(ky);
+#pragma unroll
+        for (int e = 0; e < 4; e++) part[(4 * q + e) * 9 + j0] = b4[e];
+        __builtin_amdgcn_wave_barrier();
+        double bm = part[ln * 9 + 4 * g];
+#pragma unroll
+        for (int jj = 1; jj < 4; jj++) bm = min_f64(bm, part[ln * 9 + 4 * g + jj]);
+        bm = min_f64(bm, __shfl_xor(bm, 32));
+        __builtin_amdgcn_wave_barrier();
+        const unsigned long long best = (unsigned long long)__double_as_longlong(bm);
         const int bi = (int)((uint32_t)best & 127u);
         const double D = __longlong_as_double((long long)(best & ~127ull));
-        const u32x4 o = s_bo[bi];
+        const u32x4 ow = s_bo[bi];
         const unsigned char *kxl = reinterpret_cast<const unsigned char *>(kx + ln);
-        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + o.x);
-        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + o.y);
-        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + o.z);
-        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + o.w);
+        const uint32_t w0 = *reinterpret_cast<const uint32_t *>(kxl + ow.x);
+        const uint32_t w1 = *reinterpret_cast<const uint32_t *>(kxl + ow.y);
+        const uint32_t w2 = *reinterpret_cast<const uint32_t *>(kxl + ow.z);
+        const uint32_t w3 = *reinterpret_cast<const uint32_t *>(kxl + ow.w);
         const uint32_t wm = min(min(w0, w1), min(w2, w3));
-        const uint32_t col = (w0 == wm ? o.x : w1 == wm ? o.y : w2 == wm ? o.z : o.w) >> 7;   // column slot
+        const uint32_t col = (w0 == wm ? ow.x : w1 == wm ? ow.y : w2 == wm ? ow.z : ow.w) >> 7;   // column slot
         const uint32_t row = s_bh[bi] >> 7;                                                      // row slot
         if (g == 0 && ln < nvalid) {
             if (D < tau4096) {      // Eq8
