@@ -92,6 +92,11 @@ __device__ __forceinline__ f32x16 mfma16(f16x8 a, f16x8 b, f32x16 c)
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
+// Steps (binary32 units in the last place) by which the fast assignment
+// search needs the second smallest batch sum to exceed the smallest: at
+// least 7 by its error bound (see k_assign_mfma).
+constexpr int kFastGap = 8;
+
 // Row of the 32 x 32 MFMA result held by register r of a lane in group g.
 __device__ __forceinline__ constexpr int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
@@ -988,10 +993,13 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
     // batch is seen twice (one 16-byte read fetches a column's distances of
     // its four pixels; the next batch's offsets are read ahead), and keeps
     // per pixel the smallest binary32 sum fl(min x~ + y~) of a batch, its
-    // batch, and the second smallest.  A step at v is at most 2^-23 v, so a
-    // batch's true minimum D lies within 2^-21 of its approximate sum; if
-    // the second smallest sum exceeds the smallest by at least 32 steps
-    // (> 2^-19 relative), every other batch's D exceeds the winning batch's.
+    // batch, and the second smallest.  A step at v is at most 2^-23 v, so
+    // x~ + y~ lies within relative 2^-23 of x + y and the rounded sum s
+    // within relative g = 3 2^-24 + 2^-47 of the batch's true minimum D.
+    // If the second smallest sum exceeds the smallest s_w by kFastGap steps
+    // (each more than 2^-24 s_w), so by more than 2g / (1 - g) s_w, every
+    // other batch's D exceeds the winning batch's (a sum of 0 is exact: any
+    // other distance sum is at least 1).
     // Within the winning batch (one row, exact distances of one y), a column
     // whose r~ is at least 3 steps above the batch's smallest r~ is strictly
     // farther.  When both hold the winner is the unique minimiser of the
@@ -1082,7 +1090,7 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
         const uint32_t oc = w0 == wm ? ow.x : w1 == wm ? ow.y : w2 == wm ? ow.z : ow.w;   // first column at the minimum
         const bool near = (ow.x != oc && w0 - wm < 3u) || (ow.y != oc && w1 - wm < 3u) ||
                           (ow.z != oc && w2 - wm < 3u) || (ow.w != oc && w3 - wm < 3u);
-        const bool amb = near || us - ub < 32u;
+        const bool amb = near || us - ub < (uint32_t)kFastGap;
         const bool valid = g == 0 && ln < nvalid;
         if (force_exact || __ballot(amb && valid)) return false;
         if (valid) {
