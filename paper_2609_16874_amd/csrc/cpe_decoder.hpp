@@ -37,22 +37,33 @@ struct Scratch {
 // 8) for the assignment; ok = false when the frame is too large.
 struct FusedPlan {
     bool ok;
-    int slice, grid, seg_cap;
+    int slice, grid, seg_cap, rot;
 };
 inline FusedPlan fused_plan(int64_t npix)
 {
-    FusedPlan fp{false, 64, 1, 64};
+    FusedPlan fp{false, 64, 1, 64, 0};
     if (npix < 1 || npix > kFusedMaxPixels) return fp;
-    // 64-pixel slices (one wave step); 1024 when a workgroup owns 4096
-    // pixels or more (at 1024 x 2048: eight slices each, whose foreground
-    // counts vary less between workgroups than 128 slices of 64 pixels)
+    // 64-pixel slices (one wave step) dealt in turn.  When a workgroup owns
+    // 4096 pixels or more, consecutive workgroups' slices would form
+    // columns of the frame (at 1024 x 2048: 64-pixel strips, 8 rows apart),
+    // whose foreground counts differ much: there the slices are dealt with a
+    // rotation of 37 per round when the rounds are whole, else they are of
+    // 1024 pixels (on the seeded 1024 x 2048 frame of 150 instances the
+    // largest workgroup share of the foreground is 1.051 times the mean with
+    // the rotation, 1.091 with 1024-pixel slices and 1.29 with neither)
     const int64_t per_wg = (npix + kMaxSlices - 1) / kMaxSlices;
-    const int slice = per_wg >= 4096 ? 1024 : 64;
+    int slice = 64, rot = 0;
+    if (per_wg >= 4096) {
+        if (((npix + 63) / 64) % kMaxSlices == 0)
+            rot = 37;
+        else
+            slice = 1024;
+    }
     const int64_t nsl = (npix + slice - 1) / slice;
     const int64_t grid = nsl < kMaxSlices ? nsl : kMaxSlices;
     if ((nsl + grid - 1) / grid * slice > kFusedMaxSeg) return fp;     // the vote's list in LDS
     const int64_t seg = ((npix + grid - 1) / grid + 7) / 8 * 8;
-    return FusedPlan{true, slice, (int)grid, (int)seg};
+    return FusedPlan{true, slice, (int)grid, (int)seg, rot};
 }
 
 }  // namespace cpe

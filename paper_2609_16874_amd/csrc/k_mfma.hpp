@@ -354,26 +354,44 @@ constexpr size_t kVoteLds(int wpb, bool fused)
            16 + (fused ? (size_t)kFusedMaxSeg * 4 : 0);
 }
 
-// Eight foreground values from pixel p0 on (p0 a multiple of 8): one (fp16)
-// or two (fp32) 16-byte loads when the plane is 16-byte aligned and the
-// eight lie below lim, else one load per pixel below lim (0 beyond).
+// Eight foreground values from pixel p0 on (p0 a multiple of 8), in two
+// parts: load8_raw issues one (fp16) or two (fp32) 16-byte loads when the
+// plane is 16-byte aligned and the eight lie below lim (zero words
+// otherwise); load8_values gives the values, loading pixel by pixel below
+// lim (0 beyond) where the vector loads do not apply.
 template <typename T>
-__device__ __forceinline__ void load8(const T *fg, int p0, int lim, bool vec, float v[8])
+struct Raw8 {
+    uint4 w[sizeof(T) / 2];
+};
+template <typename T>
+__device__ __forceinline__ Raw8<T> load8_raw(const T *fg, int p0, int lim, bool vec)
+{
+    Raw8<T> r = {};
+    if (vec && p0 + 8 <= lim) {
+#pragma unroll
+        for (int k = 0; k < (int)(sizeof(T) / 2); k++) r.w[k] = reinterpret_cast<const uint4 *>(fg + p0)[k];
+    }
+    return r;
+}
+template <typename T>
+__device__ __forceinline__ void load8_values(const T *fg, int p0, int lim, bool vec, const Raw8<T> &r, float v[8])
 {
     if (vec && p0 + 8 <= lim) {
         if constexpr (sizeof(T) == 2) {
-            const uint4 w = *reinterpret_cast<const uint4 *>(fg + p0);
-            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+            const uint32_t ww[4] = {r.w[0].x, r.w[0].y, r.w[0].z, r.w[0].w};
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 v[2 * i] = half_bits_to_float(ww[i] & 0xffffu);
                 v[2 * i + 1] = half_bits_to_float(ww[i] >> 16);
             }
         } else {
-            const float4 a = *reinterpret_cast<const float4 *>(fg + p0);
-            const float4 b = *reinterpret_cast<const float4 *>(fg + p0 + 4);
-            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+#pragma unroll
+            for (int k = 0; k < 2; k++) {
+                v[4 * k] = __uint_as_float(r.w[k].x);
+                v[4 * k + 1] = __uint_as_float(r.w[k].y);
+                v[4 * k + 2] = __uint_as_float(r.w[k].z);
+                v[4 * k + 3] = __uint_as_float(r.w[k].w);
+            }
         }
     } else {
 #pragma unroll
@@ -387,15 +405,18 @@ __device__ __forceinline__ void load8(const T *fg, int p0, int lim, bool vec, fl
 // frame (seg_cap a multiple of 8) into list[b * seg_cap ..], their number
 // into counts[b] -- the assignment launch reads these segments as its slices,
 // in the frame's order -- and those of the slices of `slice` pixels (a
-// multiple of 64) dealt to it in turn (slice s to workgroup s mod G), in
-// LDS, in any order: the pixels it votes on, spread over the frame so that
-// the workgroups' shares of votes stay even.  The pixels outside the list
+// multiple of 64) dealt to it in turn, in LDS, in any order: the pixels it
+// votes on, spread over the frame so that the workgroups' shares of votes
+// stay even.  Round r deals the slices G r .. G r + G - 1, slice G r + c to
+// workgroup c, or with a rotation rot > 0 (G = 256, whole rounds) slice
+// G r + ((b + rot r) mod G) to workgroup b, which moves a workgroup's slices
+// across the columns of the frame from round to round.  The pixels outside the list
 // get their final outputs here.  The launch also clears `hnext`, the
 // histograms of the next frame.
 struct FusedArgs {
     const void *fg;              // foreground plane (element type of the embedding), or null: every pixel
     float fg_thr;
-    int32_t slice, seg_cap;
+    int32_t slice, seg_cap, rot;
     int32_t *list, *counts;
     int32_t *labels;
     float *score;
@@ -485,19 +506,36 @@ __global__ __launch_bounds__((kVoteWpb<T, F> * 64)) __attribute__((amdgpu_waves_
             const int csh = __builtin_ctz(fz.slice) - 3;                // log2 of the 8-pixel chunks per slice
             const int steps = steps_a + ((mine << csh) + 63) / 64;
             int32_t *seg = fz.list + (size_t)lo;
-            for (int j = wv; j < steps; j += kWpb) {
-                const bool in_a = j < steps_a;                          // wave-uniform
-                int p0, lim;
-                if (in_a) {
+            // first pixel and limit of this lane's 8 in step j
+            auto place = [&](int j, int &p0, int &lim) {
+                if (j < steps_a) {
                     p0 = lo + j * 512 + lane * 8;
                     lim = hi;
                 } else {
                     const int c = (j - steps_a) * 64 + lane, r = c >> csh;
-                    p0 = (b + G * r) * fz.slice + ((c & ((1 << csh) - 1)) << 3);
+                    const int sb = fz.rot ? (b + fz.rot * r) & (kMaxSlices - 1) : b;   // rot: G = kMaxSlices
+                    p0 = (sb + G * r) * fz.slice + ((c & ((1 << csh) - 1)) << 3);
                     lim = r < mine ? npix : 0;
                 }
+            };
+            // the next step's foreground words are loaded before this step's
+            // are used
+            int pn = 0, limn = 0;
+            Raw8<T> rn = {};
+            if (wv < steps) {
+                place(wv, pn, limn);
+                rn = load8_raw<T>(fgp, pn, limn, vec);
+            }
+            for (int j = wv; j < steps; j += kWpb) {
+                const bool in_a = j < steps_a;                          // wave-uniform
+                const int p0 = pn, lim = limn;
+                const Raw8<T> rc = rn;
+                if (j + kWpb < steps) {
+                    place(j + kWpb, pn, limn);
+                    rn = load8_raw<T>(fgp, pn, limn, vec);
+                }
                 float v[8];
-                load8<T>(fgp, p0, lim, vec, v);
+                load8_values<T>(fgp, p0, lim, vec, rc, v);
                 uint32_t m = 0, valid = 0;
 #pragma unroll
                 for (int i = 0; i < 8; i++) {
@@ -878,6 +916,7 @@ __global__ __launch_bounds__((kAssignWpb<T, F> * 64)) __attribute__((amdgpu_wave
         AxisOp<F> X, Y;
         raw.convert(0, X, n2x);
         raw.convert(1, Y, n2y);
+        after_convert(X, Y, n2x, n2y);
         next();
         const uint32_t npx = (uint32_t)(n2x + __shfl_xor(n2x, 32));
         const uint32_t npy = (uint32_t)(n2y + __shfl_xor(n2y, 32));

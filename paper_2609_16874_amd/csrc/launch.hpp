@@ -91,7 +91,7 @@ cpe_status launch_all(cpe_decoder *h, const Scratch &sc, const FrameArgs &fa)
         }
         // launch 1: compaction of each workgroup's slices, recovery +
         // voting on them, the next frame's histograms cleared
-        const FusedArgs fz{fg, fg_thr, fp.slice, fp.seg_cap, list, sc.counts, labels, score,
+        const FusedArgs fz{fg, fg_thr, fp.slice, fp.seg_cap, fp.rot, list, sc.counts, labels, score,
                            hnext, (int32_t)nclear};
         if (sc.dirty[par] < nused) sc.dirty[par] = nused;
         if (!launch(1, k_vote_mfma<T, F, false, true>, dim3(fp.grid), dim3(wpb * 64), 0, e, dstride, yoff,

@@ -353,6 +353,22 @@ def test_argument_errors_on_device():
     dec.close()
 
 
+@pytest.mark.parametrize("H,W", [(1000, 1000), (1024, 1024), (1030, 1024)])
+def test_vote_slice_dealings_of_large_frames(H, W):
+    """The vote launch deals 64-pixel slices in turn below 4096 pixels per
+    workgroup (1000 x 1000), with a rotation per round from there when the
+    rounds are whole (1024 x 1024), else 1024-pixel slices (1030 x 1024):
+    each equals the oracle."""
+    rng = np.random.default_rng(H * 7 + W)
+    emb, fg, fx, fy = _random_frame(rng, H, W, 1, np.float16)
+    ref0 = oracle.decode(emb, fg, fx, fy, 8, 8, 16, 0.5, 0.0)
+    theta = 0.05 * ref0["hist"].max() * 2.0 ** -30
+    print(f"{H}x{W}", flush=True)
+    got, ref = run_pair(emb, fg, fx, fy, 8, 8, 16, 0.5, theta)
+    assert ref["K"] > 0
+    assert_parity(got, ref, 16)
+
+
 @pytest.mark.parametrize("H,W", [(1024, 2048), (1, 2097153)])
 def test_frames_at_the_two_launch_limit(H, W):
     """The largest frame whose vote launch lists the pixels itself (2^21
